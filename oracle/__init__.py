@@ -1,0 +1,228 @@
+"""LittleBit reference oracle -- TEST INFRASTRUCTURE ONLY.
+
+Python access to the fp64 CPU oracle in ``lb_oracle.c`` (plain C, built with
+gcc).  Only the test suite, the smoke check and the benchmark's CPU-baseline
+leg may import this package.  The GPU product path (the C-ABI library and its
+Python binding) never imports it, and it never imports them: the two share no
+code.
+
+Stored-dtype decoding lives here too, written independently of the product:
+bf16 is the upper half of an IEEE binary32, fp16 is IEEE binary16; both are
+widened to fp64 exactly.
+
+Functions and the passages of arXiv 2506.13771 they follow:
+  pack / unpack            sign binarisation, Sec. 3.1 Eq. (uv_sign), in the
+                           packed sign layout "LB layout v1";
+  forward_factored (O1)    Proposition 1, Eq. (proposition1), summed over the
+                           primary and residual paths, Sec. 3.3
+                           Eq. (final_weight_approx_res);
+  forward_sampled          O1 restricted to chosen output elements;
+  dense_weight (O2)        Eqs. (w_primary_hat), (res_approx_structure),
+                           (final_weight_approx_res);
+  dense_forward (O2)       Y = X W_hat^T, the left side of Proposition 1;
+  bpw / rank_real /
+  rank_for_bpw             Appendix "Average Bits Per Weight Calculation",
+                           Eqs. (b_calculation) and (r_calculation).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "lb_oracle.c")
+_LIB = os.path.join(_HERE, "liblb_oracle.so")
+
+F32, F16, BF16 = "f32", "f16", "bf16"
+
+
+def build(force: bool = False) -> str:
+    """Compile lb_oracle.c into liblb_oracle.so with gcc (fp64, -O2, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.run(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fno-fast-math",
+                        "-ffp-contract=off", _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        lib = ctypes.CDLL(build())
+        i64, f64, i32 = ctypes.c_int64, ctypes.c_double, ctypes.c_int
+        vp = ctypes.c_void_p
+        lib.lbo_packed_bytes.restype = i64
+        lib.lbo_packed_bytes.argtypes = [i64, i64, i32]
+        lib.lbo_pack.restype = i64
+        lib.lbo_pack.argtypes = [vp, i64, i64, i32, vp]
+        lib.lbo_unpack.restype = None
+        lib.lbo_unpack.argtypes = [vp, i64, i64, i32, vp]
+        lib.lbo_pad_bits_clear.restype = i32
+        lib.lbo_pad_bits_clear.argtypes = [vp, i64, i64, i32]
+        lib.lbo_forward_factored.restype = None
+        lib.lbo_forward_factored.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, i32, vp]
+        lib.lbo_forward_sampled.restype = None
+        lib.lbo_forward_sampled.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, i32, vp, vp, i64, vp]
+        lib.lbo_dense_weight.restype = None
+        lib.lbo_dense_weight.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, i32, vp]
+        lib.lbo_dense_forward.restype = None
+        lib.lbo_dense_forward.argtypes = [vp, i64, i64, i64, vp, vp]
+        lib.lbo_bpw.restype = f64
+        lib.lbo_bpw.argtypes = [i64, i64, i64, i32]
+        lib.lbo_total_bits.restype = f64
+        lib.lbo_total_bits.argtypes = [i64, i64, i64, i32]
+        lib.lbo_rank_real.restype = f64
+        lib.lbo_rank_real.argtypes = [i64, i64, f64]
+        lib.lbo_rank_for_bpw.restype = i64
+        lib.lbo_rank_for_bpw.argtypes = [i64, i64, f64, i64, i32]
+        _lib = lib
+    return _lib
+
+
+# ----------------------------------------------------------------------------
+# stored dtypes -> fp64 (exact)
+# ----------------------------------------------------------------------------
+def to_f64(raw: np.ndarray, dtype: str) -> np.ndarray:
+    """Widen stored values to fp64 exactly.  bf16/fp16 are given as uint16 bit patterns."""
+    raw = np.ascontiguousarray(raw)
+    if dtype == F32:
+        return raw.astype(np.float32, copy=False).astype(np.float64)
+    if dtype == F16:
+        return raw.view(np.uint16).view(np.float16).astype(np.float64)
+    if dtype == BF16:
+        return (raw.view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    raise ValueError(dtype)
+
+
+def _p(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _ptr_array(arrs):
+    arr = (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])
+    return arr
+
+
+# ----------------------------------------------------------------------------
+# packing (LB layout v1)
+# ----------------------------------------------------------------------------
+ROLE_U, ROLE_V = 0, 1
+
+
+def packed_bytes(rows: int, r: int, role: int) -> int:
+    return int(_load().lbo_packed_bytes(rows, r, role))
+
+
+def pack(src: np.ndarray, role: int):
+    """Signs of a natural-orientation matrix src[rows][r] -> (bytes as uint8 array, nan count)."""
+    src = np.ascontiguousarray(src, dtype=np.float64)
+    rows, r = src.shape
+    out = np.zeros(packed_bytes(rows, r, role), dtype=np.uint8)
+    nans = _load().lbo_pack(_p(src), rows, r, role, _p(out))
+    return out, int(nans)
+
+
+def unpack(buf: np.ndarray, rows: int, r: int, role: int) -> np.ndarray:
+    """Packed bytes -> int8 matrix [rows][r] with values -1/+1."""
+    buf = np.ascontiguousarray(buf).view(np.uint8)
+    assert buf.size == packed_bytes(rows, r, role)
+    out = np.empty((rows, r), dtype=np.int8)
+    _load().lbo_unpack(_p(buf), rows, r, role, _p(out))
+    return out
+
+
+def pad_bits_clear(buf: np.ndarray, rows: int, r: int, role: int) -> bool:
+    buf = np.ascontiguousarray(buf).view(np.uint8)
+    return bool(_load().lbo_pad_bits_clear(_p(buf), rows, r, role))
+
+
+# ----------------------------------------------------------------------------
+# forward
+# ----------------------------------------------------------------------------
+def _paths(U, V, h, g, l):
+    U = [np.ascontiguousarray(u, dtype=np.int8) for u in U]
+    V = [np.ascontiguousarray(v, dtype=np.int8) for v in V]
+    h = [np.ascontiguousarray(a, dtype=np.float64) for a in h]
+    g = [np.ascontiguousarray(a, dtype=np.float64) for a in g]
+    l = [np.ascontiguousarray(a, dtype=np.float64) for a in l]
+    n = len(U)
+    assert n in (1, 2) and all(len(a) == n for a in (V, h, g, l))
+    return U, V, h, g, l, n
+
+
+def forward_factored(x, U, V, h, g, l) -> np.ndarray:
+    """O1.  x [T,d_in] fp64; U[p] int8 [d_out,r]; V[p] int8 [d_in,r]; h,g,l fp64 per path."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    U, V, h, g, l, n = _paths(U, V, h, g, l)
+    T, d_in = x.shape
+    d_out, r = U[0].shape
+    y = np.empty((T, d_out), dtype=np.float64)
+    keep = (U, V, h, g, l)
+    _load().lbo_forward_factored(_p(x), T, d_in, d_out, r, _ptr_array(U), _ptr_array(V),
+                                 _ptr_array(h), _ptr_array(g), _ptr_array(l), n, _p(y))
+    del keep
+    return y
+
+
+def forward_sampled(x, U, V, h, g, l, ts, is_) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    U, V, h, g, l, n = _paths(U, V, h, g, l)
+    T, d_in = x.shape
+    d_out, r = U[0].shape
+    ts = np.ascontiguousarray(ts, dtype=np.int64)
+    is_ = np.ascontiguousarray(is_, dtype=np.int64)
+    assert ts.shape == is_.shape and (ts.size == 0 or (ts.min() >= 0 and ts.max() < T
+                                                       and is_.min() >= 0 and is_.max() < d_out))
+    out = np.empty(ts.size, dtype=np.float64)
+    _load().lbo_forward_sampled(_p(x), T, d_in, d_out, r, _ptr_array(U), _ptr_array(V),
+                                _ptr_array(h), _ptr_array(g), _ptr_array(l), n,
+                                _p(ts), _p(is_), ts.size, _p(out))
+    return out
+
+
+def dense_weight(U, V, h, g, l) -> np.ndarray:
+    U, V, h, g, l, n = _paths(U, V, h, g, l)
+    d_out, r = U[0].shape
+    d_in = V[0].shape[0]
+    W = np.empty((d_out, d_in), dtype=np.float64)
+    _load().lbo_dense_weight(d_in, d_out, r, _ptr_array(U), _ptr_array(V),
+                             _ptr_array(h), _ptr_array(g), _ptr_array(l), n, _p(W))
+    return W
+
+
+def dense_forward(x, W) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    W = np.ascontiguousarray(W, dtype=np.float64)
+    T, d_in = x.shape
+    d_out = W.shape[0]
+    assert W.shape[1] == d_in
+    y = np.empty((T, d_out), dtype=np.float64)
+    _load().lbo_dense_forward(_p(x), T, d_in, d_out, _p(W), _p(y))
+    return y
+
+
+# ----------------------------------------------------------------------------
+# bits per weight / rank
+# ----------------------------------------------------------------------------
+def total_bits(d_in: int, d_out: int, r: int, npaths: int = 2) -> float:
+    return float(_load().lbo_total_bits(d_in, d_out, r, npaths))
+
+
+def bpw(d_in: int, d_out: int, r: int, npaths: int = 2) -> float:
+    return float(_load().lbo_bpw(d_in, d_out, r, npaths))
+
+
+def rank_real(d_in: int, d_out: int, b: float) -> float:
+    return float(_load().lbo_rank_real(d_in, d_out, b))
+
+
+def rank_for_bpw(d_in: int, d_out: int, b: float, mult: int = 16, mode: int = 1) -> int:
+    """mode 0: nearest integer (paper's examples); mode 1: largest multiple of mult within budget."""
+    return int(_load().lbo_rank_for_bpw(d_in, d_out, b, mult, mode))

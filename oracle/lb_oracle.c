@@ -1,0 +1,285 @@
+/*
+ * LittleBit reference oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, fp64 CPU implementation of what one LittleBit linear layer
+ * computes (arXiv 2506.13771, "LittleBit: Ultra Low-Bit Quantization via
+ * Latent Factorization").  Only the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark may load this file's library.  The GPU
+ * product path never calls it and shares no code, header, table or helper
+ * with it.
+ *
+ * What it follows:
+ *   - sign binarisation of the latent factors: Sec. 3.1, Eq. (uv_sign);
+ *   - the primary effective weight diag(h) U_sign diag(l) V_sign^T diag(g):
+ *     Sec. 3.1, Eq. (w_primary_hat);
+ *   - the factored forward of Proposition 1, Eq. (proposition1), with its
+ *     proof in Appendix "Mathematical Analysis and Proofs";
+ *   - the residual path of identical structure and the sum of both paths:
+ *     Sec. 3.3, Eqs. (res_approx_structure) and (final_weight_approx_res);
+ *   - the bits-per-weight accounting and its inversion for the rank:
+ *     Appendix "Average Bits Per Weight Calculation", Eqs. (b_calculation)
+ *     and (r_calculation);
+ *   - the packed sign layout "LB layout v1" defined in the project's design
+ *     notes (the paper only says signs are packed into uint32 words,
+ *     Appendix "Inference Efficiency Analysis").
+ *
+ * Readings taken where the paper is silent (each listed in the design notes):
+ *   - sign(v) = -1 iff v < 0, else +1 (so +0 and -0 map to +1);
+ *   - a set bit means -1;
+ *   - both paths share one rank r.
+ *
+ * Parity pins: every function here is pinned by a CPU test against values
+ * the paper prints (the two worked BPW examples, the op-count example), closed
+ * forms (all-ones signs, r = 1), invariants of the factorisation (sign flips,
+ * latent permutations, path swap, linearity) and brute force on tiny inputs.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---------------------------------------------------------------------- */
+/* Sign convention (Eq. uv_sign): the codomain is {-1,+1}.                 */
+/* ---------------------------------------------------------------------- */
+int lbo_is_negative(double v) { return v < 0.0; }
+
+/* ---------------------------------------------------------------------- */
+/* LB layout v1.                                                           */
+/*                                                                         */
+/* A sign matrix is seen as M[o][q]: o = output index of the stage that    */
+/* reads it, q = its reduction index.                                      */
+/*   role U (0): M = U_sign,    o = i in [0,d_out), q = k in [0,r)         */
+/*   role V (1): M = V_sign^T,  o = k in [0,r),     q = j in [0,d_in)      */
+/* bit(o,q) = 1 iff the source value is < 0.                               */
+/* Region A: nb = n_red / 32 full blocks, uint32 A[nb][n_out] (o fastest), */
+/*   bit t (LSB = 0) of A[b][o] is bit(o, 32 b + t).                       */
+/* Region B (tail), w = n_red - 32 nb:                                     */
+/*   w == 0: absent; 1..16: uint16 B[n_out]; 17..31: uint32 B[n_out];      */
+/*   bit t of B[o] is bit(o, 32 nb + t) for t < w, else 0.                 */
+/* Region B begins at byte 4 nb n_out.  Words are little-endian.           */
+/* ---------------------------------------------------------------------- */
+static void stage_dims(int64_t rows, int64_t r, int role, int64_t* n_out, int64_t* n_red) {
+  if (role == 0) { *n_out = rows; *n_red = r; }
+  else { *n_out = r; *n_red = rows; }
+}
+
+int64_t lbo_packed_bytes(int64_t rows, int64_t r, int role) {
+  int64_t n_out, n_red;
+  stage_dims(rows, r, role, &n_out, &n_red);
+  int64_t nb = n_red / 32, w = n_red - 32 * nb;
+  int64_t tail = (w == 0) ? 0 : (w <= 16 ? 2 : 4);
+  return 4 * nb * n_out + tail * n_out;
+}
+
+/* Element of the stage view M[o][q] taken from the natural-orientation
+   matrix src[rows][r] (U is [d_out x r], V is [d_in x r]). */
+static double stage_elem(const double* src, int64_t r, int role, int64_t o, int64_t q) {
+  return role == 0 ? src[o * r + q] : src[q * r + o];
+}
+
+static void put_le(uint8_t* p, uint64_t v, int nbytes) {
+  for (int i = 0; i < nbytes; i++) p[i] = (uint8_t)(v >> (8 * i));
+}
+
+static uint64_t get_le(const uint8_t* p, int nbytes) {
+  uint64_t v = 0;
+  for (int i = 0; i < nbytes; i++) v |= (uint64_t)p[i] << (8 * i);
+  return v;
+}
+
+/* Pack the signs of src[rows][r] (fp64) into dst (lbo_packed_bytes bytes).
+   Returns the number of NaN inputs met (their bit is written as 0). */
+int64_t lbo_pack(const double* src, int64_t rows, int64_t r, int role, uint8_t* dst) {
+  int64_t n_out, n_red, nans = 0;
+  stage_dims(rows, r, role, &n_out, &n_red);
+  int64_t nb = n_red / 32, w = n_red - 32 * nb;
+  for (int64_t b = 0; b < nb; b++)
+    for (int64_t o = 0; o < n_out; o++) {
+      uint64_t word = 0;
+      for (int t = 0; t < 32; t++) {
+        double v = stage_elem(src, r, role, o, 32 * b + t);
+        if (isnan(v)) nans++;
+        if (lbo_is_negative(v)) word |= (uint64_t)1 << t;
+      }
+      put_le(dst + 4 * (b * n_out + o), word, 4);
+    }
+  if (w > 0) {
+    int tb = w <= 16 ? 2 : 4;
+    for (int64_t o = 0; o < n_out; o++) {
+      uint64_t word = 0;
+      for (int t = 0; t < w; t++) {
+        double v = stage_elem(src, r, role, o, 32 * nb + t);
+        if (isnan(v)) nans++;
+        if (lbo_is_negative(v)) word |= (uint64_t)1 << t;
+      }
+      put_le(dst + 4 * nb * n_out + tb * o, word, tb);
+    }
+  }
+  return nans;
+}
+
+/* Read bit(o,q) of a packed buffer, straight from the layout definition. */
+static int packed_bit(const uint8_t* buf, int64_t n_out, int64_t n_red, int64_t o, int64_t q) {
+  int64_t nb = n_red / 32, w = n_red - 32 * nb;
+  if (q < 32 * nb) {
+    int64_t b = q / 32;
+    return (int)((get_le(buf + 4 * (b * n_out + o), 4) >> (q - 32 * b)) & 1);
+  }
+  int tb = w <= 16 ? 2 : 4;
+  return (int)((get_le(buf + 4 * nb * n_out + tb * o, tb) >> (q - 32 * nb)) & 1);
+}
+
+/* Unpack into the natural orientation: out[rows][r] in {-1,+1}. */
+void lbo_unpack(const uint8_t* buf, int64_t rows, int64_t r, int role, int8_t* out) {
+  int64_t n_out, n_red;
+  stage_dims(rows, r, role, &n_out, &n_red);
+  for (int64_t row = 0; row < rows; row++)
+    for (int64_t k = 0; k < r; k++) {
+      int64_t o = role == 0 ? row : k;
+      int64_t q = role == 0 ? k : row;
+      out[row * r + k] = packed_bit(buf, n_out, n_red, o, q) ? -1 : +1;
+    }
+}
+
+/* Returns 1 iff every pad bit (tail bits at t >= w) of the buffer is 0. */
+int lbo_pad_bits_clear(const uint8_t* buf, int64_t rows, int64_t r, int role) {
+  int64_t n_out, n_red;
+  stage_dims(rows, r, role, &n_out, &n_red);
+  int64_t nb = n_red / 32, w = n_red - 32 * nb;
+  if (w == 0) return 1;
+  int tb = w <= 16 ? 2 : 4;
+  for (int64_t o = 0; o < n_out; o++)
+    if (get_le(buf + 4 * nb * n_out + tb * o, tb) >> w) return 0;
+  return 1;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Forward of one LittleBit linear layer, two paths.                       */
+/*                                                                         */
+/* Shapes (Sec. 3.1): X is [T x d_in] (the paper's seq x d_in), U_sign is  */
+/* [d_out x r], V_sign is [d_in x r], h in R^d_out, g in R^d_in, l in R^r. */
+/* Arrays for path p are passed as the p-th entry of two-element arrays:   */
+/* p = 0 primary, p = 1 residual.  Everything is fp64; sign matrices are   */
+/* int8 with values -1/+1 in natural orientation, row-major.               */
+/* ---------------------------------------------------------------------- */
+
+/* O1: Proposition 1, Eq. (proposition1), evaluated left to right:
+     a = X (.) g ; z = a V_sign ; w = z (.) l ; u = w U_sign^T ; y_p = u (.) h
+   and the layer output is the sum over the two paths (Eq. final_weight_approx_res
+   applied to X).  Loops run with ascending indices. */
+void lbo_forward_factored(const double* x, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                          const int8_t* const* U, const int8_t* const* V,
+                          const double* const* h, const double* const* g, const double* const* l,
+                          int npaths, double* y) {
+  double* a = (double*)malloc(sizeof(double) * (size_t)(d_in > 0 ? d_in : 1));
+  double* z = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+  for (int64_t i = 0; i < T * d_out; i++) y[i] = 0.0;
+  for (int p = 0; p < npaths; p++) {
+    for (int64_t t = 0; t < T; t++) {
+      for (int64_t j = 0; j < d_in; j++) a[j] = x[t * d_in + j] * g[p][j];
+      for (int64_t k = 0; k < r; k++) {
+        double s = 0.0;
+        for (int64_t j = 0; j < d_in; j++) s += (double)V[p][j * r + k] * a[j];
+        z[k] = s * l[p][k];
+      }
+      for (int64_t i = 0; i < d_out; i++) {
+        double s = 0.0;
+        for (int64_t k = 0; k < r; k++) s += (double)U[p][i * r + k] * z[k];
+        y[t * d_out + i] += s * h[p][i];
+      }
+    }
+  }
+  free(a);
+  free(z);
+}
+
+/* Same as lbo_forward_factored but only for the listed (t, i) output
+   elements; used to check very large layers on a sample of outputs. */
+void lbo_forward_sampled(const double* x, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                         const int8_t* const* U, const int8_t* const* V,
+                         const double* const* h, const double* const* g, const double* const* l,
+                         int npaths, const int64_t* ts, const int64_t* is, int64_t n, double* out) {
+  (void)T; (void)d_out;
+  double* z = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+  for (int64_t e = 0; e < n; e++) {
+    int64_t t = ts[e], i = is[e];
+    double acc = 0.0;
+    for (int p = 0; p < npaths; p++) {
+      for (int64_t k = 0; k < r; k++) {
+        double s = 0.0;
+        for (int64_t j = 0; j < d_in; j++) s += (double)V[p][j * r + k] * (x[t * d_in + j] * g[p][j]);
+        z[k] = s * l[p][k];
+      }
+      double s = 0.0;
+      for (int64_t k = 0; k < r; k++) s += (double)U[p][i * r + k] * z[k];
+      acc += s * h[p][i];
+    }
+    out[e] = acc;
+  }
+  free(z);
+}
+
+/* O2 part 1: the effective weight W_hat = sum_p diag(h_p) U_p diag(l_p) V_p^T diag(g_p)
+   (Eqs. w_primary_hat, res_approx_structure, final_weight_approx_res), entry by
+   entry:  W[i][j] = sum_p h_p[i] g_p[j] sum_k U_p[i][k] l_p[k] V_p[j][k]. */
+void lbo_dense_weight(int64_t d_in, int64_t d_out, int64_t r,
+                      const int8_t* const* U, const int8_t* const* V,
+                      const double* const* h, const double* const* g, const double* const* l,
+                      int npaths, double* W) {
+  for (int64_t i = 0; i < d_out; i++)
+    for (int64_t j = 0; j < d_in; j++) {
+      double acc = 0.0;
+      for (int p = 0; p < npaths; p++) {
+        double s = 0.0;
+        for (int64_t k = 0; k < r; k++) s += (double)U[p][i * r + k] * l[p][k] * (double)V[p][j * r + k];
+        acc += h[p][i] * s * g[p][j];
+      }
+      W[i * d_in + j] = acc;
+    }
+}
+
+/* O2 part 2: Y = X W_hat^T by its definition, y[t][i] = sum_j x[t][j] W[i][j]. */
+void lbo_dense_forward(const double* x, int64_t T, int64_t d_in, int64_t d_out, const double* W, double* y) {
+  for (int64_t t = 0; t < T; t++)
+    for (int64_t i = 0; i < d_out; i++) {
+      double s = 0.0;
+      for (int64_t j = 0; j < d_in; j++) s += x[t * d_in + j] * W[i * d_in + j];
+      y[t * d_out + i] = s;
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Bits per weight (Appendix "Average Bits Per Weight Calculation").       */
+/* Each path stores U_sign and V_sign at 1 bit per element and h, g, l at  */
+/* 16 bits per element; with both paths the total is                       */
+/*   2 r (d_out + d_in) + 32 (d_out + d_in) + 32 r    (Eq. b_calculation)   */
+/* divided by d_out d_in.  Without the residual path the leading factor 2  */
+/* of the per-path sum is dropped.                                         */
+/* ---------------------------------------------------------------------- */
+double lbo_total_bits(int64_t d_in, int64_t d_out, int64_t r, int npaths) {
+  double per_path = (double)d_out * r + (double)d_in * r + 16.0 * d_out + 16.0 * d_in + 16.0 * r;
+  return npaths * per_path;
+}
+
+double lbo_bpw(int64_t d_in, int64_t d_out, int64_t r, int npaths) {
+  return lbo_total_bits(d_in, d_out, r, npaths) / ((double)d_in * (double)d_out);
+}
+
+/* Eq. (r_calculation), before rounding. */
+double lbo_rank_real(int64_t d_in, int64_t d_out, double b) {
+  double s = (double)d_in + (double)d_out;
+  return (b * (double)d_out * (double)d_in - 32.0 * s) / (2.0 * s + 32.0);
+}
+
+/* Integer rank for a target b.
+   mode 0: nearest integer to Eq. (r_calculation) (the paper's examples);
+   mode 1: the largest multiple of `mult` whose total bits stay within
+           b d_in d_out (the rounding the benchmark configurations use). */
+int64_t lbo_rank_for_bpw(int64_t d_in, int64_t d_out, double b, int64_t mult, int mode) {
+  if (mode == 0) return (int64_t)floor(lbo_rank_real(d_in, d_out, b) + 0.5);
+  if (mult < 1) mult = 1;
+  double budget = b * (double)d_in * (double)d_out;
+  int64_t r = 0;
+  while (lbo_total_bits(d_in, d_out, r + mult, 2) <= budget) r += mult;
+  return r;
+}
