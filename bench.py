@@ -1,0 +1,342 @@
+#!/usr/bin/env python3
+"""Benchmark of the LittleBit linear-layer forward on one MI355X.
+
+Default workload (one "step" = one full forward of the layer through the C ABI,
+both paths, all scalings): a Llama2-7B q_proj-shaped LittleBit linear,
+d_in = d_out = 4096 at 0.1 bits per weight (rank r = 80 per path), T = 1
+token (decode), bf16 activations, fp16 scales, signs Bernoulli(1/2), inputs
+resident in HBM.  Prints ONE JSON line:
+  value      tokens/s over the timed steps
+  roofline   algorithmic bytes per launch / average launch duration vs 8 TB/s
+  cpu_baseline  the fp64 oracle timed on this host's cores on the same inputs
+
+--sweep FILE additionally writes one JSON line per (configuration, linear, T)
+for the other benchmark configurations (Llama2-7B block at 0.1/0.55 BPW and
+T in {1,16,64}; Llama2-13B prefill at T=2048; Llama2-70B 80-layer decode sweep).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ----------------------------------------------------------------------------
+# algorithmic cost model (per call)
+# ----------------------------------------------------------------------------
+def alg_bytes(T, d_in, d_out, r, e_act=2, e_scale=2):
+    signs = 2 * r * (d_in + d_out) / 8.0               # both paths, 1 bit per sign
+    scales = 2 * e_scale * (d_in + d_out + r)           # h, g, l for both paths
+    acts = T * d_in * e_act + T * d_out * e_act         # x read once, y written once
+    return signs + scales + acts, signs + scales
+
+
+def alg_flops(T, d_in, d_out, r):
+    return 2.0 * 2 * T * r * (d_in + d_out)            # two paths, multiply-add counted as 2
+
+
+# ----------------------------------------------------------------------------
+# device setup
+# ----------------------------------------------------------------------------
+class Layer:
+    """One LittleBit linear resident on the GPU, plus a pre-marshalled C-ABI call."""
+
+    def __init__(self, li, device, kernel=0, pack_on_gpu=True):
+        import torch
+        import paper_2506_13771_amd as lb
+        self.li = li
+        self.T, self.d_in, self.d_out, self.r = li.T, li.d_in, li.d_out, li.r
+        tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+        def dev(raw, code):
+            if code == "f32":
+                return torch.from_numpy(np.ascontiguousarray(raw, np.float32)).to(device)
+            return torch.from_numpy(np.ascontiguousarray(raw).view(np.int16)).to(device).view(tdt[code])
+
+        self.paths = []
+        for p in range(2):
+            if li.U_latent is not None and pack_on_gpu:
+                ub = lb.lb_pack_signs(torch.from_numpy(li.U_latent[p]).to(device), lb.LB_ROLE_U)
+                vb = lb.lb_pack_signs(torch.from_numpy(li.V_latent[p]).to(device), lb.LB_ROLE_V)
+            else:
+                ub = torch.from_numpy(li.U_words[p]).to(device)
+                vb = torch.from_numpy(li.V_words[p]).to(device)
+            self.paths.append(lb.LittleBitPath(U=ub, V=vb, h=dev(li.h[p], li.scale_dtype),
+                                               g=dev(li.g[p], li.scale_dtype), l=dev(li.l[p], li.scale_dtype)))
+        self.x = dev(li.x, li.act_dtype)
+        self.y = torch.empty((li.T, li.d_out), dtype=self.x.dtype, device=device)
+        self.ws = lb.alloc_workspace(li.T, li.d_in, li.d_out, li.r, device=device)
+        arr, sc = lb._paths_struct(self.paths)
+        self._arr = arr
+        self.lib = lb.load_library()
+        self.kernel = kernel
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.argv = (ctypes.c_void_p(self.x.data_ptr()), lb._dtype_code(self.x), li.T, li.d_in, li.d_out, li.r,
+                     arr, sc, ctypes.c_void_p(self.y.data_ptr()), ctypes.c_void_p(self.ws.data_ptr()),
+                     self.ws.numel(), kernel, ctypes.c_void_p(self.stream))
+
+    def set_stream(self, handle):
+        self.argv = self.argv[:-1] + (ctypes.c_void_p(handle),)
+
+    def call(self):
+        st = self.lib.lb_linear_forward_kernel(*self.argv)
+        if st != 0:
+            raise RuntimeError(f"lb_linear_forward failed with status {st}")
+
+    @property
+    def e_act(self):
+        return 4 if self.li.act_dtype == "f32" else 2
+
+    @property
+    def e_scale(self):
+        return 4 if self.li.scale_dtype == "f32" else 2
+
+
+def time_calls(layers, steps, warmup, use_graph=True, per_graph=None):
+    """Run every layer's forward `steps` times (after `warmup`) on the current stream, timed
+    with HIP events recorded on that stream.  With use_graph the launches of `per_graph`
+    steps are captured once into a HIP graph that is replayed.  Returns (ms per step, steps)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for L in layers:
+        L.set_stream(stream.cuda_stream)
+    fns = [L.call for L in layers]
+    for _ in range(warmup):
+        for f in fns:
+            f()
+    torch.cuda.synchronize()
+    graph = None
+    reps = steps
+    if use_graph:
+        per_graph = per_graph or max(1, min(steps, 100))
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            cap = torch.cuda.current_stream().cuda_stream
+            for L in layers:
+                L.set_stream(cap)
+            for _ in range(per_graph):
+                for f in fns:
+                    f()
+        for L in layers:
+            L.set_stream(stream.cuda_stream)
+        graph.replay()
+        torch.cuda.synchronize()
+        reps = max(1, steps // per_graph)
+        steps = reps * per_graph
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    if graph is not None:
+        for _ in range(reps):
+            graph.replay()
+    else:
+        for _ in range(steps):
+            for f in fns:
+                f()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps, steps
+
+
+def source_digest(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+DECODE_SOURCES = ["paper_2506_13771_amd/csrc/decode.hip", "paper_2506_13771_amd/csrc/lb_internal.h"]
+
+
+def measured_traffic(workload_key):
+    """HBM bytes per launch from committed rocprofv3 counter runs, or None if the kernel
+    source changed since they were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except Exception:
+        return None
+    ent = d.get(workload_key)
+    if not ent or ent.get("source_digest") != source_digest(ent.get("sources", DECODE_SOURCES)):
+        return None
+    return ent.get("bytes_per_launch")
+
+
+# ----------------------------------------------------------------------------
+# CPU baseline: the oracle as it stands, on this host
+# ----------------------------------------------------------------------------
+def cpu_baseline(li, seconds):
+    import oracle as O
+    Us, Vs = [], []
+    for p in range(2):
+        ub, _ = O.pack(li.U_latent[p].astype(np.float64), O.ROLE_U)
+        vb, _ = O.pack(li.V_latent[p].astype(np.float64), O.ROLE_V)
+        Us.append(O.unpack(ub, li.d_out, li.r, O.ROLE_U))
+        Vs.append(O.unpack(vb, li.d_in, li.r, O.ROLE_V))
+    x = O.to_f64(li.x, li.act_dtype)
+    h = [O.to_f64(a, li.scale_dtype) for a in li.h]
+    g = [O.to_f64(a, li.scale_dtype) for a in li.g]
+    l = [O.to_f64(a, li.scale_dtype) for a in li.l]
+    O.forward_factored(x, Us, Vs, h, g, l)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        O.forward_factored(x, Us, Vs, h, g, l)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": n * li.T / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} full fp64 oracle forwards of the same layer and inputs "
+                      f"({li.d_in}x{li.d_out}, r={li.r}, T={li.T}), single thread, {el:.1f} s"}
+
+
+# ----------------------------------------------------------------------------
+# sweep of the other configurations (diagnostic lines written to a file)
+# ----------------------------------------------------------------------------
+def run_sweep(path, steps, warmup):
+    import torch
+    from paper_2506_13771_amd import synth
+    out = open(path, "w")
+
+    def emit(rec):
+        out.write(json.dumps(rec) + "\n")
+        out.flush()
+        log(json.dumps(rec))
+
+    ranks_7b = {0.1: {4096: 80, 11008: 128}, 0.55: {4096: 544, 11008: 800}}
+    for bpw in (0.1, 0.55):
+        for T in (1, 16, 64):
+            for idx, (name, d_in, d_out) in enumerate(synth.LLAMA2_7B):
+                r = ranks_7b[bpw][max(d_in, d_out)]
+                L = Layer(synth.make_linear(d_in, d_out, r, T, cfg=2, linear=idx), "cuda")
+                ms, n = time_calls([L], steps, warmup)
+                b, bw = alg_bytes(T, d_in, d_out, r)
+                emit({"config": "llama2-7b-block", "linear": name, "bpw": bpw, "T": T, "d_in": d_in,
+                      "d_out": d_out, "r": r, "us_per_call": ms * 1e3, "tokens_per_s": T / (ms * 1e-3),
+                      "alg_bytes": b, "GBps": b / (ms * 1e-3) / 1e9, "hbm_frac": b / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                      "weights_GBps": bw / (ms * 1e-3) / 1e9,
+                      "mfma_frac": alg_flops(T, d_in, d_out, r) / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS})
+                del L
+    ranks_13b = {(5120, 5120): 96, (5120, 13824): 160, (13824, 5120): 160}
+    for idx, (name, d_in, d_out) in enumerate(synth.LLAMA2_13B):
+        r = ranks_13b[(d_in, d_out)]
+        T = 2048
+        L = Layer(synth.make_linear(d_in, d_out, r, T, cfg=3, linear=idx), "cuda")
+        ms, n = time_calls([L], max(10, steps // 20), max(3, warmup // 20))
+        b, bw = alg_bytes(T, d_in, d_out, r)
+        f = alg_flops(T, d_in, d_out, r)
+        emit({"config": "llama2-13b-prefill", "linear": name, "bpw": 0.1, "T": T, "d_in": d_in, "d_out": d_out,
+              "r": r, "us_per_call": ms * 1e3, "tokens_per_s": T / (ms * 1e-3), "alg_bytes": b,
+              "GBps": b / (ms * 1e-3) / 1e9, "hbm_frac": b / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+              "mfma_tflops": f / (ms * 1e-3) / 1e12, "mfma_frac": f / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS})
+        del L
+    # 70B sweep: 80 layers x 7 linears resident, back-to-back on one stream
+    ranks_70b = {(8192, 8192): 176, (8192, 1024): 16, (8192, 28672): 288, (28672, 8192): 288}
+    for T in (1, 8, 64):
+        layers = []
+        tot_b = 0.0
+        tot_w = 0.0
+        for layer in range(80):
+            for idx, (name, d_in, d_out) in enumerate(synth.LLAMA2_70B):
+                r = ranks_70b[(d_in, d_out)]
+                li = synth.make_linear(d_in, d_out, r, T, cfg=4, linear=layer * 7 + idx, direct_words=True)
+                layers.append(Layer(li, "cuda", pack_on_gpu=False))
+                b, bw = alg_bytes(T, d_in, d_out, r)
+                tot_b += b
+                tot_w += bw
+        ms, n = time_calls(layers, max(3, steps // 100), 2, use_graph=True, per_graph=1)
+        emit({"config": "llama2-70b-sweep", "T": T, "linears": len(layers), "ms_per_sweep": ms,
+              "tokens_per_s": T / (ms * 1e-3), "alg_bytes": tot_b, "weights_bytes": tot_w,
+              "GBps": tot_b / (ms * 1e-3) / 1e9, "hbm_frac": tot_b / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+              "us_per_linear": ms * 1e3 / len(layers)})
+        del layers
+        torch.cuda.empty_cache()
+    out.close()
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5000)
+    ap.add_argument("--warmup", type=int, default=500)
+    ap.add_argument("--launch", choices=["graph", "stream"], default="graph")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", default=None, help="write per-configuration JSON lines to this file")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the LittleBit linear forward is "
+                                   "measured on one MI355X (multi-GPU sharding is a design note, not a run)",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    import paper_2506_13771_amd as lb
+    from paper_2506_13771_amd import synth
+    lb.load_library()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    d_in, d_out, r, T = 4096, 4096, 80, 1
+    assert lb.lb_rank_for_bpw(d_in, d_out, 0.1, 16) == r
+    li = synth.make_linear(d_in, d_out, r, T, act_dtype="bf16", scale_dtype="f16", cfg=1, linear=0)
+    L = Layer(li, "cuda")
+    ms, steps = time_calls([L], args.steps, args.warmup, use_graph=(args.launch == "graph"))
+    ms_stream, _ = time_calls([L], min(args.steps, 2000), 100, use_graph=False)
+    b, bw = alg_bytes(T, d_in, d_out, r, L.e_act, L.e_scale)
+    achieved = b / (ms * 1e-3) / 1e9
+    traffic = measured_traffic("decode_q_proj_4096_r80_T1")
+    rec = {
+        "metric": "tokens/s + HBM GB/s (% peak) per LittleBit linear, Llama2-7B shapes @0.1 BPW",
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "LittleBit linear forward, Llama2-7B q_proj shape 4096x4096, 0.1 BPW (r=80 per "
+                               "path, 2 paths), T=1 decode, bf16 x, fp16 scales, Bernoulli(1/2) signs",
+                   "d_in": d_in, "d_out": d_out, "r": r, "T": T, "bpw": round(lb.lb_bits_per_weight(d_in, d_out, r), 5),
+                   "kernel": "decode", "launch": args.launch},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+                     "alg_bytes_per_launch": b, "weights_bytes_per_launch": bw,
+                     "avg_launch_us": ms * 1e3, "avg_launch_us_stream_issued": ms_stream * 1e3},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(li, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+    if args.sweep:
+        run_sweep(args.sweep, min(args.steps, 1000), min(args.warmup, 100))
+
+
+if __name__ == "__main__":
+    main()

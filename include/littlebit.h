@@ -1,0 +1,178 @@
+/*
+ * littlebit.h -- C ABI of the MI355X (gfx950) LittleBit linear-layer library.
+ *
+ * A LittleBit linear layer (arXiv 2506.13771, Sec. 3.1 and Sec. 3.3) replaces
+ * a dense weight W in R^{d_out x d_in} by two paths p in {primary, residual},
+ * each made of two sign matrices U_p in {-1,+1}^{d_out x r},
+ * V_p in {-1,+1}^{d_in x r} and three scale vectors h_p in R^{d_out},
+ * g_p in R^{d_in}, l_p in R^r.  The effective weight
+ *     W_hat = sum_p diag(h_p) U_p diag(l_p) V_p^T diag(g_p)
+ * (Eqs. w_primary_hat, res_approx_structure, final_weight_approx_res) is never
+ * formed on the forward path; Proposition 1 (Eq. proposition1) evaluates
+ *     y = sum_p h_p (.) ( U_p ( l_p (.) ( V_p^T ( g_p (.) x ) ) ) )
+ * as two binary contractions plus element-wise scalings.
+ *
+ * Conventions for every call:
+ *   - Buffer pointers are DEVICE pointers owned by the caller unless the
+ *     comment says "host".  The library allocates nothing and keeps no state
+ *     between calls; all state lives in caller-provided buffers.
+ *   - GPU calls are asynchronous on `stream` (0 = the null stream).  Results
+ *     are valid once the stream has been synchronised.
+ *   - Every argument is validated on the host before anything is enqueued; a
+ *     failed validation returns its code and enqueues nothing.  After a launch,
+ *     a launch error reported by the HIP runtime is returned as LB_ERR_HIP.
+ *     No call aborts, prints or throws across this boundary.
+ *   - Shapes are int64; every dimension may be any value >= 0 (ragged sizes
+ *     are supported by all kernels).  Products that index a buffer must stay
+ *     below 2^31 elements (LB_ERR_SHAPE otherwise).
+ *   - Dense activation and scale buffers are contiguous row-major, aligned to
+ *     their element size (LB_ERR_ALIGN otherwise).  Packed sign buffers are
+ *     4-byte aligned.  Workspaces are 256-byte aligned.
+ *
+ * Packed sign layout "LB layout v1" (the paper only states that signs are
+ * packed into uint32 words, Appendix "Inference Efficiency Analysis"):
+ *   A sign matrix is seen as M[o][q] with o the output index and q the
+ *   reduction index of the stage that reads it:
+ *     LB_ROLE_U: M = U_sign   (o = i < d_out, q = k < r),    rows = d_out
+ *     LB_ROLE_V: M = V_sign^T (o = k < r,     q = j < d_in), rows = d_in
+ *   bit(o,q) = 1 iff the source value is < 0 (sign -1); sign(+0) = sign(-0)
+ *   = +1.  With nb = n_red / 32 and w = n_red - 32 nb:
+ *     region A: uint32 A[nb][n_out], output index fastest; bit t (LSB = 0)
+ *               of A[b][o] is bit(o, 32 b + t);
+ *     region B: absent if w == 0; uint16 B[n_out] if 1 <= w <= 16; uint32
+ *               B[n_out] if 17 <= w <= 31; bit t of B[o] is bit(o, 32 nb + t)
+ *               for t < w and 0 above (pad bits are zero).
+ *   Region B starts at byte 4 nb n_out; words are little-endian.
+ */
+#ifndef LITTLEBIT_H
+#define LITTLEBIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LB_ABI_VERSION 1
+
+typedef enum lb_status {
+  LB_OK = 0,
+  LB_ERR_NULL = 1,      /* a required pointer is NULL                              */
+  LB_ERR_SHAPE = 2,     /* negative dimension, or a size beyond the 2^31 limit      */
+  LB_ERR_DTYPE = 3,     /* dtype code not accepted by this call                     */
+  LB_ERR_ALIGN = 4,     /* pointer not aligned as the conventions above require     */
+  LB_ERR_WORKSPACE = 5, /* workspace smaller than lb_forward_workspace_bytes()      */
+  LB_ERR_HIP = 6,       /* the HIP runtime reported an error for a launch           */
+  LB_ERR_ARG = 7        /* any other invalid argument (enum value out of range ...) */
+} lb_status;
+
+typedef enum lb_dtype { LB_F32 = 0, LB_F16 = 1, LB_BF16 = 2 } lb_dtype;
+
+typedef enum lb_role { LB_ROLE_U = 0, LB_ROLE_V = 1 } lb_role;
+
+/* Which forward kernel lb_linear_forward_kernel() runs. */
+typedef enum lb_kernel {
+  LB_KERNEL_AUTO = 0,    /* decode for T <= lb_decode_max_tokens(), prefill above */
+  LB_KERNEL_DECODE = 1,  /* single launch, packed signs streamed once, fp32 sign-flip accumulation */
+  LB_KERNEL_PREFILL = 2  /* matrix-core (MFMA) kernels on sign tiles expanded to bf16 +-1 */
+} lb_kernel;
+
+/* One path's parameters (Sec. 3.1 Eq. ghl_scales_combined; Sec. 3.3).
+   U: packed U_sign, LB_ROLE_U, lb_packed_bytes(LB_ROLE_U, d_out, r) bytes.
+   V: packed V_sign, LB_ROLE_V, lb_packed_bytes(LB_ROLE_V, d_in, r) bytes.
+   h [d_out], g [d_in], l [r]: scales in the call's scale dtype.
+   A layer without the residual path is expressed by a residual path whose
+   h is all zeros (the bits-per-weight note under Eq. b_calculation). */
+typedef struct lb_path {
+  const void* U;
+  const void* V;
+  const void* h;
+  const void* g;
+  const void* l;
+} lb_path;
+
+/* ABI version of the loaded library (LB_ABI_VERSION). */
+int lb_abi_version(void);
+
+/* Static, NUL-terminated name of a status code. */
+const char* lb_status_str(lb_status s);
+
+/* Host, pure.  Bytes of one packed sign matrix in LB layout v1; rows = d_out
+   for LB_ROLE_U and d_in for LB_ROLE_V.  Returns 0 for invalid arguments. */
+size_t lb_packed_bytes(lb_role role, int64_t rows, int64_t r);
+
+/* Host, pure.  Bits per weight of a layer with `npaths` (1 or 2) paths of rank
+   r (Appendix "Average Bits Per Weight Calculation", Eq. b_calculation: one
+   bit per sign element, 16 bits per scale element).  Returns -1 for invalid
+   arguments. */
+double lb_bits_per_weight(int64_t d_in, int64_t d_out, int64_t r, int npaths);
+
+/* Host, pure.  Per-path rank for a target bits-per-weight `bpw` with both
+   paths: the largest multiple of `mult` (>= 1) whose total bits stay within
+   bpw * d_in * d_out (Eq. b_calculation solved for r, Eq. r_calculation,
+   rounded down to a multiple of mult).  Returns -1 for invalid arguments. */
+int64_t lb_rank_for_bpw(int64_t d_in, int64_t d_out, double bpw, int64_t mult);
+
+/* Pack the signs of a real matrix src [rows x r] (row-major, src_dtype F32,
+   F16 or BF16; the latent factor U [d_out x r] for LB_ROLE_U or V [d_in x r]
+   for LB_ROLE_V) into dst (lb_packed_bytes(role, rows, r) bytes) following
+   Sec. 3.1 Eq. uv_sign and LB layout v1.  NaN elements are written as +1 and
+   counted: if nan_count (a device int32) is not NULL, the number of NaNs met
+   is atomically added to it.  dst must not overlap src. */
+lb_status lb_pack_signs(const void* src, lb_dtype src_dtype, int64_t rows, int64_t r, lb_role role,
+                        void* dst, int32_t* nan_count, hipStream_t stream);
+
+/* Host, pure.  Workspace bytes lb_linear_forward() needs for these sizes
+   (covers every kernel choice).  The workspace must be zero-filled once before
+   its first use (lb_workspace_init does it); every call leaves it ready for
+   the next one, so a workspace is reused without clearing, across calls of
+   any shape.  The decode kernel tags its intermediate values with a 32-bit
+   call counter kept in the workspace; a value left unread for exactly 2^32
+   calls could be mistaken for a fresh one.  Calls that may run concurrently
+   need distinct workspaces. */
+size_t lb_forward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
+
+/* Zero-fill a workspace of `bytes` bytes on `stream`. */
+lb_status lb_workspace_init(void* workspace, size_t bytes, hipStream_t stream);
+
+/* Largest token count the automatic dispatch sends to the decode kernel. */
+int64_t lb_decode_max_tokens(void);
+
+/* Forward of one LittleBit linear layer with both paths (Proposition 1,
+   Eq. proposition1, summed over the two paths, Eq. final_weight_approx_res):
+     y[t][i] = sum_p h_p[i] sum_k U_p[i][k] l_p[k] sum_j V_p[j][k] g_p[j] x[t][j]
+   x [T x d_in] in act_dtype (F32, F16 or BF16); y [T x d_out] in act_dtype,
+   rounded once (round-to-nearest-even) from the fp32 sum of both paths;
+   paths[0] = primary, paths[1] = residual, scales in scale_dtype (F32, F16 or
+   BF16).  Accumulation is fp32.  The decode kernel uses exact fp32 products;
+   the prefill kernel feeds MFMA with (x (.) g) and (z (.) l) formed in fp32 and
+   split into a sum of bf16 terms (two terms, 16 significant bits, for bf16/f16
+   activations; three terms, the full fp32 significand, for fp32 activations),
+   times the exact bf16 +-1 signs.  If d_in == 0 or r == 0, y is zero-filled.
+   workspace: >= lb_forward_workspace_bytes(T, d_in, d_out, r) bytes. */
+lb_status lb_linear_forward(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out,
+                            int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* lb_linear_forward with an explicit kernel choice (any kernel accepts any
+   valid input; AUTO is what lb_linear_forward uses). */
+lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in,
+                                   int64_t d_out, int64_t r, const lb_path* paths, lb_dtype scale_dtype,
+                                   void* y, void* workspace, size_t workspace_bytes, lb_kernel kernel,
+                                   hipStream_t stream);
+
+/* Checking path: the dense effective weight of both paths,
+     W[i][j] = sum_p h_p[i] g_p[j] sum_k U_p[i][k] l_p[k] V_p[j][k]
+   (Eqs. w_primary_hat, res_approx_structure, final_weight_approx_res),
+   computed from the PACKED buffers in fp32 (ascending k), written to
+   W [d_out x d_in] row-major fp32.  Not used by the forward path. */
+lb_status lb_dense_reference_weight(const lb_path* paths, lb_dtype scale_dtype, int64_t d_in,
+                                    int64_t d_out, int64_t r, float* W, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LITTLEBIT_H */

@@ -1,0 +1,246 @@
+"""LittleBit linear layer on MI355X (gfx950): Python binding of liblittlebit.so.
+
+This module only marshals arguments into the C ABI declared in
+include/littlebit.h: every step of the computation runs in the library's HIP
+kernels.  PyTorch provides device memory and the current stream.  If the
+library is not built, or a tensor is not on a GPU, calls raise instead of
+falling back to anything else.
+
+The names follow the C ABI:
+  lb_pack_signs, lb_linear_forward, lb_dense_reference_weight,
+  lb_packed_bytes, lb_bits_per_weight, lb_rank_for_bpw,
+  lb_forward_workspace_bytes, lb_workspace_init, lb_decode_max_tokens.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblittlebit.so")
+
+LB_OK, LB_ERR_NULL, LB_ERR_SHAPE, LB_ERR_DTYPE, LB_ERR_ALIGN, LB_ERR_WORKSPACE, LB_ERR_HIP, LB_ERR_ARG = range(8)
+LB_F32, LB_F16, LB_BF16 = 0, 1, 2
+LB_ROLE_U, LB_ROLE_V = 0, 1
+LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL = 0, 1, 2
+ABI_VERSION = 1
+
+
+class LittleBitError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {lb_status_str(status)} ({status})")
+        self.status = status
+
+
+class lb_path(ctypes.Structure):
+    _fields_ = [("U", ctypes.c_void_p), ("V", ctypes.c_void_p), ("h", ctypes.c_void_p),
+                ("g", ctypes.c_void_p), ("l", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load liblittlebit.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"LittleBit HIP library not built: {path} is missing "
+                           "(run __graft_entry__.build() or python paper_2506_13771_amd/_build.py)")
+    lib = ctypes.CDLL(path)
+    i64, sz, vp, i32 = ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int
+    lib.lb_abi_version.restype = i32
+    lib.lb_abi_version.argtypes = []
+    lib.lb_status_str.restype = ctypes.c_char_p
+    lib.lb_status_str.argtypes = [i32]
+    lib.lb_packed_bytes.restype = sz
+    lib.lb_packed_bytes.argtypes = [i32, i64, i64]
+    lib.lb_bits_per_weight.restype = ctypes.c_double
+    lib.lb_bits_per_weight.argtypes = [i64, i64, i64, i32]
+    lib.lb_rank_for_bpw.restype = i64
+    lib.lb_rank_for_bpw.argtypes = [i64, i64, ctypes.c_double, i64]
+    lib.lb_pack_signs.restype = i32
+    lib.lb_pack_signs.argtypes = [vp, i32, i64, i64, i32, vp, vp, vp]
+    lib.lb_forward_workspace_bytes.restype = sz
+    lib.lb_forward_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.lb_workspace_init.restype = i32
+    lib.lb_workspace_init.argtypes = [vp, sz, vp]
+    lib.lb_decode_max_tokens.restype = i64
+    lib.lb_decode_max_tokens.argtypes = []
+    lib.lb_linear_forward.restype = i32
+    lib.lb_linear_forward.argtypes = [vp, i32, i64, i64, i64, i64, ctypes.POINTER(lb_path), i32, vp, vp, sz, vp]
+    lib.lb_linear_forward_kernel.restype = i32
+    lib.lb_linear_forward_kernel.argtypes = [vp, i32, i64, i64, i64, i64, ctypes.POINTER(lb_path), i32, vp, vp,
+                                             sz, i32, vp]
+    lib.lb_dense_reference_weight.restype = i32
+    lib.lb_dense_reference_weight.argtypes = [ctypes.POINTER(lb_path), i32, i64, i64, i64, vp, vp]
+    if lib.lb_abi_version() != ABI_VERSION:
+        raise RuntimeError("liblittlebit.so ABI version mismatch")
+    _lib = lib
+    return lib
+
+
+# ----------------------------------------------------------------------------
+# pure host helpers
+# ----------------------------------------------------------------------------
+def lb_status_str(status: int) -> str:
+    return load_library().lb_status_str(status).decode()
+
+
+def lb_packed_bytes(role: int, rows: int, r: int) -> int:
+    return int(load_library().lb_packed_bytes(role, rows, r))
+
+
+def lb_bits_per_weight(d_in: int, d_out: int, r: int, npaths: int = 2) -> float:
+    return float(load_library().lb_bits_per_weight(d_in, d_out, r, npaths))
+
+
+def lb_rank_for_bpw(d_in: int, d_out: int, bpw: float, mult: int = 16) -> int:
+    return int(load_library().lb_rank_for_bpw(d_in, d_out, bpw, mult))
+
+
+def lb_forward_workspace_bytes(T: int, d_in: int, d_out: int, r: int) -> int:
+    return int(load_library().lb_forward_workspace_bytes(T, d_in, d_out, r))
+
+
+def lb_decode_max_tokens() -> int:
+    return int(load_library().lb_decode_max_tokens())
+
+
+# ----------------------------------------------------------------------------
+# tensor marshalling
+# ----------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    m = {torch.float32: LB_F32, torch.float16: LB_F16, torch.bfloat16: LB_BF16}
+    if t.dtype not in m:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return m[t.dtype]
+
+
+def _torch_dtype(code: int):
+    torch = _torch()
+    return {LB_F32: torch.float32, LB_F16: torch.float16, LB_BF16: torch.bfloat16}[code]
+
+
+def _dev_ptr(t, name: str) -> int:
+    if t is None:
+        return 0
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _check(status: int, what: str):
+    if status != LB_OK:
+        raise LittleBitError(status, what)
+
+
+@dataclass
+class LittleBitPath:
+    """One path's packed signs (uint8 device tensors in LB layout v1) and scales."""
+    U: object
+    V: object
+    h: object
+    g: object
+    l: object
+
+
+def _paths_struct(paths: Sequence[LittleBitPath]):
+    if len(paths) != 2:
+        raise ValueError("exactly two paths (primary, residual) are required")
+    arr = (lb_path * 2)()
+    for i, p in enumerate(paths):
+        arr[i] = lb_path(_dev_ptr(p.U, "U"), _dev_ptr(p.V, "V"), _dev_ptr(p.h, "h"),
+                         _dev_ptr(p.g, "g"), _dev_ptr(p.l, "l"))
+    sc = {_dtype_code(p.h) for p in paths} | {_dtype_code(p.g) for p in paths} | {_dtype_code(p.l) for p in paths}
+    if len(sc) != 1:
+        raise TypeError("all scales must share one dtype")
+    return arr, sc.pop()
+
+
+def lb_pack_signs(src, role: int, dst=None, nan_count=None, stream=None):
+    """Pack the signs of src [rows, r] (latent U or V) into dst (uint8, LB layout v1)."""
+    torch = _torch()
+    lib = load_library()
+    rows, r = src.shape
+    n = lb_packed_bytes(role, rows, r)
+    if dst is None:
+        dst = torch.empty(n, dtype=torch.uint8, device=src.device)
+    if dst.numel() * dst.element_size() < n:
+        raise ValueError("dst too small")
+    st = lib.lb_pack_signs(_dev_ptr(src, "src"), _dtype_code(src), rows, r, role, _dev_ptr(dst, "dst"),
+                           _dev_ptr(nan_count, "nan_count"), _stream(stream))
+    _check(st, "lb_pack_signs")
+    return dst
+
+
+def lb_workspace_init(ws, stream=None):
+    st = load_library().lb_workspace_init(_dev_ptr(ws, "workspace"), ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "lb_workspace_init")
+    return ws
+
+
+def alloc_workspace(T: int, d_in: int, d_out: int, r: int, device="cuda"):
+    """A zero-filled workspace tensor of lb_forward_workspace_bytes(T, d_in, d_out, r) bytes."""
+    torch = _torch()
+    n = lb_forward_workspace_bytes(T, d_in, d_out, r)
+    ws = torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+    return lb_workspace_init(ws)
+
+
+def lb_linear_forward(x, paths: Sequence[LittleBitPath], r: int, y=None, workspace=None,
+                      kernel: int = LB_KERNEL_AUTO, stream=None):
+    """y [T, d_out] = LittleBit forward of x [T, d_in] with both paths; returns y."""
+    torch = _torch()
+    lib = load_library()
+    T, d_in = x.shape
+    d_out = paths[0].h.shape[0]
+    arr, sc = _paths_struct(paths)
+    if y is None:
+        y = torch.empty((T, d_out), dtype=x.dtype, device=x.device)
+    if workspace is None:
+        workspace = alloc_workspace(T, d_in, d_out, r, device=x.device)
+    st = lib.lb_linear_forward_kernel(_dev_ptr(x, "x"), _dtype_code(x), T, d_in, d_out, r, arr, sc,
+                                      _dev_ptr(y, "y"), _dev_ptr(workspace, "workspace"),
+                                      workspace.numel() * workspace.element_size(), kernel, _stream(stream))
+    _check(st, "lb_linear_forward")
+    return y
+
+
+def lb_dense_reference_weight(paths: Sequence[LittleBitPath], d_in: int, d_out: int, r: int, W=None, stream=None):
+    """Dense fp32 W_hat [d_out, d_in] from the packed buffers (checking path)."""
+    torch = _torch()
+    lib = load_library()
+    arr, sc = _paths_struct(paths)
+    if W is None:
+        W = torch.empty((d_out, d_in), dtype=torch.float32, device=paths[0].h.device)
+    st = lib.lb_dense_reference_weight(arr, sc, d_in, d_out, r, _dev_ptr(W, "W"), _stream(stream))
+    _check(st, "lb_dense_reference_weight")
+    return W
+
+
+__all__ = [
+    "LB_OK", "LB_ERR_NULL", "LB_ERR_SHAPE", "LB_ERR_DTYPE", "LB_ERR_ALIGN", "LB_ERR_WORKSPACE", "LB_ERR_HIP",
+    "LB_ERR_ARG", "LB_F32", "LB_F16", "LB_BF16", "LB_ROLE_U", "LB_ROLE_V", "LB_KERNEL_AUTO", "LB_KERNEL_DECODE",
+    "LB_KERNEL_PREFILL", "LittleBitError", "LittleBitPath", "lb_path", "load_library", "lb_status_str",
+    "lb_packed_bytes", "lb_bits_per_weight", "lb_rank_for_bpw", "lb_forward_workspace_bytes",
+    "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "alloc_workspace", "lb_linear_forward",
+    "lb_dense_reference_weight",
+]

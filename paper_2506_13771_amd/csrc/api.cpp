@@ -1,0 +1,216 @@
+// C ABI of the LittleBit library: host-side validation, dispatch and launch.
+// Every argument is checked before anything touches HIP, so every error path
+// is testable without a GPU; nothing here allocates device memory.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "lb_internal.h"
+
+namespace {
+
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+
+bool dtype_ok(lb_dtype d) { return d == LB_F32 || d == LB_F16 || d == LB_BF16; }
+size_t dtype_size(lb_dtype d) { return d == LB_F32 ? 4 : 2; }
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t packed_bytes(int64_t n_out, int64_t n_red) {
+  const int64_t nb = n_red / 32, w = n_red - 32 * nb;
+  const int64_t tail = w == 0 ? 0 : (w <= 16 ? 2 : 4);
+  return static_cast<size_t>(4 * nb * n_out + tail * n_out);
+}
+
+bool fits(int64_t a, int64_t b) { return a == 0 || b <= kMaxElems / a; }
+
+lb_status check_sizes(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
+  if (T < 0 || d_in < 0 || d_out < 0 || r < 0) return LB_ERR_SHAPE;
+  if (!fits(T, d_in) || !fits(T, d_out) || !fits(d_in, r) || !fits(d_out, r) || !fits(2 * T, r))
+    return LB_ERR_SHAPE;
+  return LB_OK;
+}
+
+lb_status check_paths(const lb_path* paths, lb_dtype sc, int64_t d_in, int64_t d_out, int64_t r) {
+  if (!paths) return LB_ERR_NULL;
+  const size_t es = dtype_size(sc);
+  for (int p = 0; p < 2; ++p) {
+    const lb_path& P = paths[p];
+    if ((r > 0 && d_out > 0 && !P.U) || (r > 0 && d_in > 0 && !P.V) || (d_out > 0 && !P.h) ||
+        (d_in > 0 && !P.g) || (r > 0 && !P.l))
+      return LB_ERR_NULL;
+    if (!aligned(P.U, 4) || !aligned(P.V, 4) || !aligned(P.h, es) || !aligned(P.g, es) || !aligned(P.l, es))
+      return LB_ERR_ALIGN;
+  }
+  return LB_OK;
+}
+
+lb::ForwardArgs make_args(const void* x, lb_dtype act, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                          const lb_path* paths, lb_dtype sc, void* y, void* ws, size_t ws_bytes) {
+  lb::ForwardArgs a{};
+  a.x = x;
+  a.act_dt = act;
+  a.T = static_cast<int>(T);
+  a.d_in = static_cast<int>(d_in);
+  a.d_out = static_cast<int>(d_out);
+  a.r = static_cast<int>(r);
+  for (int p = 0; p < 2; ++p) {
+    a.U[p] = paths[p].U;
+    a.V[p] = paths[p].V;
+    a.h[p] = paths[p].h;
+    a.g[p] = paths[p].g;
+    a.l[p] = paths[p].l;
+  }
+  a.sc_dt = sc;
+  a.y = y;
+  a.ws = ws;
+  a.ws_bytes = ws_bytes;
+  return a;
+}
+
+bool decode_supports(int64_t T, int64_t r) { return T <= lb::kDecodeMaxTokens && r <= lb::kDecodeMaxRank; }
+
+}  // namespace
+
+extern "C" {
+
+int lb_abi_version(void) { return LB_ABI_VERSION; }
+
+const char* lb_status_str(lb_status s) {
+  switch (s) {
+    case LB_OK: return "LB_OK";
+    case LB_ERR_NULL: return "LB_ERR_NULL";
+    case LB_ERR_SHAPE: return "LB_ERR_SHAPE";
+    case LB_ERR_DTYPE: return "LB_ERR_DTYPE";
+    case LB_ERR_ALIGN: return "LB_ERR_ALIGN";
+    case LB_ERR_WORKSPACE: return "LB_ERR_WORKSPACE";
+    case LB_ERR_HIP: return "LB_ERR_HIP";
+    case LB_ERR_ARG: return "LB_ERR_ARG";
+  }
+  return "LB_ERR_UNKNOWN";
+}
+
+size_t lb_packed_bytes(lb_role role, int64_t rows, int64_t r) {
+  if (rows < 0 || r < 0 || (role != LB_ROLE_U && role != LB_ROLE_V)) return 0;
+  return role == LB_ROLE_U ? packed_bytes(rows, r) : packed_bytes(r, rows);
+}
+
+double lb_bits_per_weight(int64_t d_in, int64_t d_out, int64_t r, int npaths) {
+  if (d_in <= 0 || d_out <= 0 || r < 0 || (npaths != 1 && npaths != 2)) return -1.0;
+  // per path: 1 bit per element of U_sign [d_out x r] and V_sign [d_in x r],
+  // 16 bits per element of h [d_out], g [d_in], l [r]
+  const double per_path = double(d_out) * r + double(d_in) * r + 16.0 * (double(d_out) + double(d_in) + r);
+  return npaths * per_path / (double(d_in) * double(d_out));
+}
+
+int64_t lb_rank_for_bpw(int64_t d_in, int64_t d_out, double bpw, int64_t mult) {
+  if (d_in <= 0 || d_out <= 0 || mult < 1 || !(bpw >= 0.0) || !std::isfinite(bpw)) return -1;
+  const double budget = bpw * double(d_in) * double(d_out);
+  // total bits 2 r (d_in + d_out) + 32 (d_in + d_out) + 32 r is increasing in r
+  const double s = double(d_in) + double(d_out);
+  const double r_real = (budget - 32.0 * s) / (2.0 * s + 32.0);
+  if (r_real < mult) return 0;
+  int64_t r = static_cast<int64_t>(std::floor(r_real / mult)) * mult;
+  auto bits = [&](int64_t rr) { return 2.0 * rr * s + 32.0 * s + 32.0 * rr; };
+  while (r > 0 && bits(r) > budget) r -= mult;
+  while (bits(r + mult) <= budget) r += mult;
+  return r;
+}
+
+lb_status lb_pack_signs(const void* src, lb_dtype src_dtype, int64_t rows, int64_t r, lb_role role, void* dst,
+                        int32_t* nan_count, hipStream_t stream) {
+  if (role != LB_ROLE_U && role != LB_ROLE_V) return LB_ERR_ARG;
+  if (!dtype_ok(src_dtype)) return LB_ERR_DTYPE;
+  if (rows < 0 || r < 0 || !fits(rows, r)) return LB_ERR_SHAPE;
+  if (rows == 0 || r == 0) return LB_OK;
+  if (!src || !dst) return LB_ERR_NULL;
+  if (!aligned(src, dtype_size(src_dtype)) || !aligned(dst, 4) || !aligned(nan_count, 4)) return LB_ERR_ALIGN;
+  const size_t nbytes = lb_packed_bytes(role, rows, r);
+  const char* s = static_cast<const char*>(src);
+  const char* d = static_cast<const char*>(dst);
+  const size_t sbytes = static_cast<size_t>(rows * r) * dtype_size(src_dtype);
+  if (d < s + sbytes && s < d + nbytes) return LB_ERR_ARG;  // overlapping buffers
+  const hipError_t e = lb::launch_pack(src, src_dtype, static_cast<int>(rows), static_cast<int>(r), role, dst,
+                                       nan_count, stream);
+  return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+}
+
+int64_t lb_decode_max_tokens(void) { return lb::kDecodeMaxTokens; }
+
+size_t lb_forward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
+  if (check_sizes(T, d_in, d_out, r) != LB_OK) return 0;
+  size_t need = lb::kCtrlBytes;
+  const int iT = static_cast<int>(T), ii = static_cast<int>(d_in), io = static_cast<int>(d_out),
+            ir = static_cast<int>(r);
+  if (decode_supports(T, r)) {
+    const lb::DecodeGeom g = lb::decode_geometry(iT, ii, io, ir);
+    if (g.ws_bytes > need) need = g.ws_bytes;
+  }
+  const lb::PrefillGeom pg = lb::prefill_geometry(iT, ii, io, ir);
+  if (pg.ws_bytes > need) need = pg.ws_bytes;
+  return need;
+}
+
+lb_status lb_workspace_init(void* workspace, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return LB_OK;
+  if (!workspace) return LB_ERR_NULL;
+  if (!aligned(workspace, 256) || bytes % 4 != 0) return LB_ERR_ALIGN;
+  return lb::launch_fill_zero(workspace, bytes, stream) == hipSuccess ? LB_OK : LB_ERR_HIP;
+}
+
+lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out,
+                                   int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y, void* workspace,
+                                   size_t workspace_bytes, lb_kernel kernel, hipStream_t stream) {
+  if (kernel != LB_KERNEL_AUTO && kernel != LB_KERNEL_DECODE && kernel != LB_KERNEL_PREFILL) return LB_ERR_ARG;
+  if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype)) return LB_ERR_DTYPE;
+  lb_status st = check_sizes(T, d_in, d_out, r);
+  if (st != LB_OK) return st;
+  if (kernel == LB_KERNEL_DECODE && !decode_supports(T, r)) return LB_ERR_SHAPE;
+  if (T == 0 || d_out == 0) return LB_OK;
+  if (!y || (d_in > 0 && !x)) return LB_ERR_NULL;
+  if (!aligned(x, dtype_size(act_dtype)) || !aligned(y, dtype_size(act_dtype))) return LB_ERR_ALIGN;
+  st = check_paths(paths, scale_dtype, d_in, d_out, r);
+  if (st != LB_OK) return st;
+  const size_t need = lb_forward_workspace_bytes(T, d_in, d_out, r);
+  if (!workspace) return LB_ERR_NULL;
+  if (!aligned(workspace, 256)) return LB_ERR_ALIGN;
+  if (workspace_bytes < need) return LB_ERR_WORKSPACE;
+  lb::ForwardArgs a = make_args(x, act_dtype, T, d_in, d_out, r, paths, scale_dtype, y, workspace, workspace_bytes);
+  hipError_t e;
+  if (d_in == 0 || r == 0) {
+    // empty reduction: y = 0 (Proposition 1 with an empty sum)
+    e = lb::launch_zero_elems(y, T * d_out, act_dtype, stream);
+    return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+  }
+  const bool use_decode =
+      kernel == LB_KERNEL_DECODE || (kernel == LB_KERNEL_AUTO && decode_supports(T, r));
+  if (use_decode) {
+    e = lb::launch_decode(a, lb::decode_geometry(a.T, a.d_in, a.d_out, a.r), stream);
+  } else {
+    e = lb::launch_prefill(a, lb::prefill_geometry(a.T, a.d_in, a.d_out, a.r), stream);
+  }
+  return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+}
+
+lb_status lb_linear_forward(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                            const lb_path* paths, lb_dtype scale_dtype, void* y, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  return lb_linear_forward_kernel(x, act_dtype, T, d_in, d_out, r, paths, scale_dtype, y, workspace,
+                                  workspace_bytes, LB_KERNEL_AUTO, stream);
+}
+
+lb_status lb_dense_reference_weight(const lb_path* paths, lb_dtype scale_dtype, int64_t d_in, int64_t d_out,
+                                    int64_t r, float* W, hipStream_t stream) {
+  if (!dtype_ok(scale_dtype)) return LB_ERR_DTYPE;
+  if (d_in < 0 || d_out < 0 || r < 0 || !fits(d_in, d_out) || !fits(d_in, r) || !fits(d_out, r))
+    return LB_ERR_SHAPE;
+  if (d_out > 65535 || r > 16384) return LB_ERR_SHAPE;
+  if (d_in == 0 || d_out == 0) return LB_OK;
+  if (!W) return LB_ERR_NULL;
+  if (!aligned(W, 4)) return LB_ERR_ALIGN;
+  lb_status st = check_paths(paths, scale_dtype, d_in, d_out, r);
+  if (st != LB_OK) return st;
+  lb::ForwardArgs a = make_args(nullptr, LB_F32, 0, d_in, d_out, r, paths, scale_dtype, nullptr, nullptr, 0);
+  return lb::launch_dense_ref(a, W, stream) == hipSuccess ? LB_OK : LB_ERR_HIP;
+}
+
+}  // extern "C"

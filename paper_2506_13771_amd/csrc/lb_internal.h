@@ -1,0 +1,171 @@
+// Internal declarations shared by the LittleBit HIP kernels and the C-ABI layer.
+// Device helpers here implement the storage conventions of LB layout v1 and the
+// dtype conversions; the method's arithmetic lives in the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+#include "../../include/littlebit.h"
+
+namespace lb {
+
+constexpr int kDtF32 = LB_F32;
+constexpr int kDtF16 = LB_F16;
+constexpr int kDtBF16 = LB_BF16;
+
+// ---------------------------------------------------------------------------
+// dtype conversions (all exact widenings; one RNE narrowing at stores)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t u16) { return __uint_as_float(u16 << 16); }
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t u16) {
+  return __half2float(__ushort_as_half(static_cast<unsigned short>(u16)));
+}
+
+__device__ __forceinline__ float load_as_f32(const void* p, int64_t i, int dt) {
+  if (dt == kDtF32) return static_cast<const float*>(p)[i];
+  const uint32_t u = static_cast<const uint16_t*>(p)[i];
+  return dt == kDtBF16 ? bf16_bits_to_f32(u) : f16_bits_to_f32(u);
+}
+
+// fp32 -> bf16 bit pattern, round to nearest even; NaN stays NaN (quiet).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ void store_from_f32(void* p, int64_t i, int dt, float v) {
+  if (dt == kDtF32) {
+    static_cast<float*>(p)[i] = v;
+  } else if (dt == kDtBF16) {
+    static_cast<uint16_t*>(p)[i] = static_cast<uint16_t>(f32_to_bf16_bits(v));
+  } else {
+    static_cast<__half*>(p)[i] = __float2half_rn(v);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LB layout v1 addressing: word kb of output o for a matrix with n_out outputs,
+// nb full 32-bit blocks and a tail plane of width tailw (0, 1..16 -> uint16,
+// 17..31 -> uint32).  kb == nb addresses the tail plane (zero-extended).
+// ---------------------------------------------------------------------------
+struct PackedView {
+  const uint32_t* base;
+  int n_out;
+  int nb;     // full 32-bit blocks along the reduction dimension
+  int tailw;  // width of the tail block (0 = none)
+};
+
+__device__ __forceinline__ uint32_t load_word(const PackedView& v, int kb, int o) {
+  if (kb < v.nb) return v.base[static_cast<int64_t>(kb) * v.n_out + o];
+  const char* t = reinterpret_cast<const char*>(v.base) + static_cast<int64_t>(4) * v.nb * v.n_out;
+  if (v.tailw <= 16) return reinterpret_cast<const uint16_t*>(t)[o];
+  return reinterpret_cast<const uint32_t*>(t)[o];
+}
+
+// Number of 32-bit blocks (including a tail block) along a reduction of length n.
+__host__ __device__ __forceinline__ int nblocks32(int n) { return (n + 31) >> 5; }
+
+// ---------------------------------------------------------------------------
+// agent-scope synchronisation helpers (the L2s of the eight XCDs are not
+// coherent with each other; agent-scope release/acquire orders them)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t atomic_add_release(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t atomic_add_relaxed(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t atomic_load_relaxed(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void atomic_store_relaxed(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void atomic_store_release(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void fence_acquire_agent() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+__device__ __forceinline__ void fence_release_agent() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+
+// Bounded spin: wait until *p >= target.  Returns false if the bound is hit
+// (the caller then records an error instead of hanging the GPU).
+__device__ __forceinline__ bool spin_until_at_least(const uint32_t* p, uint32_t target) {
+  for (uint32_t it = 0; it < (1u << 22); ++it) {
+    if (atomic_load_relaxed(p) >= target) return true;
+    __builtin_amdgcn_s_sleep(2);
+  }
+  return false;
+}
+
+// ---------------------------------------------------------------------------
+// workspace control block (fixed offsets at the start of every workspace)
+// ---------------------------------------------------------------------------
+constexpr int kCtrlEpoch = 0;      // decode: tag of the last completed call
+constexpr int kCtrlDone = 1;       // decode: finished stage-2 workgroups of the running call
+constexpr int kCtrlError = 2;      // set to nonzero if a bounded wait expired
+constexpr int kCtrlArrive = 64;    // decode: per (path, k-tile) arrival counters
+constexpr int kCtrlMaxArrive = 4096;
+constexpr int kCtrlTiles = kCtrlArrive + kCtrlMaxArrive;  // prefill: per-tile counters (3 words each)
+constexpr int kCtrlMaxTiles = 8192;
+constexpr int kCtrlWords = kCtrlTiles + 3 * kCtrlMaxTiles;
+constexpr size_t kCtrlBytes = ((kCtrlWords * 4 + 255) / 256) * 256;
+
+// ---------------------------------------------------------------------------
+// kernel launchers (defined in the .hip files)
+// ---------------------------------------------------------------------------
+struct ForwardArgs {
+  const void* x;
+  int act_dt;
+  int T, d_in, d_out, r;
+  const void* U[2];
+  const void* V[2];
+  const void* h[2];
+  const void* g[2];
+  const void* l[2];
+  int sc_dt;
+  void* y;
+  void* ws;
+  size_t ws_bytes;
+};
+
+// Decode kernel geometry (pure function of the sizes; also sizes the workspace).
+struct DecodeGeom {
+  int kc, nkt, bpw, s1d, n_s1;
+  int kq_log2;  // log2 of the lanes that share one output row in stage 2
+  int rows2, n_s2;
+  int direct;
+  int tch;
+  size_t partial_off, partial_floats;
+  size_t wbuf_off, wbuf_floats;
+  size_t ws_bytes;
+};
+DecodeGeom decode_geometry(int T, int d_in, int d_out, int r);
+constexpr int kDecodeMaxTokens = 16;
+constexpr int kDecodeMaxRank = 4096;
+
+struct PrefillGeom {
+  int bm;                  // tokens per M-tile
+  int n_mt;                // M-tiles
+  int s1_nw, s1_spw;       // stage-1 waves per workgroup and 16-column subtiles per wave
+  int s1_bn, s1_nnt;       // stage-1 columns per N-tile and N-tiles
+  int ks;                  // stage-1 split of the d_in reduction
+  int s2_nw, s2_spw, s2_bn, s2_nnt;
+  size_t wbuf_off, wbuf_floats;
+  size_t ws_bytes;
+};
+PrefillGeom prefill_geometry(int T, int d_in, int d_out, int r);
+
+hipError_t launch_pack(const void* src, int dt, int rows, int r, int role, void* dst, int32_t* nan_count,
+                       hipStream_t stream);
+hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t stream);
+hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g, hipStream_t stream);
+hipError_t launch_dense_ref(const ForwardArgs& a, float* W, hipStream_t stream);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
+hipError_t launch_zero_elems(void* p, int64_t n, int dt, hipStream_t stream);
+
+}  // namespace lb

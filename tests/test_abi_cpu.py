@@ -1,0 +1,182 @@
+"""CPU tests of the C-ABI boundary: the library loads, exports every function
+include/littlebit.h declares, its pure host helpers agree with the oracle's,
+and every validation error is returned before anything is enqueued (so none
+of these calls needs a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle as O
+import paper_2506_13771_amd as lb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "littlebit.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(lb.LIB_PATH):
+        from paper_2506_13771_amd import _build
+        _build.build()
+    return lb.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lb_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    fns = declared_functions()
+    for name in ["lb_pack_signs", "lb_linear_forward", "lb_dense_reference_weight", "lb_packed_bytes",
+                 "lb_rank_for_bpw", "lb_forward_workspace_bytes"]:
+        assert name in fns
+
+
+def test_exports_every_declared_symbol(lib):
+    raw = ctypes.CDLL(lb.LIB_PATH)
+    missing = [f for f in declared_functions() if not hasattr(raw, f)]
+    assert not missing, missing
+
+
+def test_abi_version_and_status_strings(lib):
+    assert lib.lb_abi_version() == lb.ABI_VERSION
+    for code, name in [(0, "LB_OK"), (1, "LB_ERR_NULL"), (2, "LB_ERR_SHAPE"), (3, "LB_ERR_DTYPE"),
+                       (4, "LB_ERR_ALIGN"), (5, "LB_ERR_WORKSPACE"), (6, "LB_ERR_HIP"), (7, "LB_ERR_ARG")]:
+        assert lb.lb_status_str(code) == name
+
+
+@pytest.mark.parametrize("rows,r", [(4096, 80), (11008, 128), (28672, 288), (1024, 16), (40, 50), (33, 7),
+                                    (1, 1), (0, 5), (7, 0), (5, 17)])
+def test_packed_bytes_matches_oracle(lib, rows, r):
+    assert lb.lb_packed_bytes(lb.LB_ROLE_U, rows, r) == O.packed_bytes(rows, r, O.ROLE_U)
+    assert lb.lb_packed_bytes(lb.LB_ROLE_V, rows, r) == O.packed_bytes(rows, r, O.ROLE_V)
+
+
+def test_packed_bytes_invalid(lib):
+    assert lb.lb_packed_bytes(5, 10, 10) == 0
+    assert lb.lb_packed_bytes(lb.LB_ROLE_U, -1, 10) == 0
+
+
+@pytest.mark.parametrize("d_in,d_out,b", [(4096, 4096, 0.1), (4096, 4096, 0.55), (4096, 11008, 0.1),
+                                          (11008, 4096, 0.55), (5120, 13824, 0.1), (8192, 1024, 0.1),
+                                          (28672, 8192, 0.1), (100, 37, 0.9), (64, 64, 0.01)])
+def test_rank_and_bpw_match_oracle(lib, d_in, d_out, b):
+    assert lb.lb_rank_for_bpw(d_in, d_out, b, 16) == O.rank_for_bpw(d_in, d_out, b, 16, 1)
+    assert lb.lb_rank_for_bpw(d_in, d_out, b, 1) == O.rank_for_bpw(d_in, d_out, b, 1, 1)
+    for r in (0, 16, 80, 288):
+        assert lb.lb_bits_per_weight(d_in, d_out, r, 2) == pytest.approx(O.bpw(d_in, d_out, r, 2), rel=1e-15)
+        assert lb.lb_bits_per_weight(d_in, d_out, r, 1) == pytest.approx(O.bpw(d_in, d_out, r, 1), rel=1e-15)
+
+
+def test_rank_invalid(lib):
+    assert lb.lb_rank_for_bpw(0, 10, 0.1, 16) == -1
+    assert lb.lb_rank_for_bpw(10, 10, 0.1, 0) == -1
+    assert lb.lb_rank_for_bpw(10, 10, float("nan"), 16) == -1
+    assert lb.lb_bits_per_weight(10, 10, 3, 3) == -1.0
+
+
+def test_workspace_sizes(lib):
+    for T, d_in, d_out, r in [(1, 4096, 4096, 80), (64, 11008, 4096, 800), (2048, 5120, 13824, 160),
+                              (4, 512, 512, 32), (3, 33, 17, 5), (0, 10, 10, 2)]:
+        n = lb.lb_forward_workspace_bytes(T, d_in, d_out, r)
+        assert n > 0 and n % 256 == 0
+        # at least the prefill stage-1 result buffer fits
+        assert n >= 2 * T * r * 4
+    assert lb.lb_forward_workspace_bytes(-1, 4, 4, 4) == 0
+    assert lb.lb_decode_max_tokens() >= 1
+
+
+# ---------------------------------------------------------------------------
+# validation errors (no GPU needed: validation precedes every HIP call)
+# ---------------------------------------------------------------------------
+FAKE = 0x10000  # a 256-byte aligned address that is never dereferenced
+
+
+def _paths(U=FAKE, V=FAKE, h=FAKE, g=FAKE, l=FAKE):
+    arr = (lb.lb_path * 2)()
+    for i in range(2):
+        arr[i] = lb.lb_path(U, V, h, g, l)
+    return arr
+
+
+def _fwd(lib, x=FAKE, act=lb.LB_BF16, T=4, d_in=64, d_out=64, r=16, paths=None, sc=lb.LB_F16, y=FAKE,
+         ws=FAKE, ws_bytes=None, kernel=lb.LB_KERNEL_AUTO):
+    if paths is None:
+        paths = _paths()
+    if ws_bytes is None:
+        ws_bytes = lb.lb_forward_workspace_bytes(max(T, 0), max(d_in, 0), max(d_out, 0), max(r, 0)) - 1
+    return lib.lb_linear_forward_kernel(x, act, T, d_in, d_out, r, paths, sc, y, ws, ws_bytes, kernel, None)
+
+
+def test_forward_validation_errors(lib):
+    # the baseline call fails only on the (deliberately) too-small workspace
+    assert _fwd(lib) == lb.LB_ERR_WORKSPACE
+    assert _fwd(lib, act=7) == lb.LB_ERR_DTYPE
+    assert _fwd(lib, sc=-1) == lb.LB_ERR_DTYPE
+    assert _fwd(lib, T=-1) == lb.LB_ERR_SHAPE
+    assert _fwd(lib, d_in=-3) == lb.LB_ERR_SHAPE
+    assert _fwd(lib, r=-1) == lb.LB_ERR_SHAPE
+    assert _fwd(lib, T=1 << 20, d_in=1 << 12) == lb.LB_ERR_SHAPE  # T*d_in >= 2^31
+    assert _fwd(lib, kernel=9) == lb.LB_ERR_ARG
+    assert _fwd(lib, kernel=lb.LB_KERNEL_DECODE, T=lb.lb_decode_max_tokens() + 1) == lb.LB_ERR_SHAPE
+    assert _fwd(lib, x=0) == lb.LB_ERR_NULL
+    assert _fwd(lib, y=0) == lb.LB_ERR_NULL
+    assert _fwd(lib, x=FAKE + 1) == lb.LB_ERR_ALIGN
+    assert _fwd(lib, act=lb.LB_F32, y=FAKE + 2) == lb.LB_ERR_ALIGN
+    assert _fwd(lib, paths=None or _paths(U=0)) == lb.LB_ERR_NULL
+    assert _fwd(lib, paths=_paths(l=0)) == lb.LB_ERR_NULL
+    assert _fwd(lib, paths=_paths(V=FAKE + 2)) == lb.LB_ERR_ALIGN
+    assert _fwd(lib, paths=_paths(h=FAKE + 1)) == lb.LB_ERR_ALIGN
+    assert _fwd(lib, sc=lb.LB_F32, paths=_paths(g=FAKE + 2)) == lb.LB_ERR_ALIGN
+    assert _fwd(lib, ws=0) == lb.LB_ERR_NULL
+    assert _fwd(lib, ws=FAKE + 64, ws_bytes=1 << 30) == lb.LB_ERR_ALIGN
+    assert lib.lb_linear_forward_kernel(FAKE, lb.LB_BF16, 4, 64, 64, 16, None, lb.LB_F16, FAKE, FAKE, 1 << 30,
+                                        0, None) == lb.LB_ERR_NULL
+    # empty problems succeed without touching the GPU
+    assert _fwd(lib, T=0) == lb.LB_OK
+    assert _fwd(lib, d_out=0) == lb.LB_OK
+    # lb_linear_forward (AUTO) goes through the same checks
+    assert lib.lb_linear_forward(FAKE, 9, 4, 64, 64, 16, _paths(), lb.LB_F16, FAKE, FAKE, 1 << 30, None) == \
+        lb.LB_ERR_DTYPE
+
+
+def test_pack_validation_errors(lib):
+    assert lib.lb_pack_signs(FAKE, lb.LB_F32, 64, 16, 5, FAKE * 2, None, None) == lb.LB_ERR_ARG
+    assert lib.lb_pack_signs(FAKE, 3, 64, 16, lb.LB_ROLE_U, FAKE * 2, None, None) == lb.LB_ERR_DTYPE
+    assert lib.lb_pack_signs(FAKE, lb.LB_F32, -1, 16, lb.LB_ROLE_U, FAKE * 2, None, None) == lb.LB_ERR_SHAPE
+    assert lib.lb_pack_signs(0, lb.LB_F32, 64, 16, lb.LB_ROLE_U, FAKE * 2, None, None) == lb.LB_ERR_NULL
+    assert lib.lb_pack_signs(FAKE, lb.LB_F32, 64, 16, lb.LB_ROLE_U, 0, None, None) == lb.LB_ERR_NULL
+    assert lib.lb_pack_signs(FAKE + 2, lb.LB_F32, 64, 16, lb.LB_ROLE_U, FAKE * 2, None, None) == lb.LB_ERR_ALIGN
+    assert lib.lb_pack_signs(FAKE, lb.LB_F32, 64, 16, lb.LB_ROLE_U, FAKE * 2 + 2, None, None) == lb.LB_ERR_ALIGN
+    assert lib.lb_pack_signs(FAKE, lb.LB_BF16, 64, 16, lb.LB_ROLE_U, FAKE * 2, FAKE + 1, None) == lb.LB_ERR_ALIGN
+    # overlapping src/dst
+    assert lib.lb_pack_signs(FAKE, lb.LB_F32, 64, 16, lb.LB_ROLE_U, FAKE + 64, None, None) == lb.LB_ERR_ARG
+    # empty matrices are a no-op
+    assert lib.lb_pack_signs(0, lb.LB_F32, 0, 16, lb.LB_ROLE_U, 0, None, None) == lb.LB_OK
+
+
+def test_dense_ref_validation_errors(lib):
+    assert lib.lb_dense_reference_weight(_paths(), 5, 64, 64, 16, FAKE, None) == lb.LB_ERR_DTYPE
+    assert lib.lb_dense_reference_weight(_paths(), lb.LB_F16, -1, 64, 16, FAKE, None) == lb.LB_ERR_SHAPE
+    assert lib.lb_dense_reference_weight(_paths(), lb.LB_F16, 64, 64, 16, 0, None) == lb.LB_ERR_NULL
+    assert lib.lb_dense_reference_weight(_paths(), lb.LB_F16, 64, 64, 16, FAKE + 2, None) == lb.LB_ERR_ALIGN
+    assert lib.lb_dense_reference_weight(None, lb.LB_F16, 64, 64, 16, FAKE, None) == lb.LB_ERR_NULL
+    assert lib.lb_dense_reference_weight(_paths(), lb.LB_F16, 0, 64, 16, FAKE, None) == lb.LB_OK
+
+
+def test_workspace_init_validation(lib):
+    assert lib.lb_workspace_init(0, 256, None) == lb.LB_ERR_NULL
+    assert lib.lb_workspace_init(FAKE + 4, 256, None) == lb.LB_ERR_ALIGN
+    assert lib.lb_workspace_init(FAKE, 6, None) == lb.LB_ERR_ALIGN
+    assert lib.lb_workspace_init(0, 0, None) == lb.LB_OK
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    x = torch.zeros(2, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        lb.lb_pack_signs(x, lb.LB_ROLE_U)
