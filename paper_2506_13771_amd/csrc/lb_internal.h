@@ -108,9 +108,7 @@ __device__ __forceinline__ bool spin_until_at_least(const uint32_t* p, uint32_t 
 constexpr int kCtrlEpoch = 0;      // decode: tag of the last completed call
 constexpr int kCtrlDone = 1;       // decode: finished stage-2 workgroups of the running call
 constexpr int kCtrlError = 2;      // set to nonzero if a bounded wait expired
-constexpr int kCtrlArrive = 64;    // decode: per (path, k-tile) arrival counters
-constexpr int kCtrlMaxArrive = 4096;
-constexpr int kCtrlTiles = kCtrlArrive + kCtrlMaxArrive;  // prefill: per-tile counters (3 words each)
+constexpr int kCtrlTiles = 64;     // prefill: per-tile counters (3 words each)
 constexpr int kCtrlMaxTiles = 8192;
 constexpr int kCtrlWords = kCtrlTiles + 3 * kCtrlMaxTiles;
 constexpr size_t kCtrlBytes = ((kCtrlWords * 4 + 255) / 256) * 256;
@@ -135,7 +133,7 @@ struct ForwardArgs {
 
 // Decode kernel geometry (pure function of the sizes; also sizes the workspace).
 struct DecodeGeom {
-  int kc, nkt, bpw, s1d, n_s1;
+  int kc, nkt, bpw, s1d, n_s1, cb;
   int kq_log2;  // log2 of the lanes that share one output row in stage 2
   int rows2, n_s2;
   int direct;
@@ -145,8 +143,8 @@ struct DecodeGeom {
   size_t ws_bytes;
 };
 DecodeGeom decode_geometry(int T, int d_in, int d_out, int r);
-constexpr int kDecodeMaxTokens = 16;
-constexpr int kDecodeMaxRank = 4096;
+constexpr int kDecodeMaxTokens = 4;
+constexpr int kDecodeMaxRank = 1024;  // stage-2 look-up tables of one token fit in LDS
 
 struct PrefillGeom {
   int bm;                  // tokens per M-tile
