@@ -94,6 +94,18 @@ class Layer:
     def set_stream(self, handle):
         self.argv = self.argv[:-1] + (ctypes.c_void_p(handle),)
 
+    def weight_copy(self):
+        """The same layer with its packed signs and scales cloned to fresh device memory
+        (x, y and the workspace are shared): a member of a cold-cache rotation."""
+        import copy
+        import paper_2506_13771_amd as lb
+        c = copy.copy(self)
+        c.paths = [lb.LittleBitPath(U=p.U.clone(), V=p.V.clone(), h=p.h.clone(), g=p.g.clone(), l=p.l.clone())
+                   for p in self.paths]
+        c._arr, _ = lb._paths_struct(c.paths)
+        c.argv = self.argv[:6] + (c._arr,) + self.argv[7:]
+        return c
+
     def call(self):
         st = self.lib.lb_linear_forward_kernel(*self.argv)
         if st != 0:
@@ -155,6 +167,37 @@ def time_calls(layers, steps, warmup, use_graph=True, per_graph=None):
     return e0.elapsed_time(e1) / steps, steps
 
 
+def time_rotation(copies, steps, warmup):
+    """Cold-cache timing: `steps` calls cycling through `copies` (distinct weight buffers of
+    one layer, together larger than the caches), captured into one HIP graph and replayed.
+    Returns (ms per call, calls timed)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    for L in copies:
+        L.set_stream(stream.cuda_stream)
+    for i in range(warmup):
+        copies[i % len(copies)].call()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cap = torch.cuda.current_stream().cuda_stream
+        for L in copies:
+            L.set_stream(cap)
+        for i in range(steps):
+            copies[i % len(copies)].call()
+    for L in copies:
+        L.set_stream(stream.cuda_stream)
+    graph.replay()  # untimed: first replay
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps, steps
+
+
 def source_digest(files):
     h = hashlib.sha256()
     for f in files:
@@ -164,6 +207,62 @@ def source_digest(files):
 
 
 DECODE_SOURCES = ["paper_2506_13771_amd/csrc/decode.hip", "paper_2506_13771_amd/csrc/lb_internal.h"]
+
+
+def copy_probe(mib):
+    """A plain device-to-device copy of `mib` MiB, five times: the reference kernel whose
+    FETCH_SIZE / WRITE_SIZE counters calibrate those of the decode kernel."""
+    import torch
+    n = int(mib) << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy probe: 5 copies of {n} bytes")
+
+
+def _pmc_rows(path, counter):
+    import csv
+    rows = []
+    with open(path, newline="") as fh:
+        for row in csv.DictReader(fh):
+            if row.get("Counter_Name") == counter:
+                rows.append((row.get("Kernel_Name", ""), float(row["Counter_Value"])))
+    return rows
+
+
+def ingest_pmc(fetch_csv, write_csv, copy_mib, workload_key, commands):
+    """Per-launch HBM bytes of the decode kernel from two rocprofv3 --pmc runs (FETCH_SIZE,
+    then WRITE_SIZE, KiB per dispatch), each scaled by what the same counter reads for the
+    plain copy of copy_mib MiB made by --copy-probe in the same run.  Writes
+    profiles/traffic.json."""
+    n = float(int(copy_mib) << 20)
+    out = {}
+    for name, path in (("fetch", fetch_csv), ("write", write_csv)):
+        counter = "FETCH_SIZE" if name == "fetch" else "WRITE_SIZE"
+        rows = _pmc_rows(path, counter)
+        dec = [v for k, v in rows if "decode_kernel" in k]
+        # the probe's five copies are the five largest copy-kernel dispatches of the run
+        cop = sorted((v for k, v in rows if "copyBuffer" in k), reverse=True)[:5]
+        if not dec or not cop:
+            raise SystemExit(f"{path}: no {counter} rows for the decode kernel or the copy probe")
+        dec_kib = float(np.mean(dec))
+        cop_kib = float(np.median(cop))
+        factor = n / (cop_kib * 1024.0)
+        out[name] = {"dispatches": len(dec), "kib_per_dispatch": dec_kib, "kib_min": float(np.min(dec)),
+                     "kib_max": float(np.max(dec)), "copy_kib_per_dispatch": cop_kib, "copy_bytes": n,
+                     "factor": factor, "bytes_per_launch": dec_kib * 1024.0 * factor}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    d = json.load(open(path)) if os.path.exists(path) else {}
+    d[workload_key] = {"bytes_per_launch": out["fetch"]["bytes_per_launch"] + out["write"]["bytes_per_launch"],
+                       "fetch": out["fetch"], "write": out["write"], "sources": DECODE_SOURCES,
+                       "source_digest": source_digest(DECODE_SOURCES), "commands": commands}
+    with open(path, "w") as fh:
+        json.dump(d, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(d[workload_key], indent=1))
 
 
 def measured_traffic(workload_key):
@@ -284,7 +383,22 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", default=None, help="write per-configuration JSON lines to this file")
+    ap.add_argument("--no-warm", action="store_true",
+                    help="skip the warm-cache measurements (counter runs: every decode dispatch is then a "
+                         "cold-rotation one)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="after the run, copy MIB MiB device-to-device five times (counter calibration)")
+    ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"), default=None,
+                    help="no GPU: turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
+                         "WRITE_SIZE) of runs with --copy-probe into profiles/traffic.json")
+    ap.add_argument("--pmc-command", action="append", default=[],
+                    help="with --ingest-pmc: the command lines that produced the files (recorded)")
     args = ap.parse_args()
+
+    if args.ingest_pmc:
+        ingest_pmc(args.ingest_pmc[0], args.ingest_pmc[1], args.copy_probe or 64,
+                   "decode_q_proj_4096_r80_T1", args.pmc_command)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -304,9 +418,23 @@ def main():
     assert lb.lb_rank_for_bpw(d_in, d_out, 0.1, 16) == r
     li = synth.make_linear(d_in, d_out, r, T, act_dtype="bf16", scale_dtype="f16", cfg=1, linear=0)
     L = Layer(li, "cuda")
-    ms, steps = time_calls([L], args.steps, args.warmup, use_graph=(args.launch == "graph"))
-    ms_stream, _ = time_calls([L], min(args.steps, 2000), 100, use_graph=False)
     b, bw = alg_bytes(T, d_in, d_out, r, L.e_act, L.e_scale)
+    # headline: weights cold in HBM -- the calls rotate over copies of the layer's packed signs
+    # and scales that together exceed twice the 256 MB Infinity Cache (and every L2)
+    ncopies = int(np.ceil(2 * 256e6 / bw))
+    copies = [L] + [L.weight_copy() for _ in range(ncopies - 1)]
+    if args.launch == "graph":
+        ms, steps = time_rotation(copies, args.steps, args.warmup)
+    else:
+        ms, steps = time_calls(copies, max(1, args.steps // ncopies), max(1, args.warmup // ncopies),
+                               use_graph=False)
+        ms, steps = ms / ncopies, steps * ncopies
+    # the same layer called repeatedly (weights warm in the caches), graph-replayed and stream-issued
+    ms_warm = ms_stream = None
+    if not args.no_warm:
+        ms_warm, _ = time_calls([L], args.steps, args.warmup, use_graph=True)
+        ms_stream, _ = time_calls([L], min(args.steps, 2000), 100, use_graph=False)
+    del copies
     achieved = b / (ms * 1e-3) / 1e9
     traffic = measured_traffic("decode_q_proj_4096_r80_T1")
     rec = {
@@ -325,15 +453,20 @@ def main():
         "config": {"workload": "LittleBit linear forward, Llama2-7B q_proj shape 4096x4096, 0.1 BPW (r=80 per "
                                "path, 2 paths), T=1 decode, bf16 x, fp16 scales, Bernoulli(1/2) signs",
                    "d_in": d_in, "d_out": d_out, "r": r, "T": T, "bpw": round(lb.lb_bits_per_weight(d_in, d_out, r), 5),
-                   "kernel": "decode", "launch": args.launch},
+                   "kernel": "decode", "launch": args.launch,
+                   "weights": f"cold: {ncopies} copies rotated ({ncopies * bw / 1e6:.0f} MB)"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "alg_bytes_per_launch": b, "weights_bytes_per_launch": bw,
-                     "avg_launch_us": ms * 1e3, "avg_launch_us_stream_issued": ms_stream * 1e3},
+                     "avg_launch_us": ms * 1e3,
+                     "avg_launch_us_warm": ms_warm * 1e3 if ms_warm is not None else None,
+                     "avg_launch_us_warm_stream_issued": ms_stream * 1e3 if ms_stream is not None else None},
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(li, args.cpu_seconds)
     print(json.dumps(rec), flush=True)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
     if args.sweep:
         run_sweep(args.sweep, min(args.steps, 1000), min(args.warmup, 100))
 
