@@ -94,17 +94,29 @@ class Layer:
     def set_stream(self, handle):
         self.argv = self.argv[:-1] + (ctypes.c_void_p(handle),)
 
-    def weight_copy(self):
-        """The same layer with its packed signs and scales cloned to fresh device memory
-        (x, y and the workspace are shared): a member of a cold-cache rotation."""
+    def weight_copies(self, n):
+        """n - 1 more instances of the same layer whose packed signs and scales live in fresh
+        device memory (x, y and the workspace are shared): a cold-cache rotation.  All copies
+        sit in one allocation filled by one broadcast copy per tensor."""
         import copy
+        import torch
         import paper_2506_13771_amd as lb
-        c = copy.copy(self)
-        c.paths = [lb.LittleBitPath(U=p.U.clone(), V=p.V.clone(), h=p.h.clone(), g=p.g.clone(), l=p.l.clone())
-                   for p in self.paths]
-        c._arr, _ = lb._paths_struct(c.paths)
-        c.argv = self.argv[:6] + (c._arr,) + self.argv[7:]
-        return c
+        tensors = [getattr(p, f) for p in self.paths for f in ("U", "V", "h", "g", "l")]
+        sizes = [t.numel() * t.element_size() for t in tensors]
+        offs = np.concatenate([[0], np.cumsum([(b + 255) // 256 * 256 for b in sizes])]).astype(int)
+        big = torch.empty((n - 1, int(offs[-1])), dtype=torch.uint8, device=tensors[0].device)
+        for t, o, b in zip(tensors, offs[:-1], sizes):
+            big[:, o:o + b] = t.contiguous().view(torch.uint8).reshape(1, b).expand(n - 1, b)
+        out = [self]
+        for c in range(n - 1):
+            views = [big[c, o:o + b].view(t.dtype) for t, o, b in zip(tensors, offs[:-1], sizes)]
+            L = copy.copy(self)
+            L.paths = [lb.LittleBitPath(*views[5 * p:5 * p + 5]) for p in range(2)]
+            L._arr, _ = lb._paths_struct(L.paths)
+            L.argv = self.argv[:6] + (L._arr,) + self.argv[7:]
+            L._big = big
+            out.append(L)
+        return out
 
     def call(self):
         st = self.lib.lb_linear_forward_kernel(*self.argv)
@@ -422,7 +434,13 @@ def main():
     # headline: weights cold in HBM -- the calls rotate over copies of the layer's packed signs
     # and scales that together exceed twice the 256 MB Infinity Cache (and every L2)
     ncopies = int(np.ceil(2 * 256e6 / bw))
-    copies = [L] + [L.weight_copy() for _ in range(ncopies - 1)]
+    copies = L.weight_copies(ncopies)
+    # every copy computes the same output (bitwise: same inputs, deterministic kernel)
+    copies[0].call()
+    y0 = L.y.clone()
+    copies[-1].call()
+    torch.cuda.synchronize()
+    assert torch.equal(y0, L.y), "a weight copy of the rotation differs from the original layer"
     if args.launch == "graph":
         ms, steps = time_rotation(copies, args.steps, args.warmup)
     else:
