@@ -74,9 +74,16 @@ typedef enum lb_role { LB_ROLE_U = 0, LB_ROLE_V = 1 } lb_role;
 
 /* Which forward kernel lb_linear_forward_kernel() runs. */
 typedef enum lb_kernel {
-  LB_KERNEL_AUTO = 0,    /* decode for T <= lb_decode_max_tokens(), prefill above */
-  LB_KERNEL_DECODE = 1,  /* single launch, packed signs streamed once, fp32 sign-flip accumulation */
-  LB_KERNEL_PREFILL = 2  /* matrix-core (MFMA) kernels on sign tiles expanded to bf16 +-1 */
+  LB_KERNEL_AUTO = 0,         /* DECODE for T <= lb_decode_max_tokens(), DECODE_MFMA for T <= 64,
+                                 PREFILL above (each where its rank limit allows) */
+  LB_KERNEL_DECODE = 1,       /* single launch, 4-bit look-up tables, fp32 sign-flip accumulation;
+                                 T <= 4, r <= 1024 */
+  LB_KERNEL_PREFILL = 2,      /* two launches of matrix-core (MFMA) tiles, signs expanded to bf16 +-1;
+                                 any size */
+  LB_KERNEL_DECODE_MFMA = 3   /* single launch, matrix-core contractions: stage 1 multiplies exact
+                                 bf16 terms of x by the signs carried on exact bf16 terms of g,
+                                 stage 2 the +-1 signs of U by bf16 terms of l (.) z; T <= 64,
+                                 r <= 832 */
 } lb_kernel;
 
 /* One path's parameters (Sec. 3.1 Eq. ghl_scales_combined; Sec. 3.3).

@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(_HERE, "liblittlebit.so")
 LB_OK, LB_ERR_NULL, LB_ERR_SHAPE, LB_ERR_DTYPE, LB_ERR_ALIGN, LB_ERR_WORKSPACE, LB_ERR_HIP, LB_ERR_ARG = range(8)
 LB_F32, LB_F16, LB_BF16 = 0, 1, 2
 LB_ROLE_U, LB_ROLE_V = 0, 1
-LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL = 0, 1, 2
+LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL, LB_KERNEL_DECODE_MFMA = 0, 1, 2, 3
 ABI_VERSION = 1
 
 
@@ -239,7 +239,7 @@ def lb_dense_reference_weight(paths: Sequence[LittleBitPath], d_in: int, d_out: 
 __all__ = [
     "LB_OK", "LB_ERR_NULL", "LB_ERR_SHAPE", "LB_ERR_DTYPE", "LB_ERR_ALIGN", "LB_ERR_WORKSPACE", "LB_ERR_HIP",
     "LB_ERR_ARG", "LB_F32", "LB_F16", "LB_BF16", "LB_ROLE_U", "LB_ROLE_V", "LB_KERNEL_AUTO", "LB_KERNEL_DECODE",
-    "LB_KERNEL_PREFILL", "LittleBitError", "LittleBitPath", "lb_path", "load_library", "lb_status_str",
+    "LB_KERNEL_PREFILL", "LB_KERNEL_DECODE_MFMA", "LittleBitError", "LittleBitPath", "lb_path", "load_library", "lb_status_str",
     "lb_packed_bytes", "lb_bits_per_weight", "lb_rank_for_bpw", "lb_forward_workspace_bytes",
     "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "alloc_workspace", "lb_linear_forward",
     "lb_dense_reference_weight",

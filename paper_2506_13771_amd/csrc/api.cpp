@@ -145,6 +145,13 @@ size_t lb_forward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_
     const lb::DecodeGeom g = lb::decode_geometry(iT, ii, io, ir);
     if (g.ws_bytes > need) need = g.ws_bytes;
   }
+  if (lb::decode_mma_supports(T, r)) {
+    // the geometry depends on the activation dtype: cover all of them
+    for (int dt : {lb::kDtF32, lb::kDtF16, lb::kDtBF16}) {
+      const lb::MmaGeom g = lb::decode_mma_geometry(iT, ii, io, ir, dt);
+      if (g.ws_bytes > need) need = g.ws_bytes;
+    }
+  }
   const lb::PrefillGeom pg = lb::prefill_geometry(iT, ii, io, ir);
   if (pg.ws_bytes > need) need = pg.ws_bytes;
   return need;
@@ -160,11 +167,14 @@ lb_status lb_workspace_init(void* workspace, size_t bytes, hipStream_t stream) {
 lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out,
                                    int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y, void* workspace,
                                    size_t workspace_bytes, lb_kernel kernel, hipStream_t stream) {
-  if (kernel != LB_KERNEL_AUTO && kernel != LB_KERNEL_DECODE && kernel != LB_KERNEL_PREFILL) return LB_ERR_ARG;
+  if (kernel != LB_KERNEL_AUTO && kernel != LB_KERNEL_DECODE && kernel != LB_KERNEL_PREFILL &&
+      kernel != LB_KERNEL_DECODE_MFMA)
+    return LB_ERR_ARG;
   if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype)) return LB_ERR_DTYPE;
   lb_status st = check_sizes(T, d_in, d_out, r);
   if (st != LB_OK) return st;
   if (kernel == LB_KERNEL_DECODE && !decode_supports(T, r)) return LB_ERR_SHAPE;
+  if (kernel == LB_KERNEL_DECODE_MFMA && !lb::decode_mma_supports(T, r)) return LB_ERR_SHAPE;
   if (T == 0 || d_out == 0) return LB_OK;
   if (!y || (d_in > 0 && !x)) return LB_ERR_NULL;
   if (!aligned(x, dtype_size(act_dtype)) || !aligned(y, dtype_size(act_dtype))) return LB_ERR_ALIGN;
@@ -181,13 +191,20 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
     e = lb::launch_zero_elems(y, T * d_out, act_dtype, stream);
     return e == hipSuccess ? LB_OK : LB_ERR_HIP;
   }
-  const bool use_decode =
-      kernel == LB_KERNEL_DECODE || (kernel == LB_KERNEL_AUTO && decode_supports(T, r));
-  if (use_decode) {
-    e = lb::launch_decode(a, lb::decode_geometry(a.T, a.d_in, a.d_out, a.r), stream);
-  } else {
-    e = lb::launch_prefill(a, lb::prefill_geometry(a.T, a.d_in, a.d_out, a.r), stream);
+  if (kernel == LB_KERNEL_AUTO) {
+    if (decode_supports(T, r))
+      kernel = LB_KERNEL_DECODE;
+    else if (lb::decode_mma_supports(T, r))
+      kernel = LB_KERNEL_DECODE_MFMA;
+    else
+      kernel = LB_KERNEL_PREFILL;
   }
+  if (kernel == LB_KERNEL_DECODE)
+    e = lb::launch_decode(a, lb::decode_geometry(a.T, a.d_in, a.d_out, a.r), stream);
+  else if (kernel == LB_KERNEL_DECODE_MFMA)
+    e = lb::launch_decode_mma(a, lb::decode_mma_geometry(a.T, a.d_in, a.d_out, a.r, a.act_dt), stream);
+  else
+    e = lb::launch_prefill(a, lb::prefill_geometry(a.T, a.d_in, a.d_out, a.r), stream);
   return e == hipSuccess ? LB_OK : LB_ERR_HIP;
 }
 

@@ -1,0 +1,171 @@
+// Device helpers shared by the single-launch forward kernels: tagged slots
+// for the hand-off between workgroups, raw-bit loads that can all be issued
+// before any is waited on, and conversions.
+#pragma once
+#include "lb_internal.h"
+
+namespace lb {
+
+// Polls of a tagged slot before a wait gives up and records an error.
+constexpr uint32_t kSpinLimit = 1u << 19;
+
+// ---------------------------------------------------------------------------
+// tagged slots
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void put_slot(uint64_t* p, uint32_t tag, float v) {
+  const uint64_t w = (static_cast<uint64_t>(tag) << 32) | __float_as_uint(v);
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t get_slot(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float slot_value(uint64_t w) { return __uint_as_float(static_cast<uint32_t>(w)); }
+__device__ __forceinline__ bool slot_ready(uint64_t w, uint32_t tag) { return static_cast<uint32_t>(w >> 32) == tag; }
+
+// Sum of n (<= MAXN) slots spaced `stride` apart, in ascending order, once
+// every slot carries `tag` (used by the two-level reducers).
+template <int MAXN>
+__device__ __forceinline__ bool gather_sum(const uint64_t* base, int64_t stride, int n, uint32_t tag, float& sum) {
+  uint64_t v[MAXN];
+  bool ready = true;
+#pragma unroll
+  for (int c = 0; c < MAXN; ++c) {
+    v[c] = c < n ? get_slot(base + c * stride) : (static_cast<uint64_t>(tag) << 32);
+    ready = ready && slot_ready(v[c], tag);
+  }
+  for (uint32_t it = 0; !ready; ++it) {
+    if (it >= kSpinLimit) return false;
+    __builtin_amdgcn_s_sleep(1);
+    ready = true;
+#pragma unroll
+    for (int c = 0; c < MAXN; ++c) {
+      if (c < n && !slot_ready(v[c], tag)) v[c] = get_slot(base + c * stride);
+      ready = ready && slot_ready(v[c], tag);
+    }
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int c = 0; c < MAXN; ++c)
+    if (c < n) s += slot_value(v[c]);
+  sum = s;
+  return true;
+}
+
+// ---------------------------------------------------------------------------
+// loads and tables
+// ---------------------------------------------------------------------------
+// Element i of p (dtype DT) as fp32.  The dtype is a template parameter so
+// that loads are straight-line code the compiler can batch.
+template <int DT>
+__device__ __forceinline__ float ld(const void* p, int64_t i) {
+  if constexpr (DT == kDtF32) {
+    return static_cast<const float*>(p)[i];
+  } else {
+    const uint32_t u = static_cast<const uint16_t*>(p)[i];
+    return DT == kDtBF16 ? bf16_bits_to_f32(u) : f16_bits_to_f32(u);
+  }
+}
+
+// Branch-free loads: the address is clamped to a valid element and the value
+// selected afterwards, so no load sits inside a divergent branch (the compiler
+// would wait for it before the branch rejoins, serialising the round trips).
+template <int DT>
+__device__ __forceinline__ float ld_or0(const void* p, int64_t i, bool ok) {
+  const float v = ld<DT>(p, ok ? i : 0);
+  return ok ? v : 0.0f;
+}
+
+// Raw bits of an element (fp32 bits, or a 16-bit value zero-extended), so that
+// loads can be issued together and converted only after all are in flight.
+template <int DT>
+__device__ __forceinline__ uint32_t ld_bits(const void* p, int64_t i) {
+  if constexpr (DT == kDtF32)
+    return static_cast<const uint32_t*>(p)[i];
+  else
+    return static_cast<const uint16_t*>(p)[i];
+}
+template <int DT>
+__device__ __forceinline__ float bits_to_f32(uint32_t u) {
+  if constexpr (DT == kDtF32)
+    return __uint_as_float(u);
+  else if constexpr (DT == kDtBF16)
+    return bf16_bits_to_f32(u);
+  else
+    return f16_bits_to_f32(u);
+}
+
+// Four consecutive elements p[i..i+3] as raw bits.  VEC: one 16-byte (fp32) or
+// 8-byte (16-bit dtypes, two per dword) load, i a multiple of 4 and p aligned;
+// otherwise four element loads, element e at p[i + e] if e < nvalid, else at
+// p[0].  Element e is taken back with raw4_elem.
+template <int DT, bool VEC>
+__device__ __forceinline__ void ld4_bits(const void* p, int64_t i, int nvalid, uint32_t (&o)[4]) {
+  if constexpr (VEC && DT == kDtF32) {
+    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint32_t*>(p) + i);
+    o[0] = v.x, o[1] = v.y, o[2] = v.z, o[3] = v.w;
+  } else if constexpr (VEC) {
+    const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p) + i);
+    o[0] = v.x, o[1] = v.y, o[2] = 0u, o[3] = 0u;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = ld_bits<DT>(p, e < nvalid ? i + e : 0);
+  }
+}
+template <int DT, bool VEC>
+__device__ __forceinline__ float raw4_elem(const uint32_t (&o)[4], int e) {
+  if constexpr (VEC && DT != kDtF32)
+    return bits_to_f32<DT>((o[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+  else
+    return bits_to_f32<DT>(o[e]);
+}
+
+// Make the compiler treat v as produced here: computations on v stay below
+// this point (the hardware waits for v's load here, after the loads issued
+// before it).
+__device__ __forceinline__ void pin(uint32_t& v) { asm volatile("" : "+v"(v)); }
+// The epoch word of the control block, read where it is written: the index
+// goes through an opaque (and per-stage distinct) statement, so the compiler
+// neither hoists the load out of its loop nor merges the two stages' loads
+// into one before the branch (which would make a stage wait for it first).
+template <int STAGE>
+__device__ __forceinline__ uint32_t load_epoch(const uint32_t* ctrl) {
+  int idx = kCtrlEpoch;
+  asm volatile("; epoch load, stage %1" : "+s"(idx) : "i"(STAGE));
+  return atomic_load_relaxed(ctrl + idx);
+}
+
+// Region A of a packed view (its full words) when it has any, else a word the
+// kernel may read harmlessly (the control block): clamped full-word loads then
+// stay in bounds even for a view whose whole buffer is a 2-byte tail plane.
+__device__ __forceinline__ const uint32_t* full_words_or(const uint32_t* base, int nb, const uint32_t* fallback) {
+  return nb > 0 ? base : fallback;
+}
+
+// Tail word of output row o of a packed view (0 if the view has none), as two
+// 16-bit loads at clamped addresses; combined by tail_word after pinning.
+__device__ __forceinline__ void ld_tail_bits(const uint32_t* base, int nb, int n_out, int tailw, int o, bool ok,
+                                             uint32_t& lo, uint32_t& hi) {
+  const uint16_t* h = reinterpret_cast<const uint16_t*>(base);
+  const int64_t plane = static_cast<int64_t>(2) * nb * n_out;  // in 16-bit units
+  const bool has = ok && tailw != 0;
+  const int64_t e = tailw <= 16 ? o : static_cast<int64_t>(2) * o;
+  lo = h[has ? plane + e : 0];
+  hi = h[has && tailw > 16 ? plane + e + 1 : 0];
+}
+__device__ __forceinline__ uint32_t tail_word(uint32_t lo, uint32_t hi, int tailw) {
+  return tailw > 16 ? (lo | (hi << 16)) : lo;
+}
+
+template <int DT>
+__device__ __forceinline__ void st(void* p, int64_t i, float v) {
+  if constexpr (DT == kDtF32) {
+    static_cast<float*>(p)[i] = v;
+  } else if constexpr (DT == kDtBF16) {
+    static_cast<uint16_t*>(p)[i] = static_cast<uint16_t>(f32_to_bf16_bits(v));
+  } else {
+    static_cast<__half*>(p)[i] = __float2half_rn(v);
+  }
+}
+
+
+}  // namespace lb

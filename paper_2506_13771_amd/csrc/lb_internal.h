@@ -146,6 +146,24 @@ DecodeGeom decode_geometry(int T, int d_in, int d_out, int r);
 constexpr int kDecodeMaxTokens = 4;
 constexpr int kDecodeMaxRank = 1024;  // stage-2 look-up tables of one token fit in LDS
 
+// Matrix-core decode kernel geometry.
+struct MmaGeom {
+  int nmf;    // 16-latent tiles per path
+  int s1d;    // d_in runs per tile
+  int bpr;    // 32-wide input blocks per run
+  int n_s1;   // stage-1 workgroups
+  int n_s2;   // stage-2 workgroups
+  int direct;
+  size_t smem_bytes;
+  size_t partial_off, partial_slots;
+  size_t wbuf_off, wbuf_slots;
+  size_t ws_bytes;
+};
+constexpr int kMmaMaxTokens = 64;
+constexpr int kMmaMaxRank = 832;  // U words of one row (both paths) held in registers in stage 2
+MmaGeom decode_mma_geometry(int T, int d_in, int d_out, int r, int act_dt);
+bool decode_mma_supports(int64_t T, int64_t r);
+
 struct PrefillGeom {
   int bm;                  // tokens per M-tile
   int n_mt;                // M-tiles
@@ -162,6 +180,7 @@ hipError_t launch_pack(const void* src, int dt, int rows, int r, int role, void*
                        hipStream_t stream);
 hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t stream);
 hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g, hipStream_t stream);
+hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t stream);
 hipError_t launch_dense_ref(const ForwardArgs& a, float* W, hipStream_t stream);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 hipError_t launch_zero_elems(void* p, int64_t n, int dt, hipStream_t stream);

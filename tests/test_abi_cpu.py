@@ -123,6 +123,8 @@ def test_forward_validation_errors(lib):
     assert _fwd(lib, T=1 << 20, d_in=1 << 12) == lb.LB_ERR_SHAPE  # T*d_in >= 2^31
     assert _fwd(lib, kernel=9) == lb.LB_ERR_ARG
     assert _fwd(lib, kernel=lb.LB_KERNEL_DECODE, T=lb.lb_decode_max_tokens() + 1) == lb.LB_ERR_SHAPE
+    assert _fwd(lib, kernel=lb.LB_KERNEL_DECODE_MFMA, T=65) == lb.LB_ERR_SHAPE
+    assert _fwd(lib, kernel=lb.LB_KERNEL_DECODE_MFMA, r=848) == lb.LB_ERR_SHAPE
     assert _fwd(lib, x=0) == lb.LB_ERR_NULL
     assert _fwd(lib, y=0) == lb.LB_ERR_NULL
     assert _fwd(lib, x=FAKE + 1) == lb.LB_ERR_ALIGN

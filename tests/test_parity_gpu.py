@@ -22,7 +22,8 @@ if gpu_available():
     import torch
     import paper_2506_13771_amd as lb
 
-KERNELS = {"decode": 1, "prefill": 2, "auto": 0}
+KERNELS = {"decode": 1, "prefill": 2, "auto": 0, "mma": 3}
+MMA_MAX_T, MMA_MAX_R = 64, 832
 
 
 def _run(li, kernel="auto", pack_on_gpu=True):
@@ -86,7 +87,7 @@ def cfg0():
     return synth.make_linear(512, 512, 32, 4, act_dtype="f32", scale_dtype="f32", cfg=0, l_over_sqrt_r=True)
 
 
-@pytest.mark.parametrize("kernel", ["decode", "prefill", "auto"])
+@pytest.mark.parametrize("kernel", ["decode", "prefill", "mma", "auto"])
 def test_cfg0_fp32(kernel):
     li = cfg0()
     y = _run(li, kernel)
@@ -114,7 +115,7 @@ def test_dense_reference_weight_cfg0():
 # ---------------------------------------------------------------------------
 # configuration 1: Llama2-7B q_proj 4096x4096 at 0.1 BPW (r=80), T=1, bf16
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("kernel", ["auto", "prefill"])
+@pytest.mark.parametrize("kernel", ["auto", "prefill", "mma"])
 def test_cfg1_q_proj(kernel):
     li = synth.make_linear(4096, 4096, 80, 1, cfg=1)
     _check(li, _run(li, kernel), label=f"cfg1 {kernel}")
@@ -144,7 +145,7 @@ def test_cfg2_llama2_7b_block(bpw, T):
 @pytest.mark.parametrize("T", [1, 2, 4])
 def test_cfg2_both_kernels_agree_with_oracle(T):
     li = synth.make_linear(11008, 4096, 128, T, cfg=2, linear=50)
-    for k in ("decode", "prefill"):
+    for k in ("decode", "prefill", "mma"):
         _check(li, _run(li, k), label=f"down T={T} {k}")
 
 
@@ -156,6 +157,18 @@ def test_decode_large_rank_and_long_inputs(d_in, d_out, r, T):
     output row, several rows per lane."""
     li = synth.make_linear(d_in, d_out, r, T, cfg=11, linear=d_in + r, direct_words=True)
     _check(li, _run(li, "decode"), label=f"decode {d_in}x{d_out} r={r} T={T}")
+
+
+@pytest.mark.parametrize("d_in,d_out,r", [(4096, 4096, 544), (11008, 4096, 800), (4096, 11008, 800),
+                                          (8192, 28672, 288), (28672, 8192, 288), (8192, 1024, 16),
+                                          (4000, 3000, 832)])
+@pytest.mark.parametrize("T", [5, 16, 33, 64])
+def test_mma_large_rank_and_long_inputs(d_in, d_out, r, T):
+    """Matrix-core decode geometry extremes: many d_in runs (two-level sums), the
+    largest rank it takes, 1 to 4 token fragments."""
+    li = synth.make_linear(d_in, d_out, r, T, cfg=12, linear=d_in + r + T, direct_words=True)
+    tokens = None if T <= 16 else np.array([0, 1, 15, 16, T - 2, T - 1])
+    _check(li, _run(li, "mma"), tokens=tokens, label=f"mma {d_in}x{d_out} r={r} T={T}")
 
 
 # ---------------------------------------------------------------------------
@@ -199,11 +212,14 @@ RAGGED = [(100, 77, 19, 3), (33, 200, 50, 5), (257, 130, 16, 1), (31, 64, 1, 2),
 
 
 @pytest.mark.parametrize("d_in,d_out,r,T", RAGGED)
-@pytest.mark.parametrize("kernel", ["decode", "prefill"])
-@pytest.mark.parametrize("act,sc", [("bf16", "f16"), ("f32", "f32"), ("f16", "bf16")])
+@pytest.mark.parametrize("kernel", ["decode", "prefill", "mma"])
+@pytest.mark.parametrize("act,sc", [("bf16", "f16"), ("f32", "f32"), ("f16", "bf16"), ("f16", "f32"),
+                                    ("bf16", "bf16")])
 def test_ragged(d_in, d_out, r, T, kernel, act, sc):
     if kernel == "decode" and T > lb.lb_decode_max_tokens():
         pytest.skip("decode kernel covers small T only")
+    if kernel == "mma" and (T > MMA_MAX_T or r > MMA_MAX_R):
+        pytest.skip("matrix-core decode kernel covers T <= 64, r <= 832")
     li = synth.make_linear(d_in, d_out, r, T, act_dtype=act, scale_dtype=sc, cfg=9,
                            linear=d_in * 7 + d_out * 3 + r + T)
     # scales of both signs: nothing in the kernels may assume positive scales
@@ -216,7 +232,7 @@ def test_ragged(d_in, d_out, r, T, kernel, act, sc):
 
 
 @pytest.mark.parametrize("T,d_in,d_out,r", [(0, 64, 64, 16), (4, 0, 64, 16), (4, 64, 64, 0), (4, 64, 0, 16)])
-@pytest.mark.parametrize("kernel", ["decode", "prefill", "auto"])
+@pytest.mark.parametrize("kernel", ["decode", "prefill", "mma", "auto"])
 def test_degenerate_sizes(T, d_in, d_out, r, kernel):
     li = synth.make_linear(max(d_in, 1), max(d_out, 1), max(r, 1), max(T, 1), cfg=8)
     x = torch.randn(T, d_in, device="cuda").to(torch.bfloat16)
@@ -259,13 +275,14 @@ def test_fp16_subnormal_scales_exact():
 # ---------------------------------------------------------------------------
 # determinism and workspace reuse (counters must reset themselves)
 # ---------------------------------------------------------------------------
-def test_decode_bitwise_deterministic():
-    li = synth.make_linear(4096, 4096, 80, 1, cfg=1)
+@pytest.mark.parametrize("T,kernel", [(1, "decode"), (1, "mma"), (16, "mma"), (64, "mma")])
+def test_decode_bitwise_deterministic(T, kernel):
+    li = synth.make_linear(4096, 4096, 80, T, cfg=1)
     x, paths, _ = U.to_device(li)
-    ws = lb.alloc_workspace(1, 4096, 4096, 80)
+    ws = lb.alloc_workspace(T, 4096, 4096, 80)
     ys = []
     for _ in range(20):
-        ys.append(lb.lb_linear_forward(x, paths, 80, workspace=ws).clone())
+        ys.append(lb.lb_linear_forward(x, paths, 80, workspace=ws, kernel=KERNELS[kernel]).clone())
     torch.cuda.synchronize()
     for y in ys[1:]:
         assert torch.equal(y.view(torch.int16), ys[0].view(torch.int16))
@@ -313,7 +330,7 @@ def test_back_to_back_launches_stress():
         assert err <= U.TOL_BF16_ROW_INF, err
 
 
-@pytest.mark.parametrize("T,kernel", [(1, "decode"), (4, "decode"), (100, "prefill")])
+@pytest.mark.parametrize("T,kernel", [(1, "decode"), (4, "decode"), (16, "mma"), (100, "prefill")])
 def test_graph_replays_match_eager(T, kernel):
     """Launches captured in a HIP graph: every replay (with eager work and syncs in
     between) must reproduce the eager result."""
@@ -333,7 +350,7 @@ def test_graph_replays_match_eager(T, kernel):
         # eager work on the same workspace between replays
         y_mid = lb.lb_linear_forward(x, paths, 64, workspace=ws, kernel=KERNELS[kernel])
         torch.cuda.synchronize()
-        if kernel == "decode":
+        if kernel in ("decode", "mma"):
             assert torch.equal(y_graph.view(torch.int16), y_eager.view(torch.int16)), rep
             assert torch.equal(y_mid.view(torch.int16), y_eager.view(torch.int16)), rep
         else:
