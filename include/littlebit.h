@@ -74,8 +74,8 @@ typedef enum lb_role { LB_ROLE_U = 0, LB_ROLE_V = 1 } lb_role;
 
 /* Which forward kernel lb_linear_forward_kernel() runs. */
 typedef enum lb_kernel {
-  LB_KERNEL_AUTO = 0,         /* DECODE for T <= lb_decode_max_tokens(), DECODE_MFMA for T <= 64,
-                                 PREFILL above (each where its rank limit allows) */
+  LB_KERNEL_AUTO = 0,         /* DECODE for T <= 2, DECODE_MFMA for T <= 64, PREFILL above (each
+                                 where its rank limit allows) */
   LB_KERNEL_DECODE = 1,       /* single launch, 4-bit look-up tables, fp32 sign-flip accumulation;
                                  T <= 4, r <= 1024 */
   LB_KERNEL_PREFILL = 2,      /* two launches of matrix-core (MFMA) tiles, signs expanded to bf16 +-1;
@@ -144,7 +144,7 @@ size_t lb_forward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_
 /* Zero-fill a workspace of `bytes` bytes on `stream`. */
 lb_status lb_workspace_init(void* workspace, size_t bytes, hipStream_t stream);
 
-/* Largest token count the automatic dispatch sends to the decode kernel. */
+/* Largest token count LB_KERNEL_DECODE accepts. */
 int64_t lb_decode_max_tokens(void);
 
 /* Forward of one LittleBit linear layer with both paths (Proposition 1,

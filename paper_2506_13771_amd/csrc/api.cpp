@@ -68,6 +68,7 @@ lb::ForwardArgs make_args(const void* x, lb_dtype act, int64_t T, int64_t d_in, 
 }
 
 bool decode_supports(int64_t T, int64_t r) { return T <= lb::kDecodeMaxTokens && r <= lb::kDecodeMaxRank; }
+constexpr int64_t kAutoLutTokens = 2;  // AUTO sends T <= this to the look-up-table decode kernel
 
 }  // namespace
 
@@ -145,7 +146,7 @@ size_t lb_forward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_
     const lb::DecodeGeom g = lb::decode_geometry(iT, ii, io, ir);
     if (g.ws_bytes > need) need = g.ws_bytes;
   }
-  if (lb::decode_mma_supports(T, r)) {
+  if (lb::decode_mma_supports(T, d_in, d_out, r)) {
     // the geometry depends on the activation dtype: cover all of them
     for (int dt : {lb::kDtF32, lb::kDtF16, lb::kDtBF16}) {
       const lb::MmaGeom g = lb::decode_mma_geometry(iT, ii, io, ir, dt);
@@ -174,7 +175,7 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
   lb_status st = check_sizes(T, d_in, d_out, r);
   if (st != LB_OK) return st;
   if (kernel == LB_KERNEL_DECODE && !decode_supports(T, r)) return LB_ERR_SHAPE;
-  if (kernel == LB_KERNEL_DECODE_MFMA && !lb::decode_mma_supports(T, r)) return LB_ERR_SHAPE;
+  if (kernel == LB_KERNEL_DECODE_MFMA && !lb::decode_mma_supports(T, d_in, d_out, r)) return LB_ERR_SHAPE;
   if (T == 0 || d_out == 0) return LB_OK;
   if (!y || (d_in > 0 && !x)) return LB_ERR_NULL;
   if (!aligned(x, dtype_size(act_dtype)) || !aligned(y, dtype_size(act_dtype))) return LB_ERR_ALIGN;
@@ -192,9 +193,11 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
     return e == hipSuccess ? LB_OK : LB_ERR_HIP;
   }
   if (kernel == LB_KERNEL_AUTO) {
-    if (decode_supports(T, r))
+    // the look-up-table kernel is the fastest for one or two tokens; from
+    // three on the matrix-core decode kernel takes over
+    if (T <= kAutoLutTokens && decode_supports(T, r))
       kernel = LB_KERNEL_DECODE;
-    else if (lb::decode_mma_supports(T, r))
+    else if (lb::decode_mma_supports(T, d_in, d_out, r))
       kernel = LB_KERNEL_DECODE_MFMA;
     else
       kernel = LB_KERNEL_PREFILL;

@@ -5,18 +5,18 @@
 // Stage 1 (z_p = V_p^T (g_p (.) x), scaled by l_p):
 //   D[k][t] = sum_j (s(V_p[j][k]) g_p[j]) x[t][j]
 //   A operand (16 latents x 32 inputs): the packed sign bits of V_p XORed into
-//     the sign bits of bf16 terms of g_p.  g_p is split into terms whose sum is
+//     the sign bits of bf16 terms of g_p.  g_p is cut into terms whose sum is
 //     exactly g_p (1 for bf16, 2 for f16, 3 for fp32 scales), so every A value
 //     is an exact signed term of g_p.
-//   B operand (32 inputs x 16 tokens): x, also split into exact bf16 terms
-//     (1 for bf16, 2 for f16, 3 for fp32 activations).
+//   B operand (32 inputs x 16 tokens): x, cut the same way into exact bf16
+//     terms (1 for bf16, 2 for f16, 3 for fp32 activations).
 //   Every product of two bf16 terms is exact in fp32 and the matrix cores
-//   accumulate in fp32, so the contraction equals the fp32 sum of the exact
+//   accumulate in fp32, so the contraction is an fp32 sum of the exact
 //   products s * g * x.
 // Stage 2 (y = sum_p h_p (.) U_p w_p, w_p = l_p (.) z_p):
 //   D[i][t] = sum_k s(U_p[i][k]) w_p[t][k]
-//   A operand: U_p's sign bits as bf16 +-1; B operand: w_p split into bf16
-//   terms (2 for 16-bit outputs, 3 for fp32 outputs).
+//   A operand: U_p's sign bits as bf16 +-1; B operand: w_p as a sum of bf16
+//   terms (2, i.e. 16 significant bits, for 16-bit outputs; 3 for fp32).
 //
 // Fragment layout: for the 16x16x32 shape, lane l holds row l % 16 of A (and
 // column l % 16 of B) at 8 reduction slots; register v of lane group
@@ -26,14 +26,20 @@
 // high half with one shift and one mask.  The output lane holds rows
 // 4 gq + e (e < 4) of column l % 16.
 //
+// Loads are buffer loads: a read past the end of a buffer returns zero, so
+// operands of absent tokens, latents and blocks need no address clamping or
+// masking (only the inputs past d_in inside a row of x are masked, in the one
+// tail block).
+//
 // Launch structure (as in the look-up-table decode kernel): stage-1
 // workgroups (lowest block ids; one path, one tile of 16 latents, one run of
 // d_in; the 4 waves split the run and are summed in LDS in a fixed order)
-// publish l (.) z as tagged 64-bit slots; stage-2 workgroups (rows of U)
-// prefetch their U words and h, gather the slots until every tag is this
-// call's, and contract.  With many runs, the highest run of each tile first
-// adds the others ("two-level").  Waits only target lower block ids and are
-// bounded; the epoch / done-counter protocol is the same.
+// publish l (.) z as tagged 64-bit slots; stage-2 workgroups (16 rows of U
+// per wave) prefetch their U words and h, gather the slots of both paths
+// until every tag is this call's, and contract.  With many partials, the
+// highest run of each tile first adds the others ("two-level").  Waits only
+// target lower block ids and are bounded; the epoch / done-counter protocol
+// is the same.
 #include <atomic>
 
 #include "device_common.h"
@@ -44,27 +50,26 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-// floats rounded up to a multiple of 4 (16-byte alignment of what follows)
-__host__ __device__ constexpr int align4(int n) { return (n + 3) & ~3; }
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kMaxRuns = 32;         // d_in runs per latent tile (partials per z value)
-constexpr int kMaxUWords = kMmaMaxRank / 32;  // stage 2: U words per row and path held in registers
-constexpr int kSlotsPerRound = 8;    // stage 2: slots a thread gathers per round
-constexpr int kDirectMax = 512;      // stage 2 reads every partial when s1d * r <= this
+constexpr int kMaxRuns = 32;                  // d_in runs per latent tile (partials per z value)
+constexpr int kMaxUWords = kMmaMaxRank / 32;  // stage 2: full U words of one row and path in registers
+constexpr int kGather = 8;                    // stage 2: slots a thread gathers per round
+constexpr int kDirectMaxSlots = 8192;         // stage 2 reads every partial when there are at most this many
+constexpr uint32_t kOob = 0x7ffffff0u;        // a buffer offset past every buffer: loads return 0
 
-// exact bf16 terms per dtype
+// exact bf16 terms of a value stored in dtype DT
 template <int DT>
 __host__ __device__ constexpr int nterms() {
   return DT == kDtF32 ? 3 : (DT == kDtF16 ? 2 : 1);
 }
-// K-steps (32-wide input blocks) a stage-1 wave holds in registers per round
-template <int TT, int ACT>
-__host__ __device__ constexpr int kpw_max() {
-  return (TT == 1 ? 8 : (TT == 2 ? 6 : 4)) / (ACT == kDtF32 ? 2 : 1);
+// 32-wide input blocks a stage-1 wave holds in registers per round
+__host__ __device__ constexpr int kpw_of(int tt, int act) {
+  return (tt == 1 ? 8 : (tt == 2 ? 6 : 4)) / (act == kDtF32 ? 2 : 1);
 }
 
 struct MmaParams {
@@ -86,19 +91,67 @@ struct MmaParams {
   int n_s2;    // stage-2 workgroups
   int direct;  // stage 2 reads every run's partial (else the two-level sums)
   int vec;     // x and g may be read as aligned 4-element vectors
+  uint32_t x_bytes, g_bytes, v_bytes, u_bytes, h_bytes, l_bytes;
+  uint32_t magic_r;  // ceil(2^32 / r) (0 for r = 1): e / r as one multiply-high
 };
 
-// split v into N bf16 terms (round-to-nearest-even each); their sum is v for
-// the term counts used here (nterms of v's storage dtype)
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0), static_cast<int>(bytes),
+                                           0x00020000);
+}
+// raw bits of element i (dtype DT) of a buffer; 0 past its end
+template <int DT>
+__device__ __forceinline__ uint32_t bload(rsrc_t r, uint32_t i, bool valid = true) {
+  if constexpr (DT == kDtF32)
+    return __builtin_amdgcn_raw_buffer_load_b32(r, valid ? i * 4u : kOob, 0, 0);
+  else
+    return static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, valid ? i * 2u : kOob, 0, 0));
+}
+// raw bits of elements i..i+3: one 16- or 8-byte load (VEC: i a multiple of 4,
+// buffer aligned), else four element loads; taken back with raw4_elem
+template <int DT, bool VEC>
+__device__ __forceinline__ void bload4(rsrc_t r, uint32_t i, bool valid, uint32_t (&o)[4]) {
+  if constexpr (VEC && DT == kDtF32) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, valid ? i * 4u : kOob, 0, 0);
+    o[0] = v[0], o[1] = v[1], o[2] = v[2], o[3] = v[3];
+  } else if constexpr (VEC) {
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, valid ? i * 2u : kOob, 0, 0);
+    o[0] = v[0], o[1] = v[1], o[2] = 0u, o[3] = 0u;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = bload<DT>(r, i + e, valid);
+  }
+}
+// 16-bit element v of a bload4 group, raw bits
+template <bool VEC>
+__device__ __forceinline__ uint32_t raw16(const uint32_t (&o)[4], int v) {
+  return VEC ? (o[v >> 1] >> (16 * (v & 1))) & 0xffffu : o[v];
+}
+
+// v as N bf16 terms (bit patterns), each the leading 8 significant bits of
+// what the previous terms left: exact when v has at most 8N significant bits
+// (a bf16, f16 or fp32 value with N = its nterms)
 template <int N>
-__device__ __forceinline__ void split_terms(float v, uint32_t (&o)[N]) {
+__device__ __forceinline__ void split_exact(float v, uint32_t (&o)[N]) {
   float rem = v;
 #pragma unroll
   for (int s = 0; s < N; ++s) {
-    const uint32_t b = f32_to_bf16_bits(rem);
-    o[s] = b;
-    rem = rem - bf16_bits_to_f32(b);
+    const uint32_t b = __float_as_uint(rem) & 0xffff0000u;
+    o[s] = b >> 16;
+    rem = rem - __uint_as_float(b);
   }
+}
+// v (any fp32) as N bf16 terms: leading bits, the last term rounded to nearest
+template <int N>
+__device__ __forceinline__ void split_round(float v, uint32_t (&o)[N]) {
+  float rem = v;
+#pragma unroll
+  for (int s = 0; s < N - 1; ++s) {
+    const uint32_t b = __float_as_uint(rem) & 0xffff0000u;
+    o[s] = b >> 16;
+    rem = rem - __uint_as_float(b);
+  }
+  o[N - 1] = f32_to_bf16_bits(rem);
 }
 
 __device__ __forceinline__ floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
@@ -106,18 +159,21 @@ __device__ __forceinline__ floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
                                                  0, 0);
 }
 
-// raw bits of 4 consecutive elements starting at i (element e < nvalid, else p[0])
-template <int DT, bool VEC>
-__device__ __forceinline__ void ld4(const void* p, int64_t i, int nvalid, uint32_t (&o)[4]) {
-  ld4_bits<DT, VEC>(p, nvalid > 0 ? i : 0, nvalid, o);
+// signs of a packed word (this lane group's nibbles) on bf16 term pairs t[v]:
+// the low half takes the sign of bit 4gq+v, the high half of bit 4gq+v+16
+__device__ __forceinline__ u32x4 sign_terms(uint32_t word, int gq, const uint32_t (&t)[4]) {
+  const uint32_t ws = word >> (4 * gq);
+  u32x4 a;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) a[v] = ((ws << (15 - v)) & 0x80008000u) ^ t[v];
+  return a;
 }
 
 // ---------------------------------------------------------------------------
 // stage 1
 // ---------------------------------------------------------------------------
-// One K-step's loads (raw bits): the packed word of this lane's latent (full
-// blocks; the tail block's word is loaded once per round), and x, g at the 8
-// inputs of this lane's slots (runs h = 0, 1 of 4 inputs).
+// One 32-wide block's loads (raw bits): the packed word of this lane's latent,
+// and x, g at the 8 inputs of this lane's slots (runs h = 0, 1 of 4 inputs).
 template <int TT>
 struct S1Loads {
   uint32_t w;
@@ -125,74 +181,74 @@ struct S1Loads {
   uint32_t x[TT][2][4];
 };
 
+struct S1Ctx {
+  rsrc_t vr, gr, xr;
+  int ka;  // this lane's latent (A row)
+  int gq, n16;
+  int d_in, r;
+};
+
+// Loads of full block b (valid; else every load reads past the buffers: zeros).
 template <int TT, int ACT, int SC, bool VEC>
-__device__ __forceinline__ void s1_issue(const MmaParams& P, const uint32_t* Vw, const void* gp, int b, bool bvalid,
-                                         int k, bool kvalid, int gq, int n16, S1Loads<TT>& L) {
-  const int d_in = P.d_in, r = P.r;
-  const int nbv = d_in >> 5, tailv = d_in & 31;
-  const bool full = bvalid && b < nbv;
-  L.w = full_words_or(Vw, nbv, P.ctrl)[full && kvalid ? static_cast<int64_t>(b) * r + k : 0];
-  (void)tailv;
+__device__ __forceinline__ void s1_issue(const S1Ctx& C, int b, bool valid, S1Loads<TT>& L) {
+  L.w = __builtin_amdgcn_raw_buffer_load_b32(C.vr, valid ? static_cast<uint32_t>(b * C.r + C.ka) * 4u : kOob, 0, 0);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const int j0 = 32 * b + 4 * gq + 16 * h;
-    const int nv = bvalid ? min(4, max(0, d_in - j0)) : 0;
-    ld4<SC, VEC>(gp, j0, nv, L.g[h]);
+    const uint32_t j0 = 32 * b + 4 * C.gq + 16 * h;
+    bload4<SC, VEC>(C.gr, j0, valid, L.g[h]);
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
-      const int t = min(16 * tt + n16, P.T - 1);  // columns past T are computed and dropped
-      ld4<ACT, VEC>(P.x, static_cast<int64_t>(t) * d_in + j0, nv, L.x[tt][h]);
-    }
+    for (int tt = 0; tt < TT; ++tt)
+      bload4<ACT, VEC>(C.xr, static_cast<uint32_t>(16 * tt + C.n16) * C.d_in + j0, valid, L.x[tt][h]);
   }
 }
 
-template <int TT, int ACT, int SC, bool VEC>
-__device__ __forceinline__ void s1_compute(const MmaParams& P, int b, bool bvalid, int gq, const S1Loads<TT>& L,
-                                           uint32_t tailword, floatx4 (&acc)[TT]) {
+// the tail block's packed word of latent ka (from the tail plane)
+__device__ __forceinline__ uint32_t s1_tail_word(const S1Ctx& C, bool valid) {
+  const int nbv = C.d_in >> 5, tailv = C.d_in & 31;
+  const uint32_t plane = 4u * nbv * C.r;
+  const uint32_t off = tailv <= 16 ? plane + 2u * C.ka : plane + 4u * C.ka;
+  const uint32_t lo = static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(C.vr, valid ? off : kOob, 0, 0));
+  const uint32_t hi =
+      static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(C.vr, valid && tailv > 16 ? off + 2 : kOob, 0, 0));
+  return lo | (hi << 16);
+}
+
+// MASK: the tail block; inputs j >= d_in of x are zeroed (g reads zero there)
+template <int TT, int ACT, int SC, bool VEC, bool MASK>
+__device__ __forceinline__ void s1_compute(const S1Ctx& C, int b, uint32_t word, const S1Loads<TT>& L,
+                                           floatx4 (&acc)[TT]) {
   constexpr int NG = nterms<SC>(), NX = nterms<ACT>();
-  const int d_in = P.d_in;
-  const int nbv = d_in >> 5;
-  const uint32_t word = b < nbv ? L.w : tailword;
-  const uint32_t ws = word >> (4 * gq);
-  // g terms paired per register: low half input 4gq+v, high half 4gq+v+16
-  uint32_t gt[NG][4];
+  u32x4 A[NG];  // signs on the g terms
+  {
+    uint32_t gt[NG][4];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    uint32_t lo[NG], hi[NG];
-    const int j = 32 * b + 4 * gq + v;
-    const bool ok0 = bvalid && j < d_in, ok1 = bvalid && j + 16 < d_in;
-    split_terms<NG>(ok0 ? raw4_elem<SC, VEC>(L.g[0], v) : 0.0f, lo);
-    split_terms<NG>(ok1 ? raw4_elem<SC, VEC>(L.g[1], v) : 0.0f, hi);
+    for (int v = 0; v < 4; ++v) {
+      if constexpr (NG == 1) {
+        gt[0][v] = raw16<VEC>(L.g[0], v) | (raw16<VEC>(L.g[1], v) << 16);
+      } else {
+        uint32_t lo[NG], hi[NG];
+        split_exact<NG>(raw4_elem<SC, VEC>(L.g[0], v), lo);
+        split_exact<NG>(raw4_elem<SC, VEC>(L.g[1], v), hi);
 #pragma unroll
-    for (int s = 0; s < NG; ++s) gt[s][v] = lo[s] | (hi[s] << 16);
+        for (int s = 0; s < NG; ++s) gt[s][v] = lo[s] | (hi[s] << 16);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < NG; ++s) A[s] = sign_terms(word, C.gq, gt[s]);
   }
-  u32x4 A[NG];
-#pragma unroll
-  for (int s = 0; s < NG; ++s)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) A[s][v] = ((ws << (15 - v)) & 0x80008000u) ^ gt[s][v];
 #pragma unroll
   for (int tt = 0; tt < TT; ++tt) {
     u32x4 X[NX];
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int j = 32 * b + 4 * gq + v;
-      const bool ok0 = bvalid && j < d_in, ok1 = bvalid && j + 16 < d_in;
+      const int j = 32 * b + 4 * C.gq + v;
+      const bool ok0 = !MASK || j < C.d_in, ok1 = !MASK || j + 16 < C.d_in;
       if constexpr (NX == 1) {
-        // bf16 activations: the raw bits are the term (zeroed beyond d_in)
-        uint32_t a0, a1;
-        if constexpr (VEC) {
-          a0 = (L.x[tt][0][v >> 1] >> (16 * (v & 1))) & 0xffffu;
-          a1 = (L.x[tt][1][v >> 1] >> (16 * (v & 1))) & 0xffffu;
-        } else {
-          a0 = L.x[tt][0][v];
-          a1 = L.x[tt][1][v];
-        }
-        X[0][v] = (ok0 ? a0 : 0u) | ((ok1 ? a1 : 0u) << 16);
+        X[0][v] = (ok0 ? raw16<VEC>(L.x[tt][0], v) : 0u) | ((ok1 ? raw16<VEC>(L.x[tt][1], v) : 0u) << 16);
       } else {
         uint32_t lo[NX], hi[NX];
-        split_terms<NX>(ok0 ? raw4_elem<ACT, VEC>(L.x[tt][0], v) : 0.0f, lo);
-        split_terms<NX>(ok1 ? raw4_elem<ACT, VEC>(L.x[tt][1], v) : 0.0f, hi);
+        split_exact<NX>(ok0 ? raw4_elem<ACT, VEC>(L.x[tt][0], v) : 0.0f, lo);
+        split_exact<NX>(ok1 ? raw4_elem<ACT, VEC>(L.x[tt][1], v) : 0.0f, hi);
 #pragma unroll
         for (int a = 0; a < NX; ++a) X[a][v] = lo[a] | (hi[a] << 16);
       }
@@ -206,7 +262,7 @@ __device__ __forceinline__ void s1_compute(const MmaParams& P, int b, bool bvali
 
 template <int TT, int ACT, int SC, bool VEC>
 __device__ __forceinline__ void mma_stage1(const MmaParams& P, int wg, float* smem) {
-  constexpr int KPW = kpw_max<TT, ACT>();
+  constexpr int KPW = kpw_of(TT, ACT);
   const int per_path = P.nmf * P.s1d;
   const int p = wg / per_path;
   const int rem = wg - p * per_path;
@@ -215,50 +271,53 @@ __device__ __forceinline__ void mma_stage1(const MmaParams& P, int wg, float* sm
   const int T = P.T, r = P.r;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int n16 = lane & 15, gq = lane >> 4;
   const int k0 = 16 * mf;
-  const int nbt = nblocks32(P.d_in);
+  const int nbt = nblocks32(P.d_in), nbv = P.d_in >> 5;
   const int b0 = c * P.bpr;
   const int b1 = min(nbt, b0 + P.bpr);
-  const uint32_t* Vw = static_cast<const uint32_t*>(p ? P.V[1] : P.V[0]);
-  const void* gp = p ? P.g[1] : P.g[0];
-  const void* lp = p ? P.l[1] : P.l[0];
+  const int bf = min(b1, nbv);  // end of this run's full blocks
+  S1Ctx C;
+  C.vr = make_rsrc(p ? P.V[1] : P.V[0], P.v_bytes);
+  C.gr = make_rsrc(p ? P.g[1] : P.g[0], P.g_bytes);
+  C.xr = make_rsrc(P.x, P.x_bytes);
+  C.ka = k0 + (lane & 15);
+  C.gq = lane >> 4;
+  C.n16 = lane & 15;
+  C.d_in = P.d_in;
+  C.r = r;
 
-  // A-operand lane: latent k0 + n16 (its packed words); output lane: latents
-  // k0 + 4gq + e of token column n16
-  const int ka = k0 + n16;
-  const bool ka_ok = ka < r;
   floatx4 acc[TT];
 #pragma unroll
   for (int tt = 0; tt < TT; ++tt) acc[tt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // latent scales of the output lane, and the epoch (both used at the end)
+  // the tail block (if this run holds it: it is then block b1 - 1 = nbv) goes
+  // to wave 0; its loads are issued with the first round's
+  const bool tail = b1 > nbv && wave == 0;
+  S1Loads<TT> LT;
+  {
+    // x and g of the tail block, read as element loads past d_in give zero
+    // for g; x is masked in s1_compute
+    S1Ctx CT = C;
+    s1_issue<TT, ACT, SC, false>(CT, nbv, tail, LT);
+  }
+  const uint32_t tword = s1_tail_word(C, tail);
+  // latent scales of the output lane (latents k0 + 4gq + e), and the epoch
+  const rsrc_t lr = make_rsrc(p ? P.l[1] : P.l[0], P.l_bytes);
   uint32_t lbits[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) lbits[e] = ld_bits<SC>(lp, min(k0 + 4 * gq + e, r - 1));
+  for (int e = 0; e < 4; ++e) lbits[e] = bload<SC>(lr, k0 + 4 * C.gq + e);
   uint32_t epoch = load_epoch<3>(P.ctrl);
 
-  // the run's blocks, split over the waves in rounds of KPW blocks per wave
-  const int nbv = P.d_in >> 5, tailv = P.d_in & 31;
-  for (int rb = b0; rb < b1; rb += kWaves * KPW) {
-    const int wb = rb + wave * KPW;  // this wave's first block of the round
+  // full blocks, in rounds of KPW blocks per wave
+  for (int rb = b0; rb < bf; rb += kWaves * KPW) {
+    const int wb = rb + wave * KPW;
     S1Loads<TT> L[KPW];
 #pragma unroll
-    for (int u = 0; u < KPW; ++u) {
-      const int b = wb + u;
-      const bool bvalid = b < b1;
-      s1_issue<TT, ACT, SC, VEC>(P, Vw, gp, bvalid ? b : b0, bvalid, ka, ka_ok, gq, n16, L[u]);
-    }
-    // the tail block's word (if the tail block is among this wave's blocks)
-    uint32_t tlo, thi;
-    ld_tail_bits(Vw, nbv, r, tailv, ka, ka_ok && nbv >= wb && nbv < wb + KPW && nbv < b1, tlo, thi);
-    const uint32_t tailword = tail_word(tlo, thi, tailv);
+    for (int u = 0; u < KPW; ++u) s1_issue<TT, ACT, SC, VEC>(C, wb + u, wb + u < bf, L[u]);
 #pragma unroll
-    for (int u = 0; u < KPW; ++u) {
-      const int b = wb + u;
-      s1_compute<TT, ACT, SC, VEC>(P, b < b1 ? b : b0, b < b1, gq, L[u], tailword, acc);
-    }
+    for (int u = 0; u < KPW; ++u) s1_compute<TT, ACT, SC, VEC, false>(C, wb + u, L[u].w, L[u], acc);
   }
+  if (tail) s1_compute<TT, ACT, SC, false, true>(C, nbv, tword, LT, acc);
 
   // fixed-order sum over the 4 waves through LDS
   floatx4* red = reinterpret_cast<floatx4*>(smem);  // [wave][tt][lane]
@@ -269,16 +328,19 @@ __device__ __forceinline__ void mma_stage1(const MmaParams& P, int wg, float* sm
     const int tt = wave;
     const floatx4 a0 = red[(0 * TT + tt) * 64 + lane], a1 = red[(1 * TT + tt) * 64 + lane];
     const floatx4 a2 = red[(2 * TT + tt) * 64 + lane], a3 = red[(3 * TT + tt) * 64 + lane];
-    const int t = 16 * tt + n16;
+    const int t = 16 * tt + C.n16;
     pin(epoch);
     const uint32_t tag = epoch + 1u;
     const bool reducer = !P.direct && c == P.s1d - 1;
-    bool ok = true;
+    float sv[4];
 #pragma unroll
+    for (int e = 0; e < 4; ++e) sv[e] = ((a0[e] + a1[e]) + (a2[e] + a3[e])) * bits_to_f32<SC>(lbits[e]);
+    bool ok = true;
+#pragma unroll 1
     for (int e = 0; e < 4; ++e) {
-      const int k = k0 + 4 * gq + e;
+      const int k = k0 + 4 * C.gq + e;
+      const float s = e == 0 ? sv[0] : (e == 1 ? sv[1] : (e == 2 ? sv[2] : sv[3]));
       if (t < T && k < r) {
-        const float s = ((a0[e] + a1[e]) + (a2[e] + a3[e])) * bits_to_f32<SC>(lbits[e]);
         uint64_t* pt = P.partial + (static_cast<int64_t>(p) * T + t) * P.s1d * r + k;
         if (!reducer) {
           put_slot(pt + static_cast<int64_t>(c) * r, tag, s);
@@ -297,7 +359,11 @@ __device__ __forceinline__ void mma_stage1(const MmaParams& P, int wg, float* sm
 // ---------------------------------------------------------------------------
 // stage 2
 // ---------------------------------------------------------------------------
-template <int TT, int ACT, int SC>
+// q = n / d for n < 2^20, 2 <= d < 2^12, with m = ceil(2^32 / d); m = 0 stands
+// for d = 1
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t m) { return m == 0 ? n : __umulhi(n, m); }
+
+template <int ACT, int SC>
 __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* smem) {
   constexpr int NW = ACT == kDtF32 ? 3 : 2;  // bf16 terms of w
   const int T = P.T, r = P.r, d_out = P.d_out;
@@ -307,62 +373,85 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
   const int nkb = nblocks32(r);
   const int nbu = r >> 5, tailu = r & 31;
   const int nsrc = P.direct ? P.s1d : 1;
-  const int row0 = (q * kWaves + wave) * 16;  // this wave's 16 rows
+  const int tch = min(16, T);  // tokens per chunk
+  const int R32 = 32 * nkb;    // row stride of the summed w (zero past r)
+  const int qrow0 = q * kWaves * 16;
 
-  // prefetch, raw: the U words of this lane's A row (row0 + n16) and the row
-  // scales of its output rows (row0 + 4 gq + e), both paths; then the epoch
-  uint32_t uw[2][kMaxUWords];
-  uint32_t ut_lo[2], ut_hi[2];
-  uint32_t hb[2][4];
-  const int ia = row0 + n16;
-  const bool aok = ia < d_out;
+  // LDS: U words [2][nkb][64 rows] (block nbu holds the tail word), summed w
+  // [2][tch][R32], and (when there are several partials per value) the
+  // gathered partials [2][tch][nsrc][r]
+  uint32_t* uwl = reinterpret_cast<uint32_t*>(smem);
+  float* wsum = smem + 2 * nkb * 64;
+  float* raw = wsum + 2 * tch * R32;
+
+  // prefetch (cooperative, raw): the U words of this workgroup's 64 rows, and
+  // the row scales of this lane's output rows; then the epoch
+  constexpr int kUPer = (kMaxUWords + 1) * 64 / kThreads + 1;  // entries per thread and path
+  uint32_t ulo[2][kUPer], uhi[2][kUPer];
 #pragma unroll
   for (int pp = 0; pp < 2; ++pp) {
-    const uint32_t* Uw = static_cast<const uint32_t*>(pp ? P.U[1] : P.U[0]);
-    const void* hp = pp ? P.h[1] : P.h[0];
+    const rsrc_t ur = make_rsrc(pp ? P.U[1] : P.U[0], P.u_bytes);
 #pragma unroll
-    for (int kb = 0; kb < kMaxUWords; ++kb) {
-      const bool ok = aok && kb < nbu;
-      uw[pp][kb] = full_words_or(Uw, nbu, P.ctrl)[ok ? static_cast<int64_t>(kb) * d_out + ia : 0];
+    for (int j = 0; j < kUPer; ++j) {
+      const int e = tid + kThreads * j;  // (kb, row) = (e >> 6, e & 63)
+      const int kb = e >> 6, row = qrow0 + (e & 63);
+      const bool full = kb < nbu, tl = kb == nbu && tailu != 0;
+      const uint32_t plane = 4u * nbu * d_out;
+      const uint32_t toff = tailu <= 16 ? plane + 2u * row : plane + 4u * row;
+      // full word as two halves (so both cases are the same two 16-bit loads)
+      const uint32_t off = full ? static_cast<uint32_t>(kb * d_out + row) * 4u : (tl ? toff : kOob);
+      ulo[pp][j] = static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(ur, off, 0, 0));
+      uhi[pp][j] = static_cast<uint16_t>(
+          __builtin_amdgcn_raw_buffer_load_b16(ur, full || (tl && tailu > 16) ? off + 2 : kOob, 0, 0));
     }
-    ld_tail_bits(Uw, nbu, d_out, tailu, ia, aok, ut_lo[pp], ut_hi[pp]);
+  }
+  uint32_t hb[2][4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) hb[pp][e] = ld_bits<SC>(hp, min(row0 + 4 * gq + e, d_out - 1));
+  for (int pp = 0; pp < 2; ++pp) {
+    const rsrc_t hr = make_rsrc(pp ? P.h[1] : P.h[0], P.h_bytes);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) hb[pp][e] = bload<SC>(hr, qrow0 + wave * 16 + 4 * gq + e);
   }
   uint32_t epoch = load_epoch<4>(P.ctrl);
-  pin(epoch);  // waits for the epoch only (the prefetch loads were issued before it... or after)
+  pin(epoch);
   const uint32_t tag = epoch + 1u;
   // count this workgroup as one that has read the epoch (used at the end)
   uint32_t done_before = 0u;
   if (tid == 0) done_before = atomic_add_relaxed(P.ctrl + kCtrlDone, 1u);
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+    for (int j = 0; j < kUPer; ++j) {
+      const int e = tid + kThreads * j;
+      if (e < nkb * 64) uwl[pp * nkb * 64 + e] = ulo[pp][j] | (uhi[pp][j] << 16);
+    }
 
-  float* raw = smem;                                                        // [16][nsrc][r] slot values
-  u32x4* frag = reinterpret_cast<u32x4*>(smem + align4(16 * nsrc * r));     // [nkb][NW][64 lanes]
   bool ok = true;
   for (int t0 = 0; t0 < T; t0 += 16) {
     const int tn = min(16, T - t0);
-    floatx4 acc[2];
-    acc[0] = acc[1] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // zero the latents past r of every summed row
+    for (int e = tid; e < 2 * tch * (R32 - r); e += kThreads) {
+      const int row = e / (R32 - r);
+      wsum[row * R32 + r + (e - row * (R32 - r))] = 0.0f;
+    }
+    // gather both paths' slots of tokens t0..t0+tn-1 (contiguous per path):
+    // rounds of loads, then re-reads of any slot whose tag is not this call's
+    const int n1 = tn * nsrc * r;
 #pragma unroll
     for (int pp = 0; pp < 2; ++pp) {
-      // gather this path's slots for tokens t0..t0+tn-1: contiguous
-      // [tn][nsrc][r]; loads in rounds, re-reads of any slot whose tag is not
-      // yet this call's
-      const int n = tn * nsrc * r;
       const uint64_t* src = P.direct ? P.partial + (static_cast<int64_t>(pp) * T + t0) * nsrc * r
                                      : P.wbuf + (static_cast<int64_t>(pp) * T + t0) * r;
-      for (int e0 = 0; e0 < n; e0 += kThreads * kSlotsPerRound) {
-        uint64_t sv[kSlotsPerRound];
+      for (int e0 = 0; e0 < n1; e0 += kThreads * kGather) {
+        uint64_t sv[kGather];
 #pragma unroll
-        for (int j = 0; j < kSlotsPerRound; ++j) {
+        for (int j = 0; j < kGather; ++j) {
           const int e = e0 + tid + kThreads * j;
-          sv[j] = get_slot(src + (e < n ? e : 0));
+          sv[j] = get_slot(src + (e < n1 ? e : 0));
         }
         for (uint32_t it = 0;; ++it) {
           bool ready = true;
 #pragma unroll
-          for (int j = 0; j < kSlotsPerRound; ++j)
-            ready = ready && (e0 + tid + kThreads * j >= n || slot_ready(sv[j], tag));
+          for (int j = 0; j < kGather; ++j) ready = ready && (e0 + tid + kThreads * j >= n1 || slot_ready(sv[j], tag));
           if (ready) break;
           if (it >= kSpinLimit) {
             ok = false;
@@ -370,69 +459,79 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
           }
           __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-          for (int j = 0; j < kSlotsPerRound; ++j) {
+          for (int j = 0; j < kGather; ++j) {
             const int e = e0 + tid + kThreads * j;
-            if (e < n && !slot_ready(sv[j], tag)) sv[j] = get_slot(src + e);
+            if (e < n1 && !slot_ready(sv[j], tag)) sv[j] = get_slot(src + e);
           }
         }
 #pragma unroll
-        for (int j = 0; j < kSlotsPerRound; ++j) {
+        for (int j = 0; j < kGather; ++j) {
           const int e = e0 + tid + kThreads * j;
-          if (e < n) raw[e] = slot_value(sv[j]);
+          if (e < n1) {
+            if (nsrc > 1) {
+              raw[pp * tch * nsrc * r + e] = slot_value(sv[j]);
+            } else {
+              const int tl = static_cast<int>(fast_div(e, P.magic_r));
+              wsum[(pp * tch + tl) * R32 + (e - tl * r)] = slot_value(sv[j]);
+            }
+          }
         }
       }
+    }
+    if (nsrc > 1) {
+      // sum each value's partials in ascending run order
       __syncthreads();
-      // B fragments of w_p: item (kb, lane'); its 8 values are latents
-      // 32 kb + 4 gq' + v (+16) of token t0 + n16', the sum of the runs'
-      // partials in ascending order, split into NW bf16 terms
-      for (int item = tid; item < nkb * 64; item += kThreads) {
-        const int kb = item >> 6, il = item & 63;
-        const int tl = il & 15, g4 = il >> 4;
+      for (int e = tid; e < 2 * tn * r; e += kThreads) {
+        const int pt = static_cast<int>(fast_div(e, P.magic_r));  // pp * tn + tl
+        const int k = e - pt * r;
+        const int pp = pt >= tn ? 1 : 0;
+        const int tl = pt - pp * tn;
+        const float* rs = raw + ((pp * tch + tl) * nsrc) * r + k;
+        float s = 0.0f;
+        for (int c = 0; c < nsrc; ++c) s += rs[c * r];
+        wsum[(pp * tch + tl) * R32 + k] = s;
+      }
+    }
+    __syncthreads();
+    // contraction: A = the signs of U row qrow0 + wave * 16 + n16 (+-1), B = w
+    // of token column n16 at latents 32 kb + 4 gq + v (+16), as NW bf16 terms
+    floatx4 acc[2];
+    acc[0] = acc[1] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const uint32_t ones[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) {
+      const float* wrow = wsum + (pp * tch + (n16 < tch ? n16 : 0)) * R32 + 4 * gq;
+      const uint32_t* ucol = uwl + pp * nkb * 64 + wave * 16 + n16;
+      for (int kb = 0; kb < nkb; ++kb) {
+        const u32x4 A = sign_terms(ucol[kb * 64], gq, ones);
+        const float4 w0 = *reinterpret_cast<const float4*>(wrow + 32 * kb);
+        const float4 w1 = *reinterpret_cast<const float4*>(wrow + 32 * kb + 16);
+        const float wl[4] = {w0.x, w0.y, w0.z, w0.w}, wh[4] = {w1.x, w1.y, w1.z, w1.w};
         uint32_t lo[4][NW], hi[4][NW];
 #pragma unroll
-        for (int v = 0; v < 8; ++v) {
-          const int k = 32 * kb + 4 * g4 + (v & 3) + 16 * (v >> 2);
-          float sum = 0.0f;
-          if (tl < tn && k < r)
-            for (int c = 0; c < nsrc; ++c) sum += raw[(tl * nsrc + c) * r + k];
-          if (v < 4)
-            split_terms<NW>(sum, lo[v]);
-          else
-            split_terms<NW>(sum, hi[v - 4]);
+        for (int v = 0; v < 4; ++v) {
+          split_round<NW>(wl[v], lo[v]);
+          split_round<NW>(wh[v], hi[v]);
         }
 #pragma unroll
         for (int a = 0; a < NW; ++a) {
-          u32x4 f;
+          u32x4 B;
 #pragma unroll
-          for (int v = 0; v < 4; ++v) f[v] = lo[v][a] | (hi[v][a] << 16);
-          frag[(kb * NW + a) * 64 + il] = f;
+          for (int v = 0; v < 4; ++v) B[v] = lo[v][a] | (hi[v][a] << 16);
+          acc[pp] = mfma(A, B, acc[pp]);
         }
       }
-      __syncthreads();
-      // contraction with this lane's U row
-      const uint32_t tailword = tail_word(ut_lo[pp], ut_hi[pp], tailu);
-#pragma unroll
-      for (int kb = 0; kb < kMaxUWords + 1; ++kb) {
-        if (kb >= nkb) continue;
-        const uint32_t word = kb < nbu ? uw[pp][kb < kMaxUWords ? kb : 0] : tailword;
-        const uint32_t ws = word >> (4 * gq);
-        u32x4 A;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) A[v] = ((ws << (15 - v)) & 0x80008000u) | 0x3F803F80u;
-#pragma unroll
-        for (int a = 0; a < NW; ++a) acc[pp] = mfma(A, frag[(kb * NW + a) * 64 + lane], acc[pp]);
-      }
-      __syncthreads();
     }
-    // y[t][i] = h_0[i] acc_0 + h_1[i] acc_1 for rows i = row0 + 4 gq + e
+    // y[t][i] = h_0[i] acc_0 + h_1[i] acc_1 for rows i = qrow0 + wave * 16 + 4 gq + e
     const int t = t0 + n16;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int i = row0 + 4 * gq + e;
+      const int i = qrow0 + wave * 16 + 4 * gq + e;
       if (t < T && i < d_out)
         st<ACT>(P.y, static_cast<int64_t>(t) * d_out + i,
                 bits_to_f32<SC>(hb[0][e]) * acc[0][e] + bits_to_f32<SC>(hb[1][e]) * acc[1][e]);
     }
+    __syncthreads();  // the next chunk reuses the LDS
   }
   if (!ok) atomic_store_relaxed(P.ctrl + kCtrlError, 1u);
   // The last stage-2 workgroup to count itself stores the tag as the next
@@ -453,7 +552,7 @@ __global__ void __launch_bounds__(kThreads, 1) decode_mma_kernel(MmaParams P) {
   if (wg < P.n_s1)
     mma_stage1<TT, ACT, SC, VEC>(P, wg, smem);
   else
-    mma_stage2<TT, ACT, SC>(P, wg - P.n_s1, smem);
+    mma_stage2<ACT, SC>(P, wg - P.n_s1, smem);
 }
 
 template <int TT, int ACT, int SC, bool VEC>
@@ -485,7 +584,9 @@ hipError_t launch_tt(const MmaParams& P, dim3 grid, size_t smem, hipStream_t str
 
 template <int ACT, int SC>
 hipError_t launch_vec(const MmaParams& P, dim3 grid, size_t smem, hipStream_t stream) {
-  return P.vec ? launch_tt<ACT, SC, true>(P, grid, smem, stream) : launch_tt<ACT, SC, false>(P, grid, smem, stream);
+  // element-wise x and g loads (unaligned or d_in % 4 != 0) are compiled for
+  // the widest token count only; it serves every T (absent columns dropped)
+  return P.vec ? launch_tt<ACT, SC, true>(P, grid, smem, stream) : launch_one<4, ACT, SC, false>(P, grid, smem, stream);
 }
 
 template <int ACT>
@@ -499,10 +600,9 @@ hipError_t launch_sc(const MmaParams& P, int sc_dt, dim3 grid, size_t smem, hipS
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
-int kpw_for(int T, int act_dt) {
-  const int tt = (T + 15) / 16;
-  const int base = tt == 1 ? 8 : (tt == 2 ? 6 : 4);
-  return act_dt == kDtF32 ? base / 2 : base;
+int64_t packed_bytes(int64_t n_out, int64_t n_red) {
+  const int64_t w = n_red & 31;
+  return 4 * (n_red >> 5) * n_out + (w == 0 ? 0 : (w <= 16 ? 2 : 4)) * n_out;
 }
 
 }  // namespace
@@ -512,7 +612,7 @@ MmaGeom decode_mma_geometry(int T, int d_in, int d_out, int r, int act_dt) {
   const int tt = T > 0 ? (T + 15) / 16 : 1;
   g.nmf = (r + 15) / 16;
   const int nbt = nblocks32(d_in);
-  const int per_round = kWaves * kpw_for(T, act_dt);
+  const int per_round = kWaves * kpw_of(tt, act_dt);
   // one round of loads per run when possible, at most kMaxRuns runs
   int s1d = (nbt + per_round - 1) / per_round;
   if (s1d > kMaxRuns) s1d = kMaxRuns;
@@ -521,12 +621,15 @@ MmaGeom decode_mma_geometry(int T, int d_in, int d_out, int r, int act_dt) {
   g.s1d = nbt > 0 ? (nbt + g.bpr - 1) / g.bpr : 1;
   g.n_s1 = 2 * g.nmf * g.s1d;
   // stage 2 reads every partial when there are few, else the two-level sums
-  g.direct = g.s1d * r <= kDirectMax;
+  g.direct = g.s1d == 1 || static_cast<int64_t>(2) * T * g.s1d * r <= kDirectMaxSlots;
   g.n_s2 = (d_out + kWaves * 16 - 1) / (kWaves * 16);
-  const int nw = act_dt == kDtF32 ? 3 : 2;
   const int nsrc = g.direct ? g.s1d : 1;
-  const size_t s1_lds = static_cast<size_t>(kWaves) * tt * 64 * 16;
-  const size_t s2_lds = 4 * static_cast<size_t>(align4(16 * nsrc * r)) + static_cast<size_t>(nblocks32(r)) * nw * 64 * 16;
+  const size_t tch = T < 16 ? T : 16;
+  const size_t nkb = nblocks32(r);
+  // stage 1 sums the waves' [tt][64 lanes] float4 accumulators; the
+  // element-wise (unaligned) variant is compiled for 4 token fragments
+  const size_t s1_lds = static_cast<size_t>(kWaves) * 4 * 64 * 16;
+  const size_t s2_lds = 4 * (2 * nkb * 64 + 2 * tch * 32 * nkb + (nsrc > 1 ? 2 * tch * nsrc * r : 0));
   g.smem_bytes = s1_lds > s2_lds ? s1_lds : s2_lds;
   g.partial_off = kCtrlBytes;
   g.partial_slots = static_cast<size_t>(2) * g.s1d * T * r;
@@ -536,7 +639,14 @@ MmaGeom decode_mma_geometry(int T, int d_in, int d_out, int r, int act_dt) {
   return g;
 }
 
-bool decode_mma_supports(int64_t T, int64_t r) { return T <= kMmaMaxTokens && r <= kMmaMaxRank; }
+bool decode_mma_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
+  // buffer offsets are 32-bit: every operand, and every offset formed for
+  // the (up to 16 * ceil(T / 16)) token rows read, stays below 2^31 bytes
+  const int64_t lim = int64_t(1) << 31;
+  const int64_t rows = 16 * ((T + 15) / 16);
+  return T <= kMmaMaxTokens && r <= kMmaMaxRank && (rows + 1) * d_in * 4 < lim &&
+         packed_bytes(d_out, r) < lim && packed_bytes(r, d_in) < lim && d_out * 4 < lim;
+}
 
 hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t stream) {
   MmaParams P{};
@@ -563,9 +673,17 @@ hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t
   P.n_s1 = g.n_s1;
   P.n_s2 = g.n_s2;
   P.direct = g.direct;
-  const uintptr_t xa = a.act_dt == kDtF32 ? 16 : 8, ga = a.sc_dt == kDtF32 ? 16 : 8;
+  const int64_t ex = a.act_dt == kDtF32 ? 4 : 2, es = a.sc_dt == kDtF32 ? 4 : 2;
+  const uintptr_t xa = 4 * ex, ga = 4 * es;
   P.vec = (reinterpret_cast<uintptr_t>(a.x) % xa == 0) && (a.d_in % 4 == 0) &&
           (reinterpret_cast<uintptr_t>(a.g[0]) % ga == 0) && (reinterpret_cast<uintptr_t>(a.g[1]) % ga == 0);
+  P.x_bytes = static_cast<uint32_t>(static_cast<int64_t>(a.T) * a.d_in * ex);
+  P.g_bytes = static_cast<uint32_t>(a.d_in * es);
+  P.h_bytes = static_cast<uint32_t>(a.d_out * es);
+  P.l_bytes = static_cast<uint32_t>(a.r * es);
+  P.v_bytes = static_cast<uint32_t>(packed_bytes(a.r, a.d_in));
+  P.u_bytes = static_cast<uint32_t>(packed_bytes(a.d_out, a.r));
+  P.magic_r = a.r > 1 ? static_cast<uint32_t>(((uint64_t(1) << 32) + a.r - 1) / a.r) : 0u;
   const dim3 grid(g.n_s1 + g.n_s2);
   switch (a.act_dt) {
     case kDtF32: return launch_sc<kDtF32>(P, a.sc_dt, grid, g.smem_bytes, stream);

@@ -162,7 +162,7 @@ struct MmaGeom {
 constexpr int kMmaMaxTokens = 64;
 constexpr int kMmaMaxRank = 832;  // U words of one row (both paths) held in registers in stage 2
 MmaGeom decode_mma_geometry(int T, int d_in, int d_out, int r, int act_dt);
-bool decode_mma_supports(int64_t T, int64_t r);
+bool decode_mma_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
 
 struct PrefillGeom {
   int bm;                  // tokens per M-tile
