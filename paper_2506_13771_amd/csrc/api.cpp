@@ -67,7 +67,6 @@ lb::ForwardArgs make_args(const void* x, lb_dtype act, int64_t T, int64_t d_in, 
   return a;
 }
 
-bool decode_supports(int64_t T, int64_t r) { return T <= lb::kDecodeMaxTokens && r <= lb::kDecodeMaxRank; }
 constexpr int64_t kAutoLutTokens = 2;  // AUTO sends T <= this to the look-up-table decode kernel
 
 }  // namespace
@@ -142,7 +141,7 @@ size_t lb_forward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_
   size_t need = lb::kCtrlBytes;
   const int iT = static_cast<int>(T), ii = static_cast<int>(d_in), io = static_cast<int>(d_out),
             ir = static_cast<int>(r);
-  if (decode_supports(T, r)) {
+  if (lb::decode_supports(T, d_in, d_out, r)) {
     const lb::DecodeGeom g = lb::decode_geometry(iT, ii, io, ir);
     if (g.ws_bytes > need) need = g.ws_bytes;
   }
@@ -174,7 +173,7 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
   if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype)) return LB_ERR_DTYPE;
   lb_status st = check_sizes(T, d_in, d_out, r);
   if (st != LB_OK) return st;
-  if (kernel == LB_KERNEL_DECODE && !decode_supports(T, r)) return LB_ERR_SHAPE;
+  if (kernel == LB_KERNEL_DECODE && !lb::decode_supports(T, d_in, d_out, r)) return LB_ERR_SHAPE;
   if (kernel == LB_KERNEL_DECODE_MFMA && !lb::decode_mma_supports(T, d_in, d_out, r)) return LB_ERR_SHAPE;
   if (T == 0 || d_out == 0) return LB_OK;
   if (!y || (d_in > 0 && !x)) return LB_ERR_NULL;
@@ -195,7 +194,7 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
   if (kernel == LB_KERNEL_AUTO) {
     // the look-up-table kernel is the fastest for one or two tokens; from
     // three on the matrix-core decode kernel takes over
-    if (T <= kAutoLutTokens && decode_supports(T, r))
+    if (T <= kAutoLutTokens && lb::decode_supports(T, d_in, d_out, r))
       kernel = LB_KERNEL_DECODE;
     else if (lb::decode_mma_supports(T, d_in, d_out, r))
       kernel = LB_KERNEL_DECODE_MFMA;

@@ -9,26 +9,36 @@
 // values a0..a3, a 16-entry table holds every signed sum
 // sum_i (bit i of m ? -a_i : +a_i).  A packed 32-bit word (LB layout v1: 32
 // consecutive reduction indices of one output) is then 8 nibble look-ups
-// instead of 32 sign flips.  Tables are built in LDS, once per workgroup, for
-// the activations of that workgroup's inputs.
+// instead of 32 sign flips.
 //
-// Launch structure (one grid, two roles, no host round trip, latency-first):
+// At decode sizes each SIMD runs one wave and a wave64 VALU instruction takes
+// 4 cycles, so the time of a call is the length of its dependent chain of
+// instructions and memory rounds.  The kernel is written for a short chain:
+// fixed work per thread (one table and two packed words per stage-1 thread,
+// one word per path and row quarter in stage 2), buffer loads (a read past a
+// buffer returns zero, so ragged edges need no clamping or masking), 128-bit
+// table writes, and one memory round per stage.
+//
+// Launch structure (one grid, two roles, no host round trip):
 //  * stage-1 workgroups hold the LOWEST block ids.  Each owns one path, a tile
-//    of 16 latent columns and one run of d_in.  All of its global loads (V
-//    words, x, g, l) are issued before any is waited on.  Lane (kk, bs) takes
-//    column k0 + kk and every 16th 32-wide block of the run; the 16 groups are
-//    combined by cross-lane shuffles and a 4-way LDS sum in a fixed order.  The
-//    partial l (.) z goes to the workspace as tagged 64-bit slots (high word:
-//    this call's tag, low word: fp32 bits), written with relaxed agent-scope
-//    atomics, which reach the memory side without any L2 writeback.
-//  * stage-2 workgroups (higher ids, so dispatched after every stage-1
+//    of 16 latent columns and one run of d_in, processed in chunks of 32
+//    blocks of 32 inputs.  Thread tid builds the table of nibble tid % 8 of
+//    block tid / 8 (one table per token); lane (kk, m) of wave w looks up the
+//    words of column k0 + kk in blocks 8w + m and 8w + m + 4.  The 16 lanes of
+//    a column are summed by shuffles (xor 16, xor 32) and the 4 waves in LDS,
+//    in a fixed order.  The partial l (.) z of the run goes to the workspace
+//    as tagged 64-bit slots (high word: this call's tag, low word: fp32
+//    bits), written with relaxed agent-scope atomics, which reach the memory
+//    side without any L2 writeback.
+//  * stage-2 workgroups (higher ids, dispatched after every stage-1
 //    workgroup of their XCD) load their U words and h first, then read the
-//    slots with coherent agent-scope loads until every tag is current, sum the
-//    partials of each latent in a fixed order, build tables over groups of 4
-//    latents and contract with U.  KQ adjacent lanes share an output row and
-//    split its words; a butterfly joins them.  Both paths are summed in fp32
-//    and y is stored once.
-//  * When the partials are many (large T * r), the highest-id run of each
+//    slots with coherent agent-scope loads until every tag is current, sum
+//    the partials of each latent in ascending run order while building tables
+//    over groups of 4 latents, and contract with U: 4 adjacent lanes share an
+//    output row (lane q takes the row's words q, q + 4, ...), a quad butterfly
+//    joins them, and lane q stores token q.  Both paths are summed in fp32
+//    and y is rounded once.
+//  * When the partials are many (large T * r * runs), the highest run of each
 //    latent tile first adds the other runs' partials ("two-level" mode), so
 //    stage-2 workgroups read one slot per latent.
 //  * Waits only ever target workgroups with lower block ids, which are
@@ -38,11 +48,34 @@
 //    workgroup to finish (counted with one atomic per workgroup) stores it as
 //    the new epoch, so consecutive calls, graph replays included, never
 //    confuse each other's slots and the workspace needs no clearing.
+#include <atomic>
+
 #include "device_common.h"
 
 namespace lb {
 
 namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kKc = 16;                 // latent columns per stage-1 tile
+constexpr int kChunk = 32;              // blocks of 32 inputs per stage-1 chunk (one table per thread)
+constexpr int kMaxRuns = 16;            // d_in runs per latent tile (partials per z value)
+constexpr int kBlk = 8 * 16 + 16;       // floats of one block's 8 nibble tables, padded (bank spread)
+constexpr int kKQ = 4;                  // stage 2: lanes per output row
+constexpr int kRows2 = kThreads / kKQ;  // stage 2: output rows per workgroup
+constexpr int kGather = 8;              // stage 2: slots a thread gathers per round
+constexpr int kDirectMaxSlots = kThreads * kGather;  // stage 2 reads every partial up to this many
+constexpr size_t kLds2Max = 64 * 1024;  // stage-2 LDS budget per token chunk (bytes)
+
+// Table swizzle: entry m of nibble table q of a block sits at m ^ tsw(q).
+// tsw keeps 4-entry groups contiguous (128-bit writes) and spreads the writes
+// of a wave's 64 builders over all LDS banks.  XORing a packed word with kKey
+// applies tsw(q) to each nibble q at once.
+__host__ __device__ constexpr int tsw(int q) { return (q & 6) << 1; }
+constexpr uint32_t kKey = 0xCC884400u;
+static_assert(((kKey >> 8) & 15) == tsw(2) && ((kKey >> 28) & 15) == tsw(7), "swizzle key");
 
 struct DecodeParams {
   const void* x;
@@ -53,68 +86,40 @@ struct DecodeParams {
   const void* g[2];
   const void* l[2];
   uint32_t* ctrl;
-  uint64_t* partial;  // [2][T][s1d][r] tagged partial l (.) z
+  uint64_t* partial;  // [2][T][s1d][r] tagged partial l (.) z of each run
   uint64_t* wbuf;     // [2][T][r]      tagged l (.) z (two-level mode)
-  int act_dt, sc_dt;
-  int x_vec, g_vec;   // 4-element vector loads allowed for x / g
   int T, d_in, d_out, r;
-  int nkt, bpw, s1d, n_s1, cb;
-  int kq_log2, rows2, n_s2, direct, tch;
+  int nkt;     // 16-latent tiles per path
+  int s1d;     // d_in runs per tile
+  int bpr;     // 32-input blocks per run
+  int n_s1;    // stage-1 workgroups (2 * nkt * s1d)
+  int n_s2;    // stage-2 workgroups
+  int direct;  // stage 2 reads every run's partial (else the two-level sums)
+  int tch;     // tokens per stage-2 chunk
+  uint32_t magic_r;  // fast_div multiplier for r
+  uint32_t x_bytes, g_bytes, l_bytes, h_bytes, v_bytes, u_bytes;
 };
 
-constexpr int kThreads = 256;
-constexpr int kKc = 16;                 // latent columns per stage-1 tile
-constexpr int kMaxSplit = 16;           // d_in runs per latent tile (partials per z value)
-constexpr int kMaxWordsPerLane = 8;     // stage 1: V words a lane holds in registers per chunk
-constexpr int kMaxGroupsPerThread = 3;  // stage 1: table groups a thread builds per chunk
-constexpr int kRowWords = 2;            // stage 2: U words per row a lane holds (per path)
-constexpr int kMaxPasses = 4;           // stage 2: rows per lane (2 for T > 2: register budget)
-__host__ __device__ constexpr int max_passes(int tm) { return tm > 2 ? 2 : kMaxPasses; }
-constexpr int kSlotsPerPath = 4;        // stage 2: slots a thread gathers per path in one round
-constexpr int kLutBlock = 8 * 16 + 16;  // floats per 32-wide block of tables (padded: bank spread)
-constexpr int kLdsFloats = 12288;       // 48 KB of dynamic LDS
-
-// Nibble tables.  Block B of the table array holds the 8 tables (16 floats
-// each, kLutBlock floats in all) of one 32-wide block of inputs; table q of
-// block B is stored XOR-swizzled: entry m sits at position m ^ swz(B, q),
-// swz(B, q) = (2 B + q / 4) mod 16.  A wave's builders (consecutive tables)
-// then spread their writes over the LDS banks instead of hitting the same two
-// (32-way conflicts unswizzled), and a lookup applies the same swizzle to the
-// whole packed word with one XOR (word_key).
-__device__ __forceinline__ int table_swizzle(int B, int q) { return (2 * B + (q >> 2)) & 15; }
-__device__ __forceinline__ uint32_t word_key(int B) {
-  return static_cast<uint32_t>((2 * B) & 15) * 0x11111111u ^ 0x11110000u;
-}
-
-// Table q of block B: entry m = sum_i (bit i of m ? -a_i : +a_i), built as
-// (+-a0 +-a1) + (+-a2 +-a3), written at its swizzled position.
-__device__ __forceinline__ void build_lut16(float a0, float a1, float a2, float a3, float* lut, int B, int q) {
-  const float p01[4] = {a0 + a1, -a0 + a1, a0 - a1, -a0 - a1};
-  const float p23[4] = {a2 + a3, -a2 + a3, a2 - a3, -a2 - a3};
-  float* tb = lut + B * kLutBlock + 16 * q;
-  const int sw = table_swizzle(B, q);
+// The 16 entries of one nibble table over a0..a3 (entry m = sum_i (bit i of m
+// ? -a_i : a_i)), written as 4 groups of 4 at their swizzled positions.
+__device__ __forceinline__ void build_table(float* t16, int q, float a0, float a1, float a2, float a3) {
+  const float s01[4] = {a0 + a1, a1 - a0, a0 - a1, -a0 - a1};
+  const float s23[4] = {a2 + a3, a3 - a2, a2 - a3, -a2 - a3};
+  const int gs = tsw(q) >> 2;
 #pragma unroll
-  for (int m = 0; m < 16; ++m) tb[m ^ sw] = p01[m & 3] + p23[m >> 2];
+  for (int c = 0; c < 4; ++c) {
+    const f32x4 v = {s01[0] + s23[c], s01[1] + s23[c], s01[2] + s23[c], s01[3] + s23[c]};
+    *reinterpret_cast<f32x4*>(t16 + 4 * (c ^ gs)) = v;
+  }
 }
 
-// Signed sum of one packed word against the 8 tables of block B (8
-// independent reads, summed as a fixed tree).
-__device__ __forceinline__ float word_dot(const float* lut, int B, uint32_t w) {
-  const float* tb = lut + B * kLutBlock;
-  const uint32_t k = w ^ word_key(B);
+// Signed sum of one packed word against the 8 tables of a block (tb8 points
+// at the block's first table; wk is the word XORed with kKey).
+__device__ __forceinline__ float word_sum(const float* tb8, uint32_t wk) {
   float v[8];
 #pragma unroll
-  for (int q = 0; q < 8; ++q) v[q] = tb[16 * q + ((k >> (4 * q)) & 15)];
+  for (int q = 0; q < 8; ++q) v[q] = tb8[16 * q + ((wk >> (4 * q)) & 15)];
   return ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
-}
-
-// Sum over the KQ lanes (adjacent, power of two, 4..16) that share an output row.
-__device__ __forceinline__ float row_sum(float v, int kq_log2) {
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));  // xor 1
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));  // xor 2
-  if (kq_log2 >= 3) v += __shfl_xor(v, 4);
-  if (kq_log2 >= 4) v += __shfl_xor(v, 8);
-  return v;
 }
 
 // ---------------------------------------------------------------------------
@@ -123,141 +128,109 @@ __device__ __forceinline__ float row_sum(float v, int kq_log2) {
 template <int TM, int ACT, int SC, bool VEC>
 __device__ void stage1(const DecodeParams& P, int wg, float* smem) {
   const int per_path = P.nkt * P.s1d;
-  const int p = wg / per_path;
+  const int p = wg >= per_path ? 1 : 0;
   const int rem = wg - p * per_path;
   const int kt = rem / P.s1d;
   const int c = rem - kt * P.s1d;
   const int T = P.T, r = P.r, d_in = P.d_in;
-  const int k0 = kt * kKc;
-  const int kcn = min(kKc, r - k0);
-  const int nbt = nblocks32(d_in);
-  const int b0 = c * P.bpw;
-  const int b1 = min(nbt, b0 + P.bpw);
   const int tid = threadIdx.x;
-  const int kk = tid & (kKc - 1);
-  const int bs = tid >> 4;
-  const bool col_ok = kk < kcn;
-  const int CB = P.cb;
-  // per-path pointers chosen by selects (no dynamic indexing into the parameters)
-  const void* Vp = p ? P.V[1] : P.V[0];
-  const void* gp = p ? P.g[1] : P.g[0];
-  const void* lp = p ? P.l[1] : P.l[0];
-  const uint32_t* Vw = static_cast<const uint32_t*>(Vp);
+  const int wave = tid >> 6, lane = tid & 63;
+  const int kk = tid & 15, m = (tid >> 4) & 3;
+  const int k = kt * kKc + kk;  // this lane's latent column
+  const bool kok = k < r;
   const int nbv = d_in >> 5, tailv = d_in & 31;
-  float* lut = smem;  // [T][CB][kLutBlock]
+  const int nbt = nblocks32(d_in);
+  const int b0 = c * P.bpr, b1 = min(nbt, b0 + P.bpr);
+  const int tb = tid >> 3, tq = tid & 7;  // builder: table tq of chunk block tb
+  const rsrc_t vr = make_rsrc(p ? P.V[1] : P.V[0], P.v_bytes);
+  const rsrc_t gr = make_rsrc(p ? P.g[1] : P.g[0], P.g_bytes);
+  const rsrc_t xr = make_rsrc(P.x, P.x_bytes);
+  float* tbl = smem;  // [TM][kChunk][kBlk]
 
-  uint32_t lk_bits = 0u;  // latent scale of this lane's column (raw)
-  uint32_t epoch = 0u;    // the epoch left by the previous call (this call's tag is one more)
+  const uint32_t lbits = bload<SC>(make_rsrc(p ? P.l[1] : P.l[0], P.l_bytes), k, kok);
+  uint32_t epoch = load_epoch<1>(P.ctrl);
+
   float acc[TM];
 #pragma unroll
   for (int t = 0; t < TM; ++t) acc[t] = 0.0f;
 
-  for (int cb = b0; cb < b1; cb += CB) {
-    const int nblk = min(CB, b1 - cb);
-    const int ngroups = T * nblk * 8;
-    // Every load of the chunk is issued before any value is used, at clamped
-    // addresses, with validity applied afterwards: one memory round per chunk.
-    // x and g by groups of 4 inputs (group e: token t, inputs j0..j0+3)
-    uint32_t xr[kMaxGroupsPerThread][4], gr[kMaxGroupsPerThread][4];
+  for (int cb = b0; cb < b1; cb += kChunk) {
+    // this thread's table inputs: x of each token and g at inputs jb .. jb + 3
+    const int jb = 32 * (cb + tb) + 4 * tq;
+    const bool tok = cb + tb < b1;
+    uint32_t gb[4], xb[TM][4];
+    bload4<SC, VEC>(gr, jb, tok, gb);
 #pragma unroll
-    for (int gi = 0; gi < kMaxGroupsPerThread; ++gi) {
-      const int e = tid + kThreads * gi;
-      const int t = e / (nblk * 8);
-      const int j0 = 32 * cb + 4 * (e - t * nblk * 8);  // 32 (cb + bl) + 4 q
-      const int nvalid = e < ngroups ? min(4, d_in - j0) : 0;
-      ld4_bits<ACT, VEC>(P.x, nvalid > 0 ? static_cast<int64_t>(t) * d_in + j0 : 0, nvalid, xr[gi]);
-      ld4_bits<SC, VEC>(gp, nvalid > 0 ? j0 : 0, nvalid, gr[gi]);
-    }
-    // the latent scale (used once the partials, which carry l (.) z, are formed)
-    lk_bits = ld_bits<SC>(lp, col_ok ? k0 + kk : 0);
-    epoch = load_epoch<1>(P.ctrl);
-    // the tail word of d_in (if this chunk holds the tail block)
-    const int tail_bl = nbv - cb;  // local index of the tail block (when < nblk)
-    uint32_t tlo, thi;
-    ld_tail_bits(Vw, nbv, r, tailv, k0 + kk, col_ok && tail_bl < nblk, tlo, thi);
-    // full V words
-    const uint32_t* Vfull = full_words_or(Vw, nbv, P.ctrl);
-    uint32_t words[kMaxWordsPerLane];
+    for (int t = 0; t < TM; ++t) bload4<ACT, VEC>(xr, t * d_in + jb, tok && t < T, xb[t]);
+    // this lane's two packed words (blocks 8 wave + m and 8 wave + m + 4)
+    uint32_t w[2];
 #pragma unroll
-    for (int u = 0; u < kMaxWordsPerLane; ++u) {
-      const int bl = bs + 16 * u;
-      const bool ok = col_ok && bl < nblk && bl < tail_bl;
-      words[u] = Vfull[ok ? static_cast<int64_t>(cb + bl) * r + k0 + kk : 0];
-    }
-    // keep the loads above and the uses of x, g and the tail below
-    asm volatile("" ::: "memory");
-#pragma unroll
-    for (int gi = 0; gi < kMaxGroupsPerThread; ++gi)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) pin(xr[gi][i]), pin(gr[gi][i]);
-    pin(tlo), pin(thi);
-    const uint32_t tailword = tail_word(tlo, thi, tailv);
-    // nibble tables of a = x (.) g_p (zero beyond d_in)
-#pragma unroll
-    for (int gi = 0; gi < kMaxGroupsPerThread; ++gi) {
-      const int e = tid + kThreads * gi;
-      if (e < ngroups) {
-        const int t = e / (nblk * 8);
-        const int rem2 = e - t * nblk * 8;
-        const int j0 = 32 * cb + 4 * rem2;
-        float a[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          a[i] = j0 + i < d_in ? raw4_elem<ACT, VEC>(xr[gi], i) * raw4_elem<SC, VEC>(gr[gi], i) : 0.0f;
-        build_lut16(a[0], a[1], a[2], a[3], lut, t * CB + (rem2 >> 3), rem2 & 7);
+    for (int u = 0; u < 2; ++u) {
+      const int b = cb + 8 * wave + m + 4 * u;
+      const bool full = kok && b < b1 && b < nbv;
+      w[u] = __builtin_amdgcn_raw_buffer_load_b32(vr, full ? static_cast<uint32_t>(b * r + k) * 4u : kOob, 0, 0);
+      if (tailv != 0) {
+        // the tail block's word comes from the tail plane (16- or 32-bit entries)
+        const bool tl = kok && b == nbv && b < b1;
+        const uint32_t off = 4u * nbv * r + (tailv <= 16 ? 2u : 4u) * k;
+        const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(vr, tl ? off : kOob, 0, 0);
+        const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(vr, tl && tailv > 16 ? off + 2 : kOob, 0, 0);
+        w[u] |= (lo & 0xffffu) | (hi << 16);
       }
+    }
+    // tables of a = x (.) g (zero past d_in and for absent tokens)
+#pragma unroll
+    for (int t = 0; t < TM; ++t) {
+      float a[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = raw4_elem<ACT, VEC>(xb[t], i) * raw4_elem<SC, VEC>(gb, i);
+        if (tailv != 0 && jb + i >= d_in) a[i] = 0.0f;  // x past d_in belongs to the next row
+      }
+      build_table(tbl + (t * kChunk + tb) * kBlk + 16 * tq, tq, a[0], a[1], a[2], a[3]);
     }
     __syncthreads();
+    // look-ups (blocks past the run have zero words and zero tables)
 #pragma unroll
-    for (int u = 0; u < kMaxWordsPerLane; ++u) {
-      const int bl = bs + 16 * u;
-      if (col_ok && bl < nblk) {
-        const uint32_t w = bl == tail_bl ? tailword : words[u];
+    for (int u = 0; u < 2; ++u) {
+      const uint32_t wk = w[u] ^ kKey;
+      const float* tb8 = tbl + (8 * wave + m + 4 * u) * kBlk;
 #pragma unroll
-        for (int t = 0; t < TM; ++t)
-          if (t < T) acc[t] += word_dot(lut, t * CB + bl, w);
-      }
+      for (int t = 0; t < TM; ++t) acc[t] += word_sum(tb8 + t * kChunk * kBlk, wk);
     }
     __syncthreads();
   }
-  const float lk = bits_to_f32<SC>(lk_bits);
-  // this call's tag: one more than the epoch the previous call left behind
-  pin(epoch);
-  const uint32_t tag = epoch + 1u;
 
-  // fixed-order reduction over the 16 block groups: within a wave by shuffles
-  // (groups 4w..4w+3 sit in lane bands of 16), then across the 4 waves in LDS
-  float* red = smem;  // [4 waves][T][kKc]
+  // fixed-order sum of the 16 lanes of each column: lanes kk + 16 m within a
+  // wave by shuffles, then the 4 waves in LDS
+  float* red = smem;  // [4 waves][TM][16]
 #pragma unroll
   for (int t = 0; t < TM; ++t) {
-    float v = col_ok ? acc[t] * lk : 0.0f;
+    float v = acc[t];
     v += __shfl_xor(v, 16);
     v += __shfl_xor(v, 32);
-    acc[t] = v;
+    if (lane < 16) red[(wave * TM + t) * 16 + lane] = v;
   }
-  if ((tid & 63) < kKc) {
-#pragma unroll
-    for (int t = 0; t < TM; ++t)
-      if (t < T) red[((tid >> 6) * T + t) * kKc + kk] = acc[t];
-  }
+  pin(epoch);
+  const uint32_t tag = epoch + 1u;  // this call's tag: one more than the epoch the previous call left
   __syncthreads();
-  const bool reducer = !P.direct && c == P.s1d - 1;
-  for (int e = tid; e < T * kcn; e += kThreads) {
-    const int t = e / kcn;
-    const int k = e - t * kcn;
-    const float s = (red[(0 * T + t) * kKc + k] + red[(1 * T + t) * kKc + k]) +
-                    (red[(2 * T + t) * kKc + k] + red[(3 * T + t) * kKc + k]);
-    // slots of (p, t): [s1d][r]
-    uint64_t* pt_slots = P.partial + (static_cast<int64_t>(p) * T + t) * P.s1d * r + k0 + k;
-    if (!reducer) {
-      put_slot(pt_slots + static_cast<int64_t>(c) * r, tag, s);
-    } else {
-      // two-level mode: the highest run of this latent tile (it only waits for
-      // lower block ids) adds the other runs' partials in ascending order
-      float others = 0.0f;
-      const bool ok = gather_sum<kMaxSplit>(pt_slots, r, P.s1d - 1, tag, others);
-      if (!ok) atomic_store_relaxed(P.ctrl + kCtrlError, 1u);
-      put_slot(P.wbuf + (static_cast<int64_t>(p) * T + t) * r + k0 + k, tag, ok ? others + s : __builtin_nanf(""));
+  if (tid < 16 * TM) {
+    const int t = tid >> 4;  // tid & 15 == kk: this thread loaded l of its own column
+    const float s = ((red[(0 * TM + t) * 16 + kk] + red[(1 * TM + t) * 16 + kk]) +
+                     (red[(2 * TM + t) * 16 + kk] + red[(3 * TM + t) * 16 + kk])) *
+                    bits_to_f32<SC>(lbits);
+    if (t < T && kok) {
+      uint64_t* slots = P.partial + static_cast<int64_t>(p * T + t) * P.s1d * r + k;  // [p][t][run][k]
+      if (P.direct || c != P.s1d - 1) {
+        put_slot(slots + static_cast<int64_t>(c) * r, tag, s);
+      } else {
+        // two-level mode: the highest run of this tile (it only waits for lower
+        // block ids) adds the other runs' partials in ascending order
+        float others = 0.0f;
+        const bool ok = gather_sum<kMaxRuns>(slots, r, P.s1d - 1, tag, others);
+        if (!ok) atomic_store_relaxed(P.ctrl + kCtrlError, 1u);
+        put_slot(P.wbuf + static_cast<int64_t>(p * T + t) * r + k, tag, ok ? others + s : __builtin_nanf(""));
+      }
     }
   }
 }
@@ -265,171 +238,151 @@ __device__ void stage1(const DecodeParams& P, int wg, float* smem) {
 // ---------------------------------------------------------------------------
 // stage 2
 // ---------------------------------------------------------------------------
-template <int TM, int ACT, int SC>
-__device__ void stage2(const DecodeParams& P, int q, float* smem) {
+// Sum over the 4 lanes of a row (quad butterfly: xor 1, xor 2).
+__device__ __forceinline__ float quad_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+  return v;
+}
+
+template <int TM, int ACT, int SC, int WPL>
+__device__ void stage2(const DecodeParams& P, int q2, float* smem) {
   const int tid = threadIdx.x;
-  const int kq_log2 = P.kq_log2;
-  const int KQ = 1 << kq_log2;
-  const int rows_per_pass = kThreads >> kq_log2;
-  const int rl = tid >> kq_log2;
-  const int kq = tid & (KQ - 1);
+  const int kq = tid & (kKQ - 1);
+  const int i = q2 * kRows2 + (tid >> 2);  // output row
   const int T = P.T, r = P.r, d_out = P.d_out;
-  const int nw = nblocks32(r);
-  const int i_base = q * P.rows2 + rl;
-  const int passes = P.rows2 / rows_per_pass;
-  const int nsrc = P.direct ? P.s1d : 1;  // slots per latent value
-  float* raw = smem;                                      // [2][tch][nsrc][r] slot values
-  float* lut = smem + 2 * P.tch * nsrc * r;               // [2][tch][nw][kLutBlock]
+  const bool iok = i < d_out;
+  const int nw = nblocks32(r), nbu = r >> 5, tailu = r & 31;
+  const int nsrc = P.direct ? P.s1d : 1;
+  const int R4 = (r + 3) & ~3;  // LDS row of the gathered partials (padded to 16 bytes)
+  const int tch = P.tch;
+  float* raw = smem;                         // [2][tch][nsrc][R4]
+  float* tb2 = smem + 2 * tch * nsrc * R4;   // [2][tch][nw][kBlk]
 
-  // every U word and row scale this lane will use, loaded (raw) before any
-  // wait; they are combined once the first gather round is in flight
-  constexpr int NP = max_passes(TM);
-  // the epoch left by the previous call (this call's tag is one more)
-  uint32_t epoch = load_epoch<2>(P.ctrl);
-  uint32_t words[NP][2][kRowWords];
-  uint32_t tlo[NP][2], thi[NP][2], hbits[NP][2];
-  const int nbu = r >> 5;        // full words per row of U
-  const int tailw = r & 31;      // width of the tail word (0: none)
+  // prefetch: this lane's U words (words kq, kq + 4, ... of row i, as two 16-bit
+  // halves so that full words and the tail word are the same loads) and h
+  uint32_t wlo[2][WPL], whi[2][WPL], hb[2];
+  const uint32_t plane = 4u * nbu * d_out;
+  const uint32_t toff = plane + (tailu <= 16 ? 2u : 4u) * i;
 #pragma unroll
-  for (int m = 0; m < NP; ++m) {
-    const int i = i_base + rows_per_pass * m;
-    const bool live = m < passes && i < d_out;
+  for (int pp = 0; pp < 2; ++pp) {
+    const rsrc_t ur = make_rsrc(pp ? P.U[1] : P.U[0], P.u_bytes);
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp) {
-      const uint32_t* base = static_cast<const uint32_t*>(pp ? P.U[1] : P.U[0]);
-      ld_tail_bits(base, nbu, d_out, tailw, i, live && kq == nbu % KQ, tlo[m][pp], thi[m][pp]);
-#pragma unroll
-      for (int e = 0; e < kRowWords; ++e) {
-        const int kb = kq + KQ * e;
-        const bool okf = live && kb < nbu;
-        words[m][pp][e] = full_words_or(base, nbu, P.ctrl)[okf ? static_cast<int64_t>(kb) * d_out + i : 0];
-      }
-      hbits[m][pp] = ld_bits<SC>(pp ? P.h[1] : P.h[0], live ? i : 0);
+    for (int e = 0; e < WPL; ++e) {
+      const int kb = kq + kKQ * e;
+      const bool full = iok && kb < nbu, tl = iok && kb == nbu && tailu != 0;
+      const uint32_t off = full ? static_cast<uint32_t>(kb * d_out + i) * 4u : (tl ? toff : kOob);
+      wlo[pp][e] = __builtin_amdgcn_raw_buffer_load_b16(ur, off, 0, 0);
+      whi[pp][e] = __builtin_amdgcn_raw_buffer_load_b16(ur, full || (tl && tailu > 16) ? off + 2 : kOob, 0, 0);
     }
+    hb[pp] = bload<SC>(make_rsrc(pp ? P.h[1] : P.h[0], P.h_bytes), i, iok);
   }
-  float hrow[NP][2];
+  uint32_t epoch = load_epoch<2>(P.ctrl);
   uint32_t tag = 0u, done_before = 0u;
-
   bool ok = true;
-  for (int t0 = 0; t0 < T; t0 += P.tch) {
-    const int tn = min(P.tch, T - t0);
-    // gather this token chunk's slots: per path they are contiguous
-    // ([t][nsrc][r]); one round of coherent loads, then re-reads of any slot
-    // whose tag is not yet current
-    const int per_path = tn * nsrc * r;
-    const uint64_t* src[2];
-#pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
-      src[pp] = P.direct ? P.partial + (static_cast<int64_t>(pp) * T + t0) * nsrc * r
-                         : P.wbuf + (static_cast<int64_t>(pp) * T + t0) * r;
-    uint64_t sv[2][kSlotsPerPath];
-#pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-      for (int j = 0; j < kSlotsPerPath; ++j) {
-        const int e = tid + kThreads * j;
-        sv[pp][j] = get_slot(src[pp] + (e < per_path ? e : 0));  // slots past the chunk are ignored
-      }
-    if (t0 == 0) {
-      // the prefetched U words and row scales (their loads precede the gather)
-      asm volatile("" ::: "memory");
-      pin(epoch);
-      tag = epoch + 1u;
-      // count this workgroup as one that has read the epoch (issued once the
-      // epoch has arrived; the returned count is used at the end)
-      if (tid == 0) done_before = atomic_add_relaxed(P.ctrl + kCtrlDone, 1u);
-#pragma unroll
-      for (int m = 0; m < NP; ++m)
-#pragma unroll
-        for (int pp = 0; pp < 2; ++pp) {
-          pin(tlo[m][pp]), pin(thi[m][pp]), pin(hbits[m][pp]);
-#pragma unroll
-          for (int e = 0; e < kRowWords; ++e) pin(words[m][pp][e]);
-          const int i = i_base + rows_per_pass * m;
-          const bool live = m < passes && i < d_out;
-          // the word after a row's full words is its tail word (words past the row are never used)
-#pragma unroll
-          for (int e = 0; e < kRowWords; ++e)
-            if (kq + KQ * e == nbu) words[m][pp][e] = tail_word(tlo[m][pp], thi[m][pp], tailw);
-          hrow[m][pp] = live ? bits_to_f32<SC>(hbits[m][pp]) : 0.0f;
-        }
-    }
-    for (uint32_t it = 0;; ++it) {
-      bool ready = true;
-#pragma unroll
-      for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-        for (int j = 0; j < kSlotsPerPath; ++j)
-          ready = ready && (tid + kThreads * j >= per_path || slot_ready(sv[pp][j], tag));
-      if (ready) break;
-      if (it >= kSpinLimit) {
-        ok = false;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-      for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-        for (int j = 0; j < kSlotsPerPath; ++j)
-          if (tid + kThreads * j < per_path && !slot_ready(sv[pp][j], tag))
-            sv[pp][j] = get_slot(src[pp] + tid + kThreads * j);
-    }
-#pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-      for (int j = 0; j < kSlotsPerPath; ++j) {
-        const int e = tid + kThreads * j;
-        if (e < per_path) raw[pp * per_path + e] = slot_value(sv[pp][j]);
-      }
-    __syncthreads();
-    // l (.) z = sum of the partials (ascending run order), then nibble tables
-    // over groups of 4 latents
-    for (int e = tid; e < 2 * tn * 8 * nw; e += kThreads) {
-      const int pt = e / (8 * nw);
-      const int gi = e - pt * 8 * nw;
-      const float* rs = raw + pt * nsrc * r;
-      float w[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-      for (int cc = 0; cc < nsrc; ++cc) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (4 * gi + i < r) w[i] += rs[cc * r + 4 * gi + i];
-      }
-      build_lut16(w[0], w[1], w[2], w[3], lut, pt * nw + (gi >> 3), gi & 7);
-    }
-    __syncthreads();
 
+  // pre-computed split of the builders: row pt = tid / ngrp of 4-latent groups
+  const int ngrp = 8 * nw;
+  const int bpt = tid / ngrp, bgrp = tid - bpt * ngrp, bstep = kThreads / ngrp;
+
+  for (int t0 = 0; t0 < T; t0 += tch) {
+    const int tn = min(tch, T - t0);
+    // zero the padding of the gathered rows (latents r .. R4 - 1)
+    if (R4 != r) {
+      for (int e = tid; e < 2 * tch * nsrc * (R4 - r); e += kThreads) {
+        const int row = e / (R4 - r);
+        raw[row * R4 + r + (e - row * (R4 - r))] = 0.0f;
+      }
+    }
+    // gather both paths' slots of tokens t0 .. t0 + tn - 1 (contiguous per
+    // path): rounds of loads, then re-reads of any slot whose tag is not this
+    // call's
+    const int per_path = tn * nsrc * r;
+    const int n = 2 * per_path;
+    for (int e0 = 0; e0 < n; e0 += kThreads * kGather) {
+      uint64_t sv[kGather];
+      const uint64_t* src[kGather];
 #pragma unroll
-    for (int m = 0; m < NP; ++m) {
-      if (m >= passes) break;
-      const int i = i_base + rows_per_pass * m;
-      float acc[2][TM];
+      for (int j = 0; j < kGather; ++j) {
+        const int e = e0 + tid + kThreads * j;
+        const int pp = e >= per_path ? 1 : 0;
+        const int el = e - pp * per_path;
+        src[j] = (P.direct ? P.partial + static_cast<int64_t>(pp * T + t0) * nsrc * r
+                           : P.wbuf + static_cast<int64_t>(pp * T + t0) * r) + el;
+        sv[j] = get_slot(e < n ? src[j] : P.partial);
+      }
+      if (t0 == 0 && e0 == 0) {
+        pin(epoch);
+        tag = epoch + 1u;
+        // count this workgroup as one that has read the epoch (the returned
+        // count is used at the end)
+        if (tid == 0) done_before = atomic_add_relaxed(P.ctrl + kCtrlDone, 1u);
+      }
+      for (uint32_t it = 0;; ++it) {
+        bool ready = true;
 #pragma unroll
-      for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-        for (int t = 0; t < TM; ++t) acc[pp][t] = 0.0f;
-#pragma unroll
-      for (int e = 0; e < kRowWords; ++e) {
-        const int kb = kq + KQ * e;
-        if (kb < nw) {
-#pragma unroll
-          for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-            for (int t = 0; t < TM; ++t)
-              if (t < tn) acc[pp][t] += word_dot(lut, (pp * tn + t) * nw + kb, words[m][pp][e]);
+        for (int j = 0; j < kGather; ++j) ready = ready && (e0 + tid + kThreads * j >= n || slot_ready(sv[j], tag));
+        if (ready) break;
+        if (it >= kSpinLimit) {
+          ok = false;
+          break;
         }
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int j = 0; j < kGather; ++j)
+          if (e0 + tid + kThreads * j < n && !slot_ready(sv[j], tag)) sv[j] = get_slot(src[j]);
       }
 #pragma unroll
-      for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-        for (int t = 0; t < TM; ++t) acc[pp][t] = row_sum(acc[pp][t], kq_log2);
-      if (kq == 0 && i < d_out) {
-#pragma unroll
-        for (int t = 0; t < TM; ++t)
-          if (t < tn)
-            st<ACT>(P.y, static_cast<int64_t>(t0 + t) * d_out + i, hrow[m][0] * acc[0][t] + hrow[m][1] * acc[1][t]);
+      for (int j = 0; j < kGather; ++j) {
+        const int e = e0 + tid + kThreads * j;
+        if (e < n) {
+          const int pp = e >= per_path ? 1 : 0;
+          const int el = e - pp * per_path;
+          const int row = static_cast<int>(fast_div(static_cast<uint32_t>(el), P.magic_r));  // tl * nsrc + run
+          raw[(pp * tch * nsrc + row) * R4 + (el - row * r)] = slot_value(sv[j]);
+        }
       }
     }
     __syncthreads();
+    // l (.) z of 4 latents = the sum of their partials (ascending run order),
+    // then the nibble table over them
+    for (int pt = bpt; bpt < bstep && pt < 2 * tn; pt += bstep) {
+      const int pp = pt >= tn ? 1 : 0;
+      const int tl = pt - pp * tn;
+      f32x4 w4 = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (4 * bgrp < R4) {
+        const float* rs = raw + ((pp * tch + tl) * nsrc) * R4 + 4 * bgrp;
+        for (int cc = 0; cc < nsrc; ++cc) w4 += *reinterpret_cast<const f32x4*>(rs + cc * R4);
+      }
+      build_table(tb2 + ((pp * tch + tl) * nw + (bgrp >> 3)) * kBlk + 16 * (bgrp & 7), bgrp & 7, w4[0], w4[1],
+                  w4[2], w4[3]);
+    }
+    __syncthreads();
+    // contraction of row i with both paths; lane kq covers words kq, kq + 4, ...
+    float acc[2][TM];
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+      for (int t = 0; t < TM; ++t) acc[pp][t] = 0.0f;
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+      for (int e = 0; e < WPL; ++e) {
+        const int kb = kq + kKQ * e;
+        if (kb < nw) {
+          const uint32_t wk = ((wlo[pp][e] & 0xffffu) | (whi[pp][e] << 16)) ^ kKey;
+#pragma unroll
+          for (int t = 0; t < TM; ++t)
+            if (t < tn) acc[pp][t] += word_sum(tb2 + ((pp * tch + t) * nw + kb) * kBlk, wk);
+        }
+      }
+    const float h0 = bits_to_f32<SC>(hb[0]), h1 = bits_to_f32<SC>(hb[1]);
+#pragma unroll
+    for (int t = 0; t < TM; ++t) {
+      const float v = h0 * quad_sum(acc[0][t]) + h1 * quad_sum(acc[1][t]);
+      if (iok && t < tn && kq == t) st<ACT>(P.y, static_cast<int64_t>(t0 + t) * d_out + i, v);
+    }
+    __syncthreads();  // the next token chunk reuses the LDS
   }
   if (!ok) atomic_store_relaxed(P.ctrl + kCtrlError, 1u);
 
@@ -444,120 +397,119 @@ __device__ void stage2(const DecodeParams& P, int q, float* smem) {
   }
 }
 
-template <int TM, int ACT, int SC, bool VEC>
+template <int TM, int ACT, int SC, bool VEC, int WPL>
 __global__ void __launch_bounds__(kThreads, 2) decode_kernel(DecodeParams P) {
-  extern __shared__ float smem[];
-  // each stage loads the epoch itself, together with its other loads
+  extern __shared__ __attribute__((aligned(16))) float smem[];
   const int wg = blockIdx.x;
   if (wg < P.n_s1)
     stage1<TM, ACT, SC, VEC>(P, wg, smem);
   else
-    stage2<TM, ACT, SC>(P, wg - P.n_s1, smem);
+    stage2<TM, ACT, SC, WPL>(P, wg - P.n_s1, smem);
 }
 
-template <int ACT, int SC>
-hipError_t launch_typed(const DecodeParams& P, dim3 grid, size_t smem, hipStream_t stream) {
-  // x and g read as 4-element vectors when aligned (decided on the host); the
-  // element-wise form is compiled for the widest token count only
-  if (!P.x_vec || !P.g_vec)
-    hipLaunchKernelGGL((decode_kernel<kDecodeMaxTokens, ACT, SC, false>), grid, dim3(kThreads), smem, stream, P);
-  else if (P.T <= 1)
-    hipLaunchKernelGGL((decode_kernel<1, ACT, SC, true>), grid, dim3(kThreads), smem, stream, P);
-  else if (P.T <= 2)
-    hipLaunchKernelGGL((decode_kernel<2, ACT, SC, true>), grid, dim3(kThreads), smem, stream, P);
-  else if (P.T <= 4)
-    hipLaunchKernelGGL((decode_kernel<4, ACT, SC, true>), grid, dim3(kThreads), smem, stream, P);
-  else
-    return hipErrorInvalidValue;  // T <= kDecodeMaxTokens is checked by the caller
+template <int TM, int ACT, int SC, bool VEC, int WPL>
+hipError_t launch_one(const DecodeParams& P, dim3 grid, size_t smem, hipStream_t stream) {
+  // more than the default dynamic LDS limit: raise the kernel's limit once per
+  // size increase, so calls captured in a graph after an eager call of the
+  // same shape make no attribute call
+  static std::atomic<size_t> limit{65536};
+  if (smem > limit.load()) {
+    const void* fn = reinterpret_cast<const void*>(&decode_kernel<TM, ACT, SC, VEC, WPL>);
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
+    if (e != hipSuccess) return e;
+    limit.store(smem);
+  }
+  hipLaunchKernelGGL((decode_kernel<TM, ACT, SC, VEC, WPL>), grid, dim3(kThreads), smem, stream, P);
   return hipGetLastError();
 }
 
+template <int TM, int ACT, int SC, bool VEC>
+hipError_t launch_wpl(const DecodeParams& P, int wpl, dim3 grid, size_t smem, hipStream_t stream) {
+  switch (wpl) {
+    case 1: return launch_one<TM, ACT, SC, VEC, 1>(P, grid, smem, stream);
+    case 2: return launch_one<TM, ACT, SC, VEC, 2>(P, grid, smem, stream);
+    case 4: return launch_one<TM, ACT, SC, VEC, 4>(P, grid, smem, stream);
+    default: return launch_one<TM, ACT, SC, VEC, 8>(P, grid, smem, stream);
+  }
+}
+
+template <int ACT, int SC>
+hipError_t launch_typed(const DecodeParams& P, bool vec, int wpl, dim3 grid, size_t smem, hipStream_t stream) {
+  // x and g read as 4-element vectors when aligned (decided on the host); the
+  // element-wise form is compiled for the widest token count only
+  if (!vec) return launch_wpl<kDecodeMaxTokens, ACT, SC, false>(P, wpl, grid, smem, stream);
+  if (P.T <= 1) return launch_wpl<1, ACT, SC, true>(P, wpl, grid, smem, stream);
+  if (P.T <= 2) return launch_wpl<2, ACT, SC, true>(P, wpl, grid, smem, stream);
+  return launch_wpl<4, ACT, SC, true>(P, wpl, grid, smem, stream);
+}
+
 template <int ACT>
-hipError_t launch_act(const DecodeParams& P, dim3 grid, size_t smem, hipStream_t stream) {
-  switch (P.sc_dt) {
-    case kDtF32: return launch_typed<ACT, kDtF32>(P, grid, smem, stream);
-    case kDtF16: return launch_typed<ACT, kDtF16>(P, grid, smem, stream);
-    default: return launch_typed<ACT, kDtBF16>(P, grid, smem, stream);
+hipError_t launch_act(const DecodeParams& P, int sc_dt, bool vec, int wpl, dim3 grid, size_t smem,
+                      hipStream_t stream) {
+  switch (sc_dt) {
+    case kDtF32: return launch_typed<ACT, kDtF32>(P, vec, wpl, grid, smem, stream);
+    case kDtF16: return launch_typed<ACT, kDtF16>(P, vec, wpl, grid, smem, stream);
+    default: return launch_typed<ACT, kDtBF16>(P, vec, wpl, grid, smem, stream);
   }
 }
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
-size_t stage2_floats_per_token(int r, int nsrc) {
-  const int nw = nblocks32(r);
-  return static_cast<size_t>(2) * (static_cast<size_t>(nsrc) * r + static_cast<size_t>(nw) * kLutBlock);
+int64_t packed_bytes(int64_t n_out, int64_t n_red) {
+  const int64_t w = n_red & 31;
+  return 4 * (n_red >> 5) * n_out + (w == 0 ? 0 : (w <= 16 ? 2 : 4)) * n_out;
 }
 
-size_t decode_smem_bytes(const DecodeGeom& g, int T, int r) {
-  const size_t s1a = static_cast<size_t>(T) * g.cb * kLutBlock;
-  const size_t s1b = static_cast<size_t>(4) * T * kKc;
-  const size_t s2 = g.tch * stage2_floats_per_token(r, g.direct ? g.s1d : 1);
-  size_t m = s1a > s1b ? s1a : s1b;
-  if (s2 > m) m = s2;
-  return 4 * m;
+size_t stage2_floats_per_token(int r, int nsrc) {
+  const size_t R4 = (static_cast<size_t>(r) + 3) & ~static_cast<size_t>(3);
+  return 2 * (static_cast<size_t>(nsrc) * R4 + static_cast<size_t>(nblocks32(r)) * kBlk);
 }
+
+int tm_of(int T) { return T <= 1 ? 1 : (T <= 2 ? 2 : 4); }
 
 }  // namespace
 
 DecodeGeom decode_geometry(int T, int d_in, int d_out, int r) {
   DecodeGeom g{};
-  g.kc = kKc;
+  const int tt = T > 0 ? T : 1;
   g.nkt = (r + kKc - 1) / kKc;
   const int nbt = nblocks32(d_in);
-  const int tt = T > 0 ? T : 1;
-  const int nw = nblocks32(r);
-  // blocks per staged chunk: bounded by the LDS tables, the table groups a
-  // thread builds and the V words a lane holds
-  int cb = kLdsFloats / (kLutBlock * tt);
-  const int cb_groups = kThreads * kMaxGroupsPerThread / (8 * tt);
-  if (cb > cb_groups) cb = cb_groups;
-  if (cb > 16 * kMaxWordsPerLane) cb = 16 * kMaxWordsPerLane;
-  if (cb < 1) cb = 1;
-  // d_in runs: one staged chunk per workgroup when T is small, so that every
-  // load of stage 1 is a single round; at most kMaxSplit partials per value
-  int s1d = (nbt + cb - 1) / cb;
-  if (s1d > kMaxSplit) s1d = kMaxSplit;
+  int s1d = (nbt + kChunk - 1) / kChunk;
+  if (s1d > kMaxRuns) s1d = kMaxRuns;
   if (s1d < 1) s1d = 1;
-  g.bpw = nbt > 0 ? (nbt + s1d - 1) / s1d : 1;
-  g.s1d = nbt > 0 ? (nbt + g.bpw - 1) / g.bpw : 0;
-  if (cb > g.bpw) cb = g.bpw;
-  g.cb = cb;
+  g.bpr = nbt > 0 ? (nbt + s1d - 1) / s1d : 1;
+  g.s1d = nbt > 0 ? (nbt + g.bpr - 1) / g.bpr : 1;
   g.n_s1 = 2 * g.nkt * g.s1d;
-  // stage 2 reads every partial when one token's slots fit one gather round and
-  // the LDS, else the two-level reducers' sums
-  g.direct = (g.s1d * r <= kThreads * kSlotsPerPath) &&
-             stage2_floats_per_token(r, g.s1d) <= static_cast<size_t>(kLdsFloats);
-  // lanes per output row (4..16): the fewest that leave each lane at most
-  // kRowWords of the row's words per path
-  int kq_log2 = 2;
-  while (kq_log2 < 4 && (nw + (1 << kq_log2) - 1) >> kq_log2 > kRowWords) ++kq_log2;
-  g.kq_log2 = kq_log2;
-  // rows per lane: enough to keep the stage-2 workgroups near 256
-  const int rows_per_pass = kThreads >> kq_log2;
-  const int groups = (d_out + rows_per_pass - 1) / rows_per_pass;
-  int passes = (groups + 255) / 256;
-  if (passes > max_passes(T)) passes = max_passes(T);
-  if (passes < 1) passes = 1;
-  g.rows2 = rows_per_pass * passes;
-  g.n_s2 = (d_out + g.rows2 - 1) / g.rows2;
-  // tokens per stage-2 chunk: LDS for the gathered slots and the tables, and one
-  // gather round per chunk
+  g.direct = g.s1d == 1 || static_cast<int64_t>(2) * tt * g.s1d * r <= kDirectMaxSlots;
   const int nsrc = g.direct ? g.s1d : 1;
   const size_t per_tok = stage2_floats_per_token(r, nsrc);
-  int tch = per_tok > 0 ? static_cast<int>(kLdsFloats / per_tok) : tt;
-  const int per_tok_slots = nsrc * r;  // per path
-  const int tch_slots = per_tok_slots > 0 ? kThreads * kSlotsPerPath / per_tok_slots : tt;
-  if (tch > tch_slots) tch = tch_slots;
+  int tch = per_tok > 0 ? static_cast<int>(kLds2Max / (4 * per_tok)) : tt;
   if (tch > tt) tch = tt;
   if (tch < 1) tch = 1;
   g.tch = tch;
-  // tagged 8-byte slots
+  g.n_s2 = (d_out + kRows2 - 1) / kRows2;
+  const int nw = nblocks32(r);
+  g.wpl = nw <= kKQ ? 1 : (nw <= 2 * kKQ ? 2 : (nw <= 4 * kKQ ? 4 : 8));
+  // LDS: stage-1 tables of tm_of(T) tokens (of kDecodeMaxTokens for the
+  // element-wise variant, smem_bytes_elem), stage-2 gathered partials and tables
+  const size_t s1 = static_cast<size_t>(4) * tm_of(tt) * kChunk * kBlk;
+  const size_t s1e = static_cast<size_t>(4) * kDecodeMaxTokens * kChunk * kBlk;
+  const size_t s2 = 4 * tch * per_tok;
+  g.smem_bytes = s1 > s2 ? s1 : s2;
+  g.smem_bytes_elem = s1e > s2 ? s1e : s2;
   g.partial_off = kCtrlBytes;
-  g.partial_floats = static_cast<size_t>(2) * g.s1d * T * r;
-  g.wbuf_off = g.partial_off + align256(8 * g.partial_floats);
-  g.wbuf_floats = g.direct ? 0 : static_cast<size_t>(2) * T * r;
-  g.ws_bytes = g.wbuf_off + align256(8 * g.wbuf_floats);
+  g.partial_slots = static_cast<size_t>(2) * g.s1d * T * r;
+  g.wbuf_off = g.partial_off + align256(8 * g.partial_slots);
+  g.wbuf_slots = g.direct ? 0 : static_cast<size_t>(2) * T * r;
+  g.ws_bytes = g.wbuf_off + align256(8 * g.wbuf_slots);
   return g;
+}
+
+bool decode_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
+  // buffer offsets are 32-bit: every operand stays below 2^31 bytes
+  const int64_t lim = int64_t(1) << 31;
+  return T <= kDecodeMaxTokens && r <= kDecodeMaxRank && T * d_in * 4 < lim && packed_bytes(d_out, r) < lim &&
+         packed_bytes(r, d_in) < lim && d_out * 4 < lim && d_in * 4 < lim;
 }
 
 hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t stream) {
@@ -575,31 +527,34 @@ hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t 
   P.ctrl = reinterpret_cast<uint32_t*>(ws);
   P.partial = reinterpret_cast<uint64_t*>(ws + g.partial_off);
   P.wbuf = reinterpret_cast<uint64_t*>(ws + g.wbuf_off);
-  P.act_dt = a.act_dt;
-  P.sc_dt = a.sc_dt;
-  const uintptr_t xa = a.act_dt == kDtF32 ? 16 : 8, ga = a.sc_dt == kDtF32 ? 16 : 8;
-  P.x_vec = (reinterpret_cast<uintptr_t>(a.x) % xa == 0) && (a.d_in % 4 == 0);
-  P.g_vec = (reinterpret_cast<uintptr_t>(a.g[0]) % ga == 0) && (reinterpret_cast<uintptr_t>(a.g[1]) % ga == 0);
   P.T = a.T;
   P.d_in = a.d_in;
   P.d_out = a.d_out;
   P.r = a.r;
   P.nkt = g.nkt;
-  P.cb = g.cb;
-  P.bpw = g.bpw;
   P.s1d = g.s1d;
+  P.bpr = g.bpr;
   P.n_s1 = g.n_s1;
-  P.kq_log2 = g.kq_log2;
-  P.rows2 = g.rows2;
   P.n_s2 = g.n_s2;
   P.direct = g.direct;
   P.tch = g.tch;
-  const size_t smem = decode_smem_bytes(g, a.T, a.r);
+  P.magic_r = a.r > 1 ? static_cast<uint32_t>(((uint64_t(1) << 32) + a.r - 1) / a.r) : 0u;
+  const int64_t ex = a.act_dt == kDtF32 ? 4 : 2, es = a.sc_dt == kDtF32 ? 4 : 2;
+  P.x_bytes = static_cast<uint32_t>(static_cast<int64_t>(a.T) * a.d_in * ex);
+  P.g_bytes = static_cast<uint32_t>(a.d_in * es);
+  P.h_bytes = static_cast<uint32_t>(a.d_out * es);
+  P.l_bytes = static_cast<uint32_t>(a.r * es);
+  P.v_bytes = static_cast<uint32_t>(packed_bytes(a.r, a.d_in));
+  P.u_bytes = static_cast<uint32_t>(packed_bytes(a.d_out, a.r));
+  const uintptr_t xa = 4 * ex, ga = 4 * es;
+  const bool vec = (reinterpret_cast<uintptr_t>(a.x) % xa == 0) && (a.d_in % 4 == 0) &&
+                   (reinterpret_cast<uintptr_t>(a.g[0]) % ga == 0) && (reinterpret_cast<uintptr_t>(a.g[1]) % ga == 0);
   const dim3 grid(g.n_s1 + g.n_s2);
+  const size_t smem = vec ? g.smem_bytes : g.smem_bytes_elem;
   switch (a.act_dt) {
-    case kDtF32: return launch_act<kDtF32>(P, grid, smem, stream);
-    case kDtF16: return launch_act<kDtF16>(P, grid, smem, stream);
-    default: return launch_act<kDtBF16>(P, grid, smem, stream);
+    case kDtF32: return launch_act<kDtF32>(P, a.sc_dt, vec, g.wpl, grid, smem, stream);
+    case kDtF16: return launch_act<kDtF16>(P, a.sc_dt, vec, g.wpl, grid, smem, stream);
+    default: return launch_act<kDtBF16>(P, a.sc_dt, vec, g.wpl, grid, smem, stream);
   }
 }
 

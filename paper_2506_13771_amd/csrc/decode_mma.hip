@@ -50,9 +50,6 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
@@ -60,7 +57,6 @@ constexpr int kMaxRuns = 32;                  // d_in runs per latent tile (part
 constexpr int kMaxUWords = kMmaMaxRank / 32;  // stage 2: full U words of one row and path in registers
 constexpr int kGather = 8;                    // stage 2: slots a thread gathers per round
 constexpr int kDirectMaxSlots = 8192;         // stage 2 reads every partial when there are at most this many
-constexpr uint32_t kOob = 0x7ffffff0u;        // a buffer offset past every buffer: loads return 0
 
 // exact bf16 terms of a value stored in dtype DT
 template <int DT>
@@ -94,39 +90,6 @@ struct MmaParams {
   uint32_t x_bytes, g_bytes, v_bytes, u_bytes, h_bytes, l_bytes;
   uint32_t magic_r;  // ceil(2^32 / r) (0 for r = 1): e / r as one multiply-high
 };
-
-__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0), static_cast<int>(bytes),
-                                           0x00020000);
-}
-// raw bits of element i (dtype DT) of a buffer; 0 past its end
-template <int DT>
-__device__ __forceinline__ uint32_t bload(rsrc_t r, uint32_t i, bool valid = true) {
-  if constexpr (DT == kDtF32)
-    return __builtin_amdgcn_raw_buffer_load_b32(r, valid ? i * 4u : kOob, 0, 0);
-  else
-    return static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, valid ? i * 2u : kOob, 0, 0));
-}
-// raw bits of elements i..i+3: one 16- or 8-byte load (VEC: i a multiple of 4,
-// buffer aligned), else four element loads; taken back with raw4_elem
-template <int DT, bool VEC>
-__device__ __forceinline__ void bload4(rsrc_t r, uint32_t i, bool valid, uint32_t (&o)[4]) {
-  if constexpr (VEC && DT == kDtF32) {
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, valid ? i * 4u : kOob, 0, 0);
-    o[0] = v[0], o[1] = v[1], o[2] = v[2], o[3] = v[3];
-  } else if constexpr (VEC) {
-    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, valid ? i * 2u : kOob, 0, 0);
-    o[0] = v[0], o[1] = v[1], o[2] = 0u, o[3] = 0u;
-  } else {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = bload<DT>(r, i + e, valid);
-  }
-}
-// 16-bit element v of a bload4 group, raw bits
-template <bool VEC>
-__device__ __forceinline__ uint32_t raw16(const uint32_t (&o)[4], int v) {
-  return VEC ? (o[v >> 1] >> (16 * (v & 1))) & 0xffffu : o[v];
-}
 
 // v as N bf16 terms (bit patterns), each the leading 8 significant bits of
 // what the previous terms left: exact when v has at most 8N significant bits
@@ -359,10 +322,6 @@ __device__ __forceinline__ void mma_stage1(const MmaParams& P, int wg, float* sm
 // ---------------------------------------------------------------------------
 // stage 2
 // ---------------------------------------------------------------------------
-// q = n / d for n < 2^20, 2 <= d < 2^12, with m = ceil(2^32 / d); m = 0 stands
-// for d = 1
-__device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t m) { return m == 0 ? n : __umulhi(n, m); }
-
 template <int ACT, int SC>
 __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* smem) {
   constexpr int NW = ACT == kDtF32 ? 3 : 2;  // bf16 terms of w

@@ -167,5 +167,50 @@ __device__ __forceinline__ void st(void* p, int64_t i, float v) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// buffer loads: 32-bit byte offsets into a buffer of known size; a read past
+// the end returns zero, so absent rows, columns and blocks need no clamping
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr uint32_t kOob = 0x7ffffff0u;  // a buffer offset past every buffer: loads return 0
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0), static_cast<int>(bytes),
+                                           0x00020000);
+}
+// raw bits of element i (dtype DT) of a buffer; 0 past its end
+template <int DT>
+__device__ __forceinline__ uint32_t bload(rsrc_t r, uint32_t i, bool valid = true) {
+  if constexpr (DT == kDtF32)
+    return __builtin_amdgcn_raw_buffer_load_b32(r, valid ? i * 4u : kOob, 0, 0);
+  else
+    return static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, valid ? i * 2u : kOob, 0, 0));
+}
+// raw bits of elements i..i+3: one 16- or 8-byte load (VEC: i a multiple of 4,
+// buffer aligned), else four element loads; taken back with raw4_elem
+template <int DT, bool VEC>
+__device__ __forceinline__ void bload4(rsrc_t r, uint32_t i, bool valid, uint32_t (&o)[4]) {
+  if constexpr (VEC && DT == kDtF32) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, valid ? i * 4u : kOob, 0, 0);
+    o[0] = v[0], o[1] = v[1], o[2] = v[2], o[3] = v[3];
+  } else if constexpr (VEC) {
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, valid ? i * 2u : kOob, 0, 0);
+    o[0] = v[0], o[1] = v[1], o[2] = 0u, o[3] = 0u;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = bload<DT>(r, i + e, valid);
+  }
+}
+// 16-bit element v of a bload4 group, raw bits
+template <bool VEC>
+__device__ __forceinline__ uint32_t raw16(const uint32_t (&o)[4], int v) {
+  return VEC ? (o[v >> 1] >> (16 * (v & 1))) & 0xffffu : o[v];
+}
+
+// q = n / d for n < 2^20, 2 <= d < 2^12, with m = ceil(2^32 / d); m = 0 stands
+// for d = 1
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t m) { return m == 0 ? n : __umulhi(n, m); }
 
 }  // namespace lb

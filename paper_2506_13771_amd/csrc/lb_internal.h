@@ -131,20 +131,26 @@ struct ForwardArgs {
   size_t ws_bytes;
 };
 
-// Decode kernel geometry (pure function of the sizes; also sizes the workspace).
+// Look-up-table decode kernel geometry (pure function of the sizes; also sizes
+// the workspace).
 struct DecodeGeom {
-  int kc, nkt, bpw, s1d, n_s1, cb;
-  int kq_log2;  // log2 of the lanes that share one output row in stage 2
-  int rows2, n_s2;
-  int direct;
-  int tch;
-  size_t partial_off, partial_floats;
-  size_t wbuf_off, wbuf_floats;
+  int nkt;     // 16-latent tiles per path
+  int s1d;     // d_in runs per tile
+  int bpr;     // 32-input blocks per run
+  int n_s1;    // stage-1 workgroups
+  int n_s2;    // stage-2 workgroups
+  int direct;  // stage 2 reads every run's partial (else two-level sums)
+  int tch;     // tokens per stage-2 chunk
+  int wpl;     // stage 2: U words per lane and path (1, 2, 4 or 8)
+  size_t smem_bytes, smem_bytes_elem;  // vector-load and element-wise variants
+  size_t partial_off, partial_slots;
+  size_t wbuf_off, wbuf_slots;
   size_t ws_bytes;
 };
 DecodeGeom decode_geometry(int T, int d_in, int d_out, int r);
+bool decode_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
 constexpr int kDecodeMaxTokens = 4;
-constexpr int kDecodeMaxRank = 1024;  // stage-2 look-up tables of one token fit in LDS
+constexpr int kDecodeMaxRank = 1024;  // stage-2 tables of one token fit in LDS
 
 // Matrix-core decode kernel geometry.
 struct MmaGeom {
