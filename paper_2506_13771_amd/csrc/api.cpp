@@ -175,6 +175,7 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
   if (st != LB_OK) return st;
   if (kernel == LB_KERNEL_DECODE && !lb::decode_supports(T, d_in, d_out, r)) return LB_ERR_SHAPE;
   if (kernel == LB_KERNEL_DECODE_MFMA && !lb::decode_mma_supports(T, d_in, d_out, r)) return LB_ERR_SHAPE;
+  if (kernel == LB_KERNEL_PREFILL && !lb::prefill_supports(T, d_in, d_out, r)) return LB_ERR_SHAPE;
   if (T == 0 || d_out == 0) return LB_OK;
   if (!y || (d_in > 0 && !x)) return LB_ERR_NULL;
   if (!aligned(x, dtype_size(act_dtype)) || !aligned(y, dtype_size(act_dtype))) return LB_ERR_ALIGN;
@@ -198,8 +199,10 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
       kernel = LB_KERNEL_DECODE;
     else if (lb::decode_mma_supports(T, d_in, d_out, r))
       kernel = LB_KERNEL_DECODE_MFMA;
-    else
+    else if (lb::prefill_supports(T, d_in, d_out, r))
       kernel = LB_KERNEL_PREFILL;
+    else
+      return LB_ERR_SHAPE;
   }
   if (kernel == LB_KERNEL_DECODE)
     e = lb::launch_decode(a, lb::decode_geometry(a.T, a.d_in, a.d_out, a.r), stream);

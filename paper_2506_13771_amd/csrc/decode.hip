@@ -134,7 +134,7 @@ __device__ void stage1(const DecodeParams& P, int wg, float* smem) {
   const int c = rem - kt * P.s1d;
   const int T = P.T, r = P.r, d_in = P.d_in;
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;  // wave index in a scalar
   const int kk = tid & 15, m = (tid >> 4) & 3;
   const int k = kt * kKc + kk;  // this lane's latent column
   const bool kok = k < r;

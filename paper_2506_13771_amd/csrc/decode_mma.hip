@@ -48,9 +48,6 @@ namespace lb {
 
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr int kMaxRuns = 32;                  // d_in runs per latent tile (partials per z value)
@@ -58,11 +55,6 @@ constexpr int kMaxUWords = kMmaMaxRank / 32;  // stage 2: full U words of one ro
 constexpr int kGather = 8;                    // stage 2: slots a thread gathers per round
 constexpr int kDirectMaxSlots = 8192;         // stage 2 reads every partial when there are at most this many
 
-// exact bf16 terms of a value stored in dtype DT
-template <int DT>
-__host__ __device__ constexpr int nterms() {
-  return DT == kDtF32 ? 3 : (DT == kDtF16 ? 2 : 1);
-}
 // 32-wide input blocks a stage-1 wave holds in registers per round
 __host__ __device__ constexpr int kpw_of(int tt, int act) {
   return (tt == 1 ? 8 : (tt == 2 ? 6 : 4)) / (act == kDtF32 ? 2 : 1);
@@ -90,47 +82,6 @@ struct MmaParams {
   uint32_t x_bytes, g_bytes, v_bytes, u_bytes, h_bytes, l_bytes;
   uint32_t magic_r;  // ceil(2^32 / r) (0 for r = 1): e / r as one multiply-high
 };
-
-// v as N bf16 terms (bit patterns), each the leading 8 significant bits of
-// what the previous terms left: exact when v has at most 8N significant bits
-// (a bf16, f16 or fp32 value with N = its nterms)
-template <int N>
-__device__ __forceinline__ void split_exact(float v, uint32_t (&o)[N]) {
-  float rem = v;
-#pragma unroll
-  for (int s = 0; s < N; ++s) {
-    const uint32_t b = __float_as_uint(rem) & 0xffff0000u;
-    o[s] = b >> 16;
-    rem = rem - __uint_as_float(b);
-  }
-}
-// v (any fp32) as N bf16 terms: leading bits, the last term rounded to nearest
-template <int N>
-__device__ __forceinline__ void split_round(float v, uint32_t (&o)[N]) {
-  float rem = v;
-#pragma unroll
-  for (int s = 0; s < N - 1; ++s) {
-    const uint32_t b = __float_as_uint(rem) & 0xffff0000u;
-    o[s] = b >> 16;
-    rem = rem - __uint_as_float(b);
-  }
-  o[N - 1] = f32_to_bf16_bits(rem);
-}
-
-__device__ __forceinline__ floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
-                                                 0, 0);
-}
-
-// signs of a packed word (this lane group's nibbles) on bf16 term pairs t[v]:
-// the low half takes the sign of bit 4gq+v, the high half of bit 4gq+v+16
-__device__ __forceinline__ u32x4 sign_terms(uint32_t word, int gq, const uint32_t (&t)[4]) {
-  const uint32_t ws = word >> (4 * gq);
-  u32x4 a;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) a[v] = ((ws << (15 - v)) & 0x80008000u) ^ t[v];
-  return a;
-}
 
 // ---------------------------------------------------------------------------
 // stage 1
@@ -233,7 +184,7 @@ __device__ __forceinline__ void mma_stage1(const MmaParams& P, int wg, float* sm
   const int c = rem - mf * P.s1d;
   const int T = P.T, r = P.r;
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;  // wave index in a scalar
   const int k0 = 16 * mf;
   const int nbt = nblocks32(P.d_in), nbv = P.d_in >> 5;
   const int b0 = c * P.bpr;
@@ -327,7 +278,7 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
   constexpr int NW = ACT == kDtF32 ? 3 : 2;  // bf16 terms of w
   const int T = P.T, r = P.r, d_out = P.d_out;
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;  // wave index in a scalar
   const int n16 = lane & 15, gq = lane >> 4;
   const int nkb = nblocks32(r);
   const int nbu = r >> 5, tailu = r & 31;

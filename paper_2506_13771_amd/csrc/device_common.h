@@ -180,6 +180,17 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0), static_cast<int>(bytes),
                                            0x00020000);
 }
+// A buffer descriptor from a pointer and size the compiler cannot prove
+// uniform (computed from block indices through 64-bit arithmetic): read back
+// from the first lane, so the descriptor lives in scalar registers and the
+// accesses need no per-lane descriptor loop.
+__device__ __forceinline__ rsrc_t make_rsrc_uniform(const void* p, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32));
+  return make_rsrc(reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo),
+                   __builtin_amdgcn_readfirstlane(bytes));
+}
 // raw bits of element i (dtype DT) of a buffer; 0 past its end
 template <int DT>
 __device__ __forceinline__ uint32_t bload(rsrc_t r, uint32_t i, bool valid = true) {
@@ -212,5 +223,64 @@ __device__ __forceinline__ uint32_t raw16(const uint32_t (&o)[4], int v) {
 // q = n / d for n < 2^20, 2 <= d < 2^12, with m = ceil(2^32 / d); m = 0 stands
 // for d = 1
 __device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t m) { return m == 0 ? n : __umulhi(n, m); }
+
+// ---------------------------------------------------------------------------
+// matrix-core operands (v_mfma_f32_16x16x32_bf16).  Fragment layout: lane l
+// holds row l % 16 of A (column l % 16 of B) at 8 reduction slots; register v
+// of lane group gq = l / 16 holds the pair of reduction indices
+// (4 gq + v, 4 gq + v + 16) of a 32-wide block (low, high half), the same
+// relabelling of K for both operands, which puts bit 4 gq + v of a packed word
+// (LB layout v1) at the bf16 sign of the low half and bit 4 gq + v + 16 at the
+// high half with one shift and one mask.  The result lane holds rows
+// 4 gq + e (e < 4) of column l % 16.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// exact bf16 terms of a value stored in dtype DT
+template <int DT>
+__host__ __device__ constexpr int nterms() {
+  return DT == kDtF32 ? 3 : (DT == kDtF16 ? 2 : 1);
+}
+// v as N bf16 terms (bit patterns), each the leading 8 significant bits of
+// what the previous terms left: exact when v has at most 8N significant bits
+// (a bf16, f16 or fp32 value with N = its nterms)
+template <int N>
+__device__ __forceinline__ void split_exact(float v, uint32_t (&o)[N]) {
+  float rem = v;
+#pragma unroll
+  for (int s = 0; s < N; ++s) {
+    const uint32_t b = __float_as_uint(rem) & 0xffff0000u;
+    o[s] = b >> 16;
+    rem = rem - __uint_as_float(b);
+  }
+}
+// v (any fp32) as N bf16 terms: leading bits, the last term rounded to nearest
+template <int N>
+__device__ __forceinline__ void split_round(float v, uint32_t (&o)[N]) {
+  float rem = v;
+#pragma unroll
+  for (int s = 0; s < N - 1; ++s) {
+    const uint32_t b = __float_as_uint(rem) & 0xffff0000u;
+    o[s] = b >> 16;
+    rem = rem - __uint_as_float(b);
+  }
+  o[N - 1] = f32_to_bf16_bits(rem);
+}
+
+__device__ __forceinline__ floatx4 mfma(u32x4 a, u32x4 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
+
+// signs of a packed word (this lane group's nibbles) on bf16 term pairs t[v]:
+// the low half takes the sign of bit 4gq+v, the high half of bit 4gq+v+16
+__device__ __forceinline__ u32x4 sign_terms(uint32_t word, int gq, const uint32_t (&t)[4]) {
+  const uint32_t ws = word >> (4 * gq);
+  u32x4 a;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) a[v] = ((ws << (15 - v)) & 0x80008000u) ^ t[v];
+  return a;
+}
 
 }  // namespace lb

@@ -32,10 +32,9 @@ __device__ __forceinline__ float load_as_f32(const void* p, int64_t i, int dt) {
 
 // fp32 -> bf16 bit pattern, round to nearest even; NaN stays NaN (quiet).
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  return (u & 0x7fffffffu) > 0x7f800000u ? ((u >> 16) | 0x40u) : rne;  // a select, not a branch
 }
 
 __device__ __forceinline__ void store_from_f32(void* p, int64_t i, int dt, float v) {
@@ -171,16 +170,19 @@ MmaGeom decode_mma_geometry(int T, int d_in, int d_out, int r, int act_dt);
 bool decode_mma_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
 
 struct PrefillGeom {
-  int bm;                  // tokens per M-tile
-  int n_mt;                // M-tiles
-  int s1_nw, s1_spw;       // stage-1 waves per workgroup and 16-column subtiles per wave
-  int s1_bn, s1_nnt;       // stage-1 columns per N-tile and N-tiles
-  int ks;                  // stage-1 split of the d_in reduction
-  int s2_nw, s2_spw, s2_bn, s2_nnt;
-  size_t wbuf_off, wbuf_floats;
+  int nkb;           // 32-latent blocks per path
+  int npt;           // stage-1 (path, latent block) pairs per tile
+  int n_lt, n_tt;    // stage-1 latent tiles, token tiles (32 tokens)
+  int ks, kb_per;    // stage-1 splits of d_in, 32-input steps per split
+  int n_ot, n_tt2;   // stage-2 output tiles (256 outputs), token tiles (64 tokens)
+  int kbc;           // stage-2 32-latent blocks staged in LDS per round
+  size_t smem1;      // stage-1 dynamic LDS
+  size_t pbuf_off, pbuf_floats;
+  size_t wterm_off, wterm_bytes;
   size_t ws_bytes;
 };
 PrefillGeom prefill_geometry(int T, int d_in, int d_out, int r);
+bool prefill_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
 
 hipError_t launch_pack(const void* src, int dt, int rows, int r, int role, void* dst, int32_t* nan_count,
                        hipStream_t stream);
