@@ -107,9 +107,7 @@ __device__ __forceinline__ bool spin_until_at_least(const uint32_t* p, uint32_t 
 constexpr int kCtrlEpoch = 0;      // decode: tag of the last completed call
 constexpr int kCtrlDone = 1;       // decode: finished stage-2 workgroups of the running call
 constexpr int kCtrlError = 2;      // set to nonzero if a bounded wait expired
-constexpr int kCtrlTiles = 64;     // prefill: per-tile counters (3 words each)
-constexpr int kCtrlMaxTiles = 8192;
-constexpr int kCtrlWords = kCtrlTiles + 3 * kCtrlMaxTiles;
+constexpr int kCtrlWords = 64;
 constexpr size_t kCtrlBytes = ((kCtrlWords * 4 + 255) / 256) * 256;
 
 // ---------------------------------------------------------------------------
@@ -171,12 +169,16 @@ bool decode_mma_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
 
 struct PrefillGeom {
   int nkb;           // 32-latent blocks per path
-  int npt;           // stage-1 (path, latent block) pairs per tile
-  int n_lt, n_tt;    // stage-1 latent tiles, token tiles (32 tokens)
+  int ns16;          // 16-latent subtiles per path
+  int ms, n_lt;      // stage-1 subtiles per wave, latent tiles
+  int n_tt;          // stage-1 token tiles (64 tokens)
   int ks, kb_per;    // stage-1 splits of d_in, 32-input steps per split
-  int n_ot, n_tt2;   // stage-2 output tiles (256 outputs), token tiles (64 tokens)
-  int kbc;           // stage-2 32-latent blocks staged in LDS per round
-  size_t smem1;      // stage-1 dynamic LDS
+  int ns16p;         // stage-1 partial-sum subtile slots per path
+  int n_un, n_og;    // stage-2 output units (128 outputs), output groups
+  int n_tt2;         // stage-2 token tiles (64 tokens)
+  int res;           // stage 2 holds every w fragment of its tile in LDS
+  int kbc;           // stage-2 32-latent blocks per chunk when not resident
+  size_t smem1, smem2;  // dynamic LDS of the two matrix-core stages
   size_t pbuf_off, pbuf_floats;
   size_t wterm_off, wterm_bytes;
   size_t ws_bytes;

@@ -7,33 +7,41 @@
 //   P1b: w_p[t][k] = l_p[k] z_p[t][k], cut into bf16 terms
 //   P2:  y[t][i]   = sum_p h_p[i] sum_k s(U_p)[i][k] w_p[t][k]    (M = outputs, N = tokens, K = r)
 //
-// P1.  The A operand is the sign of V_p XORed into the sign bits of exact
-// bf16 terms of g_p (1 term for bf16, 2 for f16, 3 for fp32 scales), the B
-// operand the exact bf16 terms of x (1, 2 or 3 by the activation dtype), so
-// every product is exact and the matrix cores accumulate in fp32.  A
-// workgroup owns 64 tokens (each A fragment feeds 4 token subtiles: the
-// VALU work of cutting it stays below the matrix-core work) and a tile of up
-// to 6 (path, 32-latent block) pairs -- all latents of both paths for r <= 96
-// -- so x is read once per latent tile.  Its range of d_in is split over `ks`
-// workgroups (about 256 workgroups in all); its 4 waves take interleaved
-// 32-input steps with the next step's loads in flight, the g terms of its
-// range are cut once into LDS, and the 4 waves are summed in LDS in a fixed
-// order into the workgroup's partial sums.
-// P1b.  Sums the ks partials in ascending order, scales by l and stores w as
-// NW bf16 terms (2 for bf16/f16 outputs: 16 significant bits; 3 for fp32
-// outputs: all 24), already laid out as B fragments of P2.  The launch
-// boundaries order P1 -> P1b -> P2: no workgroup waits for another.
-// P2.  A = the U signs as bf16 +-1 (exact), B = the w terms.  A workgroup owns
-// 256 outputs x 64 tokens (a wave 64 x 64, 16 accumulator tiles per path).
-// Per path it loads the w fragments, U words and row scales it needs straight
-// into LDS (global-to-LDS loads, no registers), then runs its products from
-// LDS; registers hold the accumulators only, so two workgroups share a CU and
-// one's loads and stores overlap the other's products.  Both paths accumulate
-// separately and y = h_0 acc_0 + h_1 acc_1 is rounded once.
+// Every product is exact: the A operand of P1 is the sign of V_p XORed into
+// the sign bits of exact bf16 terms of g_p (1 term for bf16, 2 for f16, 3 for
+// fp32 scales), its B operand the exact bf16 terms of x (1, 2 or 3 by the
+// activation dtype); P2 multiplies exact +-1 signs by w cut into NW bf16 terms
+// (2 for bf16/f16 outputs: 16 significant bits; 3 for fp32 outputs: all 24).
+// The matrix cores accumulate in fp32.
 //
-// At 2048 tokens the matrix cores, not HBM, bound P1 and P2: each does
-// 2 * T * 2r * d fp32-accumulated multiply-adds times the number of term pairs
-// (2 for bf16 x with f16 scales in P1, 2 w terms in P2).
+// P1.  A workgroup owns 64 tokens, a range of d_in (split over `ks`
+// workgroups, about 256 in all) and a tile of latents; its waves split the
+// latents: waves 0-1 take path 0, waves 2-3 path 1, each MS interleaved
+// 16-latent subtiles of its path, so a wave holds MS x 4 accumulator tiles
+// and no sum crosses waves.  The 32-input steps of the range stream through a
+// ring of kRing1 LDS slots filled by global-to-LDS loads (x of the 64 tokens,
+// written in B-fragment order, and the V words of every wave), kRing1 - 1
+// steps in flight; one barrier per step hands a slot from its loads to its
+// readers and back.  The g terms of the range are cut once into LDS.  Each
+// wave stores its sums to its own slice of the partial buffer.
+// P1b.  Sums the ks partials in ascending order, scales by l and stores w as
+// NW bf16 terms laid out as B fragments of P2.
+// P2.  A workgroup owns 64 tokens and a group of 128-output units.  It loads
+// the w fragments of its tokens into LDS once (when they fit; else per chunk)
+// and then runs its units: waves split a unit into 2 x 64 outputs times
+// 2 x 32 tokens.  The packed U words of the next unit are loaded into LDS and
+// its row scales into registers while the current unit runs.  Both paths
+// accumulate separately and y = h_0 acc_0 + h_1 acc_1 is rounded once.
+//
+// P1 fragment order.  A 32-input step of B (x) is read as 16 bytes per lane:
+// lane group gq holds inputs 8 gq .. 8 gq + 7 of the step, register v the pair
+// (8 gq + 2 v, 8 gq + 2 v + 1), which is the memory order of x.  The A operand
+// takes the same order from a packed word: with t = word >> 8 gq,
+// d = (t & 0xffff) | ((t << 15) & 0xffff0000) holds the bit of input 2 v of the
+// group at bit 2 v and that of input 2 v + 1 at bit 2 v + 16, and one shift
+// by 15 - 2 v moves the pair onto the two bf16 sign bits.  P2 uses the
+// relabelled order of sign_terms (its B operand is produced by P1b in that
+// order).
 #include <atomic>
 
 #include "device_common.h"
@@ -44,19 +52,25 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kTok1 = 64;          // P1: tokens per workgroup (4 subtiles)
+// P1
+constexpr int kThreads1 = 512;  // 8 waves: two halves of 4 take alternate 32-input steps
+constexpr int kTok1 = 64;       // tokens per workgroup (4 subtiles of 16)
 constexpr int kTn1 = 4;
-constexpr int kMaxPairs = 6;       // P1: (path, latent block) pairs per tile
-constexpr int kMaxKbPer = 128;     // P1: 32-input steps per workgroup (g terms held in LDS)
-constexpr int kRedPairs = 2;       // P1: pairs summed across the waves per LDS round
-constexpr int kTok2 = 64;          // P2: tokens per workgroup (4 subtiles)
-constexpr int kTn2 = 4;
-constexpr int kIm2 = 4;            // P2: 16-output subtiles per wave
-constexpr int kOut2 = kWaves * kIm2 * 16;  // P2: outputs per workgroup
-constexpr int kRing = 2;           // P1: steps of loads in flight per wave
-constexpr int kMaxKbc = 8;         // P2: 32-latent blocks of one path staged per round (LDS: kMaxKbc * NW * 4 KB)
-constexpr int kPbufItem = 8;       // P1 partial floats per (pair, token, lane group)
-constexpr int kPbufPair = kTok1 * 4 * kPbufItem;
+constexpr int kMaxMs = 6;       // 16-latent subtiles per wave
+constexpr int kMinSteps = 12;   // fewest 32-input steps per split (when d_in allows)
+constexpr int kMaxKbPer = 64;   // most 32-input steps per split (its g terms are held in LDS)
+constexpr int kPart = kTn1 * 64 * 4;  // partial floats per (token tile, path, subtile)
+// P2
+constexpr int kThreads2 = 512;  // 8 waves: two halves of 4 take alternate units
+constexpr int kWaves2 = 8;
+constexpr int kTok2 = 64;       // tokens per workgroup
+constexpr int kUnit = 128;      // outputs per unit: 2 waves x 64
+constexpr int kIm2 = 4;         // 16-output subtiles per wave
+constexpr int kTn2 = 2;         // 16-token subtiles per wave
+constexpr int kMaxKbc = 8;      // 32-latent blocks per chunk when w is not resident
+constexpr size_t kLdsBudget = 160 * 1024;
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
 
 struct PrefillParams {
   const void* x;
@@ -66,307 +80,299 @@ struct PrefillParams {
   const void* h[2];
   const void* g[2];
   const void* l[2];
-  float* pbuf;      // P1: [ks][tile][npt][64 tokens][4 lane groups][8] partial sums
-  uint32_t* wterm;  // [2][NW][nkb][T][4 lane groups][4] w terms as B fragments
+  float* pbuf;      // P1: [ks][token tile][path][ns16p][4 token subtiles][64 lanes][4] partial sums
+  uint32_t* wterm;  // [2][NW][nkb][T][4 lane groups] x 16 B: w terms as P2 B fragments
   int T, d_in, d_out, r;
-  int nkb;          // 32-latent blocks per path
+  int nkb, ns16;    // 32-latent blocks, 16-latent subtiles per path
   int n_tt, n_lt;   // P1 token tiles, latent tiles
-  int npt;          // P1 pairs per latent tile
-  int ks, kb_per;   // P1 splits of d_in and 32-input steps per split
-  int n_ot;         // P2 output tiles
-  int kbc;          // P2 32-latent blocks staged in LDS per round
-  int xvec, hvec, yvec;  // aligned vector access allowed for x / h / y
+  int ks, kb_per;   // P1 splits of d_in, 32-input steps per split
+  int ns16p;        // P1 partial subtile slots per path
+  int n_un, n_og, n_tt2;  // P2 units, unit groups, token tiles
+  int res, kbc;     // P2: w resident / blocks per chunk
+  int xdma;         // x rows are whole 16-byte chunks: global-to-LDS loads
+  int hvec, yvec;   // aligned 4-element access allowed for h / y
   uint32_t v_bytes, u_bytes, g_bytes, h_bytes, l_bytes, wt_bytes;
+  uint32_t wd_off;  // P2: byte offset of the U-word buffers in LDS
 };
 
-// Raw bits of x[row][j0 + v] and x[row][j0 + 16 + v] (v < 4): the inputs of one
-// lane's slots in a 32-input step, always in the vector layout of bload4
-// (16-bit elements two to a dword), whichever load form read them.
-template <int ACT>
-__device__ __forceinline__ void load_x8(rsrc_t xr, uint32_t e0, bool vec, uint32_t (&lo)[4], uint32_t (&hi)[4]) {
-  if (vec) {
-    bload4<ACT, true>(xr, e0, true, lo);
-    bload4<ACT, true>(xr, e0 + 16, true, hi);
-  } else {
-    uint32_t a[4], b[4];
-    bload4<ACT, false>(xr, e0, true, a);
-    bload4<ACT, false>(xr, e0 + 16, true, b);
-    if constexpr (ACT == kDtF32) {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) lo[v] = a[v], hi[v] = b[v];
-    } else {
-      lo[0] = a[0] | (a[1] << 16), lo[1] = a[2] | (a[3] << 16), lo[2] = lo[3] = 0u;
-      hi[0] = b[0] | (b[1] << 16), hi[1] = b[2] | (b[3] << 16), hi[2] = hi[3] = 0u;
-    }
-  }
-}
-
-// B fragment(s) of x: E exact bf16 terms.  MASK (the step that holds the end
-// of d_in): inputs at or past jmax are zero (x past d_in is the next row).
-template <int ACT, int E, bool MASK>
-__device__ __forceinline__ void x_frag(const uint32_t (&lo)[4], const uint32_t (&hi)[4], int j0, int jmax,
-                                       u32x4 (&B)[E]) {
-  if constexpr (E == 1) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const uint32_t a = (!MASK || j0 + v < jmax) ? raw16<true>(lo, v) : 0u;
-      const uint32_t b = (!MASK || j0 + 16 + v < jmax) ? raw16<true>(hi, v) : 0u;
-      B[0][v] = a | (b << 16);
-    }
-  } else {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      uint32_t a[E], b[E];
-      split_exact<E>((!MASK || j0 + v < jmax) ? raw4_elem<ACT, true>(lo, v) : 0.0f, a);
-      split_exact<E>((!MASK || j0 + 16 + v < jmax) ? raw4_elem<ACT, true>(hi, v) : 0.0f, b);
-#pragma unroll
-      for (int e = 0; e < E; ++e) B[e][v] = a[e] | (b[e] << 16);
-    }
-  }
-}
-
-// Packed sign word of V_p for latent k at 32-input step kb (0 when k >= r).
-__device__ __forceinline__ uint32_t v_word(rsrc_t vr, int kb, int k, int r, int nbv, int tailv, bool kok) {
-  if (kb < nbv) return __builtin_amdgcn_raw_buffer_load_b32(vr, kok ? static_cast<uint32_t>(kb * r + k) * 4u : kOob, 0, 0);
-  const uint32_t off = 4u * nbv * r + (tailv <= 16 ? 2u : 4u) * k;
-  const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(vr, kok ? off : kOob, 0, 0);
-  const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(vr, kok && tailv > 16 ? off + 2 : kOob, 0, 0);
-  return (lo & 0xffffu) | (hi << 16);
+// s_waitcnt: at most VM vector-memory operations outstanding, no LDS access
+template <int VM>
+__device__ __forceinline__ void wait_vm_lds() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
 }
 
 // ---------------------------------------------------------------------------
 // P1
 // ---------------------------------------------------------------------------
-template <int NPT, int ACT, int SC>
-__global__ void __launch_bounds__(kThreads, 1) prefill_p1(PrefillParams P) {
+__host__ __device__ constexpr int p1_nx(int act) { return act == kDtF32 ? 2 : 1; }  // 16-byte chunks per lane
+__host__ __device__ constexpr int p1_nv(int ms) { return (ms + 3) / 4; }            // V-word loads per wave
+__host__ __device__ constexpr size_t p1_gt_bytes(int kb_per, int G) {
+  return static_cast<size_t>(2) * kb_per * 4 * G * 16;
+}
+__host__ __device__ constexpr size_t p1_xslot(int nx) { return static_cast<size_t>(kTn1) * nx * 1024; }
+__host__ __device__ constexpr size_t p1_vslot(int nv) { return static_cast<size_t>(kWaves) * nv * 256; }
+// 32-input steps staged in LDS (fp32 x takes twice the room per step)
+__host__ __device__ constexpr int p1_ring(int act) { return act == kDtF32 ? 8 : 12; }
+__host__ __device__ constexpr size_t p1_lds(int kb_per, int G, int act, int ms) {
+  const size_t ring = p1_gt_bytes(kb_per, G) + p1_ring(act) * (p1_xslot(p1_nx(act)) + p1_vslot(p1_nv(ms)));
+  const size_t red = static_cast<size_t>(kWaves) * ms * kTn1 * 64 * 16;
+  return ring > red ? ring : red;
+}
+
+template <int MS, int ACT, int SC>
+__global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
   constexpr int G = nterms<SC>(), E = nterms<ACT>();
+  constexpr int NX = p1_nx(ACT), NV = p1_nv(MS), RING = p1_ring(ACT), R2 = RING / 2;
+  constexpr int XSLOT = static_cast<int>(p1_xslot(NX)), VSLOT = static_cast<int>(p1_vslot(NV));
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int n16 = lane & 15, gq = lane >> 4;
+  const int half = wave >> 2, w4 = wave & 3;  // step parity; the wave's role within its half
+  const int pw = w4 >> 1, hw = w4 & 1;        // path and subtile half
   const int tiles = P.n_tt * P.n_lt;
   const int ksi = blockIdx.x / tiles;
   const int tile = blockIdx.x - ksi * tiles;
   const int lt = tile / P.n_tt;
   const int tt = tile - lt * P.n_tt;
-  const int T = P.T, d_in = P.d_in, r = P.r, nkb = P.nkb;
+  const int T = P.T, d_in = P.d_in, r = P.r;
   const int t0 = tt * kTok1;
-  const int q0 = lt * NPT;
-  const int nq = min(NPT, 2 * nkb - q0);  // pairs of this tile
   const int nbv = d_in >> 5, tailv = d_in & 31, nbt = nblocks32(d_in);
-  const int kbs = ksi * P.kb_per, kbe = min(nbt, kbs + P.kb_per), nk = kbe - kbs;
-  const bool vec = P.xvec != 0;
+  const int kbs = ksi * P.kb_per, kbe = min(nbt, kbs + P.kb_per), ns = kbe - kbs;
+  const int sb0 = lt * 2 * MS + hw;  // subtile of slot m: sb0 + 2 m
 
-  u32x4* gt = reinterpret_cast<u32x4*>(lds);  // g terms: [2][nk][4 lane groups][G]
-  // x of this tile's tokens (a buffer from the tile's first row: reads past the
-  // last token return zero)
+  u32x4* gt = reinterpret_cast<u32x4*>(lds);  // g terms [2][ns][4 lane groups][G]
+  char* xs = lds + p1_gt_bytes(P.kb_per, G);  // x ring [RING][4 token subtiles][NX][64] x 16 B
+  char* vs = xs + RING * XSLOT;               // V-word ring [RING][4 roles][NV][64] x 4 B
   const int ex = ACT == kDtF32 ? 4 : 2;
   const int rows = min(kTok1, T - t0);
+  // x of this tile's tokens (reads past the last token return zero)
   const rsrc_t xr = make_rsrc_uniform(static_cast<const char*>(P.x) + static_cast<int64_t>(t0) * d_in * ex,
                                       static_cast<uint32_t>(rows * d_in * ex));
-  const rsrc_t vr0 = make_rsrc(P.V[0], P.v_bytes), vr1 = make_rsrc(P.V[1], P.v_bytes);
+  const rsrc_t vr = make_rsrc(pw ? P.V[1] : P.V[0], P.v_bytes);
 
-  floatx4 acc[NPT][2][kTn1];
+  // loads of step n (split-local) into its ring slot, by the waves of its
+  // parity: the packed V words of this wave's subtiles (lane l: slot
+  // 4 d + l / 16, latent l % 16 of it; zero past r, past the range and for the
+  // tail step, whose words come through registers) and token subtile w4 of x
+  // (zero past d_in and past the range)
+  auto issue = [&](int n) {
+    const int kb = kbs + n, sl = n % RING;
+    const bool valid = n < ns;
 #pragma unroll
-  for (int i = 0; i < NPT; ++i)
+    for (int d = 0; d < NV; ++d) {
+      const int m = 4 * d + gq;
+      const int k = 16 * (sb0 + 2 * m) + n16;
+      const bool ok = valid && kb < nbv && m < MS && k < r;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr)(vs + sl * VSLOT + (w4 * NV + d) * 256), 4,
+                                               ok ? static_cast<uint32_t>(kb * r + k) * 4u : kOob, 0, 0, 0);
+    }
+    const int row = 16 * w4 + n16;
+    char* xd = xs + sl * XSLOT + w4 * NX * 1024;
+    if (P.xdma) {
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
+      for (int c = 0; c < NX; ++c) {
+        const int j = 32 * kb + 8 * gq + 4 * c;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            xr, (lds_ptr)(xd + c * 1024), 16,
+            valid && j < d_in ? static_cast<uint32_t>(row * d_in + j) * static_cast<uint32_t>(ex) : kOob, 0, 0, 0);
+      }
+    } else {
+      // element loads (rows not whole 16-byte chunks), written in the same order
 #pragma unroll
-      for (int tn = 0; tn < kTn1; ++tn) acc[i][sb][tn] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  // step loads: x slots of both token subtiles, the packed words of every pair
-  // (pairs past the tile read zero words; their sums are never finalised)
-  struct StepLoads {
-    uint32_t xl[kTn1][4], xh[kTn1][4];
-    uint32_t w[NPT][2];
-  };
-  // (a step past the range, valid == false, reads past every buffer: zeros,
-  // with the same instructions, so the prefetch needs no branch)
-  auto issue = [&](int kb, bool tail, bool valid, StepLoads& L) {
-    const int j0 = 32 * kb + 4 * gq;
-    const uint32_t xoff = valid ? static_cast<uint32_t>(n16 * d_in + j0) : (kOob >> 2);
+      for (int c = 0; c < NX; ++c) {
+        const int j = 32 * kb + 8 * gq + 4 * c;
+        const uint32_t e0 = static_cast<uint32_t>(row * d_in + j);
+        u32x4 dv;
+        if constexpr (ACT == kDtF32) {
 #pragma unroll
-    for (int tn = 0; tn < kTn1; ++tn)
-      load_x8<ACT>(xr, xoff + (valid ? 16 * tn * d_in : 0), vec, L.xl[tn], L.xh[tn]);
-#pragma unroll
-    for (int i = 0; i < NPT; ++i) {
-      const int q = q0 + i;
-      const bool p1 = q >= nkb;
-      const int kbl = q - (p1 ? nkb : 0);
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        const int k = 32 * kbl + 16 * sb + n16;
-        const bool kok = valid && i < nq && k < r;
-        if (!tail) {
-          L.w[i][sb] = __builtin_amdgcn_raw_buffer_load_b32(p1 ? vr1 : vr0,
-                                                            kok ? static_cast<uint32_t>(kb * r + k) * 4u : kOob, 0, 0);
+          for (int e = 0; e < 4; ++e) dv[e] = bload<ACT>(xr, e0 + e, valid && j + e < d_in);
         } else {
-          // the tail block's word comes from the tail plane (16- or 32-bit entries)
-          const uint32_t off = 4u * nbv * r + (tailv <= 16 ? 2u : 4u) * k;
-          const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(p1 ? vr1 : vr0, kok ? off : kOob, 0, 0);
-          const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(p1 ? vr1 : vr0, kok && tailv > 16 ? off + 2 : kOob, 0, 0);
-          L.w[i][sb] = (lo & 0xffffu) | (hi << 16);
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            dv[v] = bload<ACT>(xr, e0 + 2 * v, valid && j + 2 * v < d_in) |
+                    (bload<ACT>(xr, e0 + 2 * v + 1, valid && j + 2 * v + 1 < d_in) << 16);
         }
+        *reinterpret_cast<u32x4*>(xd + c * 1024 + lane * 16) = dv;
       }
     }
   };
-  auto compute = [&](int kb, bool tail, const StepLoads& L) {
-    u32x4 B[kTn1][E];
+
+  // the first R2 - 1 rounds (two steps each, one per half) in flight
 #pragma unroll
-    for (int tn = 0; tn < kTn1; ++tn) {
-      if (tail)
-        x_frag<ACT, E, true>(L.xl[tn], L.xh[tn], 32 * kb + 4 * gq, d_in, B[tn]);
-      else
-        x_frag<ACT, E, false>(L.xl[tn], L.xh[tn], 32 * kb + 4 * gq, d_in, B[tn]);
-    }
+  for (int d = 0; d < R2 - 1; ++d) issue(2 * d + half);
+
+  // packed V words of the tail step (tail plane: 16- or 32-bit entries)
+  uint32_t tw[MS];
+  const bool has_tail = tailv != 0 && kbe == nbt;
 #pragma unroll
-    for (int i = 0; i < NPT; ++i) {
-      const int p = q0 + i >= nkb ? 1 : 0;
-      const u32x4* gp = gt + ((p * nk + (kb - kbs)) * 4 + gq) * G;
-      u32x4 gv[G];
-#pragma unroll
-      for (int s = 0; s < G; ++s) gv[s] = gp[s];
-#pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        const uint32_t ws = L.w[i][sb] >> (4 * gq);
-        u32x4 msk;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) msk[v] = (ws << (15 - v)) & 0x80008000u;
-#pragma unroll
-        for (int s = 0; s < G; ++s) {
-          const u32x4 A = msk ^ gv[s];
-#pragma unroll
-          for (int tn = 0; tn < kTn1; ++tn)
-#pragma unroll
-            for (int e = 0; e < E; ++e) acc[i][sb][tn] = mfma(A, B[tn][e], acc[i][sb][tn]);
-        }
-      }
-    }
-  };
-  // this wave's full steps kb(n) = kbs + wave + kWaves n, n < ns, through a
-  // ring of kRing steps of loads in flight (ring slot n % kRing; a slot past
-  // the last step reads zeros, with the same instructions); then the tail step
-  const int kfe = min(kbe, nbv);
-  const int kw0 = kbs + wave;
-  const int ns = kw0 < kfe ? (kfe - kw0 + kWaves - 1) / kWaves : 0;
-  StepLoads ring[kRing];
-#pragma unroll
-  for (int d2 = 0; d2 < kRing; ++d2) issue(kw0 + kWaves * d2, false, d2 < ns, ring[d2]);
-  // g terms of both paths for this workgroup's steps, as A-operand register
-  // pairs: gt[p][step][lane group][term] = 4 dwords
+  for (int m = 0; m < MS; ++m) {
+    const int k = 16 * (sb0 + 2 * m) + n16;
+    const bool ok = has_tail && k < r;
+    const uint32_t off = 4u * nbv * r + (tailv <= 16 ? 2u : 4u) * k;
+    const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(vr, ok ? off : kOob, 0, 0);
+    const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(vr, ok && tailv > 16 ? off + 2 : kOob, 0, 0);
+    tw[m] = (lo & 0xffffu) | (hi << 16);
+  }
+  // g terms of both paths for this split's steps, in A-operand order:
+  // gt[p][step][lane group][term], register v = terms of inputs 2 v, 2 v + 1
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     const rsrc_t gr = make_rsrc(p ? P.g[1] : P.g[0], P.g_bytes);
-    for (int it = tid; it < nk * 4; it += kThreads) {
+    for (int it = tid; it < ns * 4; it += kThreads1) {
       const int kbl = it >> 2, g4 = it & 3;
-      const uint32_t j0 = 32 * (kbs + kbl) + 4 * g4;
-      uint32_t tl[4][G], th[4][G];
+      const int j0 = 32 * (kbs + kbl) + 8 * g4;
+      uint32_t tm[8][G];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        split_exact<G>(bits_to_f32<SC>(bload<SC>(gr, j0 + v)), tl[v]);
-        split_exact<G>(bits_to_f32<SC>(bload<SC>(gr, j0 + 16 + v)), th[v]);
-      }
+      for (int e = 0; e < 8; ++e) split_exact<G>(bits_to_f32<SC>(bload<SC>(gr, j0 + e, j0 + e < d_in)), tm[e]);
 #pragma unroll
       for (int s = 0; s < G; ++s) {
-        u32x4 d;
+        u32x4 dv;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) d[v] = tl[v][s] | (th[v][s] << 16);
-        gt[((p * nk + kbl) * 4 + g4) * G + s] = d;
+        for (int v = 0; v < 4; ++v) dv[v] = tm[2 * v][s] | (tm[2 * v + 1][s] << 16);
+        gt[((p * ns + kbl) * 4 + g4) * G + s] = dv;
       }
     }
   }
-  __syncthreads();
 
-  // whole rounds of the ring (every product unconditional: conditional
-  // products would make the compiler copy accumulators), then the remainder
-  int n0 = 0;
-  for (; n0 + kRing <= ns; n0 += kRing) {
+  floatx4 acc[MS][kTn1];
 #pragma unroll
-    for (int d2 = 0; d2 < kRing; ++d2) {
-      const int n = n0 + d2;
-      asm volatile("" ::: "memory");  // keep the ring's loads where they are issued
-      compute(kw0 + kWaves * n, false, ring[d2]);
-      issue(kw0 + kWaves * (n + kRing), false, n + kRing < ns, ring[d2]);
-    }
-  }
-  static_assert(kRing == 2, "the remainder below handles one step");
-  if (n0 < ns) compute(kw0 + kWaves * n0, false, ring[0]);
-  if (tailv != 0 && nbv >= kbs && nbv < kbe && (nbv - kbs) % kWaves == wave) {
-    StepLoads tl;
-    issue(nbv, true, true, tl);
-    compute(nbv, true, tl);
-  }
-  __syncthreads();  // the g terms are dead: the LDS is reused below
+  for (int m = 0; m < MS; ++m)
+#pragma unroll
+    for (int tn = 0; tn < kTn1; ++tn) acc[m][tn] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // fixed-order sum over the 4 waves, kRedPairs pairs at a time, into this
-  // workgroup's partial: pbuf[ks][tile][pair][token][lane group][8]
-  float* red = reinterpret_cast<float*>(lds);  // [4 waves][kRedPairs][kTn1][64 lanes][8]
-  float* part = P.pbuf + (static_cast<int64_t>(ksi) * tiles + tile) * NPT * kPbufPair;
+  const u32x4* gtp = gt + pw * ns * 4 * G;
+  const int nr = (ns + 1) >> 1;  // rounds: step 2 i + half in round i
+  for (int i = 0; i < nr; ++i) {
+    // round i has landed (each wave waits for its own loads, the barrier for
+    // everyone's) and every wave is done with the slots of round i - 1
+    asm volatile("" ::: "memory");  // round i - 1's LDS reads stay above the barrier
+    wait_vm_lds<(R2 - 2) * (NX + NV)>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    issue(2 * (i + R2 - 1) + half);
+    const int n = 2 * i + half;
+    if (n >= ns) continue;  // (an odd count: the second half sits out the last round)
+    const int sl = n % RING;
+    const bool tail = kbs + n == nbv;
+
+    // B: x of the 4 token subtiles as E exact bf16 terms
+    u32x4 B[kTn1][E];
+    const char* xsl = xs + sl * XSLOT;
 #pragma unroll
-  for (int c0 = 0; c0 < NPT; c0 += kRedPairs) {
+    for (int tn = 0; tn < kTn1; ++tn) {
+      if constexpr (ACT == kDtBF16) {
+        B[tn][0] = *reinterpret_cast<const u32x4*>(xsl + tn * 1024 + lane * 16);
+      } else {
+        uint32_t el[8];
+        if constexpr (ACT == kDtF32) {
+          const u32x4 a = *reinterpret_cast<const u32x4*>(xsl + (2 * tn) * 1024 + lane * 16);
+          const u32x4 b = *reinterpret_cast<const u32x4*>(xsl + (2 * tn + 1) * 1024 + lane * 16);
 #pragma unroll
-    for (int il = 0; il < kRedPairs; ++il) {
-      if (c0 + il < NPT) {
+          for (int e = 0; e < 4; ++e) el[e] = a[e], el[4 + e] = b[e];
+        } else {
+          const u32x4 a = *reinterpret_cast<const u32x4*>(xsl + tn * 1024 + lane * 16);
 #pragma unroll
-        for (int tn = 0; tn < kTn1; ++tn) {
-          floatx4* d = reinterpret_cast<floatx4*>(red + (((wave * kRedPairs + il) * kTn1 + tn) * 64 + lane) * 8);
-          d[0] = acc[c0 + il][0][tn];
-          d[1] = acc[c0 + il][1][tn];
+          for (int v = 0; v < 4; ++v) el[2 * v] = a[v] & 0xffffu, el[2 * v + 1] = a[v] >> 16;
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          uint32_t lo[E], hi[E];
+          split_exact<E>(bits_to_f32<ACT>(el[2 * v]), lo);
+          split_exact<E>(bits_to_f32<ACT>(el[2 * v + 1]), hi);
+#pragma unroll
+          for (int e = 0; e < E; ++e) B[tn][e][v] = lo[e] | (hi[e] << 16);
         }
       }
     }
-    __syncthreads();
-    for (int it = tid; it < kRedPairs * kTn1 * 64; it += kThreads) {
-      const int il = it / (kTn1 * 64);
-      const int tn = (it >> 6) % kTn1;
-      const int ln = it & 63;
-      if (c0 + il >= NPT) continue;
-      floatx4 s0[kWaves], s1[kWaves];
+    // A: V signs on the g terms of this wave's path
+    u32x4 gv[G];
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        const floatx4* sp = reinterpret_cast<const floatx4*>(red + (((w * kRedPairs + il) * kTn1 + tn) * 64 + ln) * 8);
-        s0[w] = sp[0];
-        s1[w] = sp[1];
+    for (int s = 0; s < G; ++s) gv[s] = gtp[(n * 4 + gq) * G + s];
+    const uint32_t* vw = reinterpret_cast<const uint32_t*>(vs + sl * VSLOT + w4 * NV * 256);
+    u32x4 A[MS][G];
+#pragma unroll
+    for (int m = 0; m < MS; ++m) {
+      const uint32_t word = tail ? tw[m] : vw[16 * m + n16];
+      const uint32_t t = word >> (8 * gq);
+      const uint32_t dd = (t & 0xffffu) | ((t << 15) & 0xffff0000u);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const uint32_t sv = (dd << (15 - 2 * v)) & 0x80008000u;
+#pragma unroll
+        for (int s = 0; s < G; ++s) A[m][s][v] = sv ^ gv[s][v];
       }
-      const int t = 16 * tn + (ln & 15), g4 = ln >> 4;
-      floatx4* dst = reinterpret_cast<floatx4*>(part + (c0 + il) * kPbufPair + (t * 4 + g4) * kPbufItem);
-      dst[0] = (s0[0] + s0[1]) + (s0[2] + s0[3]);
-      dst[1] = (s1[0] + s1[1]) + (s1[2] + s1[3]);
     }
-    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < G; ++s)
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+#pragma unroll
+        for (int m = 0; m < MS; ++m)
+#pragma unroll
+          for (int tn = 0; tn < kTn1; ++tn) acc[m][tn] = mfma(A[m][s], B[tn][e], acc[m][tn]);
   }
 
+  // the two halves' sums, in a fixed order (half 0 + half 1), through LDS
+  // (the ring is dead after this barrier), then this role's partial sums:
+  // pbuf[ks][token tile][path][subtile][token subtile][lane][4]
+  asm volatile("" ::: "memory");
+  wait_vm_lds<0>();
+  __syncthreads();
+  floatx4* red = reinterpret_cast<floatx4*>(lds) + w4 * MS * kTn1 * 64;
+  if (half == 1) {
+#pragma unroll
+    for (int m = 0; m < MS; ++m)
+#pragma unroll
+      for (int tn = 0; tn < kTn1; ++tn) red[(m * kTn1 + tn) * 64 + lane] = acc[m][tn];
+  }
+  __syncthreads();
+  if (half == 0) {
+    float* part = P.pbuf + ((static_cast<int64_t>(ksi) * P.n_tt + tt) * 2 + pw) * P.ns16p * kPart;
+#pragma unroll
+    for (int m = 0; m < MS; ++m) {
+      const int s = sb0 + 2 * m;
+      if (s < P.ns16) {
+#pragma unroll
+        for (int tn = 0; tn < kTn1; ++tn)
+          *reinterpret_cast<floatx4*>(part + (s * kTn1 + tn) * 256 + lane * 4) =
+              acc[m][tn] + red[(m * kTn1 + tn) * 64 + lane];
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
 // P1b: w = l (.) (sum of the ks partials, ascending) as NW bf16 terms in P2's
 // B-fragment layout wterm[p][term][kbl][t][lane group]; one thread per
-// (token, pair, lane group)
+// (pair, token tile, token subtile, P2 lane), so a wave reads 1 KB runs
 // ---------------------------------------------------------------------------
 template <int ACT, int SC>
 __global__ void __launch_bounds__(kThreads) prefill_p1b(PrefillParams P) {
   constexpr int NW = ACT == kDtF32 ? 3 : 2;
-  const int NPT = P.npt;
-  const int nq2 = 2 * P.nkb;
   const int item = blockIdx.x * kThreads + threadIdx.x;
-  if (item >= P.T * nq2 * 4) return;
-  const int g4 = item & 3;
-  const int rest = item >> 2;
-  const int t = rest / nq2;
-  const int q = rest - t * nq2;
-  const int tile = (q / NPT) * P.n_tt + t / kTok1;
-  const int tiles = P.n_tt * P.n_lt;
-  const float* src = P.pbuf + (static_cast<int64_t>(tile) * NPT + q % NPT) * kPbufPair + ((t % kTok1) * 4 + g4) * kPbufItem;
-  const int64_t kstride = static_cast<int64_t>(tiles) * NPT * kPbufPair;
+  const int ln = item & 63;
+  const int tn = (item >> 6) & 3;
+  const int rest = item >> 8;
+  const int tt = rest % P.n_tt;
+  const int q = rest / P.n_tt;  // (path, 32-latent block)
+  if (q >= 2 * P.nkb) return;
+  const int t = tt * kTok1 + 16 * tn + (ln & 15);
+  if (t >= P.T) return;
+  const int g4 = ln >> 4;
+  const int p = q >= P.nkb ? 1 : 0;
+  const int kbl = q - p * P.nkb;
+  // subtiles 2 kbl (latents 32 kbl + 4 g4 + v) and 2 kbl + 1 (the same + 16)
+  const float* src = P.pbuf + ((static_cast<int64_t>(tt) * 2 + p) * P.ns16p + 2 * kbl) * kPart + tn * 256 + ln * 4;
+  const int64_t kstride = static_cast<int64_t>(P.n_tt) * 2 * P.ns16p * kPart;
   floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0;
 #pragma unroll 8
   for (int k2 = 0; k2 < P.ks; ++k2) {
-    const floatx4* sp = reinterpret_cast<const floatx4*>(src + k2 * kstride);
-    s0 += sp[0];
-    s1 += sp[1];
+    const float* sp = src + k2 * kstride;
+    s0 += *reinterpret_cast<const floatx4*>(sp);
+    s1 += *reinterpret_cast<const floatx4*>(sp + kPart);
   }
-  const int p = q >= P.nkb ? 1 : 0;
-  const int kbl = q - p * P.nkb;
   const int r = P.r;
   const rsrc_t lr = make_rsrc(p ? P.l[1] : P.l[0], P.l_bytes);
   uint32_t lo[NW][4], hi[NW][4];
@@ -393,165 +399,298 @@ __global__ void __launch_bounds__(kThreads) prefill_p1b(PrefillParams P) {
 // ---------------------------------------------------------------------------
 // P2
 // ---------------------------------------------------------------------------
-// LDS of P2: w fragments [kbc][kTn2][NW][64 lanes] x 16 B and U words
-// [4 waves][kbc][64] x 4 B
-__host__ __device__ constexpr size_t p2_b_bytes(int kbc, int nw) { return static_cast<size_t>(kbc) * kTn2 * nw * 64 * 16; }
-__host__ __device__ constexpr size_t p2_lds_bytes(int kbc, int nw) {
-  return p2_b_bytes(kbc, nw) + static_cast<size_t>(kWaves) * kbc * 64 * 4;
+// LDS of P2: w fragments [held pairs][4 token subtiles][NW][64 lanes] x 16 B,
+// then per buffer and wave: U words [held pairs][64] x 4 B, row scales
+// [2 paths][256 B] and 16-bit tail words [2 paths][256 B]
+__host__ __device__ constexpr size_t p2_w_bytes(int pairs, int nw) {
+  return static_cast<size_t>(pairs) * 4 * nw * 1024;
+}
+__host__ __device__ constexpr int p2_wave_bytes(int pairs) { return pairs * 256 + 1024; }
+__host__ __device__ constexpr size_t p2_wd_bytes(int pairs, int bufs) {
+  return static_cast<size_t>(bufs) * kWaves2 * p2_wave_bytes(pairs);
 }
 
-typedef __attribute__((address_space(3))) void* lds_ptr;
+// two fp32 values rounded to nearest-even bf16 / f16, packed (the gfx950
+// packed converts)
+template <int DT>
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  const f2 v = {a, b};
+  if constexpr (DT == kDtBF16) {
+    typedef __bf16 h2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
+  } else {
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
+  }
+}
 
-template <int ACT, int SC>
-__global__ void __launch_bounds__(kThreads, 2) prefill_p2(PrefillParams P) {
+// FAST: d_out % 4 == 0 and aligned row scales, so the scales and 16-bit tail
+// words of a unit come in whole dwords through global-to-LDS loads like the U
+// words (prefetched a unit ahead); otherwise they are read per unit into
+// registers
+template <int ACT, int SC, bool FAST>
+__global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
   constexpr int NW = ACT == kDtF32 ? 3 : 2;
+  constexpr int ES = SC == kDtF32 ? 4 : 2;
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int n16 = lane & 15, gq = lane >> 4;
-  const int ot = blockIdx.x % P.n_ot;
-  const int tt = blockIdx.x / P.n_ot;
-  const int T = P.T, d_out = P.d_out, r = P.r, nkb = P.nkb, kbc = P.kbc;
-  const int i0 = ot * kOut2 + wave * (kIm2 * 16);  // this wave's 64 outputs i0 .. i0 + 63
+  const int hu = wave >> 2, w4 = wave & 3;  // unit parity; the wave's role within its half
+  const int oh = w4 & 1, th = w4 >> 1;      // output half, token half of a unit
+  const int tt = blockIdx.x % P.n_tt2;
+  const int og = blockIdx.x / P.n_tt2;
+  const int T = P.T, d_out = P.d_out, r = P.r, nkb = P.nkb;
   const int t0 = tt * kTok2;
   const int nbu = r >> 5, tailu = r & 31;
+  const int nfull = nbu + (tailu > 16 ? 1 : 0);  // blocks with 32-bit words
+  const bool t16 = tailu != 0 && tailu <= 16;     // block nbu has 16-bit words
+  const bool res = P.res != 0;
+  const int held = res ? 2 * nkb : P.kbc;  // pairs in LDS at once
+  const int wvb = p2_wave_bytes(held);
   const rsrc_t wr = make_rsrc(P.wterm, P.wt_bytes);
-  const rsrc_t ur[2] = {make_rsrc(P.U[0], P.u_bytes), make_rsrc(P.U[1], P.u_bytes)};  // compile-time path index
+  const rsrc_t ur[2] = {make_rsrc(P.U[0], P.u_bytes), make_rsrc(P.U[1], P.u_bytes)};
   const rsrc_t hr[2] = {make_rsrc(P.h[0], P.h_bytes), make_rsrc(P.h[1], P.h_bytes)};
-  char* bl = lds;                                              // w fragments
-  char* ul = bl + p2_b_bytes(kbc, NW);                         // U words
-  const bool iok = i0 + lane < d_out;
+  char* wl = lds;
+  char* wd = lds + P.wd_off;
+  auto region = [&](int buf) { return wd + (buf * kWaves2 + wave) * wvb; };
 
-  // row scales of this lane's outputs i0 + 16 im + 4 gq + e (raw; used at the
-  // end).  (Global-to-LDS loads are used for 4- and 16-byte elements only.)
-  uint32_t hb[2][kIm2][4];
-#pragma unroll
-  for (int pp = 0; pp < 2; ++pp)
-#pragma unroll
-    for (int im = 0; im < kIm2; ++im) {
-      if (P.hvec)
-        bload4<SC, true>(hr[pp], i0 + 16 * im + 4 * gq, true, hb[pp][im]);
-      else
-        bload4<SC, false>(hr[pp], i0 + 16 * im + 4 * gq, true, hb[pp][im]);
+  // w fragments of pairs (p, kb0 .. kb0 + nb - 1) into held slots from hs0
+  auto load_w = [&](int p, int kb0, int nb, int hs0) {
+    const int ng = nb * 4 * NW;
+    for (int gi = wave; gi < ng; gi += kWaves2) {
+      const int e = gi % NW;
+      const int tn = (gi / NW) & 3;
+      const int kbl = gi / (4 * NW);
+      const int t = t0 + 16 * tn + n16;
+      const uint32_t off =
+          static_cast<uint32_t>(((static_cast<int64_t>(p * NW + e) * nkb + kb0 + kbl) * T + t) * 4 + gq) * 16u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_ptr)(wl + ((hs0 + kbl) * 4 * NW + (gi % (4 * NW))) * 1024),
+                                               16, t < T ? off : kOob, 0, 0, 0);
     }
-
-  floatx4 acc[2][kIm2][kTn2];
+  };
+  // U words (32-bit: full words and a tail block of more than 16 latents) of
+  // blocks kb0 .. kb0 + nb - 1 of path p for this wave's 64 outputs of unit u
+  auto load_words = [&](int u, int p, int kb0, int nb, int buf, int hs0) {
+    const int o = u * kUnit + 64 * oh + lane;
+    const bool ok = o < d_out;
+    char* dst = region(buf) + hs0 * 256;
+    for (int kbl = 0; kbl < nb; ++kbl) {
+      const int kb = kb0 + kbl;
+      if (kb >= nfull) break;
+      const uint32_t off = kb < nbu ? static_cast<uint32_t>(kb * d_out + o) * 4u : 4u * nbu * d_out + 4u * o;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ur[p], (lds_ptr)(dst + kbl * 256), 4, ok ? off : kOob, 0, 0, 0);
+    }
+  };
+  // FAST: row scales and 16-bit tail words of unit u as whole dwords (lane l:
+  // scales of outputs 2 l, 2 l + 1 for 16-bit scales, l for fp32; tail words
+  // of outputs 2 l, 2 l + 1)
+  auto load_side = [&](int u, int buf) {
+    const int ob = u * kUnit + 64 * oh;
+    char* dst = region(buf) + held * 256;
+    const int oe = ES == 2 ? ob + 2 * lane : ob + lane;
+    const int ot = ob + 2 * lane;
 #pragma unroll
-  for (int pp = 0; pp < 2; ++pp)
+    for (int p = 0; p < 2; ++p) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(hr[p], (lds_ptr)(dst + p * 256), 4,
+                                               oe < d_out ? static_cast<uint32_t>(oe) * ES : kOob, 0, 0, 0);
+      if (t16)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ur[p], (lds_ptr)(dst + 512 + p * 256), 4,
+                                                 ot < d_out ? 4u * nbu * d_out + 2u * ot : kOob, 0, 0, 0);
+    }
+  };
+  // not FAST: 16-bit tail words of this wave's outputs of unit u in registers
+  auto load_tw = [&](int u, uint32_t (&tw)[2][kIm2]) {
+    const int ob = u * kUnit + 64 * oh;
 #pragma unroll
-    for (int im = 0; im < kIm2; ++im)
-#pragma unroll
-      for (int tn = 0; tn < kTn2; ++tn) acc[pp][im][tn] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  const uint32_t ones[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
-#pragma unroll
-  for (int pp = 0; pp < 2; ++pp) {
-    for (int kb0 = 0; kb0 < nkb; kb0 += kbc) {
-      const int nb = min(kbc, nkb - kb0);
-      // one round of global-to-LDS loads: w fragment groups (one wave
-      // instruction each: 64 lanes x 16 bytes, lane l's fragment at l * 16) ...
-      const int ngroups = nb * kTn2 * NW;
-      for (int gi = wave; gi < ngroups; gi += kWaves) {
-        int rest = gi;
-        const int e = rest % NW;
-        rest /= NW;
-        const int tn = rest % kTn2;
-        const int kbl = rest / kTn2;
-        const int t = t0 + 16 * tn + n16;
-        const uint32_t off = static_cast<uint32_t>(
-            ((static_cast<int64_t>(pp * NW + e) * nkb + kb0 + kbl) * T + t) * 4 + gq) * 16u;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_ptr)(bl + gi * 1024), 16, t < T ? off : kOob, 0, 0, 0);
-      }
-      // ... and the U words of this wave's outputs (full words; the tail word
-      // from the tail plane, 16- or 32-bit entries)
-      for (int kbl = 0; kbl < nb; ++kbl) {
-        const int kb = kb0 + kbl;
-        if (kb < nbu) {
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(ur[pp], (lds_ptr)(ul + (wave * kbc + kbl) * 256), 4,
-                                                   iok ? static_cast<uint32_t>(kb * d_out + i0 + lane) * 4u : kOob, 0,
-                                                   0, 0);
-        } else if (tailu > 16) {
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(ur[pp], (lds_ptr)(ul + (wave * kbc + kbl) * 256), 4,
-                                                   iok ? 4u * nbu * d_out + 4u * (i0 + lane) : kOob, 0, 0, 0);
-        }
-      }
-      // 16-bit tail words (the step past the full words, r % 32 in 1..16) in
-      // registers
-      uint32_t tw[kIm2];
-      const bool has16 = tailu != 0 && tailu <= 16 && nbu >= kb0 && nbu < kb0 + nb;
+    for (int p = 0; p < 2; ++p)
 #pragma unroll
       for (int im = 0; im < kIm2; ++im) {
-        const int i = i0 + 16 * im + n16;
-        tw[im] = __builtin_amdgcn_raw_buffer_load_b16(ur[pp], has16 && i < d_out ? 4u * nbu * d_out + 2u * i : kOob, 0,
-                                                      0);
+        const int i = ob + 16 * im + n16;
+        tw[p][im] = __builtin_amdgcn_raw_buffer_load_b16(ur[p], t16 && i < d_out ? 4u * nbu * d_out + 2u * i : kOob,
+                                                         0, 0);
       }
-      __builtin_amdgcn_s_waitcnt(0);  // global-to-LDS loads count as memory loads
-      __syncthreads();
-      // products from LDS
-      for (int kbl = 0; kbl < nb; ++kbl) {
-        const int kb = kb0 + kbl;
-        const bool tail16 = kb >= nbu && tailu <= 16;
-        u32x4 B[kTn2][NW];
+  };
+  // row scales of outputs ob + 16 im + 4 gq + e as floats
+  auto scales = [&](int u, int buf, float (&hf)[2][kIm2][4]) {
+    const int ob = u * kUnit + 64 * oh;
 #pragma unroll
-        for (int tn = 0; tn < kTn2; ++tn)
+    for (int p = 0; p < 2; ++p)
 #pragma unroll
-          for (int e = 0; e < NW; ++e)
-            B[tn][e] = reinterpret_cast<const u32x4*>(bl)[((kbl * kTn2 + tn) * NW + e) * 64 + lane];
+      for (int im = 0; im < kIm2; ++im) {
+        uint32_t raw[4];
+        if constexpr (FAST) {
+          const char* src = region(buf) + held * 256 + p * 256 + (16 * im + 4 * gq) * ES;
+          if constexpr (ES == 4) {
+            const u32x4 v = *reinterpret_cast<const u32x4*>(src);
+            raw[0] = v[0], raw[1] = v[1], raw[2] = v[2], raw[3] = v[3];
+          } else {
+            const u32x2 v = *reinterpret_cast<const u32x2*>(src);
+            raw[0] = v[0], raw[1] = v[1], raw[2] = raw[3] = 0u;
+          }
 #pragma unroll
-        for (int im = 0; im < kIm2; ++im) {
-          const uint32_t word = tail16 ? (tw[im] & 0xffffu)
-                                       : reinterpret_cast<const uint32_t*>(ul)[(wave * kbc + kbl) * 64 + 16 * im + n16];
-          const u32x4 A = sign_terms(word, gq, ones);
+          for (int e = 0; e < 4; ++e) hf[p][im][e] = raw4_elem<SC, true>(raw, e);
+        } else {
+          bload4<SC, false>(hr[p], ob + 16 * im + 4 * gq, true, raw);
 #pragma unroll
-          for (int tn = 0; tn < kTn2; ++tn)
-#pragma unroll
-            for (int e = 0; e < NW; ++e) acc[pp][im][tn] = mfma(A, B[tn][e], acc[pp][im][tn]);
+          for (int e = 0; e < 4; ++e) hf[p][im][e] = raw4_elem<SC, false>(raw, e);
         }
       }
-      __syncthreads();  // the next round reuses the LDS
-    }
-  }
+  };
 
-  // y[t][i] = h_0[i] acc_0 + h_1[i] acc_1 for outputs i = i0 + 16 im + 4 gq + e
-  // of token t = t0 + 16 tn + n16
+  floatx4 acc[2][kIm2][kTn2];
+  const uint32_t ones[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+  // products of one held pair: w from held slot hs, the U words from LDS
+  // (full) or the 16-bit tail words (W16)
+  auto pair = [&](auto pc, auto w16, int hs, const uint32_t* words, int buf, const uint32_t (&tw)[kIm2]) {
+    constexpr int p = decltype(pc)::value;
+    constexpr bool W16 = decltype(w16)::value;
+    u32x4 B[kTn2][NW];
+#pragma unroll
+    for (int tn = 0; tn < kTn2; ++tn)
+#pragma unroll
+      for (int e = 0; e < NW; ++e)
+        B[tn][e] = *reinterpret_cast<const u32x4*>(wl + ((hs * 4 + 2 * th + tn) * NW + e) * 1024 + lane * 16);
+#pragma unroll
+    for (int im = 0; im < kIm2; ++im) {
+      uint32_t word;
+      if constexpr (!W16)
+        word = words[16 * im + n16];
+      else if constexpr (FAST)
+        word = *reinterpret_cast<const uint16_t*>(region(buf) + held * 256 + 512 + p * 256 + (16 * im + n16) * 2);
+      else
+        word = tw[im] & 0xffffu;
+      const u32x4 A = sign_terms(word, gq, ones);
+#pragma unroll
+      for (int e = 0; e < NW; ++e)
+#pragma unroll
+        for (int tn = 0; tn < kTn2; ++tn) acc[p][im][tn] = mfma(A, B[tn][e], acc[p][im][tn]);
+    }
+  };
+  using False = std::integral_constant<bool, false>;
+  using True = std::integral_constant<bool, true>;
+  // products of held pairs (p, kb0 .. kb0 + nb - 1) at held slots from hs0
+  auto run = [&](auto pc, int kb0, int nb, int hs0, int buf, const uint32_t (&tw)[kIm2]) {
+    const uint32_t* words = reinterpret_cast<const uint32_t*>(region(buf) + hs0 * 256);
+    const int nf = max(0, min(nb, nfull - kb0));
+    for (int kbl = 0; kbl < nf; ++kbl) pair(pc, False{}, hs0 + kbl, words + kbl * 64, buf, tw);
+    if (t16 && nbu >= kb0 && nbu < kb0 + nb) pair(pc, True{}, hs0 + nbu - kb0, words, buf, tw);
+  };
+  // y[t][i] = h_0[i] acc_0 + h_1[i] acc_1, outputs i = ob + 16 im + 4 gq + e of
+  // token t = t0 + 16 (2 th + tn) + n16
   const int ey = ACT == kDtF32 ? 4 : 2;
   const rsrc_t yr = make_rsrc_uniform(static_cast<char*>(P.y) + static_cast<int64_t>(t0) * d_out * ey,
                                       static_cast<uint32_t>(min(kTok2, T - t0) * d_out * ey));
+  auto store = [&](int u, const float (&hf)[2][kIm2][4]) {
+    const int ob = u * kUnit + 64 * oh;
 #pragma unroll
-  for (int im = 0; im < kIm2; ++im) {
-    const int ib = i0 + 16 * im + 4 * gq;
-    float h0[4], h1[4];
+    for (int im = 0; im < kIm2; ++im) {
+      const int ib = ob + 16 * im + 4 * gq;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      h0[e] = P.hvec ? raw4_elem<SC, true>(hb[0][im], e) : raw4_elem<SC, false>(hb[0][im], e);
-      h1[e] = P.hvec ? raw4_elem<SC, true>(hb[1][im], e) : raw4_elem<SC, false>(hb[1][im], e);
-    }
+      for (int tn = 0; tn < kTn2; ++tn) {
+        const int t = t0 + 16 * (2 * th + tn) + n16;
+        float v[4];
 #pragma unroll
-    for (int tn = 0; tn < kTn2; ++tn) {
-      const int t = t0 + 16 * tn + n16;
-      float v[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = h0[e] * acc[0][im][tn][e] + h1[e] * acc[1][im][tn][e];
-      const uint32_t base = static_cast<uint32_t>((t - t0) * d_out + ib);  // within the tile's rows
-      if (P.yvec) {
-        // whole groups of 4 outputs (d_out % 4 == 0); rows past T are past the buffer
-        const bool ok = t < T && ib < d_out;
-        if constexpr (ACT == kDtF32) {
-          const u32x4 d = {__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])};
-          __builtin_amdgcn_raw_buffer_store_b128(d, yr, ok ? base * 4u : kOob, 0, 0);
-        } else {
-          uint32_t b[4];
+        for (int e = 0; e < 4; ++e) v[e] = hf[0][im][e] * acc[0][im][tn][e] + hf[1][im][e] * acc[1][im][tn][e];
+        const uint32_t base = static_cast<uint32_t>((t - t0) * d_out + ib);  // within the tile's rows
+        if (P.yvec) {
+          // whole groups of 4 outputs (d_out % 4 == 0); rows past T are past the buffer
+          const bool ok = t < T && ib < d_out;
+          if constexpr (ACT == kDtF32) {
+            const u32x4 d = {__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                             __float_as_uint(v[3])};
+            __builtin_amdgcn_raw_buffer_store_b128(d, yr, ok ? base * 4u : kOob, 0, 0);
+          } else {
+            const u32x2 d = {pack2<ACT>(v[0], v[1]), pack2<ACT>(v[2], v[3])};
+            __builtin_amdgcn_raw_buffer_store_b64(d, yr, ok ? base * 2u : kOob, 0, 0);
+          }
+        } else if (t < T) {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            b[e] = ACT == kDtBF16 ? f32_to_bf16_bits(v[e])
-                                  : static_cast<uint32_t>(__half_as_ushort(__float2half_rn(v[e])));
-          const u32x2 d = {b[0] | (b[1] << 16), b[2] | (b[3] << 16)};
-          __builtin_amdgcn_raw_buffer_store_b64(d, yr, ok ? base * 2u : kOob, 0, 0);
+            if (ib + e < d_out) st<ACT>(P.y, static_cast<int64_t>(t) * d_out + ib + e, v[e]);
         }
-      } else if (t < T) {
+      }
+    }
+  };
+  auto zero_acc = [&]() {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (ib + e < d_out) st<ACT>(P.y, static_cast<int64_t>(t) * d_out + ib + e, v[e]);
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int im = 0; im < kIm2; ++im)
+#pragma unroll
+        for (int tn = 0; tn < kTn2; ++tn) acc[p][im][tn] = floatx4{0.f, 0.f, 0.f, 0.f};
+  };
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+
+  uint32_t tw[2][kIm2] = {};
+  float hf[2][kIm2][4];
+  if (FAST && res) {
+    // every w fragment of the tile, once; then the units, each with the next
+    // unit's words, scales and tail words in flight (global-to-LDS loads only:
+    // the one wait per unit sits before its stores, so no unit waits for its
+    // own stores)
+    load_w(0, 0, nkb, 0);
+    load_w(1, 0, nkb, nkb);
+    int u = og + hu * P.n_og;
+    if (u < P.n_un) {
+      load_words(u, 0, 0, nkb, 0, 0);
+      load_words(u, 1, 0, nkb, 0, nkb);
+      load_side(u, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // global-to-LDS loads count as memory loads
+    __syncthreads();
+    for (int k = 0; u < P.n_un; ++k, u += 2 * P.n_og) {
+      asm volatile("" ::: "memory");  // the previous unit's LDS reads stay above the next loads
+      const int un = u + 2 * P.n_og;
+      const int buf = k & 1;
+      if (un < P.n_un) {
+        load_words(un, 0, 0, nkb, buf ^ 1, 0);
+        load_words(un, 1, 0, nkb, buf ^ 1, nkb);
+        load_side(un, buf ^ 1);
+      }
+      zero_acc();
+      run(P0{}, 0, nkb, 0, buf, tw[0]);
+      run(P1{}, 0, nkb, nkb, buf, tw[1]);
+      // the next unit's loads (issued a unit ago) and the previous unit's
+      // stores have landed: this wait is before the stores, not after them
+      __builtin_amdgcn_s_waitcnt(0);
+      scales(u, buf, hf);
+      store(u, hf);
+    }
+  } else {
+    // per pair of units (one per half), per chunk of held blocks of one
+    // path, everything waited for (a half without a unit only keeps the
+    // barriers)
+    for (int u0 = og; u0 < P.n_un; u0 += 2 * P.n_og) {
+      const int u = u0 + hu * P.n_og;
+      const bool act = u < P.n_un;
+      if (!FAST && act) load_tw(u, tw);
+      zero_acc();
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        for (int kb0 = 0; kb0 < nkb; kb0 += held) {
+          const int nb = min(held, nkb - kb0);
+          __syncthreads();  // the previous chunk's readers are done
+          load_w(p, kb0, nb, 0);
+          if (act) {
+            load_words(u, p, kb0, nb, 0, 0);
+            if (FAST && p == 0 && kb0 == 0) load_side(u, 0);
+          }
+          __builtin_amdgcn_s_waitcnt(0);
+          __syncthreads();
+          if (act) {
+            if (p == 0)
+              run(P0{}, kb0, nb, 0, 0, tw[0]);
+            else
+              run(P1{}, kb0, nb, 0, 0, tw[1]);
+          }
+        }
+      }
+      if (act) {
+        scales(u, 0, hf);
+        store(u, hf);
       }
     }
   }
@@ -572,41 +711,48 @@ hipError_t raise_lds_limit(K* fn, size_t bytes, std::atomic<size_t>& limit) {
   return hipSuccess;
 }
 
-template <int NPT, int ACT, int SC>
+template <int MS, int ACT, int SC>
 hipError_t launch_p1(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
   static std::atomic<size_t> limit{65536};
-  hipError_t e = raise_lds_limit(&prefill_p1<NPT, ACT, SC>, g.smem1, limit);
+  hipError_t e = raise_lds_limit(&prefill_p1<MS, ACT, SC>, g.smem1, limit);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((prefill_p1<NPT, ACT, SC>), dim3(g.n_tt * g.n_lt * g.ks), dim3(kThreads), g.smem1, stream, P);
+  hipLaunchKernelGGL((prefill_p1<MS, ACT, SC>), dim3(g.n_tt * g.n_lt * g.ks), dim3(kThreads1), g.smem1, stream, P);
+  return hipGetLastError();
+}
+
+template <int ACT, int SC, bool FAST>
+hipError_t launch_p2(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
+  static std::atomic<size_t> limit{65536};
+  hipError_t e = raise_lds_limit(&prefill_p2<ACT, SC, FAST>, g.smem2, limit);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((prefill_p2<ACT, SC, FAST>), dim3(g.n_og * g.n_tt2), dim3(kThreads2), g.smem2, stream, P);
   return hipGetLastError();
 }
 
 template <int ACT, int SC>
-hipError_t launch_both(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
+hipError_t launch_all(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
   hipError_t e;
-  switch (g.npt) {
+  switch (g.ms) {
+    case 1: e = launch_p1<1, ACT, SC>(P, g, stream); break;
     case 2: e = launch_p1<2, ACT, SC>(P, g, stream); break;
+    case 3: e = launch_p1<3, ACT, SC>(P, g, stream); break;
     case 4: e = launch_p1<4, ACT, SC>(P, g, stream); break;
     case 5: e = launch_p1<5, ACT, SC>(P, g, stream); break;
-    default: e = launch_p1<kMaxPairs, ACT, SC>(P, g, stream); break;
+    default: e = launch_p1<kMaxMs, ACT, SC>(P, g, stream); break;
   }
   if (e != hipSuccess) return e;
-  const int items = P.T * 2 * P.nkb * 4;
+  const int items = 2 * P.nkb * P.n_tt * 256;
   hipLaunchKernelGGL((prefill_p1b<ACT, SC>), dim3((items + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, P);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  static std::atomic<size_t> limit{65536};
-  const size_t smem2 = p2_lds_bytes(P.kbc, ACT == kDtF32 ? 3 : 2);
-  if ((e = raise_lds_limit(&prefill_p2<ACT, SC>, smem2, limit)) != hipSuccess) return e;
-  hipLaunchKernelGGL((prefill_p2<ACT, SC>), dim3(g.n_ot * g.n_tt2), dim3(kThreads), smem2, stream, P);
-  return hipGetLastError();
+  return P.hvec ? launch_p2<ACT, SC, true>(P, g, stream) : launch_p2<ACT, SC, false>(P, g, stream);
 }
 
 template <int ACT>
 hipError_t launch_act(const PrefillParams& P, int sc_dt, const PrefillGeom& g, hipStream_t stream) {
   switch (sc_dt) {
-    case kDtF32: return launch_both<ACT, kDtF32>(P, g, stream);
-    case kDtF16: return launch_both<ACT, kDtF16>(P, g, stream);
-    default: return launch_both<ACT, kDtBF16>(P, g, stream);
+    case kDtF32: return launch_all<ACT, kDtF32>(P, g, stream);
+    case kDtF16: return launch_all<ACT, kDtF16>(P, g, stream);
+    default: return launch_all<ACT, kDtBF16>(P, g, stream);
   }
 }
 
@@ -617,42 +763,56 @@ int64_t packed_bytes(int64_t n_out, int64_t n_red) {
   return 4 * (n_red >> 5) * n_out + (w == 0 ? 0 : (w <= 16 ? 2 : 4)) * n_out;
 }
 
+// LDS sizes and the P2 plan for the activation / scale dtypes: P2 holds all w
+// fragments of its token tile when they fit, else chunks of kMaxKbc blocks,
+// and runs about 256 workgroups per CU-round (two per CU when the LDS allows)
+void plan_lds(PrefillGeom& g, int act, int sc) {
+  const int G = sc == kDtF32 ? 3 : (sc == kDtF16 ? 2 : 1);
+  g.smem1 = p1_lds(g.kb_per, G, act, g.ms);
+  const int nw = act == kDtF32 ? 3 : 2;
+  const size_t res_bytes = p2_w_bytes(2 * g.nkb, nw) + p2_wd_bytes(2 * g.nkb, 2);
+  g.res = res_bytes <= kLdsBudget ? 1 : 0;
+  g.kbc = g.nkb < kMaxKbc ? g.nkb : kMaxKbc;
+  g.smem2 = g.res ? res_bytes : p2_w_bytes(g.kbc, nw) + p2_wd_bytes(g.kbc, 1);
+  int og = 256 / g.n_tt2;
+  if (og < 1) og = 1;
+  if (og > g.n_un) og = g.n_un;
+  // the fewest groups that give the same number of units per group
+  const int upg = (g.n_un + og - 1) / og;
+  g.n_og = (g.n_un + upg - 1) / upg;
+}
+
 }  // namespace
 
 PrefillGeom prefill_geometry(int T, int d_in, int d_out, int r) {
   PrefillGeom g{};
   const int tt = T > 0 ? T : 1;
-  g.nkb = nblocks32(r > 0 ? r : 1);
-  const int npairs = 2 * g.nkb;
-  // latent tiles of at most kMaxPairs pairs, as even as possible (2, 4, 5 or 6)
-  g.n_lt = (npairs + kMaxPairs - 1) / kMaxPairs;
-  g.npt = (npairs + g.n_lt - 1) / g.n_lt;
-  if (g.npt == 3) g.npt = 4;
+  const int rr = r > 0 ? r : 1;
+  g.nkb = nblocks32(rr);
+  g.ns16 = (rr + 15) / 16;
+  // P1: each wave takes ms interleaved subtiles of its path (2 waves a path)
+  g.n_lt = (g.ns16 + 2 * kMaxMs - 1) / (2 * kMaxMs);
+  g.ms = (g.ns16 + 2 * g.n_lt - 1) / (2 * g.n_lt);
+  g.ns16p = g.n_lt * 2 * g.ms;
   g.n_tt = (tt + kTok1 - 1) / kTok1;
   const int nbt = nblocks32(d_in > 0 ? d_in : 1);
   const int tiles = g.n_tt * g.n_lt;
-  // about 256 workgroups, every split at most kMaxKbPer steps, at least one
-  // step per wave when the reduction is long enough
+  // about 256 workgroups; splits of at least kMinSteps steps (when d_in has
+  // them) and at most kMaxKbPer
   int ks = (256 + tiles - 1) / tiles;
-  if (ks > nbt / kWaves) ks = nbt / kWaves;
+  if (ks > nbt / kMinSteps) ks = nbt / kMinSteps;
   const int ks_min = (nbt + kMaxKbPer - 1) / kMaxKbPer;
   if (ks < ks_min) ks = ks_min;
   if (ks < 1) ks = 1;
   g.kb_per = (nbt + ks - 1) / ks;
   g.ks = (nbt + g.kb_per - 1) / g.kb_per;
-  g.n_ot = (d_out + kOut2 - 1) / kOut2;
-  if (g.n_ot < 1) g.n_ot = 1;
+  g.n_un = (d_out > 0 ? d_out + kUnit - 1 : kUnit) / kUnit;
   g.n_tt2 = (tt + kTok2 - 1) / kTok2;
-  // P2 stages up to kMaxKbc 32-latent blocks of one path per round
-  g.kbc = g.nkb < kMaxKbc ? g.nkb : kMaxKbc;
-  // LDS of P1: the g terms (both paths, up to 3 terms) or the wave reduction
-  const size_t gterm = static_cast<size_t>(2) * g.kb_per * 4 * 3 * 16;
-  const size_t red = static_cast<size_t>(kWaves) * kRedPairs * kTn1 * 64 * 32;
-  g.smem1 = gterm > red ? gterm : red;
+  plan_lds(g, kDtF32, kDtF32);
   // workspace (nothing beyond the control block when there is nothing to compute)
   const bool work = T > 0 && d_in > 0 && r > 0;
   g.pbuf_off = kCtrlBytes;
-  g.pbuf_floats = work ? static_cast<size_t>(g.ks) * tiles * g.npt * kPbufPair : 0;
+  g.pbuf_floats = work ? static_cast<size_t>(g.ks) * g.n_tt * 2 * g.ns16p * kPart : 0;
   g.wterm_off = g.pbuf_off + align256(4 * g.pbuf_floats);
   g.wterm_bytes = work ? static_cast<size_t>(2) * 3 * g.nkb * T * 64 : 0;
   g.ws_bytes = g.wterm_off + align256(g.wterm_bytes);
@@ -660,16 +820,17 @@ PrefillGeom prefill_geometry(int T, int d_in, int d_out, int r) {
 }
 
 bool prefill_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
-  // 32-bit buffer offsets, and one arrival counter per P1 tile
+  // 32-bit buffer offsets
   const int64_t lim = int64_t(1) << 31;
   const PrefillGeom g = prefill_geometry(static_cast<int>(T), static_cast<int>(d_in), static_cast<int>(d_out),
                                          static_cast<int>(r));
   return int64_t(kTok2) * d_out * 4 < lim && int64_t(kTok1) * d_in * 4 < lim && packed_bytes(d_out, r) < lim &&
-         packed_bytes(r, d_in) < lim && static_cast<int64_t>(g.wterm_bytes) < lim &&
-         (g.ks == 1 || static_cast<int64_t>(g.n_tt) * g.n_lt <= kCtrlMaxTiles);
+         packed_bytes(r, d_in) < lim && static_cast<int64_t>(g.wterm_bytes) < lim;
 }
 
-hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g, hipStream_t stream) {
+hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g0, hipStream_t stream) {
+  PrefillGeom g = g0;
+  plan_lds(g, a.act_dt, a.sc_dt);
   PrefillParams P{};
   P.x = a.x;
   P.y = a.y;
@@ -688,15 +849,20 @@ hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g, hipStream_
   P.d_out = a.d_out;
   P.r = a.r;
   P.nkb = g.nkb;
+  P.ns16 = g.ns16;
   P.n_tt = g.n_tt;
   P.n_lt = g.n_lt;
   P.ks = g.ks;
   P.kb_per = g.kb_per;
-  P.n_ot = g.n_ot;
+  P.ns16p = g.ns16p;
+  P.n_un = g.n_un;
+  P.n_og = g.n_og;
+  P.n_tt2 = g.n_tt2;
+  P.res = g.res;
   P.kbc = g.kbc;
-  P.npt = g.npt;
   const int64_t ex = a.act_dt == kDtF32 ? 4 : 2, es = a.sc_dt == kDtF32 ? 4 : 2;
-  P.xvec = (reinterpret_cast<uintptr_t>(a.x) % (4 * ex) == 0) && (a.d_in % 4 == 0);
+  // global-to-LDS x loads need 16-byte aligned rows of whole 16-byte chunks
+  P.xdma = (reinterpret_cast<uintptr_t>(a.x) % 16 == 0) && ((a.d_in * ex) % 16 == 0);
   P.yvec = (reinterpret_cast<uintptr_t>(a.y) % (4 * ex) == 0) && (a.d_out % 4 == 0);
   // 4-element vector loads of h never straddle its end only when d_out % 4 == 0
   P.hvec = (reinterpret_cast<uintptr_t>(a.h[0]) % (4 * es) == 0) &&
@@ -708,6 +874,7 @@ hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g, hipStream_
   P.l_bytes = static_cast<uint32_t>(a.r * es);
   const int nw = a.act_dt == kDtF32 ? 3 : 2;
   P.wt_bytes = static_cast<uint32_t>(static_cast<int64_t>(2) * nw * g.nkb * a.T * 64);
+  P.wd_off = static_cast<uint32_t>(p2_w_bytes(g.res ? 2 * g.nkb : g.kbc, nw));
   switch (a.act_dt) {
     case kDtF32: return launch_act<kDtF32>(P, a.sc_dt, g, stream);
     case kDtF16: return launch_act<kDtF16>(P, a.sc_dt, g, stream);
