@@ -90,9 +90,11 @@ struct PrefillParams {
   int n_un, n_og, n_tt2;  // P2 units, unit groups, token tiles
   int res, kbc;     // P2: w resident / blocks per chunk
   int xdma;         // x rows are whole 16-byte chunks: global-to-LDS loads
-  int hvec, yvec;   // aligned 4-element access allowed for h / y
+  int vw;           // P1 V words in 16-byte loads (r % 4 == 0, V 16-byte aligned)
+  int fast;         // P2 fast path (see prefill_p2)
   uint32_t v_bytes, u_bytes, g_bytes, h_bytes, l_bytes, wt_bytes;
   uint32_t wd_off;  // P2: byte offset of the U-word buffers in LDS
+  int wdp;          // P2: U-word block slots per wave and buffer
 };
 
 // s_waitcnt: at most VM vector-memory operations outstanding, no LDS access
@@ -106,25 +108,29 @@ __device__ __forceinline__ void wait_vm_lds() {
 // P1
 // ---------------------------------------------------------------------------
 __host__ __device__ constexpr int p1_nx(int act) { return act == kDtF32 ? 2 : 1; }  // 16-byte chunks per lane
-__host__ __device__ constexpr int p1_nv(int ms) { return (ms + 3) / 4; }            // V-word loads per wave
+// V-word loads per wave and step: one 16-byte load (4 words a lane) when
+// r % 4 == 0 and V is 16-byte aligned (VW), else dword loads of 64 words
+__host__ __device__ constexpr int p1_nv(int ms, bool vw) { return vw ? 1 : (ms + 3) / 4; }
 __host__ __device__ constexpr size_t p1_gt_bytes(int kb_per, int G) {
   return static_cast<size_t>(2) * kb_per * 4 * G * 16;
 }
 __host__ __device__ constexpr size_t p1_xslot(int nx) { return static_cast<size_t>(kTn1) * nx * 1024; }
-__host__ __device__ constexpr size_t p1_vslot(int nv) { return static_cast<size_t>(kWaves) * nv * 256; }
+__host__ __device__ constexpr size_t p1_vslot(int ms, bool vw) {
+  return static_cast<size_t>(kWaves) * (vw ? 1024 : p1_nv(ms, false) * 256);
+}
 // 32-input steps staged in LDS (fp32 x takes twice the room per step)
 __host__ __device__ constexpr int p1_ring(int act) { return act == kDtF32 ? 8 : 12; }
-__host__ __device__ constexpr size_t p1_lds(int kb_per, int G, int act, int ms) {
-  const size_t ring = p1_gt_bytes(kb_per, G) + p1_ring(act) * (p1_xslot(p1_nx(act)) + p1_vslot(p1_nv(ms)));
+__host__ __device__ constexpr size_t p1_lds(int kb_per, int G, int act, int ms, bool vw) {
+  const size_t ring = p1_gt_bytes(kb_per, G) + p1_ring(act) * (p1_xslot(p1_nx(act)) + p1_vslot(ms, vw));
   const size_t red = static_cast<size_t>(kWaves) * ms * kTn1 * 64 * 16;
   return ring > red ? ring : red;
 }
 
-template <int MS, int ACT, int SC>
+template <int MS, int ACT, int SC, bool VW>
 __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
   constexpr int G = nterms<SC>(), E = nterms<ACT>();
-  constexpr int NX = p1_nx(ACT), NV = p1_nv(MS), RING = p1_ring(ACT), R2 = RING / 2;
-  constexpr int XSLOT = static_cast<int>(p1_xslot(NX)), VSLOT = static_cast<int>(p1_vslot(NV));
+  constexpr int NX = p1_nx(ACT), NV = p1_nv(MS, VW), RING = p1_ring(ACT), R2 = RING / 2;
+  constexpr int XSLOT = static_cast<int>(p1_xslot(NX)), VSLOT = static_cast<int>(p1_vslot(MS, VW));
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
@@ -144,7 +150,7 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
 
   u32x4* gt = reinterpret_cast<u32x4*>(lds);  // g terms [2][ns][4 lane groups][G]
   char* xs = lds + p1_gt_bytes(P.kb_per, G);  // x ring [RING][4 token subtiles][NX][64] x 16 B
-  char* vs = xs + RING * XSLOT;               // V-word ring [RING][4 roles][NV][64] x 4 B
+  char* vs = xs + RING * XSLOT;               // V-word ring [RING][4 roles][VSLOT / 4]
   const int ex = ACT == kDtF32 ? 4 : 2;
   const int rows = min(kTok1, T - t0);
   // x of this tile's tokens (reads past the last token return zero)
@@ -153,20 +159,31 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
   const rsrc_t vr = make_rsrc(pw ? P.V[1] : P.V[0], P.v_bytes);
 
   // loads of step n (split-local) into its ring slot, by the waves of its
-  // parity: the packed V words of this wave's subtiles (lane l: slot
-  // 4 d + l / 16, latent l % 16 of it; zero past r, past the range and for the
-  // tail step, whose words come through registers) and token subtile w4 of x
-  // (zero past d_in and past the range)
+  // parity: the packed V words of this wave's subtiles (word of latent
+  // 16 (sb0 + 2 m) + i at word 16 m + i of the wave's slice; zero past r, past
+  // the range and for the tail step, whose words come through registers) and
+  // token subtile w4 of x (zero past d_in and past the range)
   auto issue = [&](int n) {
     const int kb = kbs + n, sl = n % RING;
     const bool valid = n < ns;
-#pragma unroll
-    for (int d = 0; d < NV; ++d) {
-      const int m = 4 * d + gq;
-      const int k = 16 * (sb0 + 2 * m) + n16;
+    char* vd = vs + sl * VSLOT + w4 * (VSLOT / kWaves);
+    if constexpr (VW) {
+      // lane l: words of latents 16 (sb0 + 2 (l / 4)) + 4 (l % 4) .. + 3
+      const int m = lane >> 2;
+      const int k = 16 * (sb0 + 2 * m) + 4 * (lane & 3);
       const bool ok = valid && kb < nbv && m < MS && k < r;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr)(vs + sl * VSLOT + (w4 * NV + d) * 256), 4,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr)vd, 16,
                                                ok ? static_cast<uint32_t>(kb * r + k) * 4u : kOob, 0, 0, 0);
+    } else {
+      // lane l of load d: the word of latent 16 (sb0 + 2 m) + l % 16, m = 4 d + l / 16
+#pragma unroll
+      for (int d = 0; d < NV; ++d) {
+        const int m = 4 * d + gq;
+        const int k = 16 * (sb0 + 2 * m) + n16;
+        const bool ok = valid && kb < nbv && m < MS && k < r;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_ptr)(vd + d * 256), 4,
+                                                 ok ? static_cast<uint32_t>(kb * r + k) * 4u : kOob, 0, 0, 0);
+      }
     }
     const int row = 16 * w4 + n16;
     char* xd = xs + sl * XSLOT + w4 * NX * 1024;
@@ -251,9 +268,11 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
     wait_vm_lds<(R2 - 2) * (NX + NV)>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    issue(2 * (i + R2 - 1) + half);
     const int n = 2 * i + half;
-    if (n >= ns) continue;  // (an odd count: the second half sits out the last round)
+    if (n >= ns) {  // (an odd count: the second half sits out the last round)
+      issue(2 * (i + R2 - 1) + half);
+      continue;
+    }
     const int sl = n % RING;
     const bool tail = kbs + n == nbv;
 
@@ -290,11 +309,17 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
     u32x4 gv[G];
 #pragma unroll
     for (int s = 0; s < G; ++s) gv[s] = gtp[(n * 4 + gq) * G + s];
-    const uint32_t* vw = reinterpret_cast<const uint32_t*>(vs + sl * VSLOT + w4 * NV * 256);
+    const uint32_t* vw = reinterpret_cast<const uint32_t*>(vs + sl * VSLOT + w4 * (VSLOT / kWaves));
+    uint32_t words[MS];
+#pragma unroll
+    for (int m = 0; m < MS; ++m) words[m] = tail ? tw[m] : vw[16 * m + n16];
+    // the loads of round i + R2 - 1 (into the slots of round i - 1, free since
+    // the barrier), issued once this step's LDS reads are out
+    issue(2 * (i + R2 - 1) + half);
     u32x4 A[MS][G];
 #pragma unroll
     for (int m = 0; m < MS; ++m) {
-      const uint32_t word = tail ? tw[m] : vw[16 * m + n16];
+      const uint32_t word = words[m];
       const uint32_t t = word >> (8 * gq);
       const uint32_t dd = (t & 0xffffu) | ((t << 15) & 0xffff0000u);
 #pragma unroll
@@ -425,10 +450,11 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
   }
 }
 
-// FAST: d_out % 4 == 0 and aligned row scales, so the scales and 16-bit tail
-// words of a unit come in whole dwords through global-to-LDS loads like the U
-// words (prefetched a unit ahead); otherwise they are read per unit into
-// registers
+// FAST: d_out % 4 == 0 and aligned U, h and y, so the U words of a unit come
+// in 16-byte global-to-LDS loads (4 blocks of 64 outputs a load), its scales
+// and 16-bit tail words in dword ones (all prefetched a unit ahead) and y in
+// 4-output stores; otherwise words come in dword loads, scales and tail words
+// per unit through registers and y element by element
 template <int ACT, int SC, bool FAST>
 __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
   constexpr int NW = ACT == kDtF32 ? 3 : 2;
@@ -447,8 +473,10 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
   const int nfull = nbu + (tailu > 16 ? 1 : 0);  // blocks with 32-bit words
   const bool t16 = tailu != 0 && tailu <= 16;     // block nbu has 16-bit words
   const bool res = P.res != 0;
-  const int held = res ? 2 * nkb : P.kbc;  // pairs in LDS at once
-  const int wvb = p2_wave_bytes(held);
+  const int held = res ? 2 * nkb : P.kbc;  // w pairs in LDS at once
+  const int wdp = P.wdp;                   // U-word block slots per wave and buffer
+  const int ws1 = res ? wdp / 2 : 0;       // slot of path 1's first block (resident)
+  const int wvb = p2_wave_bytes(wdp);
   const rsrc_t wr = make_rsrc(P.wterm, P.wt_bytes);
   const rsrc_t ur[2] = {make_rsrc(P.U[0], P.u_bytes), make_rsrc(P.U[1], P.u_bytes)};
   const rsrc_t hr[2] = {make_rsrc(P.h[0], P.h_bytes), make_rsrc(P.h[1], P.h_bytes)};
@@ -473,14 +501,26 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
   // U words (32-bit: full words and a tail block of more than 16 latents) of
   // blocks kb0 .. kb0 + nb - 1 of path p for this wave's 64 outputs of unit u
   auto load_words = [&](int u, int p, int kb0, int nb, int buf, int hs0) {
-    const int o = u * kUnit + 64 * oh + lane;
-    const bool ok = o < d_out;
     char* dst = region(buf) + hs0 * 256;
-    for (int kbl = 0; kbl < nb; ++kbl) {
-      const int kb = kb0 + kbl;
-      if (kb >= nfull) break;
-      const uint32_t off = kb < nbu ? static_cast<uint32_t>(kb * d_out + o) * 4u : 4u * nbu * d_out + 4u * o;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ur[p], (lds_ptr)(dst + kbl * 256), 4, ok ? off : kOob, 0, 0, 0);
+    const int nf = min(nb, nfull - kb0);
+    if constexpr (FAST) {
+      // lane l: block kb0 + kbl0 + l / 16, outputs ob + 4 (l % 16) .. + 3
+      const int o = u * kUnit + 64 * oh + 4 * (lane & 15);
+      for (int kbl0 = 0; kbl0 < nf; kbl0 += 4) {
+        const int kbl = kbl0 + (lane >> 4);
+        const int kb = kb0 + kbl;
+        const uint32_t off = kb < nbu ? static_cast<uint32_t>(kb * d_out + o) * 4u : 4u * nbu * d_out + 4u * o;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ur[p], (lds_ptr)(dst + kbl0 * 256), 16,
+                                                 kbl < nf && o < d_out ? off : kOob, 0, 0, 0);
+      }
+    } else {
+      const int o = u * kUnit + 64 * oh + lane;
+      const bool ok = o < d_out;
+      for (int kbl = 0; kbl < nf; ++kbl) {
+        const int kb = kb0 + kbl;
+        const uint32_t off = kb < nbu ? static_cast<uint32_t>(kb * d_out + o) * 4u : 4u * nbu * d_out + 4u * o;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ur[p], (lds_ptr)(dst + kbl * 256), 4, ok ? off : kOob, 0, 0, 0);
+      }
     }
   };
   // FAST: row scales and 16-bit tail words of unit u as whole dwords (lane l:
@@ -488,7 +528,7 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
   // of outputs 2 l, 2 l + 1)
   auto load_side = [&](int u, int buf) {
     const int ob = u * kUnit + 64 * oh;
-    char* dst = region(buf) + held * 256;
+    char* dst = region(buf) + wdp * 256;
     const int oe = ES == 2 ? ob + 2 * lane : ob + lane;
     const int ot = ob + 2 * lane;
 #pragma unroll
@@ -521,7 +561,7 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
       for (int im = 0; im < kIm2; ++im) {
         uint32_t raw[4];
         if constexpr (FAST) {
-          const char* src = region(buf) + held * 256 + p * 256 + (16 * im + 4 * gq) * ES;
+          const char* src = region(buf) + wdp * 256 + p * 256 + (16 * im + 4 * gq) * ES;
           if constexpr (ES == 4) {
             const u32x4 v = *reinterpret_cast<const u32x4*>(src);
             raw[0] = v[0], raw[1] = v[1], raw[2] = v[2], raw[3] = v[3];
@@ -558,7 +598,7 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
       if constexpr (!W16)
         word = words[16 * im + n16];
       else if constexpr (FAST)
-        word = *reinterpret_cast<const uint16_t*>(region(buf) + held * 256 + 512 + p * 256 + (16 * im + n16) * 2);
+        word = *reinterpret_cast<const uint16_t*>(region(buf) + wdp * 256 + 512 + p * 256 + (16 * im + n16) * 2);
       else
         word = tw[im] & 0xffffu;
       const u32x4 A = sign_terms(word, gq, ones);
@@ -570,9 +610,10 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
   };
   using False = std::integral_constant<bool, false>;
   using True = std::integral_constant<bool, true>;
-  // products of held pairs (p, kb0 .. kb0 + nb - 1) at held slots from hs0
-  auto run = [&](auto pc, int kb0, int nb, int hs0, int buf, const uint32_t (&tw)[kIm2]) {
-    const uint32_t* words = reinterpret_cast<const uint32_t*>(region(buf) + hs0 * 256);
+  // products of held pairs (p, kb0 .. kb0 + nb - 1): w at held slots from
+  // hs0, U words at word slots from ds0
+  auto run = [&](auto pc, int kb0, int nb, int hs0, int ds0, int buf, const uint32_t (&tw)[kIm2]) {
+    const uint32_t* words = reinterpret_cast<const uint32_t*>(region(buf) + ds0 * 256);
     const int nf = max(0, min(nb, nfull - kb0));
     for (int kbl = 0; kbl < nf; ++kbl) pair(pc, False{}, hs0 + kbl, words + kbl * 64, buf, tw);
     if (t16 && nbu >= kb0 && nbu < kb0 + nb) pair(pc, True{}, hs0 + nbu - kb0, words, buf, tw);
@@ -594,7 +635,7 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = hf[0][im][e] * acc[0][im][tn][e] + hf[1][im][e] * acc[1][im][tn][e];
         const uint32_t base = static_cast<uint32_t>((t - t0) * d_out + ib);  // within the tile's rows
-        if (P.yvec) {
+        if constexpr (FAST) {
           // whole groups of 4 outputs (d_out % 4 == 0); rows past T are past the buffer
           const bool ok = t < T && ib < d_out;
           if constexpr (ACT == kDtF32) {
@@ -605,10 +646,12 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
             const u32x2 d = {pack2<ACT>(v[0], v[1]), pack2<ACT>(v[2], v[3])};
             __builtin_amdgcn_raw_buffer_store_b64(d, yr, ok ? base * 2u : kOob, 0, 0);
           }
-        } else if (t < T) {
+        } else {
+          if (t < T) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (ib + e < d_out) st<ACT>(P.y, static_cast<int64_t>(t) * d_out + ib + e, v[e]);
+            for (int e = 0; e < 4; ++e)
+              if (ib + e < d_out) st<ACT>(P.y, static_cast<int64_t>(t) * d_out + ib + e, v[e]);
+          }
         }
       }
     }
@@ -636,7 +679,7 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
     int u = og + hu * P.n_og;
     if (u < P.n_un) {
       load_words(u, 0, 0, nkb, 0, 0);
-      load_words(u, 1, 0, nkb, 0, nkb);
+      load_words(u, 1, 0, nkb, 0, ws1);
       load_side(u, 0);
     }
     __builtin_amdgcn_s_waitcnt(0);  // global-to-LDS loads count as memory loads
@@ -647,12 +690,12 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
       const int buf = k & 1;
       if (un < P.n_un) {
         load_words(un, 0, 0, nkb, buf ^ 1, 0);
-        load_words(un, 1, 0, nkb, buf ^ 1, nkb);
+        load_words(un, 1, 0, nkb, buf ^ 1, ws1);
         load_side(un, buf ^ 1);
       }
       zero_acc();
-      run(P0{}, 0, nkb, 0, buf, tw[0]);
-      run(P1{}, 0, nkb, nkb, buf, tw[1]);
+      run(P0{}, 0, nkb, 0, 0, buf, tw[0]);
+      run(P1{}, 0, nkb, nkb, ws1, buf, tw[1]);
       // the next unit's loads (issued a unit ago) and the previous unit's
       // stores have landed: this wait is before the stores, not after them
       __builtin_amdgcn_s_waitcnt(0);
@@ -682,9 +725,9 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
           __syncthreads();
           if (act) {
             if (p == 0)
-              run(P0{}, kb0, nb, 0, 0, tw[0]);
+              run(P0{}, kb0, nb, 0, 0, 0, tw[0]);
             else
-              run(P1{}, kb0, nb, 0, 0, tw[1]);
+              run(P1{}, kb0, nb, 0, 0, 0, tw[1]);
           }
         }
       }
@@ -711,13 +754,18 @@ hipError_t raise_lds_limit(K* fn, size_t bytes, std::atomic<size_t>& limit) {
   return hipSuccess;
 }
 
+template <int MS, int ACT, int SC, bool VW>
+hipError_t launch_p1v(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
+  static std::atomic<size_t> limit{65536};
+  hipError_t e = raise_lds_limit(&prefill_p1<MS, ACT, SC, VW>, g.smem1, limit);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((prefill_p1<MS, ACT, SC, VW>), dim3(g.n_tt * g.n_lt * g.ks), dim3(kThreads1), g.smem1, stream,
+                     P);
+  return hipGetLastError();
+}
 template <int MS, int ACT, int SC>
 hipError_t launch_p1(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
-  static std::atomic<size_t> limit{65536};
-  hipError_t e = raise_lds_limit(&prefill_p1<MS, ACT, SC>, g.smem1, limit);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((prefill_p1<MS, ACT, SC>), dim3(g.n_tt * g.n_lt * g.ks), dim3(kThreads1), g.smem1, stream, P);
-  return hipGetLastError();
+  return P.vw ? launch_p1v<MS, ACT, SC, true>(P, g, stream) : launch_p1v<MS, ACT, SC, false>(P, g, stream);
 }
 
 template <int ACT, int SC, bool FAST>
@@ -744,7 +792,7 @@ hipError_t launch_all(const PrefillParams& P, const PrefillGeom& g, hipStream_t 
   const int items = 2 * P.nkb * P.n_tt * 256;
   hipLaunchKernelGGL((prefill_p1b<ACT, SC>), dim3((items + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, P);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  return P.hvec ? launch_p2<ACT, SC, true>(P, g, stream) : launch_p2<ACT, SC, false>(P, g, stream);
+  return P.fast ? launch_p2<ACT, SC, true>(P, g, stream) : launch_p2<ACT, SC, false>(P, g, stream);
 }
 
 template <int ACT>
@@ -763,17 +811,26 @@ int64_t packed_bytes(int64_t n_out, int64_t n_red) {
   return 4 * (n_red >> 5) * n_out + (w == 0 ? 0 : (w <= 16 ? 2 : 4)) * n_out;
 }
 
+// U-word block slots per wave and buffer of P2
+int p2_wdp(const PrefillGeom& g, bool fast) {
+  const int nkb4 = fast ? (g.nkb + 3) / 4 * 4 : g.nkb;
+  return g.res ? 2 * nkb4 : (fast ? (g.kbc + 3) / 4 * 4 : g.kbc);
+}
+
 // LDS sizes and the P2 plan for the activation / scale dtypes: P2 holds all w
 // fragments of its token tile when they fit, else chunks of kMaxKbc blocks,
 // and runs about 256 workgroups per CU-round (two per CU when the LDS allows)
-void plan_lds(PrefillGeom& g, int act, int sc) {
+void plan_lds(PrefillGeom& g, int act, int sc, bool vw, bool fast) {
   const int G = sc == kDtF32 ? 3 : (sc == kDtF16 ? 2 : 1);
-  g.smem1 = p1_lds(g.kb_per, G, act, g.ms);
+  g.smem1 = p1_lds(g.kb_per, G, act, g.ms, vw);
   const int nw = act == kDtF32 ? 3 : 2;
-  const size_t res_bytes = p2_w_bytes(2 * g.nkb, nw) + p2_wd_bytes(2 * g.nkb, 2);
+  // U-word slots: 16-byte loads fill 4 blocks at a time, so each path's run
+  // of slots is a multiple of 4 (FAST)
+  const int nkb4 = fast ? (g.nkb + 3) / 4 * 4 : g.nkb;
+  const size_t res_bytes = p2_w_bytes(2 * g.nkb, nw) + p2_wd_bytes(2 * nkb4, 2);
   g.res = res_bytes <= kLdsBudget ? 1 : 0;
   g.kbc = g.nkb < kMaxKbc ? g.nkb : kMaxKbc;
-  g.smem2 = g.res ? res_bytes : p2_w_bytes(g.kbc, nw) + p2_wd_bytes(g.kbc, 1);
+  g.smem2 = g.res ? res_bytes : p2_w_bytes(g.kbc, nw) + p2_wd_bytes(p2_wdp(g, fast), 1);
   int og = 256 / g.n_tt2;
   if (og < 1) og = 1;
   if (og > g.n_un) og = g.n_un;
@@ -808,7 +865,7 @@ PrefillGeom prefill_geometry(int T, int d_in, int d_out, int r) {
   g.ks = (nbt + g.kb_per - 1) / g.kb_per;
   g.n_un = (d_out > 0 ? d_out + kUnit - 1 : kUnit) / kUnit;
   g.n_tt2 = (tt + kTok2 - 1) / kTok2;
-  plan_lds(g, kDtF32, kDtF32);
+  plan_lds(g, kDtF32, kDtF32, false, false);
   // workspace (nothing beyond the control block when there is nothing to compute)
   const bool work = T > 0 && d_in > 0 && r > 0;
   g.pbuf_off = kCtrlBytes;
@@ -829,8 +886,15 @@ bool prefill_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
 }
 
 hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g0, hipStream_t stream) {
+  const int64_t ex = a.act_dt == kDtF32 ? 4 : 2, es = a.sc_dt == kDtF32 ? 4 : 2;
+  auto al = [](const void* q, int64_t n) { return reinterpret_cast<uintptr_t>(q) % n == 0; };
+  // 16-byte V-word loads: whole 4-word groups per latent block row
+  const bool vw = a.r % 4 == 0 && al(a.V[0], 16) && al(a.V[1], 16);
+  // P2 fast path: whole 4-output groups, 16-byte aligned U words, aligned h and y
+  const bool fast = a.d_out % 4 == 0 && al(a.U[0], 16) && al(a.U[1], 16) && al(a.h[0], 4 * es) &&
+                    al(a.h[1], 4 * es) && al(a.y, 4 * ex);
   PrefillGeom g = g0;
-  plan_lds(g, a.act_dt, a.sc_dt);
+  plan_lds(g, a.act_dt, a.sc_dt, vw, fast);
   PrefillParams P{};
   P.x = a.x;
   P.y = a.y;
@@ -860,13 +924,11 @@ hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g0, hipStream
   P.n_tt2 = g.n_tt2;
   P.res = g.res;
   P.kbc = g.kbc;
-  const int64_t ex = a.act_dt == kDtF32 ? 4 : 2, es = a.sc_dt == kDtF32 ? 4 : 2;
   // global-to-LDS x loads need 16-byte aligned rows of whole 16-byte chunks
-  P.xdma = (reinterpret_cast<uintptr_t>(a.x) % 16 == 0) && ((a.d_in * ex) % 16 == 0);
-  P.yvec = (reinterpret_cast<uintptr_t>(a.y) % (4 * ex) == 0) && (a.d_out % 4 == 0);
-  // 4-element vector loads of h never straddle its end only when d_out % 4 == 0
-  P.hvec = (reinterpret_cast<uintptr_t>(a.h[0]) % (4 * es) == 0) &&
-           (reinterpret_cast<uintptr_t>(a.h[1]) % (4 * es) == 0) && (a.d_out % 4 == 0);
+  P.xdma = al(a.x, 16) && (a.d_in * ex) % 16 == 0;
+  P.vw = vw;
+  P.fast = fast;
+  P.wdp = p2_wdp(g, fast);
   P.v_bytes = static_cast<uint32_t>(packed_bytes(a.r, a.d_in));
   P.u_bytes = static_cast<uint32_t>(packed_bytes(a.d_out, a.r));
   P.g_bytes = static_cast<uint32_t>(a.d_in * es);
