@@ -218,7 +218,8 @@ def source_digest(files):
     return h.hexdigest()[:16]
 
 
-DECODE_SOURCES = ["paper_2506_13771_amd/csrc/decode.hip", "paper_2506_13771_amd/csrc/lb_internal.h"]
+DECODE_SOURCES = ["paper_2506_13771_amd/csrc/decode.hip", "paper_2506_13771_amd/csrc/lb_internal.h",
+                  "paper_2506_13771_amd/csrc/device_common.h"]
 
 
 def copy_probe(mib):
@@ -325,7 +326,7 @@ def cpu_baseline(li, seconds):
 # ----------------------------------------------------------------------------
 # sweep of the other configurations (diagnostic lines written to a file)
 # ----------------------------------------------------------------------------
-def run_sweep(path, steps, warmup):
+def run_sweep(path, steps, warmup, only=("7b", "13b", "70b")):
     import torch
     from paper_2506_13771_amd import synth
     out = open(path, "w")
@@ -336,7 +337,7 @@ def run_sweep(path, steps, warmup):
         log(json.dumps(rec))
 
     ranks_7b = {0.1: {4096: 80, 11008: 128}, 0.55: {4096: 544, 11008: 800}}
-    for bpw in (0.1, 0.55):
+    for bpw in ((0.1, 0.55) if "7b" in only else ()):
         for T in (1, 16, 64):
             for idx, (name, d_in, d_out) in enumerate(synth.LLAMA2_7B):
                 r = ranks_7b[bpw][max(d_in, d_out)]
@@ -350,7 +351,7 @@ def run_sweep(path, steps, warmup):
                       "mfma_frac": alg_flops(T, d_in, d_out, r) / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS})
                 del L
     ranks_13b = {(5120, 5120): 96, (5120, 13824): 160, (13824, 5120): 160}
-    for idx, (name, d_in, d_out) in enumerate(synth.LLAMA2_13B):
+    for idx, (name, d_in, d_out) in enumerate(synth.LLAMA2_13B if "13b" in only else ()):
         r = ranks_13b[(d_in, d_out)]
         T = 2048
         L = Layer(synth.make_linear(d_in, d_out, r, T, cfg=3, linear=idx), "cuda")
@@ -364,7 +365,7 @@ def run_sweep(path, steps, warmup):
         del L
     # 70B sweep: 80 layers x 7 linears resident, back-to-back on one stream
     ranks_70b = {(8192, 8192): 176, (8192, 1024): 16, (8192, 28672): 288, (28672, 8192): 288}
-    for T in (1, 8, 64):
+    for T in ((1, 8, 64) if "70b" in only else ()):
         layers = []
         tot_b = 0.0
         tot_w = 0.0
@@ -395,6 +396,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", default=None, help="write per-configuration JSON lines to this file")
+    ap.add_argument("--sweep-only", default="7b,13b,70b",
+                    help="comma list of the sweep's parts to run (7b block, 13b prefill, 70b decode sweep)")
     ap.add_argument("--no-warm", action="store_true",
                     help="skip the warm-cache measurements (counter runs: every decode dispatch is then a "
                          "cold-rotation one)")
@@ -486,7 +489,7 @@ def main():
     if args.copy_probe:
         copy_probe(args.copy_probe)
     if args.sweep:
-        run_sweep(args.sweep, min(args.steps, 1000), min(args.warmup, 100))
+        run_sweep(args.sweep, min(args.steps, 1000), min(args.warmup, 100), tuple(args.sweep_only.split(",")))
 
 
 if __name__ == "__main__":
