@@ -74,12 +74,14 @@ typedef enum lb_role { LB_ROLE_U = 0, LB_ROLE_V = 1 } lb_role;
 
 /* Which forward kernel lb_linear_forward_kernel() runs. */
 typedef enum lb_kernel {
-  LB_KERNEL_AUTO = 0,         /* DECODE for T <= 2, DECODE_MFMA for T <= 64, PREFILL above (each
-                                 where its rank limit allows) */
+  LB_KERNEL_AUTO = 0,         /* DECODE for T <= 2; from T = 3 DECODE_MFMA while T r d_out is
+                                 small (T < 16, or T < 32 with r d_out < 3e6, and r d_out < 8e6),
+                                 PREFILL otherwise (each where its size limits allow) */
   LB_KERNEL_DECODE = 1,       /* single launch, 4-bit look-up tables, fp32 sign-flip accumulation;
                                  T <= 4, r <= 1024 */
-  LB_KERNEL_PREFILL = 2,      /* two launches of matrix-core (MFMA) tiles, signs expanded to bf16 +-1;
-                                 any size */
+  LB_KERNEL_PREFILL = 2,      /* three launches of matrix-core (MFMA) tiles with exact bf16 term
+                                 products (latent sums, latent scale and term split, outputs);
+                                 any size within 32-bit buffer offsets */
   LB_KERNEL_DECODE_MFMA = 3   /* single launch, matrix-core contractions: stage 1 multiplies exact
                                  bf16 terms of x by the signs carried on exact bf16 terms of g,
                                  stage 2 the +-1 signs of U by bf16 terms of l (.) z; T <= 64,

@@ -69,6 +69,16 @@ lb::ForwardArgs make_args(const void* x, lb_dtype act, int64_t T, int64_t d_in, 
 
 constexpr int64_t kAutoLutTokens = 2;  // AUTO sends T <= this to the look-up-table decode kernel
 
+// AUTO between the matrix-core decode kernel and the prefill kernels: the
+// decode kernel's single launch wins while T r d_out is small; the prefill
+// kernels' cost barely grows with T up to one 64-token tile.  Thresholds from
+// timings of both kernels on the Llama2-7B and -70B linear shapes (0.1 and
+// 0.55 bits per weight, T = 4 .. 64).
+bool prefer_prefill(int64_t T, int64_t d_out, int64_t r) {
+  const int64_t rd = r * d_out;
+  return T >= 32 || (T >= 16 && rd >= 3000000) || rd >= 8000000;
+}
+
 }  // namespace
 
 extern "C" {
@@ -197,7 +207,8 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
     // three on the matrix-core decode kernel takes over
     if (T <= kAutoLutTokens && lb::decode_supports(T, d_in, d_out, r))
       kernel = LB_KERNEL_DECODE;
-    else if (lb::decode_mma_supports(T, d_in, d_out, r))
+    else if (lb::decode_mma_supports(T, d_in, d_out, r) &&
+             !(prefer_prefill(T, d_out, r) && lb::prefill_supports(T, d_in, d_out, r)))
       kernel = LB_KERNEL_DECODE_MFMA;
     else if (lb::prefill_supports(T, d_in, d_out, r))
       kernel = LB_KERNEL_PREFILL;
