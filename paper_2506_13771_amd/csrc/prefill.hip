@@ -14,24 +14,25 @@
 // (2 for bf16/f16 outputs: 16 significant bits; 3 for fp32 outputs: all 24).
 // The matrix cores accumulate in fp32.
 //
-// P1.  A workgroup owns 64 tokens, a range of d_in (split over `ks`
-// workgroups, about 256 in all) and a tile of latents; its waves split the
-// latents: waves 0-1 take path 0, waves 2-3 path 1, each MS interleaved
-// 16-latent subtiles of its path, so a wave holds MS x 4 accumulator tiles
-// and no sum crosses waves.  The 32-input steps of the range stream through a
-// ring of kRing1 LDS slots filled by global-to-LDS loads (x of the 64 tokens,
-// written in B-fragment order, and the V words of every wave), kRing1 - 1
-// steps in flight; one barrier per step hands a slot from its loads to its
-// readers and back.  The g terms of the range are cut once into LDS.  Each
-// wave stores its sums to its own slice of the partial buffer.
+// P1.  A workgroup of 8 waves owns 64 tokens, a range of d_in (split over
+// `ks` workgroups, about 256 in all) and a tile of latents.  Waves 0-1 take
+// path 0 and waves 2-3 path 1, each MS interleaved 16-latent subtiles of its
+// path, so a wave holds MS x 4 accumulator tiles and no sum crosses paths;
+// waves 4-7 repeat these roles on the odd 32-input steps, and the two halves
+// are added once in LDS at the end, in a fixed order.  The steps stream
+// through an LDS ring filled by global-to-LDS loads (x of the 64 tokens,
+// written in B-fragment order, and each wave's V words), several rounds in
+// flight; one barrier per round hands slots from their loads to their
+// readers and back.  The g terms of the range are cut once into LDS.
 // P1b.  Sums the ks partials in ascending order, scales by l and stores w as
 // NW bf16 terms laid out as B fragments of P2.
-// P2.  A workgroup owns 64 tokens and a group of 128-output units.  It loads
-// the w fragments of its tokens into LDS once (when they fit; else per chunk)
-// and then runs its units: waves split a unit into 2 x 64 outputs times
-// 2 x 32 tokens.  The packed U words of the next unit are loaded into LDS and
-// its row scales into registers while the current unit runs.  Both paths
-// accumulate separately and y = h_0 acc_0 + h_1 acc_1 is rounded once.
+// P2.  A workgroup of 8 waves owns 64 tokens and a group of 128-output
+// units.  It loads the w fragments of its tokens into LDS once (when they
+// fit; else per chunk) and then runs its units: the two halves of 4 waves
+// take alternate units, a wave 64 outputs x 32 tokens.  The packed U words,
+// row scales and tail words of a half's next unit are loaded into LDS while
+// its current unit runs.  Both paths accumulate separately and
+// y = h_0 acc_0 + h_1 acc_1 is rounded once.
 //
 // P1 fragment order.  A 32-input step of B (x) is read as 16 bytes per lane:
 // lane group gq holds inputs 8 gq .. 8 gq + 7 of the step, register v the pair
