@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define LB_ABI_VERSION 1
+#define LB_ABI_VERSION 2
 
 typedef enum lb_status {
   LB_OK = 0,
@@ -155,11 +155,12 @@ int64_t lb_decode_max_tokens(void);
    x [T x d_in] in act_dtype (F32, F16 or BF16); y [T x d_out] in act_dtype,
    rounded once (round-to-nearest-even) from the fp32 sum of both paths;
    paths[0] = primary, paths[1] = residual, scales in scale_dtype (F32, F16 or
-   BF16).  Accumulation is fp32.  The decode kernel uses exact fp32 products;
-   the prefill kernel feeds MFMA with (x (.) g) and (z (.) l) formed in fp32 and
-   split into a sum of bf16 terms (two terms, 16 significant bits, for bf16/f16
-   activations; three terms, the full fp32 significand, for fp32 activations),
-   times the exact bf16 +-1 signs.  If d_in == 0 or r == 0, y is zero-filled.
+   BF16).  Accumulation is fp32.  The look-up-table decode kernel uses exact
+   fp32 products; the matrix-core kernels multiply exact bf16 terms (the
+   stored x and g cut into 1, 2 or 3 terms, the V sign carried on the g
+   terms; then the +-1 U signs times l (.) z cut into two bf16 terms, 16
+   significant bits, for bf16/f16 outputs, or three, the full fp32
+   significand, for fp32 outputs).  If d_in == 0 or r == 0, y is zero-filled.
    workspace: >= lb_forward_workspace_bytes(T, d_in, d_out, r) bytes. */
 lb_status lb_linear_forward(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out,
                             int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y,
@@ -171,6 +172,41 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
                                    int64_t d_out, int64_t r, const lb_path* paths, lb_dtype scale_dtype,
                                    void* y, void* workspace, size_t workspace_bytes, lb_kernel kernel,
                                    hipStream_t stream);
+
+/* One linear of a list for lb_linear_forward_many: the arguments
+   lb_linear_forward takes for it. */
+typedef struct lb_linear_desc {
+  const void* x;
+  lb_dtype act_dtype;
+  int64_t T, d_in, d_out, r;
+  lb_path paths[2];
+  lb_dtype scale_dtype;
+  void* y;
+} lb_linear_desc;
+
+/* Host, pure.  Workspace bytes lb_linear_forward_many needs for this list:
+   the sum of lb_forward_workspace_bytes of its linears, each rounded up to
+   256 bytes (0 if n <= 0, descs is NULL or a size is invalid).  Linear i uses
+   the slice after those of linears 0 .. i-1, with the same zero-fill-once and
+   reuse rules as lb_forward_workspace_bytes. */
+size_t lb_forward_many_workspace_bytes(const lb_linear_desc* descs, int64_t n);
+
+/* Forward of n independent LittleBit linears (each as lb_linear_forward
+   computes it, Proposition 1 summed over both paths; the paper's end-to-end
+   decoding measurement replaces every nn.Linear of the model by this
+   forward, appendix "End-to-End Decoding Throughput"), enqueued on one
+   stream with fewer launches: consecutive linears with T <= 2 and the same
+   activation and scale dtypes run as one launch of the look-up-table decode
+   kernel per up to 16 linears; every other linear is its own call with the
+   automatic kernel choice.  Results are those of lb_linear_forward for each
+   linear.  descs: host array of n descriptors (device pointers inside, as
+   for lb_linear_forward).  No y may overlap another linear's x or y (they run
+   concurrently): LB_ERR_ARG.  Every descriptor is validated as
+   lb_linear_forward validates its arguments, and the whole list before
+   anything is enqueued; n == 0 enqueues nothing.  workspace: 256-byte
+   aligned, >= lb_forward_many_workspace_bytes(descs, n) bytes. */
+lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
 
 /* Checking path: the dense effective weight of both paths,
      W[i][j] = sum_p h_p[i] g_p[j] sum_k U_p[i][k] l_p[k] V_p[j][k]

@@ -25,7 +25,7 @@ LB_OK, LB_ERR_NULL, LB_ERR_SHAPE, LB_ERR_DTYPE, LB_ERR_ALIGN, LB_ERR_WORKSPACE, 
 LB_F32, LB_F16, LB_BF16 = 0, 1, 2
 LB_ROLE_U, LB_ROLE_V = 0, 1
 LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL, LB_KERNEL_DECODE_MFMA = 0, 1, 2, 3
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 
 class LittleBitError(RuntimeError):
@@ -37,6 +37,12 @@ class LittleBitError(RuntimeError):
 class lb_path(ctypes.Structure):
     _fields_ = [("U", ctypes.c_void_p), ("V", ctypes.c_void_p), ("h", ctypes.c_void_p),
                 ("g", ctypes.c_void_p), ("l", ctypes.c_void_p)]
+
+
+class lb_linear_desc(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("act_dtype", ctypes.c_int), ("T", ctypes.c_int64),
+                ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64), ("r", ctypes.c_int64),
+                ("paths", lb_path * 2), ("scale_dtype", ctypes.c_int), ("y", ctypes.c_void_p)]
 
 
 _lib = None
@@ -75,6 +81,10 @@ def load_library(path: str = LIB_PATH):
     lib.lb_linear_forward_kernel.restype = i32
     lib.lb_linear_forward_kernel.argtypes = [vp, i32, i64, i64, i64, i64, ctypes.POINTER(lb_path), i32, vp, vp,
                                              sz, i32, vp]
+    lib.lb_forward_many_workspace_bytes.restype = sz
+    lib.lb_forward_many_workspace_bytes.argtypes = [ctypes.POINTER(lb_linear_desc), i64]
+    lib.lb_linear_forward_many.restype = i32
+    lib.lb_linear_forward_many.argtypes = [ctypes.POINTER(lb_linear_desc), i64, vp, sz, vp]
     lib.lb_dense_reference_weight.restype = i32
     lib.lb_dense_reference_weight.argtypes = [ctypes.POINTER(lb_path), i32, i64, i64, i64, vp, vp]
     if lib.lb_abi_version() != ABI_VERSION:
@@ -224,6 +234,43 @@ def lb_linear_forward(x, paths: Sequence[LittleBitPath], r: int, y=None, workspa
     return y
 
 
+def make_descs(items):
+    """A ctypes array of lb_linear_desc for items (x, paths, r, y) (y allocated when None); returns
+    (array, list of y).  The tensors must outlive every call that uses the array."""
+    torch = _torch()
+    arr = (lb_linear_desc * max(len(items), 1))()
+    ys = []
+    for i, (x, paths, r, y) in enumerate(items):
+        T, d_in = x.shape
+        d_out = paths[0].h.shape[0]
+        parr, sc = _paths_struct(paths)
+        if y is None:
+            y = torch.empty((T, d_out), dtype=x.dtype, device=x.device)
+        arr[i] = lb_linear_desc(_dev_ptr(x, "x"), _dtype_code(x), T, d_in, d_out, r, parr, sc, _dev_ptr(y, "y"))
+        ys.append(y)
+    return arr, ys
+
+
+def lb_forward_many_workspace_bytes(descs, n: int) -> int:
+    return int(load_library().lb_forward_many_workspace_bytes(descs, n))
+
+
+def lb_linear_forward_many(items, workspace=None, stream=None):
+    """The LittleBit forward of every (x, paths, r, y) of items (independent linears) in as few launches as
+    the library can; returns the list of y."""
+    torch = _torch()
+    lib = load_library()
+    arr, ys = make_descs(items)
+    n = len(items)
+    if workspace is None:
+        need = lb_forward_many_workspace_bytes(arr, n)
+        workspace = lb_workspace_init(torch.empty(max(need, 256), dtype=torch.uint8, device=ys[0].device if ys else "cuda"))
+    st = lib.lb_linear_forward_many(arr, n, _dev_ptr(workspace, "workspace"),
+                                    workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "lb_linear_forward_many")
+    return ys
+
+
 def lb_dense_reference_weight(paths: Sequence[LittleBitPath], d_in: int, d_out: int, r: int, W=None, stream=None):
     """Dense fp32 W_hat [d_out, d_in] from the packed buffers (checking path)."""
     torch = _torch()
@@ -242,5 +289,6 @@ __all__ = [
     "LB_KERNEL_PREFILL", "LB_KERNEL_DECODE_MFMA", "LittleBitError", "LittleBitPath", "lb_path", "load_library", "lb_status_str",
     "lb_packed_bytes", "lb_bits_per_weight", "lb_rank_for_bpw", "lb_forward_workspace_bytes",
     "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "alloc_workspace", "lb_linear_forward",
-    "lb_dense_reference_weight",
+    "lb_dense_reference_weight", "lb_linear_desc", "make_descs", "lb_forward_many_workspace_bytes",
+    "lb_linear_forward_many",
 ]

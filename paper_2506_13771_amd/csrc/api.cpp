@@ -231,6 +231,120 @@ lb_status lb_linear_forward(const void* x, lb_dtype act_dtype, int64_t T, int64_
                                   workspace_bytes, LB_KERNEL_AUTO, stream);
 }
 
+namespace {
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+// the checks of lb_linear_forward_kernel before its workspace checks
+lb_status check_forward(const lb_linear_desc& d) {
+  if (!dtype_ok(d.act_dtype) || !dtype_ok(d.scale_dtype)) return LB_ERR_DTYPE;
+  const lb_status st = check_sizes(d.T, d.d_in, d.d_out, d.r);
+  if (st != LB_OK) return st;
+  if (d.T == 0 || d.d_out == 0) return LB_OK;
+  if (!d.y || (d.d_in > 0 && !d.x)) return LB_ERR_NULL;
+  if (!aligned(d.x, dtype_size(d.act_dtype)) || !aligned(d.y, dtype_size(d.act_dtype))) return LB_ERR_ALIGN;
+  return check_paths(d.paths, d.scale_dtype, d.d_in, d.d_out, d.r);
+}
+
+// a linear with work that no kernel of the automatic choice takes
+bool auto_unsupported(const lb_linear_desc& d) {
+  if (d.T == 0 || d.d_out == 0 || d.d_in == 0 || d.r == 0) return false;
+  return !(d.T <= kAutoLutTokens && lb::decode_supports(d.T, d.d_in, d.d_out, d.r)) &&
+         !lb::decode_mma_supports(d.T, d.d_in, d.d_out, d.r) && !lb::prefill_supports(d.T, d.d_in, d.d_out, d.r);
+}
+
+// linears the list launch of the look-up-table decode kernel takes
+bool lut_listable(const lb_linear_desc& d) {
+  return d.T >= 1 && d.d_out >= 1 && d.d_in >= 1 && d.r >= 1 && d.T <= kAutoLutTokens &&
+         lb::decode_supports(d.T, d.d_in, d.d_out, d.r);
+}
+
+size_t slice_bytes(const lb_linear_desc& d) {
+  return align256(lb_forward_workspace_bytes(d.T, d.d_in, d.d_out, d.r));
+}
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (na == 0 || nb == 0) return false;
+  const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+  return pa < pb + nb && pb < pa + na;
+}
+
+}  // namespace
+
+size_t lb_forward_many_workspace_bytes(const lb_linear_desc* descs, int64_t n) {
+  if (n <= 0 || !descs) return 0;
+  size_t need = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (check_sizes(descs[i].T, descs[i].d_in, descs[i].d_out, descs[i].r) != LB_OK) return 0;
+    need += slice_bytes(descs[i]);
+  }
+  return need;
+}
+
+lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
+  if (n < 0) return LB_ERR_ARG;
+  if (n == 0) return LB_OK;
+  if (!descs) return LB_ERR_NULL;
+  for (int64_t i = 0; i < n; ++i) {
+    const lb_status st = check_forward(descs[i]);
+    if (st != LB_OK) return st;
+    if (auto_unsupported(descs[i])) return LB_ERR_SHAPE;
+  }
+  // the linears run concurrently: no output may overlap another linear's
+  // input or output
+  for (int64_t i = 0; i < n; ++i) {
+    const lb_linear_desc& a = descs[i];
+    const size_t ny = static_cast<size_t>(a.T * a.d_out) * dtype_size(a.act_dtype);
+    for (int64_t j = 0; j < n; ++j) {
+      if (j == i) continue;
+      const lb_linear_desc& b = descs[j];
+      const size_t es = dtype_size(b.act_dtype);
+      if (overlap(a.y, ny, b.y, static_cast<size_t>(b.T * b.d_out) * es) ||
+          overlap(a.y, ny, b.x, static_cast<size_t>(b.T * b.d_in) * es))
+        return LB_ERR_ARG;
+    }
+  }
+  const size_t need = lb_forward_many_workspace_bytes(descs, n);
+  if (!workspace) return LB_ERR_NULL;
+  if (!aligned(workspace, 256)) return LB_ERR_ALIGN;
+  if (workspace_bytes < need) return LB_ERR_WORKSPACE;
+
+  // runs of look-up-table decode linears of one dtype pair go out as list
+  // launches of up to kDecodeMaxBatch; every other linear as its own call
+  lb::ForwardArgs batch[lb::kDecodeMaxBatch];
+  int nb = 0;
+  auto flush = [&]() -> lb_status {
+    if (nb == 0) return LB_OK;
+    const hipError_t e = nb == 1 ? lb::launch_decode(batch[0], lb::decode_geometry(batch[0].T, batch[0].d_in,
+                                                                                     batch[0].d_out, batch[0].r),
+                                                     stream)
+                                 : lb::launch_decode_batch(batch, nb, stream);
+    nb = 0;
+    return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+  };
+  char* ws = static_cast<char*>(workspace);
+  size_t off = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const lb_linear_desc& d = descs[i];
+    const size_t sb = slice_bytes(d);
+    if (lut_listable(d)) {
+      if (nb > 0 && (nb == lb::kDecodeMaxBatch || static_cast<int>(d.act_dtype) != batch[0].act_dt ||
+                     static_cast<int>(d.scale_dtype) != batch[0].sc_dt)) {
+        const lb_status st = flush();
+        if (st != LB_OK) return st;
+      }
+      batch[nb++] = make_args(d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.paths, d.scale_dtype, d.y, ws + off, sb);
+    } else {
+      const lb_status st = lb_linear_forward_kernel(d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.paths,
+                                                    d.scale_dtype, d.y, ws + off, sb, LB_KERNEL_AUTO, stream);
+      if (st != LB_OK) return st;
+    }
+    off += sb;
+  }
+  return flush();
+}
+
 lb_status lb_dense_reference_weight(const lb_path* paths, lb_dtype scale_dtype, int64_t d_in, int64_t d_out,
                                     int64_t r, float* W, hipStream_t stream) {
   if (!dtype_ok(scale_dtype)) return LB_ERR_DTYPE;

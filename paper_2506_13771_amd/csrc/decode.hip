@@ -49,6 +49,7 @@
 //    the new epoch, so consecutive calls, graph replays included, never
 //    confuse each other's slots and the workspace needs no clearing.
 #include <atomic>
+#include <type_traits>
 
 #include "device_common.h"
 
@@ -407,49 +408,98 @@ __global__ void __launch_bounds__(kThreads, 2) decode_kernel(DecodeParams P) {
     stage2<TM, ACT, SC, WPL>(P, wg - P.n_s1, smem);
 }
 
+// A list of independent linears in one launch: the stage-1 workgroups of
+// every linear first (linear 0's, then linear 1's, ...), then the stage-2
+// workgroups in the same order, so every wait still targets lower block ids.
+// Each linear keeps its own workspace slice and call protocol; one
+// instantiation serves all of them (TM, WPL: the largest of the list; VEC:
+// only when every member is aligned; stage 2 masks the words a rank does
+// not have).
+struct DecodeBatch {
+  int n;
+  int s1_end[kDecodeMaxBatch];  // one past each linear's last stage-1 workgroup
+  int s2_end[kDecodeMaxBatch];  // the same for stage 2, counted from the first stage-2 workgroup
+  DecodeParams p[kDecodeMaxBatch];
+};
+
 template <int TM, int ACT, int SC, bool VEC, int WPL>
-hipError_t launch_one(const DecodeParams& P, dim3 grid, size_t smem, hipStream_t stream) {
+__global__ void __launch_bounds__(kThreads, 2) decode_batch_kernel(DecodeBatch B) {
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  const int wg = blockIdx.x;
+  const int s1tot = B.s1_end[B.n - 1];
+  if (wg < s1tot) {
+    int i = 0;
+    while (wg >= B.s1_end[i]) ++i;
+    const DecodeParams P = B.p[i];
+    stage1<TM, ACT, SC, VEC>(P, wg - (i ? B.s1_end[i - 1] : 0), smem);
+  } else {
+    const int w2 = wg - s1tot;
+    int i = 0;
+    while (w2 >= B.s2_end[i]) ++i;
+    const DecodeParams P = B.p[i];
+    stage2<TM, ACT, SC, WPL>(P, w2 - (i ? B.s2_end[i - 1] : 0), smem);
+  }
+}
+
+// one launch of the single-linear (DecodeParams) or list (DecodeBatch) kernel
+template <int TM, int ACT, int SC, bool VEC, int WPL, typename A>
+hipError_t launch_one(const A& args, dim3 grid, size_t smem, hipStream_t stream) {
+  constexpr bool kOne = std::is_same<A, DecodeParams>::value;
   // more than the default dynamic LDS limit: raise the kernel's limit once per
   // size increase, so calls captured in a graph after an eager call of the
   // same shape make no attribute call
   static std::atomic<size_t> limit{65536};
   if (smem > limit.load()) {
-    const void* fn = reinterpret_cast<const void*>(&decode_kernel<TM, ACT, SC, VEC, WPL>);
+    const void* fn = kOne ? reinterpret_cast<const void*>(&decode_kernel<TM, ACT, SC, VEC, WPL>)
+                          : reinterpret_cast<const void*>(&decode_batch_kernel<TM, ACT, SC, VEC, WPL>);
     const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
     if (e != hipSuccess) return e;
     limit.store(smem);
   }
-  hipLaunchKernelGGL((decode_kernel<TM, ACT, SC, VEC, WPL>), grid, dim3(kThreads), smem, stream, P);
+  if constexpr (kOne)
+    hipLaunchKernelGGL((decode_kernel<TM, ACT, SC, VEC, WPL>), grid, dim3(kThreads), smem, stream, args);
+  else
+    hipLaunchKernelGGL((decode_batch_kernel<TM, ACT, SC, VEC, WPL>), grid, dim3(kThreads), smem, stream, args);
   return hipGetLastError();
 }
 
-template <int TM, int ACT, int SC, bool VEC>
-hipError_t launch_wpl(const DecodeParams& P, int wpl, dim3 grid, size_t smem, hipStream_t stream) {
+template <int TM, int ACT, int SC, bool VEC, typename A>
+hipError_t launch_wpl(const A& args, int wpl, dim3 grid, size_t smem, hipStream_t stream) {
   switch (wpl) {
-    case 1: return launch_one<TM, ACT, SC, VEC, 1>(P, grid, smem, stream);
-    case 2: return launch_one<TM, ACT, SC, VEC, 2>(P, grid, smem, stream);
-    case 4: return launch_one<TM, ACT, SC, VEC, 4>(P, grid, smem, stream);
-    default: return launch_one<TM, ACT, SC, VEC, 8>(P, grid, smem, stream);
+    case 1: return launch_one<TM, ACT, SC, VEC, 1>(args, grid, smem, stream);
+    case 2: return launch_one<TM, ACT, SC, VEC, 2>(args, grid, smem, stream);
+    case 4: return launch_one<TM, ACT, SC, VEC, 4>(args, grid, smem, stream);
+    default: return launch_one<TM, ACT, SC, VEC, 8>(args, grid, smem, stream);
   }
 }
 
-template <int ACT, int SC>
-hipError_t launch_typed(const DecodeParams& P, bool vec, int wpl, dim3 grid, size_t smem, hipStream_t stream) {
+template <int ACT, int SC, typename A>
+hipError_t launch_typed(const A& args, int T, bool vec, int wpl, dim3 grid, size_t smem, hipStream_t stream) {
   // x and g read as 4-element vectors when aligned (decided on the host); the
   // element-wise form is compiled for the widest token count only
-  if (!vec) return launch_wpl<kDecodeMaxTokens, ACT, SC, false>(P, wpl, grid, smem, stream);
-  if (P.T <= 1) return launch_wpl<1, ACT, SC, true>(P, wpl, grid, smem, stream);
-  if (P.T <= 2) return launch_wpl<2, ACT, SC, true>(P, wpl, grid, smem, stream);
-  return launch_wpl<4, ACT, SC, true>(P, wpl, grid, smem, stream);
+  if (!vec) return launch_wpl<kDecodeMaxTokens, ACT, SC, false>(args, wpl, grid, smem, stream);
+  if (T <= 1) return launch_wpl<1, ACT, SC, true>(args, wpl, grid, smem, stream);
+  if (T <= 2) return launch_wpl<2, ACT, SC, true>(args, wpl, grid, smem, stream);
+  return launch_wpl<4, ACT, SC, true>(args, wpl, grid, smem, stream);
 }
 
-template <int ACT>
-hipError_t launch_act(const DecodeParams& P, int sc_dt, bool vec, int wpl, dim3 grid, size_t smem,
+template <int ACT, typename A>
+hipError_t launch_act(const A& args, int T, int sc_dt, bool vec, int wpl, dim3 grid, size_t smem,
                       hipStream_t stream) {
   switch (sc_dt) {
-    case kDtF32: return launch_typed<ACT, kDtF32>(P, vec, wpl, grid, smem, stream);
-    case kDtF16: return launch_typed<ACT, kDtF16>(P, vec, wpl, grid, smem, stream);
-    default: return launch_typed<ACT, kDtBF16>(P, vec, wpl, grid, smem, stream);
+    case kDtF32: return launch_typed<ACT, kDtF32>(args, T, vec, wpl, grid, smem, stream);
+    case kDtF16: return launch_typed<ACT, kDtF16>(args, T, vec, wpl, grid, smem, stream);
+    default: return launch_typed<ACT, kDtBF16>(args, T, vec, wpl, grid, smem, stream);
+  }
+}
+
+template <typename A>
+hipError_t launch_any(const A& args, int act_dt, int T, int sc_dt, bool vec, int wpl, dim3 grid, size_t smem,
+                      hipStream_t stream) {
+  switch (act_dt) {
+    case kDtF32: return launch_act<kDtF32>(args, T, sc_dt, vec, wpl, grid, smem, stream);
+    case kDtF16: return launch_act<kDtF16>(args, T, sc_dt, vec, wpl, grid, smem, stream);
+    default: return launch_act<kDtBF16>(args, T, sc_dt, vec, wpl, grid, smem, stream);
   }
 }
 
@@ -512,8 +562,12 @@ bool decode_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
          packed_bytes(r, d_in) < lim && d_out * 4 < lim && d_in * 4 < lim;
 }
 
-hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t stream) {
-  DecodeParams P{};
+namespace {
+
+// kernel parameters of one linear; returns whether x and g may be read as
+// 4-element vectors
+bool decode_params(const ForwardArgs& a, const DecodeGeom& g, DecodeParams& P) {
+  P = DecodeParams{};
   P.x = a.x;
   P.y = a.y;
   for (int p = 0; p < 2; ++p) {
@@ -547,15 +601,41 @@ hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t 
   P.v_bytes = static_cast<uint32_t>(packed_bytes(a.r, a.d_in));
   P.u_bytes = static_cast<uint32_t>(packed_bytes(a.d_out, a.r));
   const uintptr_t xa = 4 * ex, ga = 4 * es;
-  const bool vec = (reinterpret_cast<uintptr_t>(a.x) % xa == 0) && (a.d_in % 4 == 0) &&
-                   (reinterpret_cast<uintptr_t>(a.g[0]) % ga == 0) && (reinterpret_cast<uintptr_t>(a.g[1]) % ga == 0);
+  return (reinterpret_cast<uintptr_t>(a.x) % xa == 0) && (a.d_in % 4 == 0) &&
+         (reinterpret_cast<uintptr_t>(a.g[0]) % ga == 0) && (reinterpret_cast<uintptr_t>(a.g[1]) % ga == 0);
+}
+
+}  // namespace
+
+hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t stream) {
+  DecodeParams P;
+  const bool vec = decode_params(a, g, P);
   const dim3 grid(g.n_s1 + g.n_s2);
   const size_t smem = vec ? g.smem_bytes : g.smem_bytes_elem;
-  switch (a.act_dt) {
-    case kDtF32: return launch_act<kDtF32>(P, a.sc_dt, vec, g.wpl, grid, smem, stream);
-    case kDtF16: return launch_act<kDtF16>(P, a.sc_dt, vec, g.wpl, grid, smem, stream);
-    default: return launch_act<kDtBF16>(P, a.sc_dt, vec, g.wpl, grid, smem, stream);
+  return launch_any(P, a.act_dt, a.T, a.sc_dt, vec, g.wpl, grid, smem, stream);
+}
+
+hipError_t launch_decode_batch(const ForwardArgs* a, int n, hipStream_t stream) {
+  if (n <= 0 || n > kDecodeMaxBatch) return hipErrorInvalidValue;
+  DecodeBatch B{};
+  B.n = n;
+  bool vec = true;
+  int T = 0, wpl = 1, s1 = 0, s2 = 0;
+  size_t smem_vec = 0, smem_elem = 0;
+  for (int i = 0; i < n; ++i) {
+    if (a[i].act_dt != a[0].act_dt || a[i].sc_dt != a[0].sc_dt) return hipErrorInvalidValue;
+    const DecodeGeom g = decode_geometry(a[i].T, a[i].d_in, a[i].d_out, a[i].r);
+    vec = decode_params(a[i], g, B.p[i]) && vec;
+    T = a[i].T > T ? a[i].T : T;
+    wpl = g.wpl > wpl ? g.wpl : wpl;
+    smem_vec = g.smem_bytes > smem_vec ? g.smem_bytes : smem_vec;
+    smem_elem = g.smem_bytes_elem > smem_elem ? g.smem_bytes_elem : smem_elem;
+    s1 += g.n_s1;
+    s2 += g.n_s2;
+    B.s1_end[i] = s1;
+    B.s2_end[i] = s2;
   }
+  return launch_any(B, a[0].act_dt, T, a[0].sc_dt, vec, wpl, dim3(s1 + s2), vec ? smem_vec : smem_elem, stream);
 }
 
 }  // namespace lb

@@ -147,6 +147,7 @@ struct DecodeGeom {
 DecodeGeom decode_geometry(int T, int d_in, int d_out, int r);
 bool decode_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
 constexpr int kDecodeMaxTokens = 4;
+constexpr int kDecodeMaxBatch = 16;  // linears per list launch of the look-up-table decode kernel
 constexpr int kDecodeMaxRank = 1024;  // stage-2 tables of one token fit in LDS
 
 // Matrix-core decode kernel geometry.
@@ -189,6 +190,9 @@ bool prefill_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
 hipError_t launch_pack(const void* src, int dt, int rows, int r, int role, void* dst, int32_t* nan_count,
                        hipStream_t stream);
 hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t stream);
+// n (1 .. kDecodeMaxBatch) independent linears of one activation and scale
+// dtype, each with its own workspace slice in a[i].ws, in one launch
+hipError_t launch_decode_batch(const ForwardArgs* a, int n, hipStream_t stream);
 hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g, hipStream_t stream);
 hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t stream);
 hipError_t launch_dense_ref(const ForwardArgs& a, float* W, hipStream_t stream);

@@ -182,3 +182,62 @@ def test_binding_refuses_cpu_tensors(lib):
     x = torch.zeros(2, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         lb.lb_pack_signs(x, lb.LB_ROLE_U)
+
+
+# ---------------------------------------------------------------------------
+# list forward (lb_linear_forward_many): validation and workspace sizing
+# ---------------------------------------------------------------------------
+def _desc(x=FAKE, act=lb.LB_BF16, T=1, d_in=64, d_out=64, r=16, paths=None, sc=lb.LB_F16, y=FAKE):
+    d = lb.lb_linear_desc()
+    d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.scale_dtype, d.y = x, act, T, d_in, d_out, r, sc, y
+    p = paths if paths is not None else _paths()
+    d.paths[0], d.paths[1] = p[0], p[1]
+    return d
+
+
+def _descs(*ds):
+    arr = (lb.lb_linear_desc * len(ds))()
+    for i, d in enumerate(ds):
+        arr[i] = d
+    return arr
+
+
+def test_many_workspace_bytes_is_the_sum_of_rounded_slices(lib):
+    shapes = [(1, 4096, 4096, 80), (2, 512, 1000, 17), (16, 64, 64, 16), (0, 5, 5, 5), (300, 100, 77, 48)]
+    arr = _descs(*[_desc(T=T, d_in=a, d_out=b, r=r) for T, a, b, r in shapes])
+    want = sum((lb.lb_forward_workspace_bytes(*s) + 255) // 256 * 256 for s in shapes)
+    assert lb.lb_forward_many_workspace_bytes(arr, len(shapes)) == want
+    assert lb.lb_forward_many_workspace_bytes(arr, 0) == 0
+    assert lb.lb_forward_many_workspace_bytes(None, 3) == 0
+    assert lb.lb_forward_many_workspace_bytes(_descs(_desc(T=-1)), 1) == 0
+
+
+def test_many_validation_errors(lib):
+    y2 = FAKE + (1 << 20)
+    ok2 = [_desc(), _desc(y=y2, x=FAKE + (2 << 20))]
+    need = lb.lb_forward_many_workspace_bytes(_descs(*ok2), 2)
+
+    def call(ds, ws=FAKE * 64, ws_bytes=None, n=None):
+        arr = _descs(*ds)
+        return lib.lb_linear_forward_many(arr, len(ds) if n is None else n, ws,
+                                          need - 1 if ws_bytes is None else ws_bytes, None)
+
+    # the baseline list fails only on the (deliberately) too-small workspace
+    assert call(ok2) == lb.LB_ERR_WORKSPACE
+    assert call(ok2, n=-1) == lb.LB_ERR_ARG
+    assert lib.lb_linear_forward_many(None, 0, 0, 0, None) == lb.LB_OK
+    assert lib.lb_linear_forward_many(None, 2, FAKE, 1 << 30, None) == lb.LB_ERR_NULL
+    # every descriptor is validated before anything is enqueued
+    assert call([ok2[0], _desc(act=9, y=y2)]) == lb.LB_ERR_DTYPE
+    assert call([ok2[0], _desc(T=-1, y=y2)]) == lb.LB_ERR_SHAPE
+    assert call([ok2[0], _desc(x=0, y=y2)]) == lb.LB_ERR_NULL
+    assert call([ok2[0], _desc(y=y2 + 2, act=lb.LB_F32)]) == lb.LB_ERR_ALIGN
+    assert call([ok2[0], _desc(y=y2, paths=_paths(h=0))]) == lb.LB_ERR_NULL
+    # outputs overlapping another linear's output or input
+    assert call([_desc(), _desc(y=FAKE + 64)]) == lb.LB_ERR_ARG
+    assert call([_desc(y=y2), _desc(x=y2 + 32, y=FAKE + (3 << 20))]) == lb.LB_ERR_ARG
+    # workspace
+    assert call(ok2, ws=0, ws_bytes=1 << 30) == lb.LB_ERR_NULL
+    assert call(ok2, ws=FAKE * 64 + 128, ws_bytes=1 << 30) == lb.LB_ERR_ALIGN
+    # empty linears need no work and no GPU
+    assert call([_desc(T=0), _desc(d_out=0, y=y2)], ws_bytes=1 << 20) == lb.LB_OK

@@ -1,0 +1,133 @@
+"""GPU parity of the list forward (lb_linear_forward_many): every linear of a
+list must give exactly what lb_linear_forward gives for it alone (same kernel,
+same arithmetic), and that result must meet the oracle bar.  Lists mix shapes,
+token counts (look-up-table decode linears batched into list launches, the
+rest as single calls), dtypes (which split the list launches), empty linears,
+more linears than one list launch takes, repeated calls on one workspace and
+graph replays."""
+import numpy as np
+import pytest
+
+from paper_2506_13771_amd import synth
+import lbtest_utils as U
+from conftest import gpu_available
+
+pytestmark = pytest.mark.gpu
+
+if gpu_available():
+    import torch
+    import paper_2506_13771_amd as lb
+
+from test_parity_gpu import _check
+
+
+def _linears(specs, cfg):
+    out = []
+    for i, (T, d_in, d_out, r, act, sc) in enumerate(specs):
+        li = synth.make_linear(d_in, d_out, r, T, act_dtype=act, scale_dtype=sc, cfg=cfg, linear=i)
+        x, paths, _ = U.to_device(li)
+        out.append((li, x, paths))
+    return out
+
+
+def _many(lins, ws=None, ys=None):
+    items = [(x, paths, li.r, None if ys is None else ys[i]) for i, (li, x, paths) in enumerate(lins)]
+    if ws is None:
+        arr, _ = lb.make_descs(items)
+        need = lb.lb_forward_many_workspace_bytes(arr, len(items))
+        ws = lb.lb_workspace_init(torch.empty(max(need, 256), dtype=torch.uint8, device="cuda"))
+    out = lb.lb_linear_forward_many(items, workspace=ws)
+    torch.cuda.synchronize()
+    return out, ws
+
+
+def _singles(lins):
+    out = []
+    for li, x, paths in lins:
+        out.append(lb.lb_linear_forward(x, paths, li.r))
+    torch.cuda.synchronize()
+    return out
+
+
+def _same_bits(a, b):
+    if a.numel() == 0:
+        return b.numel() == 0
+    return torch.equal(a.view(torch.int16 if a.element_size() == 2 else torch.int32),
+                       b.view(torch.int16 if b.element_size() == 2 else torch.int32))
+
+
+MIXED = [
+    (1, 4096, 4096, 80, "bf16", "f16"),
+    (1, 512, 512, 32, "bf16", "f16"),
+    (2, 1000, 300, 48, "bf16", "f16"),
+    (1, 700, 900, 17, "bf16", "f16"),
+    (2, 4096, 11008, 128, "bf16", "f16"),
+    (1, 333, 65, 16, "f32", "f32"),     # another dtype pair: a list launch of its own
+    (2, 96, 64, 31, "f32", "f32"),
+    (1, 64, 64, 16, "bf16", "f16"),
+    (3, 512, 512, 32, "bf16", "f16"),   # T = 3: a single call (matrix-core decode)
+    (100, 256, 384, 48, "bf16", "f16"),  # a single call (prefill)
+    (0, 64, 64, 16, "bf16", "f16"),     # empty
+    (1, 96, 0, 16, "bf16", "f16"),      # empty
+]
+
+
+def test_many_matches_single_calls_and_the_oracle():
+    lins = _linears(MIXED, cfg=21)
+    ys, _ = _many(lins)
+    ref = _singles(lins)
+    for i, ((li, _, _), y, r) in enumerate(zip(lins, ys, ref)):
+        assert _same_bits(y, r), (i, MIXED[i])
+        if li.T > 0 and li.d_out > 0:
+            tokens = None if li.T <= 16 else np.arange(0, li.T, 7)
+            _check(li, U.torch_to_raw(y, li.act_dtype), tokens=tokens, label=f"many {i}")
+
+
+def test_many_more_than_one_list_launch():
+    specs = [(1 + (i % 2), 128 + 32 * (i % 5), 64 + 16 * (i % 7), 16 * (1 + i % 4), "bf16", "f16")
+             for i in range(37)]
+    lins = _linears(specs, cfg=22)
+    ys, _ = _many(lins)
+    ref = _singles(lins)
+    for i, (y, r) in enumerate(zip(ys, ref)):
+        assert _same_bits(y, r), (i, specs[i])
+    for i in (0, 16, 17, 36):
+        _check(lins[i][0], U.torch_to_raw(ys[i], "bf16"), label=f"long list {i}")
+
+
+def test_many_repeated_calls_on_one_workspace():
+    specs = [(1, 4096, 4096, 80, "bf16", "f16"), (2, 1024, 2048, 48, "bf16", "f16"),
+             (1, 2048, 512, 64, "bf16", "f16")]
+    lins = _linears(specs, cfg=23)
+    ws = None
+    g = torch.Generator(device="cuda").manual_seed(23)
+    for rep in range(4):
+        if rep:
+            for _, x, _ in lins:
+                x.copy_(torch.randn(x.shape, generator=g, device="cuda").to(x.dtype))
+        ys, ws = _many(lins, ws=ws)
+        ref = _singles(lins)
+        for i, (y, r) in enumerate(zip(ys, ref)):
+            assert _same_bits(y, r), (rep, i)
+
+
+def test_many_graph_replays_match_eager():
+    specs = [(1, 2048, 1536, 64, "bf16", "f16"), (1, 1024, 4096, 80, "bf16", "f16"),
+             (2, 512, 512, 32, "bf16", "f16"), (16, 512, 768, 48, "bf16", "f16")]
+    lins = _linears(specs, cfg=24)
+    y_eager, ws = _many(lins)
+    y_eager = [y.clone() for y in y_eager]
+    y_graph = [torch.empty_like(y) for y in y_eager]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        lb.lb_linear_forward_many([(x, paths, li.r, y_graph[i]) for i, (li, x, paths) in enumerate(lins)],
+                                  workspace=ws)
+    for rep in range(4):
+        for y in y_graph:
+            y.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        y_mid, _ = _many(lins, ws=ws)  # eager work on the same workspace between replays
+        for i in range(len(lins)):
+            assert _same_bits(y_graph[i], y_eager[i]), (rep, i)
+            assert _same_bits(y_mid[i], y_eager[i]), (rep, i)
