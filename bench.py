@@ -132,6 +132,30 @@ class Layer:
         return 4 if self.li.scale_dtype == "f32" else 2
 
 
+class LayerList:
+    """Resident layers run by one lb_linear_forward_many call (pre-marshalled descriptors and
+    one workspace with a slice per layer); times like a Layer."""
+
+    def __init__(self, layers):
+        import torch
+        import paper_2506_13771_amd as lb
+        self.layers = layers
+        self.arr, _ = lb.make_descs([(L.x, L.paths, L.r, L.y) for L in layers])
+        need = lb.lb_forward_many_workspace_bytes(self.arr, len(layers))
+        self.ws = lb.lb_workspace_init(torch.empty(max(need, 256), dtype=torch.uint8, device=layers[0].x.device))
+        self.lib = lb.load_library()
+        self.argv = (self.arr, len(layers), ctypes.c_void_p(self.ws.data_ptr()), self.ws.numel(),
+                     ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+
+    def set_stream(self, handle):
+        self.argv = self.argv[:-1] + (ctypes.c_void_p(handle),)
+
+    def call(self):
+        st = self.lib.lb_linear_forward_many(*self.argv)
+        if st != 0:
+            raise RuntimeError(f"lb_linear_forward_many failed with status {st}")
+
+
 def time_calls(layers, steps, warmup, use_graph=True, per_graph=None):
     """Run every layer's forward `steps` times (after `warmup`) on the current stream, timed
     with HIP events recorded on that stream.  With use_graph the launches of `per_graph`
@@ -377,11 +401,15 @@ def run_sweep(path, steps, warmup, only=("7b", "13b", "70b")):
                 b, bw = alg_bytes(T, d_in, d_out, r)
                 tot_b += b
                 tot_w += bw
-        ms, n = time_calls(layers, max(3, steps // 100), 2, use_graph=True, per_graph=1)
-        emit({"config": "llama2-70b-sweep", "T": T, "linears": len(layers), "ms_per_sweep": ms,
-              "tokens_per_s": T / (ms * 1e-3), "alg_bytes": tot_b, "weights_bytes": tot_w,
+        # one lb_linear_forward_many call for the whole sweep (list launches of up to 16
+        # look-up-table decode linears where T <= 2), and one call per linear beside it
+        ms, n = time_calls([LayerList(layers)], max(3, steps // 100), 2, use_graph=True, per_graph=1)
+        ms1, _ = time_calls(layers, max(3, steps // 100), 2, use_graph=True, per_graph=1)
+        emit({"config": "llama2-70b-sweep", "T": T, "linears": len(layers), "launch": "lb_linear_forward_many",
+              "ms_per_sweep": ms, "tokens_per_s": T / (ms * 1e-3), "alg_bytes": tot_b, "weights_bytes": tot_w,
               "GBps": tot_b / (ms * 1e-3) / 1e9, "hbm_frac": tot_b / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
-              "us_per_linear": ms * 1e3 / len(layers)})
+              "us_per_linear": ms * 1e3 / len(layers), "ms_per_sweep_single_calls": ms1,
+              "us_per_linear_single_calls": ms1 * 1e3 / len(layers)})
         del layers
         torch.cuda.empty_cache()
     out.close()
