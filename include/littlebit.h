@@ -195,10 +195,11 @@ size_t lb_forward_many_workspace_bytes(const lb_linear_desc* descs, int64_t n);
    computes it, Proposition 1 summed over both paths; the paper's end-to-end
    decoding measurement replaces every nn.Linear of the model by this
    forward, appendix "End-to-End Decoding Throughput"), enqueued on one
-   stream with fewer launches: consecutive linears with T <= 2 and the same
-   activation and scale dtypes run as one launch of the look-up-table decode
-   kernel per up to 16 linears; every other linear is its own call with the
-   automatic kernel choice.  Results are those of lb_linear_forward for each
+   stream with fewer launches: consecutive linears for which the automatic
+   choice is the same decode kernel (look-up-table or matrix-core) and that
+   share the activation and scale dtypes run as one launch of that kernel per
+   up to 16 linears; every other linear (prefill sizes) is its own call with
+   the automatic kernel choice.  Results are those of lb_linear_forward for each
    linear.  descs: host array of n descriptors (device pointers inside, as
    for lb_linear_forward).  No y may overlap another linear's x or y (they run
    concurrently): LB_ERR_ARG.  Every descriptor is validated as

@@ -79,6 +79,16 @@ bool prefer_prefill(int64_t T, int64_t d_out, int64_t r) {
   return T >= 32 || (T >= 16 && rd >= 3000000) || rd >= 8000000;
 }
 
+// The kernel AUTO runs for a linear with work (T, d_in, d_out, r >= 1), or
+// LB_KERNEL_AUTO itself when no kernel takes the sizes.
+lb_kernel auto_kernel(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
+  if (T <= kAutoLutTokens && lb::decode_supports(T, d_in, d_out, r)) return LB_KERNEL_DECODE;
+  const bool pf = lb::prefill_supports(T, d_in, d_out, r);
+  if (lb::decode_mma_supports(T, d_in, d_out, r) && !(prefer_prefill(T, d_out, r) && pf))
+    return LB_KERNEL_DECODE_MFMA;
+  return pf ? LB_KERNEL_PREFILL : LB_KERNEL_AUTO;
+}
+
 }  // namespace
 
 extern "C" {
@@ -204,16 +214,9 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
   }
   if (kernel == LB_KERNEL_AUTO) {
     // the look-up-table kernel is the fastest for one or two tokens; from
-    // three on the matrix-core decode kernel takes over
-    if (T <= kAutoLutTokens && lb::decode_supports(T, d_in, d_out, r))
-      kernel = LB_KERNEL_DECODE;
-    else if (lb::decode_mma_supports(T, d_in, d_out, r) &&
-             !(prefer_prefill(T, d_out, r) && lb::prefill_supports(T, d_in, d_out, r)))
-      kernel = LB_KERNEL_DECODE_MFMA;
-    else if (lb::prefill_supports(T, d_in, d_out, r))
-      kernel = LB_KERNEL_PREFILL;
-    else
-      return LB_ERR_SHAPE;
+    // three on the matrix-core decode kernel, then the prefill kernels
+    kernel = auto_kernel(T, d_in, d_out, r);
+    if (kernel == LB_KERNEL_AUTO) return LB_ERR_SHAPE;
   }
   if (kernel == LB_KERNEL_DECODE)
     e = lb::launch_decode(a, lb::decode_geometry(a.T, a.d_in, a.d_out, a.r), stream);
@@ -246,17 +249,19 @@ lb_status check_forward(const lb_linear_desc& d) {
   return check_paths(d.paths, d.scale_dtype, d.d_in, d.d_out, d.r);
 }
 
+bool has_work(const lb_linear_desc& d) { return d.T > 0 && d.d_out > 0 && d.d_in > 0 && d.r > 0; }
+
 // a linear with work that no kernel of the automatic choice takes
 bool auto_unsupported(const lb_linear_desc& d) {
-  if (d.T == 0 || d.d_out == 0 || d.d_in == 0 || d.r == 0) return false;
-  return !(d.T <= kAutoLutTokens && lb::decode_supports(d.T, d.d_in, d.d_out, d.r)) &&
-         !lb::decode_mma_supports(d.T, d.d_in, d.d_out, d.r) && !lb::prefill_supports(d.T, d.d_in, d.d_out, d.r);
+  return has_work(d) && auto_kernel(d.T, d.d_in, d.d_out, d.r) == LB_KERNEL_AUTO;
 }
 
-// linears the list launch of the look-up-table decode kernel takes
-bool lut_listable(const lb_linear_desc& d) {
-  return d.T >= 1 && d.d_out >= 1 && d.d_in >= 1 && d.r >= 1 && d.T <= kAutoLutTokens &&
-         lb::decode_supports(d.T, d.d_in, d.d_out, d.r);
+// the list launch a linear joins: the look-up-table or the matrix-core decode
+// kernel (what AUTO runs for it), or none (a call of its own)
+lb_kernel list_kernel(const lb_linear_desc& d) {
+  if (!has_work(d)) return LB_KERNEL_AUTO;
+  const lb_kernel k = auto_kernel(d.T, d.d_in, d.d_out, d.r);
+  return k == LB_KERNEL_DECODE || k == LB_KERNEL_DECODE_MFMA ? k : LB_KERNEL_AUTO;
 }
 
 size_t slice_bytes(const lb_linear_desc& d) {
@@ -310,16 +315,23 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
   if (!aligned(workspace, 256)) return LB_ERR_ALIGN;
   if (workspace_bytes < need) return LB_ERR_WORKSPACE;
 
-  // runs of look-up-table decode linears of one dtype pair go out as list
-  // launches of up to kDecodeMaxBatch; every other linear as its own call
+  // runs of linears that one decode kernel takes, of one dtype pair, go out
+  // as list launches of up to kDecodeMaxBatch; every other linear as its own
+  // call
   lb::ForwardArgs batch[lb::kDecodeMaxBatch];
   int nb = 0;
+  lb_kernel bk = LB_KERNEL_AUTO;
   auto flush = [&]() -> lb_status {
     if (nb == 0) return LB_OK;
-    const hipError_t e = nb == 1 ? lb::launch_decode(batch[0], lb::decode_geometry(batch[0].T, batch[0].d_in,
-                                                                                     batch[0].d_out, batch[0].r),
-                                                     stream)
-                                 : lb::launch_decode_batch(batch, nb, stream);
+    const lb::ForwardArgs& a0 = batch[0];
+    hipError_t e;
+    if (bk == LB_KERNEL_DECODE)
+      e = nb == 1 ? lb::launch_decode(a0, lb::decode_geometry(a0.T, a0.d_in, a0.d_out, a0.r), stream)
+                  : lb::launch_decode_batch(batch, nb, stream);
+    else
+      e = nb == 1 ? lb::launch_decode_mma(a0, lb::decode_mma_geometry(a0.T, a0.d_in, a0.d_out, a0.r, a0.act_dt),
+                                          stream)
+                  : lb::launch_decode_mma_batch(batch, nb, stream);
     nb = 0;
     return e == hipSuccess ? LB_OK : LB_ERR_HIP;
   };
@@ -328,12 +340,14 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
   for (int64_t i = 0; i < n; ++i) {
     const lb_linear_desc& d = descs[i];
     const size_t sb = slice_bytes(d);
-    if (lut_listable(d)) {
-      if (nb > 0 && (nb == lb::kDecodeMaxBatch || static_cast<int>(d.act_dtype) != batch[0].act_dt ||
+    const lb_kernel k = list_kernel(d);
+    if (k != LB_KERNEL_AUTO) {
+      if (nb > 0 && (nb == lb::kDecodeMaxBatch || k != bk || static_cast<int>(d.act_dtype) != batch[0].act_dt ||
                      static_cast<int>(d.scale_dtype) != batch[0].sc_dt)) {
         const lb_status st = flush();
         if (st != LB_OK) return st;
       }
+      bk = k;
       batch[nb++] = make_args(d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.paths, d.scale_dtype, d.y, ws + off, sb);
     } else {
       const lb_status st = lb_linear_forward_kernel(d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.paths,

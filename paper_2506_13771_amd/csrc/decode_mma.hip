@@ -41,6 +41,7 @@
 // target lower block ids and are bounded; the epoch / done-counter protocol
 // is the same.
 #include <atomic>
+#include <type_traits>
 
 #include "device_common.h"
 
@@ -465,46 +466,93 @@ __global__ void __launch_bounds__(kThreads, 1) decode_mma_kernel(MmaParams P) {
     mma_stage2<ACT, SC>(P, wg - P.n_s1, smem);
 }
 
+// A list of independent linears in one launch (the stage-1 workgroups of
+// every linear, then the stage-2 workgroups, in list order, so every wait
+// still targets lower block ids); its members share the token tiles TT and
+// the load form VEC.
+struct MmaBatch {
+  int n;
+  int s1_end[kDecodeMaxBatch];  // one past each linear's last stage-1 workgroup
+  int s2_end[kDecodeMaxBatch];  // the same for stage 2, counted from the first stage-2 workgroup
+  MmaParams p[kDecodeMaxBatch];
+};
+
 template <int TT, int ACT, int SC, bool VEC>
-hipError_t launch_one(const MmaParams& P, dim3 grid, size_t smem, hipStream_t stream) {
+__global__ void __launch_bounds__(kThreads, 1) decode_mma_batch_kernel(MmaBatch B) {
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  const int wg = blockIdx.x;
+  const int s1tot = B.s1_end[B.n - 1];
+  if (wg < s1tot) {
+    int i = 0;
+    while (wg >= B.s1_end[i]) ++i;
+    const MmaParams P = B.p[i];
+    mma_stage1<TT, ACT, SC, VEC>(P, wg - (i ? B.s1_end[i - 1] : 0), smem);
+  } else {
+    const int w2 = wg - s1tot;
+    int i = 0;
+    while (w2 >= B.s2_end[i]) ++i;
+    const MmaParams P = B.p[i];
+    mma_stage2<ACT, SC>(P, w2 - (i ? B.s2_end[i - 1] : 0), smem);
+  }
+}
+
+// one launch of the single-linear (MmaParams) or list (MmaBatch) kernel
+template <int TT, int ACT, int SC, bool VEC, typename A>
+hipError_t launch_one(const A& args, dim3 grid, size_t smem, hipStream_t stream) {
+  constexpr bool kOne = std::is_same<A, MmaParams>::value;
   // more than the default dynamic LDS limit (the CU has 160 KB): raise the
   // kernel's limit once per size increase, so calls captured in a graph after
   // an eager call of the same shape make no attribute call
   static std::atomic<size_t> limit{65536};
   if (smem > limit.load()) {
-    const void* fn = reinterpret_cast<const void*>(&decode_mma_kernel<TT, ACT, SC, VEC>);
+    const void* fn = kOne ? reinterpret_cast<const void*>(&decode_mma_kernel<TT, ACT, SC, VEC>)
+                          : reinterpret_cast<const void*>(&decode_mma_batch_kernel<TT, ACT, SC, VEC>);
     const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
     if (e != hipSuccess) return e;
     limit.store(smem);
   }
-  hipLaunchKernelGGL((decode_mma_kernel<TT, ACT, SC, VEC>), grid, dim3(kThreads), smem, stream, P);
+  if constexpr (kOne)
+    hipLaunchKernelGGL((decode_mma_kernel<TT, ACT, SC, VEC>), grid, dim3(kThreads), smem, stream, args);
+  else
+    hipLaunchKernelGGL((decode_mma_batch_kernel<TT, ACT, SC, VEC>), grid, dim3(kThreads), smem, stream, args);
   return hipGetLastError();
 }
 
-template <int ACT, int SC, bool VEC>
-hipError_t launch_tt(const MmaParams& P, dim3 grid, size_t smem, hipStream_t stream) {
-  switch ((P.T + 15) / 16) {
-    case 1: return launch_one<1, ACT, SC, VEC>(P, grid, smem, stream);
-    case 2: return launch_one<2, ACT, SC, VEC>(P, grid, smem, stream);
-    case 3: return launch_one<3, ACT, SC, VEC>(P, grid, smem, stream);
-    case 4: return launch_one<4, ACT, SC, VEC>(P, grid, smem, stream);
+template <int ACT, int SC, bool VEC, typename A>
+hipError_t launch_tt(const A& args, int T, dim3 grid, size_t smem, hipStream_t stream) {
+  switch ((T + 15) / 16) {
+    case 1: return launch_one<1, ACT, SC, VEC>(args, grid, smem, stream);
+    case 2: return launch_one<2, ACT, SC, VEC>(args, grid, smem, stream);
+    case 3: return launch_one<3, ACT, SC, VEC>(args, grid, smem, stream);
+    case 4: return launch_one<4, ACT, SC, VEC>(args, grid, smem, stream);
     default: return hipErrorInvalidValue;  // T <= kMmaMaxTokens is checked by the caller
   }
 }
 
-template <int ACT, int SC>
-hipError_t launch_vec(const MmaParams& P, dim3 grid, size_t smem, hipStream_t stream) {
+template <int ACT, int SC, typename A>
+hipError_t launch_vec(const A& args, int T, bool vec, dim3 grid, size_t smem, hipStream_t stream) {
   // element-wise x and g loads (unaligned or d_in % 4 != 0) are compiled for
   // the widest token count only; it serves every T (absent columns dropped)
-  return P.vec ? launch_tt<ACT, SC, true>(P, grid, smem, stream) : launch_one<4, ACT, SC, false>(P, grid, smem, stream);
+  return vec ? launch_tt<ACT, SC, true>(args, T, grid, smem, stream)
+             : launch_one<4, ACT, SC, false>(args, grid, smem, stream);
 }
 
-template <int ACT>
-hipError_t launch_sc(const MmaParams& P, int sc_dt, dim3 grid, size_t smem, hipStream_t stream) {
+template <int ACT, typename A>
+hipError_t launch_sc(const A& args, int T, bool vec, int sc_dt, dim3 grid, size_t smem, hipStream_t stream) {
   switch (sc_dt) {
-    case kDtF32: return launch_vec<ACT, kDtF32>(P, grid, smem, stream);
-    case kDtF16: return launch_vec<ACT, kDtF16>(P, grid, smem, stream);
-    default: return launch_vec<ACT, kDtBF16>(P, grid, smem, stream);
+    case kDtF32: return launch_vec<ACT, kDtF32>(args, T, vec, grid, smem, stream);
+    case kDtF16: return launch_vec<ACT, kDtF16>(args, T, vec, grid, smem, stream);
+    default: return launch_vec<ACT, kDtBF16>(args, T, vec, grid, smem, stream);
+  }
+}
+
+template <typename A>
+hipError_t launch_any(const A& args, int act_dt, int T, bool vec, int sc_dt, dim3 grid, size_t smem,
+                      hipStream_t stream) {
+  switch (act_dt) {
+    case kDtF32: return launch_sc<kDtF32>(args, T, vec, sc_dt, grid, smem, stream);
+    case kDtF16: return launch_sc<kDtF16>(args, T, vec, sc_dt, grid, smem, stream);
+    default: return launch_sc<kDtBF16>(args, T, vec, sc_dt, grid, smem, stream);
   }
 }
 
@@ -558,8 +606,11 @@ bool decode_mma_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
          packed_bytes(d_out, r) < lim && packed_bytes(r, d_in) < lim && d_out * 4 < lim;
 }
 
-hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t stream) {
-  MmaParams P{};
+namespace {
+
+// kernel parameters of one linear
+void mma_params(const ForwardArgs& a, const MmaGeom& g, MmaParams& P) {
+  P = MmaParams{};
   P.x = a.x;
   P.y = a.y;
   for (int p = 0; p < 2; ++p) {
@@ -594,12 +645,54 @@ hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t
   P.v_bytes = static_cast<uint32_t>(packed_bytes(a.r, a.d_in));
   P.u_bytes = static_cast<uint32_t>(packed_bytes(a.d_out, a.r));
   P.magic_r = a.r > 1 ? static_cast<uint32_t>(((uint64_t(1) << 32) + a.r - 1) / a.r) : 0u;
-  const dim3 grid(g.n_s1 + g.n_s2);
-  switch (a.act_dt) {
-    case kDtF32: return launch_sc<kDtF32>(P, a.sc_dt, grid, g.smem_bytes, stream);
-    case kDtF16: return launch_sc<kDtF16>(P, a.sc_dt, grid, g.smem_bytes, stream);
-    default: return launch_sc<kDtBF16>(P, a.sc_dt, grid, g.smem_bytes, stream);
+}
+
+}  // namespace
+
+hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t stream) {
+  MmaParams P;
+  mma_params(a, g, P);
+  return launch_any(P, a.act_dt, a.T, P.vec != 0, a.sc_dt, dim3(g.n_s1 + g.n_s2), g.smem_bytes, stream);
+}
+
+hipError_t launch_decode_mma_batch(const ForwardArgs* a, int n, hipStream_t stream) {
+  if (n <= 0 || n > kDecodeMaxBatch) return hipErrorInvalidValue;
+  // a stage-1 wave's blocks per round depend on the token tiles and on the
+  // load form, so members are launched in sub-lists of equal (tiles, form):
+  // each linear then runs exactly the arithmetic of its own call
+  MmaParams P[kDecodeMaxBatch];
+  MmaGeom G[kDecodeMaxBatch];
+  bool done[kDecodeMaxBatch] = {};
+  for (int i = 0; i < n; ++i) {
+    if (a[i].act_dt != a[0].act_dt || a[i].sc_dt != a[0].sc_dt) return hipErrorInvalidValue;
+    G[i] = decode_mma_geometry(a[i].T, a[i].d_in, a[i].d_out, a[i].r, a[i].act_dt);
+    mma_params(a[i], G[i], P[i]);
   }
+  for (int i = 0; i < n; ++i) {
+    if (done[i]) continue;
+    const int tt = (a[i].T + 15) / 16;
+    const bool vec = P[i].vec != 0;
+    MmaBatch B{};
+    int s1 = 0, s2 = 0, T = 0;
+    size_t smem = 0;
+    for (int j = i; j < n; ++j) {
+      if (done[j] || (a[j].T + 15) / 16 != tt || (P[j].vec != 0) != vec) continue;
+      done[j] = true;
+      B.p[B.n] = P[j];
+      s1 += G[j].n_s1;
+      s2 += G[j].n_s2;
+      B.s1_end[B.n] = s1;
+      B.s2_end[B.n] = s2;
+      T = a[j].T > T ? a[j].T : T;
+      smem = G[j].smem_bytes > smem ? G[j].smem_bytes : smem;
+      ++B.n;
+    }
+    const hipError_t e = B.n == 1 ? launch_any(P[i], a[i].act_dt, a[i].T, vec, a[i].sc_dt,
+                                               dim3(G[i].n_s1 + G[i].n_s2), G[i].smem_bytes, stream)
+                                  : launch_any(B, a[0].act_dt, T, vec, a[0].sc_dt, dim3(s1 + s2), smem, stream);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace lb

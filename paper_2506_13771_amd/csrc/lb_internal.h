@@ -195,6 +195,10 @@ hipError_t launch_decode(const ForwardArgs& a, const DecodeGeom& g, hipStream_t 
 hipError_t launch_decode_batch(const ForwardArgs* a, int n, hipStream_t stream);
 hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g, hipStream_t stream);
 hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t stream);
+// n (1 .. kDecodeMaxBatch) independent linears of one activation and scale
+// dtype (T <= 64 each), each with its own workspace slice, in one launch per
+// group of equal token tiles and load form
+hipError_t launch_decode_mma_batch(const ForwardArgs* a, int n, hipStream_t stream);
 hipError_t launch_dense_ref(const ForwardArgs& a, float* W, hipStream_t stream);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 hipError_t launch_zero_elems(void* p, int64_t n, int dt, hipStream_t stream);

@@ -18,12 +18,13 @@
 // `ks` workgroups, about 256 in all) and a tile of latents.  Waves 0-1 take
 // path 0 and waves 2-3 path 1, each MS interleaved 16-latent subtiles of its
 // path, so a wave holds MS x 4 accumulator tiles and no sum crosses paths;
-// waves 4-7 repeat these roles on the odd 32-input steps, and the two halves
-// are added once in LDS at the end, in a fixed order.  The steps stream
-// through an LDS ring filled by global-to-LDS loads (x of the 64 tokens,
-// written in B-fragment order, and each wave's V words), several rounds in
-// flight; one barrier per round hands slots from their loads to their
-// readers and back.  The g terms of the range are cut once into LDS.
+// waves 4-7 repeat these roles on the odd 32-input steps (kSplit1 groups of 4
+// waves take turns), and the groups are added once in LDS at the end, in a
+// fixed order.  The steps stream through an LDS ring filled by global-to-LDS
+// loads (x of the 64 tokens, written in B-fragment order, and each wave's V
+// words), several rounds in flight; one barrier per round hands slots from
+// their loads to their readers and back.  The g terms of the range are cut
+// once into LDS.
 // P1b.  Sums the ks partials in ascending order, scales by l and stores w as
 // NW bf16 terms laid out as B fragments of P2.
 // P2.  A workgroup of 8 waves owns 64 tokens and a group of 128-output
@@ -54,7 +55,8 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 // P1
-constexpr int kThreads1 = 512;  // 8 waves: two halves of 4 take alternate 32-input steps
+constexpr int kSplit1 = 2;      // groups of 4 waves taking turns over the 32-input steps
+constexpr int kThreads1 = 256 * kSplit1;
 constexpr int kTok1 = 64;       // tokens per workgroup (4 subtiles of 16)
 constexpr int kTn1 = 4;
 constexpr int kMaxMs = 6;       // 16-latent subtiles per wave
@@ -119,8 +121,9 @@ __host__ __device__ constexpr size_t p1_xslot(int nx) { return static_cast<size_
 __host__ __device__ constexpr size_t p1_vslot(int ms, bool vw) {
   return static_cast<size_t>(kWaves) * (vw ? 1024 : p1_nv(ms, false) * 256);
 }
-// 32-input steps staged in LDS (fp32 x takes twice the room per step)
-__host__ __device__ constexpr int p1_ring(int act) { return act == kDtF32 ? 8 : 12; }
+// 32-input steps staged in LDS, a whole number of rounds (fp32 x takes twice
+// the room per step)
+__host__ __device__ constexpr int p1_ring(int act) { return kSplit1 * (act == kDtF32 ? 4 : 6); }
 __host__ __device__ constexpr size_t p1_lds(int kb_per, int G, int act, int ms, bool vw) {
   const size_t ring = p1_gt_bytes(kb_per, G) + p1_ring(act) * (p1_xslot(p1_nx(act)) + p1_vslot(ms, vw));
   const size_t red = static_cast<size_t>(kWaves) * ms * kTn1 * 64 * 16;
@@ -130,13 +133,13 @@ __host__ __device__ constexpr size_t p1_lds(int kb_per, int G, int act, int ms, 
 template <int MS, int ACT, int SC, bool VW>
 __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
   constexpr int G = nterms<SC>(), E = nterms<ACT>();
-  constexpr int NX = p1_nx(ACT), NV = p1_nv(MS, VW), RING = p1_ring(ACT), R2 = RING / 2;
+  constexpr int NX = p1_nx(ACT), NV = p1_nv(MS, VW), RING = p1_ring(ACT), RR = RING / kSplit1;
   constexpr int XSLOT = static_cast<int>(p1_xslot(NX)), VSLOT = static_cast<int>(p1_vslot(MS, VW));
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int n16 = lane & 15, gq = lane >> 4;
-  const int half = wave >> 2, w4 = wave & 3;  // step parity; the wave's role within its half
+  const int grp = wave >> 2, w4 = wave & 3;  // step group; the wave's role within its group
   const int pw = w4 >> 1, hw = w4 & 1;        // path and subtile half
   const int tiles = P.n_tt * P.n_lt;
   const int ksi = blockIdx.x / tiles;
@@ -160,7 +163,7 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
   const rsrc_t vr = make_rsrc(pw ? P.V[1] : P.V[0], P.v_bytes);
 
   // loads of step n (split-local) into its ring slot, by the waves of its
-  // parity: the packed V words of this wave's subtiles (word of latent
+  // group: the packed V words of this wave's subtiles (word of latent
   // 16 (sb0 + 2 m) + i at word 16 m + i of the wave's slice; zero past r, past
   // the range and for the tail step, whose words come through registers) and
   // token subtile w4 of x (zero past d_in and past the range)
@@ -217,9 +220,9 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
     }
   };
 
-  // the first R2 - 1 rounds (two steps each, one per half) in flight
+  // the first RR - 1 rounds (kSplit1 steps each, one per group) in flight
 #pragma unroll
-  for (int d = 0; d < R2 - 1; ++d) issue(2 * d + half);
+  for (int d = 0; d < RR - 1; ++d) issue(kSplit1 * d + grp);
 
   // packed V words of the tail step (tail plane: 16- or 32-bit entries)
   uint32_t tw[MS];
@@ -261,17 +264,17 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
     for (int tn = 0; tn < kTn1; ++tn) acc[m][tn] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const u32x4* gtp = gt + pw * ns * 4 * G;
-  const int nr = (ns + 1) >> 1;  // rounds: step 2 i + half in round i
+  const int nr = (ns + kSplit1 - 1) / kSplit1;  // rounds: step kSplit1 i + grp in round i
   for (int i = 0; i < nr; ++i) {
     // round i has landed (each wave waits for its own loads, the barrier for
     // everyone's) and every wave is done with the slots of round i - 1
     asm volatile("" ::: "memory");  // round i - 1's LDS reads stay above the barrier
-    wait_vm_lds<(R2 - 2) * (NX + NV)>();
+    wait_vm_lds<(RR - 2) * (NX + NV)>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    const int n = 2 * i + half;
-    if (n >= ns) {  // (an odd count: the second half sits out the last round)
-      issue(2 * (i + R2 - 1) + half);
+    const int n = kSplit1 * i + grp;
+    if (n >= ns) {  // (a short last round: the later groups sit it out)
+      issue(kSplit1 * (i + RR - 1) + grp);
       continue;
     }
     const int sl = n % RING;
@@ -314,9 +317,9 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
     uint32_t words[MS];
 #pragma unroll
     for (int m = 0; m < MS; ++m) words[m] = tail ? tw[m] : vw[16 * m + n16];
-    // the loads of round i + R2 - 1 (into the slots of round i - 1, free since
+    // the loads of round i + RR - 1 (into the slots of round i - 1, free since
     // the barrier), issued once this step's LDS reads are out
-    issue(2 * (i + R2 - 1) + half);
+    issue(kSplit1 * (i + RR - 1) + grp);
     u32x4 A[MS][G];
 #pragma unroll
     for (int m = 0; m < MS; ++m) {
@@ -340,21 +343,30 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
           for (int tn = 0; tn < kTn1; ++tn) acc[m][tn] = mfma(A[m][s], B[tn][e], acc[m][tn]);
   }
 
-  // the two halves' sums, in a fixed order (half 0 + half 1), through LDS
-  // (the ring is dead after this barrier), then this role's partial sums:
-  // pbuf[ks][token tile][path][subtile][token subtile][lane][4]
+  // the groups' sums, in a fixed order (((group 0 + group 1) + group 2) ...),
+  // through LDS (the ring is dead after the first barrier), then this role's
+  // partial sums: pbuf[ks][token tile][path][subtile][token subtile][lane][4]
   asm volatile("" ::: "memory");
   wait_vm_lds<0>();
-  __syncthreads();
   floatx4* red = reinterpret_cast<floatx4*>(lds) + w4 * MS * kTn1 * 64;
-  if (half == 1) {
 #pragma unroll
-    for (int m = 0; m < MS; ++m)
+  for (int src = 1; src < kSplit1; ++src) {
+    __syncthreads();
+    if (grp == src) {
 #pragma unroll
-      for (int tn = 0; tn < kTn1; ++tn) red[(m * kTn1 + tn) * 64 + lane] = acc[m][tn];
+      for (int m = 0; m < MS; ++m)
+#pragma unroll
+        for (int tn = 0; tn < kTn1; ++tn) red[(m * kTn1 + tn) * 64 + lane] = acc[m][tn];
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+      for (int m = 0; m < MS; ++m)
+#pragma unroll
+        for (int tn = 0; tn < kTn1; ++tn) acc[m][tn] += red[(m * kTn1 + tn) * 64 + lane];
+    }
   }
-  __syncthreads();
-  if (half == 0) {
+  if (grp == 0) {
     float* part = P.pbuf + ((static_cast<int64_t>(ksi) * P.n_tt + tt) * 2 + pw) * P.ns16p * kPart;
 #pragma unroll
     for (int m = 0; m < MS; ++m) {
@@ -362,8 +374,7 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
       if (s < P.ns16) {
 #pragma unroll
         for (int tn = 0; tn < kTn1; ++tn)
-          *reinterpret_cast<floatx4*>(part + (s * kTn1 + tn) * 256 + lane * 4) =
-              acc[m][tn] + red[(m * kTn1 + tn) * 64 + lane];
+          *reinterpret_cast<floatx4*>(part + (s * kTn1 + tn) * 256 + lane * 4) = acc[m][tn];
       }
     }
   }

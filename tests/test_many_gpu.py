@@ -95,9 +95,28 @@ def test_many_more_than_one_list_launch():
         _check(lins[i][0], U.torch_to_raw(ys[i], "bf16"), label=f"long list {i}")
 
 
+def test_many_matrix_core_decode_lists():
+    # T = 3 .. 64 linears that the matrix-core decode kernel takes, in runs
+    # broken by a look-up-table linear, a prefill-sized one and a dtype change
+    specs = [(8, 1024, 1024, 80, "bf16", "f16"), (16, 512, 768, 48, "bf16", "f16"),
+             (3, 700, 900, 17, "bf16", "f16"), (64, 256, 512, 32, "bf16", "f16"),
+             (1, 512, 512, 32, "bf16", "f16"), (8, 2048, 1024, 64, "bf16", "f16"),
+             (40, 512, 4096, 128, "bf16", "f16"), (5, 96, 64, 31, "f32", "f32"),
+             (8, 64, 160, 16, "f32", "f32")] + [(4 + i, 256 + 64 * i, 128 + 32 * i, 16 + 16 * (i % 3), "bf16", "f16")
+                                                for i in range(18)]
+    lins = _linears(specs, cfg=25)
+    ys, _ = _many(lins)
+    ref = _singles(lins)
+    for i, ((li, _, _), y, r) in enumerate(zip(lins, ys, ref)):
+        assert _same_bits(y, r), (i, specs[i])
+    for i in (0, 3, 7, 26):
+        _check(lins[i][0], U.torch_to_raw(ys[i], specs[i][4]), label=f"mma list {i}")
+
+
 def test_many_repeated_calls_on_one_workspace():
     specs = [(1, 4096, 4096, 80, "bf16", "f16"), (2, 1024, 2048, 48, "bf16", "f16"),
-             (1, 2048, 512, 64, "bf16", "f16")]
+             (1, 2048, 512, 64, "bf16", "f16"), (8, 1024, 1024, 80, "bf16", "f16"),
+             (16, 2048, 512, 64, "bf16", "f16")]
     lins = _linears(specs, cfg=23)
     ws = None
     g = torch.Generator(device="cuda").manual_seed(23)
@@ -113,7 +132,8 @@ def test_many_repeated_calls_on_one_workspace():
 
 def test_many_graph_replays_match_eager():
     specs = [(1, 2048, 1536, 64, "bf16", "f16"), (1, 1024, 4096, 80, "bf16", "f16"),
-             (2, 512, 512, 32, "bf16", "f16"), (16, 512, 768, 48, "bf16", "f16")]
+             (2, 512, 512, 32, "bf16", "f16"), (16, 512, 768, 48, "bf16", "f16"),
+             (8, 1024, 1024, 80, "bf16", "f16")]
     lins = _linears(specs, cfg=24)
     y_eager, ws = _many(lins)
     y_eager = [y.clone() for y in y_eager]
