@@ -62,6 +62,7 @@ constexpr int kTn1 = 4;
 constexpr int kMaxMs = 6;       // 16-latent subtiles per wave
 constexpr int kMinSteps = 12;   // fewest 32-input steps per split (when d_in allows)
 constexpr int kMaxKbPer = 64;   // most 32-input steps per split (its g terms are held in LDS)
+constexpr int kMinWg1 = 128;    // P1 workgroups wanted before latent tiles get thinner
 constexpr int kPart = kTn1 * 64 * 4;  // partial floats per (token tile, path, subtile)
 // P2
 constexpr int kThreads2 = 512;  // 8 waves: two halves of 4 take alternate units
@@ -859,22 +860,30 @@ PrefillGeom prefill_geometry(int T, int d_in, int d_out, int r) {
   const int rr = r > 0 ? r : 1;
   g.nkb = nblocks32(rr);
   g.ns16 = (rr + 15) / 16;
-  // P1: each wave takes ms interleaved subtiles of its path (2 waves a path)
-  g.n_lt = (g.ns16 + 2 * kMaxMs - 1) / (2 * kMaxMs);
-  g.ms = (g.ns16 + 2 * g.n_lt - 1) / (2 * g.n_lt);
-  g.ns16p = g.n_lt * 2 * g.ms;
+  // P1: each wave takes ms interleaved subtiles of its path (2 waves a path);
+  // about 256 workgroups, splits of d_in of at least kMinSteps steps (when
+  // d_in has them) and at most kMaxKbPer.  With few token tiles, fewer
+  // subtiles per wave (more latent tiles, x re-read per tile) rather than
+  // more splits: the largest ms that still gives kMinWg1 workgroups.
   g.n_tt = (tt + kTok1 - 1) / kTok1;
   const int nbt = nblocks32(d_in > 0 ? d_in : 1);
-  const int tiles = g.n_tt * g.n_lt;
-  // about 256 workgroups; splits of at least kMinSteps steps (when d_in has
-  // them) and at most kMaxKbPer
-  int ks = (256 + tiles - 1) / tiles;
-  if (ks > nbt / kMinSteps) ks = nbt / kMinSteps;
   const int ks_min = (nbt + kMaxKbPer - 1) / kMaxKbPer;
-  if (ks < ks_min) ks = ks_min;
-  if (ks < 1) ks = 1;
-  g.kb_per = (nbt + ks - 1) / ks;
-  g.ks = (nbt + g.kb_per - 1) / g.kb_per;
+  // the plan for at most `ms` subtiles per wave; returns its workgroup count
+  auto plan = [&](int ms) {
+    g.n_lt = (g.ns16 + 2 * ms - 1) / (2 * ms);
+    g.ms = (g.ns16 + 2 * g.n_lt - 1) / (2 * g.n_lt);
+    const int tiles = g.n_tt * g.n_lt;
+    int ks = (256 + tiles - 1) / tiles;
+    if (ks > nbt / kMinSteps) ks = nbt / kMinSteps;
+    if (ks < ks_min) ks = ks_min;
+    if (ks < 1) ks = 1;
+    g.kb_per = (nbt + ks - 1) / ks;
+    g.ks = (nbt + g.kb_per - 1) / g.kb_per;
+    return tiles * g.ks;
+  };
+  int ms = kMaxMs;
+  while (plan(ms) < kMinWg1 && ms > 1) --ms;
+  g.ns16p = g.n_lt * 2 * g.ms;
   g.n_un = (d_out > 0 ? d_out + kUnit - 1 : kUnit) / kUnit;
   g.n_tt2 = (tt + kTok2 - 1) / kTok2;
   plan_lds(g, kDtF32, kDtF32, false, false);
