@@ -70,6 +70,10 @@ def _load():
         lib.lbo_forward_factored.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, i32, vp]
         lib.lbo_forward_sampled.restype = None
         lib.lbo_forward_sampled.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, i32, vp, vp, i64, vp]
+        lib.lbo_latent.restype = None
+        lib.lbo_latent.argtypes = [vp, i64, i64, i64, vp, vp, vp, i32, vp]
+        lib.lbo_from_latent.restype = None
+        lib.lbo_from_latent.argtypes = [vp, i64, i64, i64, vp, vp, i32, vp]
         lib.lbo_dense_weight.restype = None
         lib.lbo_dense_weight.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, i32, vp]
         lib.lbo_dense_forward.restype = None
@@ -168,6 +172,32 @@ def forward_factored(x, U, V, h, g, l) -> np.ndarray:
     _load().lbo_forward_factored(_p(x), T, d_in, d_out, r, _ptr_array(U), _ptr_array(V),
                                  _ptr_array(h), _ptr_array(g), _ptr_array(l), n, _p(y))
     del keep
+    return y
+
+
+def latent(x, V, g, l) -> np.ndarray:
+    """O5.  The cached latent w [npaths, T, r] of x [T, d_in] (fp64)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    V = [np.ascontiguousarray(v, dtype=np.int8) for v in V]
+    g = [np.ascontiguousarray(a, dtype=np.float64) for a in g]
+    l = [np.ascontiguousarray(a, dtype=np.float64) for a in l]
+    n = len(V)
+    T, d_in = x.shape
+    r = V[0].shape[1]
+    w = np.empty((n, T, r), dtype=np.float64)
+    _load().lbo_latent(_p(x), T, d_in, r, _ptr_array(V), _ptr_array(g), _ptr_array(l), n, _p(w))
+    return w
+
+
+def from_latent(w, U, h) -> np.ndarray:
+    """O5.  y [T, d_out] from a cached latent w [npaths, T, r] (fp64)."""
+    w = np.ascontiguousarray(w, dtype=np.float64)
+    U = [np.ascontiguousarray(u, dtype=np.int8) for u in U]
+    h = [np.ascontiguousarray(a, dtype=np.float64) for a in h]
+    n, T, r = w.shape
+    d_out = U[0].shape[0]
+    y = np.empty((T, d_out), dtype=np.float64)
+    _load().lbo_from_latent(_p(w), T, d_out, r, _ptr_array(U), _ptr_array(h), n, _p(y))
     return y
 
 

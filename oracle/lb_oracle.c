@@ -16,6 +16,8 @@
  *     proof in Appendix "Mathematical Analysis and Proofs";
  *   - the residual path of identical structure and the sum of both paths:
  *     Sec. 3.3, Eqs. (res_approx_structure) and (final_weight_approx_res);
+ *   - the rank-r latent that replaces keys and values in the cache, and the
+ *     forward from it: Sec. "Analysis", paragraph "KV Cache Compression";
  *   - the bits-per-weight accounting and its inversion for the rank:
  *     Appendix "Average Bits Per Weight Calculation", Eqs. (b_calculation)
  *     and (r_calculation);
@@ -191,6 +193,44 @@ void lbo_forward_factored(const double* x, int64_t T, int64_t d_in, int64_t d_ou
   }
   free(a);
   free(z);
+}
+
+/* O5: the latent cache of Sec. "Analysis", paragraph "KV Cache Compression"
+   (Fig. kv_cache_viz): the rank-r intermediate of Proposition 1 that is
+   cached instead of d_model-wide keys or values, for both paths:
+     w_p[t][k] = l_p[k] * sum_j V_p[j][k] (x[t][j] g_p[j])     (ascending j)
+   written to w [npaths][T][r]; and the rest of the forward from such a cache:
+     y[t][i] = sum_p h_p[i] * sum_k U_p[i][k] w_p[t][k]         (ascending k,
+   paths in order).  The two compose to lbo_forward_factored exactly (the same
+   operations in the same order). */
+void lbo_latent(const double* x, int64_t T, int64_t d_in, int64_t r, const int8_t* const* V,
+                const double* const* g, const double* const* l, int npaths, double* w) {
+  double* a = (double*)malloc(sizeof(double) * (size_t)(d_in > 0 ? d_in : 1));
+  for (int p = 0; p < npaths; p++) {
+    for (int64_t t = 0; t < T; t++) {
+      for (int64_t j = 0; j < d_in; j++) a[j] = x[t * d_in + j] * g[p][j];
+      for (int64_t k = 0; k < r; k++) {
+        double s = 0.0;
+        for (int64_t j = 0; j < d_in; j++) s += (double)V[p][j * r + k] * a[j];
+        w[(p * T + t) * r + k] = s * l[p][k];
+      }
+    }
+  }
+  free(a);
+}
+
+void lbo_from_latent(const double* w, int64_t T, int64_t d_out, int64_t r, const int8_t* const* U,
+                     const double* const* h, int npaths, double* y) {
+  for (int64_t i = 0; i < T * d_out; i++) y[i] = 0.0;
+  for (int p = 0; p < npaths; p++) {
+    for (int64_t t = 0; t < T; t++) {
+      for (int64_t i = 0; i < d_out; i++) {
+        double s = 0.0;
+        for (int64_t k = 0; k < r; k++) s += (double)U[p][i * r + k] * w[(p * T + t) * r + k];
+        y[t * d_out + i] += s * h[p][i];
+      }
+    }
+  }
 }
 
 /* Same as lbo_forward_factored but only for the listed (t, i) output

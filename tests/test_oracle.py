@@ -210,6 +210,69 @@ def test_identity_like_layer():
 
 
 # ---------------------------------------------------------------------------
+# the latent cache (O5): composition with the rest of the forward, closed
+# forms, the latent-scale sign invariant, brute force
+# ---------------------------------------------------------------------------
+def test_latent_composes_to_the_forward():
+    rs = np.random.default_rng(31)
+    for T, d_in, d_out, r in [(3, 33, 17, 5), (1, 64, 40, 16), (4, 7, 9, 1)]:
+        x, U, V, h, g, l = _rand_layer(rs, T, d_in, d_out, r)
+        w = O.latent(x, V, g, l)
+        assert w.shape == (2, T, r)
+        assert np.array_equal(O.from_latent(w, U, h), O.forward_factored(x, U, V, h, g, l))
+        W = O.dense_weight(U, V, h, g, l)
+        assert np.allclose(O.from_latent(w, U, h), O.dense_forward(x, W), rtol=1e-12, atol=1e-12)
+
+
+def test_latent_closed_forms():
+    """All V signs +1: w_p[t,k] = l_p[k] sum_j g_p[j] x[t,j]; all U signs +1:
+    y[t,i] = sum_p h_p[i] sum_k w_p[t,k]."""
+    rs = np.random.default_rng(32)
+    T, d_in, d_out, r = 3, 40, 24, 16
+    x, U, V, h, g, l = _rand_layer(rs, T, d_in, d_out, r)
+    w = O.latent(x, [np.ones_like(v) for v in V], g, l)
+    ref = np.stack([np.outer(x @ g[p], l[p]) for p in range(2)])
+    assert np.allclose(w, ref, rtol=1e-12, atol=1e-12 * np.abs(ref).max())
+    wr = rs.standard_normal((2, T, r))
+    y = O.from_latent(wr, [np.ones_like(u) for u in U], h)
+    ref = sum(np.outer(wr[p].sum(axis=1), h[p]) for p in range(2))
+    assert np.allclose(y, ref, rtol=1e-12, atol=1e-12 * np.abs(ref).max())
+
+
+def test_latent_sign_invariant():
+    """Negating column k of V_p together with l_p[k] leaves the latent unchanged."""
+    rs = np.random.default_rng(33)
+    x, U, V, h, g, l = _rand_layer(rs, 2, 48, 40, 20)
+    w = O.latent(x, V, g, l)
+    for p, k in [(0, 0), (1, 7)]:
+        V2, l2 = [a.copy() for a in V], [a.copy() for a in l]
+        V2[p][:, k] *= -1
+        l2[p][k] *= -1
+        assert np.array_equal(O.latent(x, V2, g, l2), w)
+
+
+def test_latent_brute_force_python_loops():
+    rs = np.random.default_rng(34)
+    T, d_in, d_out, r = 2, 5, 4, 3
+    x, U, V, h, g, l = _rand_layer(rs, T, d_in, d_out, r)
+    w = O.latent(x, V, g, l)
+    for p in range(2):
+        for t in range(T):
+            for k in range(r):
+                s = 0.0
+                for j in range(d_in):
+                    s += float(V[p][j, k]) * float(x[t, j]) * float(g[p][j])
+                assert abs(w[p, t, k] - s * l[p][k]) <= 1e-12 * (1 + abs(s))
+    y = O.from_latent(w, U, h)
+    for t in range(T):
+        for i in range(d_out):
+            s = 0.0
+            for p in range(2):
+                s += h[p][i] * sum(float(U[p][i, k]) * w[p, t, k] for k in range(r))
+            assert abs(y[t, i] - s) <= 1e-12 * (1 + abs(s))
+
+
+# ---------------------------------------------------------------------------
 # invariants (bitwise in fp64 where the arithmetic is exact)
 # ---------------------------------------------------------------------------
 @pytest.fixture
@@ -383,6 +446,12 @@ MUTANTS = [
     ("residual path ignored", "for (int p = 0; p < npaths; p++) {\n    for (int64_t t = 0; t < T; t++) {",
      "for (int p = 0; p < 1; p++) {\n    for (int64_t t = 0; t < T; t++) {"),
     ("sign flipped", "s += (double)U[p][i * r + k] * z[k];", "s -= (double)U[p][i * r + k] * z[k];"),
+    ("latent: dropped latent scale", "w[(p * T + t) * r + k] = s * l[p][k];", "w[(p * T + t) * r + k] = s;"),
+    ("latent: transposed V index", "s += (double)V[p][j * r + k] * a[j];\n        w[",
+     "s += (double)V[p][(j % r) * r + (k % r)] * a[j];\n        w["),
+    ("from latent: wrong path", "U[p][i * r + k] * w[(p * T + t) * r + k];", "U[p][i * r + k] * w[(0 * T + t) * r + k];"),
+    ("from latent: dropped row scale", "        y[t * d_out + i] += s * h[p][i];\n      }\n    }\n  }\n}",
+     "        y[t * d_out + i] += s;\n      }\n    }\n  }\n}"),
 ]
 
 
@@ -392,6 +461,10 @@ def _checks_fail_for(lib_path):
     vp, i64 = ctypes.c_void_p, ctypes.c_int64
     lib.lbo_forward_factored.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, ctypes.c_int, vp]
     lib.lbo_forward_factored.restype = None
+    lib.lbo_latent.argtypes = [vp, i64, i64, i64, vp, vp, vp, ctypes.c_int, vp]
+    lib.lbo_latent.restype = None
+    lib.lbo_from_latent.argtypes = [vp, i64, i64, i64, vp, vp, ctypes.c_int, vp]
+    lib.lbo_from_latent.restype = None
 
     def fwd(x, U, V, h, g, l):
         x = np.ascontiguousarray(x, np.float64)
@@ -410,7 +483,19 @@ def _checks_fail_for(lib_path):
                            rtol=1e-12, atol=1e-12)
     fx, xt, Ut, Vt, ht, gt, lt = _load_tiny(os.path.join(os.path.dirname(__file__), "golden"))
     ok_tiny = np.array_equal(fwd(xt, Ut, Vt, ht, gt, lt), np.array(fx["y"], dtype=np.float64))
-    return not (ok_dense and ok_tiny)
+    # the latent pair composes to the dense result
+    arrs = [[np.ascontiguousarray(a, dt) for a in A] for A, dt in
+            ((U, np.int8), (V, np.int8), (h, np.float64), (g, np.float64), (l, np.float64))]
+    pU, pV, ph, pg, pl = [(ctypes.c_void_p * len(A))(*[a.ctypes.data for a in A]) for A in arrs]
+    T, d_in = x.shape
+    d_out, r = U[0].shape
+    xc = np.ascontiguousarray(x, np.float64)
+    w = np.empty((2, T, r))
+    lib.lbo_latent(xc.ctypes.data, T, d_in, r, pV, pg, pl, 2, w.ctypes.data)
+    y2 = np.empty((T, d_out))
+    lib.lbo_from_latent(w.ctypes.data, T, d_out, r, pU, ph, 2, y2.ctypes.data)
+    ok_latent = np.allclose(y2, O.dense_forward(x, O.dense_weight(U, V, h, g, l)), rtol=1e-12, atol=1e-12)
+    return not (ok_dense and ok_tiny and ok_latent)
 
 
 @pytest.mark.parametrize("desc,orig,repl", MUTANTS, ids=[m[0] for m in MUTANTS])
