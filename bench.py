@@ -156,6 +156,42 @@ class LayerList:
             raise RuntimeError(f"lb_linear_forward_many failed with status {st}")
 
 
+class LatentCall:
+    """A layer's latent-cache call, pre-marshalled: "latent" writes the cache [T, 2, r] (bf16) of
+    the layer's x, "from" computes y from that cache; times like a Layer."""
+
+    def __init__(self, layer, mode):
+        import torch
+        import paper_2506_13771_amd as lb
+        L = layer
+        self.layer, self.mode = L, mode
+        self.lib = lb.load_library()
+        self.cache = torch.zeros((L.T, 2, L.r), dtype=torch.bfloat16, device=L.x.device)
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        if mode == "latent":
+            n = lb.lb_latent_workspace_bytes(L.T, L.d_in, L.r)
+            self.ws = torch.empty(max(n, 256), dtype=torch.uint8, device=L.x.device)
+            self.fn = self.lib.lb_linear_latent
+            self.argv = (ctypes.c_void_p(L.x.data_ptr()), lb._dtype_code(L.x), L.T, L.d_in, L.r, L._arr,
+                         lb._dtype_code(L.paths[0].h), ctypes.c_void_p(self.cache.data_ptr()), lb.LB_BF16,
+                         ctypes.c_void_p(self.ws.data_ptr()), self.ws.numel(), stream)
+        else:
+            n = lb.lb_from_latent_workspace_bytes(L.T, L.r)
+            self.ws = torch.empty(max(n, 256), dtype=torch.uint8, device=L.x.device)
+            self.fn = self.lib.lb_linear_from_latent
+            self.argv = (ctypes.c_void_p(self.cache.data_ptr()), lb.LB_BF16, L.T, L.d_out, L.r, L._arr,
+                         lb._dtype_code(L.paths[0].h), ctypes.c_void_p(L.y.data_ptr()), lb._dtype_code(L.y),
+                         ctypes.c_void_p(self.ws.data_ptr()), self.ws.numel(), stream)
+
+    def set_stream(self, handle):
+        self.argv = self.argv[:-1] + (ctypes.c_void_p(handle),)
+
+    def call(self):
+        st = self.fn(*self.argv)
+        if st != 0:
+            raise RuntimeError(f"latent-cache call ({self.mode}) failed with status {st}")
+
+
 def time_calls(layers, steps, warmup, use_graph=True, per_graph=None):
     """Run every layer's forward `steps` times (after `warmup`) on the current stream, timed
     with HIP events recorded on that stream.  With use_graph the launches of `per_graph`
@@ -350,7 +386,7 @@ def cpu_baseline(li, seconds):
 # ----------------------------------------------------------------------------
 # sweep of the other configurations (diagnostic lines written to a file)
 # ----------------------------------------------------------------------------
-def run_sweep(path, steps, warmup, only=("7b", "13b", "70b")):
+def run_sweep(path, steps, warmup, only=("7b", "13b", "kv", "70b")):
     import torch
     from paper_2506_13771_amd import synth
     out = open(path, "w")
@@ -387,6 +423,27 @@ def run_sweep(path, steps, warmup, only=("7b", "13b", "70b")):
               "GBps": b / (ms * 1e-3) / 1e9, "hbm_frac": b / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
               "mfma_tflops": f / (ms * 1e-3) / 1e12, "mfma_frac": f / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS})
         del L
+    # latent K/V cache on the Llama2-7B k_proj shape: the cache write (x -> bf16 latents of both
+    # paths) and the output from the cache, beside the forward of the same tokens
+    for bpw, r in ((0.1, 80), (0.55, 544)) if "kv" in only else ():
+        for T in (1, 64, 2048):
+            d_in = d_out = 4096
+            L = Layer(synth.make_linear(d_in, d_out, r, T, cfg=5, linear=1), "cuda")
+            n_st, n_wu = (steps, warmup) if T < 2048 else (max(10, steps // 20), max(3, warmup // 20))
+            ms_f, _ = time_calls([L], n_st, n_wu)
+            lat, frm = LatentCall(L, "latent"), LatentCall(L, "from")
+            ms_l, _ = time_calls([lat], n_st, n_wu)
+            ms_u, _ = time_calls([frm], n_st, n_wu)
+            e = L.e_act
+            b_l = 2 * r * d_in / 8.0 + 2 * (d_in + r) * L.e_scale + T * d_in * e + 2 * T * r * 2
+            b_u = 2 * r * d_out / 8.0 + 2 * d_out * L.e_scale + 2 * T * r * 2 + T * d_out * e
+            emit({"config": "llama2-7b-kv-cache", "linear": "k_proj", "bpw": bpw, "T": T, "d_in": d_in,
+                  "d_out": d_out, "r": r, "cache_values_per_token": 2 * r, "cache_reduction": d_out / (2 * r),
+                  "us_latent": ms_l * 1e3, "us_from_latent": ms_u * 1e3, "us_forward": ms_f * 1e3,
+                  "latent_GBps": b_l / (ms_l * 1e-3) / 1e9, "from_latent_GBps": b_u / (ms_u * 1e-3) / 1e9,
+                  "latent_tflops": 4 * T * d_in * r / (ms_l * 1e-3) / 1e12,
+                  "from_latent_tflops": 4 * T * r * d_out / (ms_u * 1e-3) / 1e12})
+            del L, lat, frm
     # 70B sweep: 80 layers x 7 linears resident, back-to-back on one stream
     ranks_70b = {(8192, 8192): 176, (8192, 1024): 16, (8192, 28672): 288, (28672, 8192): 288}
     for T in ((1, 8, 64) if "70b" in only else ()):
@@ -424,8 +481,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", default=None, help="write per-configuration JSON lines to this file")
-    ap.add_argument("--sweep-only", default="7b,13b,70b",
-                    help="comma list of the sweep's parts to run (7b block, 13b prefill, 70b decode sweep)")
+    ap.add_argument("--sweep-only", default="7b,13b,kv,70b",
+                    help="comma list of the sweep's parts to run (7b block, 13b prefill, 7b latent K/V cache, "
+                         "70b decode sweep)")
     ap.add_argument("--no-warm", action="store_true",
                     help="skip the warm-cache measurements (counter runs: every decode dispatch is then a "
                          "cold-rotation one)")

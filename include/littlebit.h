@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define LB_ABI_VERSION 2
+#define LB_ABI_VERSION 3
 
 typedef enum lb_status {
   LB_OK = 0,
@@ -208,6 +208,45 @@ size_t lb_forward_many_workspace_bytes(const lb_linear_desc* descs, int64_t n);
    aligned, >= lb_forward_many_workspace_bytes(descs, n) bytes. */
 lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/* Latent K/V cache (paragraph "KV Cache Compression", Fig. kv_cache_viz,
+   Table kv_cache_reduction: applied to the key and value projections, the
+   factored forward lets a cache hold rank-r vectors per token instead of
+   d_model-wide ones).  The cached vector of token t and path p is the scaled
+   stage-1 latent of Proposition 1,
+     w[t][p][k] = l_p[k] sum_j V_p[j][k] g_p[j] x[t][j],
+   stored token-major: w [T x 2 x r] in latent_dtype (F32, F16 or BF16),
+   element (t, p, k) at (2 t + p) r + k, so that the latents of new tokens are
+   appended to a cache as one contiguous run.  16-bit latents are rounded to
+   nearest even from fp32; an F32 cache holds the fp32 values the prefill
+   kernels compute, and lb_linear_from_latent on it gives bit for bit what
+   lb_linear_forward_kernel(..., LB_KERNEL_PREFILL) gives for the same x.
+
+   lb_linear_latent: w of x [T x d_in] (act_dtype).  Only V, g and l of the
+   paths are read (U and h may be NULL).  Stage 1 of the prefill kernels
+   (exact bf16 term products, fp32 accumulation), then one pass that sums its
+   partial results, scales by l and stores w.  d_in == 0 zero-fills w.  w must
+   not overlap x (LB_ERR_ARG).  workspace: 256-byte aligned, >=
+   lb_latent_workspace_bytes(T, d_in, r) bytes (no zero-fill needed). */
+size_t lb_latent_workspace_bytes(int64_t T, int64_t d_in, int64_t r);
+lb_status lb_linear_latent(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t r,
+                           const lb_path* paths, lb_dtype scale_dtype, void* w, lb_dtype latent_dtype,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* lb_linear_from_latent: the output of the layer from cached latents,
+     y[t][i] = sum_p h_p[i] sum_k U_p[i][k] w[t][p][k],
+   w [T x 2 x r] (latent_dtype) as lb_linear_latent writes it, y [T x d_out]
+   in out_dtype (F32, F16 or BF16), rounded once from the fp32 sum of both
+   paths.  Only U and h of the paths are read (V, g and l may be NULL).  One
+   pass cuts w into bf16 terms (two for 16-bit outputs, three for fp32 ones,
+   as lb_linear_forward does), then stage 2 of the prefill kernels.  r == 0
+   zero-fills y.  y must not overlap w (LB_ERR_ARG).  workspace: 256-byte
+   aligned, >= lb_from_latent_workspace_bytes(T, r) bytes (no zero-fill
+   needed). */
+size_t lb_from_latent_workspace_bytes(int64_t T, int64_t r);
+lb_status lb_linear_from_latent(const void* w, lb_dtype latent_dtype, int64_t T, int64_t d_out, int64_t r,
+                                const lb_path* paths, lb_dtype scale_dtype, void* y, lb_dtype out_dtype,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Checking path: the dense effective weight of both paths,
      W[i][j] = sum_p h_p[i] g_p[j] sum_k U_p[i][k] l_p[k] V_p[j][k]

@@ -9,7 +9,10 @@ falling back to anything else.
 The names follow the C ABI:
   lb_pack_signs, lb_linear_forward, lb_dense_reference_weight,
   lb_packed_bytes, lb_bits_per_weight, lb_rank_for_bpw,
-  lb_forward_workspace_bytes, lb_workspace_init, lb_decode_max_tokens.
+  lb_forward_workspace_bytes, lb_workspace_init, lb_decode_max_tokens,
+  lb_linear_forward_many, lb_forward_many_workspace_bytes,
+  lb_linear_latent, lb_latent_workspace_bytes,
+  lb_linear_from_latent, lb_from_latent_workspace_bytes.
 """
 from __future__ import annotations
 
@@ -25,7 +28,7 @@ LB_OK, LB_ERR_NULL, LB_ERR_SHAPE, LB_ERR_DTYPE, LB_ERR_ALIGN, LB_ERR_WORKSPACE, 
 LB_F32, LB_F16, LB_BF16 = 0, 1, 2
 LB_ROLE_U, LB_ROLE_V = 0, 1
 LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL, LB_KERNEL_DECODE_MFMA = 0, 1, 2, 3
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 
 class LittleBitError(RuntimeError):
@@ -85,6 +88,15 @@ def load_library(path: str = LIB_PATH):
     lib.lb_forward_many_workspace_bytes.argtypes = [ctypes.POINTER(lb_linear_desc), i64]
     lib.lb_linear_forward_many.restype = i32
     lib.lb_linear_forward_many.argtypes = [ctypes.POINTER(lb_linear_desc), i64, vp, sz, vp]
+    lib.lb_latent_workspace_bytes.restype = sz
+    lib.lb_latent_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.lb_linear_latent.restype = i32
+    lib.lb_linear_latent.argtypes = [vp, i32, i64, i64, i64, ctypes.POINTER(lb_path), i32, vp, i32, vp, sz, vp]
+    lib.lb_from_latent_workspace_bytes.restype = sz
+    lib.lb_from_latent_workspace_bytes.argtypes = [i64, i64]
+    lib.lb_linear_from_latent.restype = i32
+    lib.lb_linear_from_latent.argtypes = [vp, i32, i64, i64, i64, ctypes.POINTER(lb_path), i32, vp, i32, vp, sz,
+                                          vp]
     lib.lb_dense_reference_weight.restype = i32
     lib.lb_dense_reference_weight.argtypes = [ctypes.POINTER(lb_path), i32, i64, i64, i64, vp, vp]
     if lib.lb_abi_version() != ABI_VERSION:
@@ -179,7 +191,7 @@ def _paths_struct(paths: Sequence[LittleBitPath]):
     for i, p in enumerate(paths):
         arr[i] = lb_path(_dev_ptr(p.U, "U"), _dev_ptr(p.V, "V"), _dev_ptr(p.h, "h"),
                          _dev_ptr(p.g, "g"), _dev_ptr(p.l, "l"))
-    sc = {_dtype_code(p.h) for p in paths} | {_dtype_code(p.g) for p in paths} | {_dtype_code(p.l) for p in paths}
+    sc = {_dtype_code(t) for p in paths for t in (p.h, p.g, p.l) if t is not None}
     if len(sc) != 1:
         raise TypeError("all scales must share one dtype")
     return arr, sc.pop()
@@ -271,6 +283,59 @@ def lb_linear_forward_many(items, workspace=None, stream=None):
     return ys
 
 
+def lb_latent_workspace_bytes(T: int, d_in: int, r: int) -> int:
+    return int(load_library().lb_latent_workspace_bytes(T, d_in, r))
+
+
+def lb_from_latent_workspace_bytes(T: int, r: int) -> int:
+    return int(load_library().lb_from_latent_workspace_bytes(T, r))
+
+
+def _scratch(n: int, device):
+    torch = _torch()
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+def lb_linear_latent(x, paths: Sequence[LittleBitPath], r: int, w=None, latent_dtype=None, workspace=None,
+                     stream=None):
+    """The latent cache entries w [T, 2, r] of x [T, d_in] (only V, g, l of the paths are read; latent_dtype
+    defaults to float32); returns w."""
+    torch = _torch()
+    lib = load_library()
+    T, d_in = x.shape
+    arr, sc = _paths_struct(paths)
+    if w is None:
+        w = torch.empty((T, 2, r), dtype=latent_dtype or torch.float32, device=x.device)
+    if workspace is None:
+        workspace = _scratch(lb_latent_workspace_bytes(T, d_in, r), x.device)
+    st = lib.lb_linear_latent(_dev_ptr(x, "x"), _dtype_code(x), T, d_in, r, arr, sc, _dev_ptr(w, "w"),
+                              _dtype_code(w), _dev_ptr(workspace, "workspace"),
+                              workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "lb_linear_latent")
+    return w
+
+
+def lb_linear_from_latent(w, paths: Sequence[LittleBitPath], y=None, out_dtype=None, workspace=None, stream=None):
+    """y [T, d_out] of the layer from cached latents w [T, 2, r] (only U, h of the paths are read; out_dtype
+    defaults to w's dtype); returns y."""
+    torch = _torch()
+    lib = load_library()
+    T, two, r = w.shape
+    if two != 2:
+        raise ValueError("w must be [T, 2, r]")
+    d_out = paths[0].h.shape[0]
+    arr, sc = _paths_struct(paths)
+    if y is None:
+        y = torch.empty((T, d_out), dtype=out_dtype or w.dtype, device=w.device)
+    if workspace is None:
+        workspace = _scratch(lb_from_latent_workspace_bytes(T, r), w.device)
+    st = lib.lb_linear_from_latent(_dev_ptr(w, "w"), _dtype_code(w), T, d_out, r, arr, sc, _dev_ptr(y, "y"),
+                                   _dtype_code(y), _dev_ptr(workspace, "workspace"),
+                                   workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "lb_linear_from_latent")
+    return y
+
+
 def lb_dense_reference_weight(paths: Sequence[LittleBitPath], d_in: int, d_out: int, r: int, W=None, stream=None):
     """Dense fp32 W_hat [d_out, d_in] from the packed buffers (checking path)."""
     torch = _torch()
@@ -290,5 +355,6 @@ __all__ = [
     "lb_packed_bytes", "lb_bits_per_weight", "lb_rank_for_bpw", "lb_forward_workspace_bytes",
     "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "alloc_workspace", "lb_linear_forward",
     "lb_dense_reference_weight", "lb_linear_desc", "make_descs", "lb_forward_many_workspace_bytes",
-    "lb_linear_forward_many",
+    "lb_linear_forward_many", "lb_latent_workspace_bytes", "lb_from_latent_workspace_bytes", "lb_linear_latent",
+    "lb_linear_from_latent",
 ]

@@ -30,13 +30,15 @@ lb_status check_sizes(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
   return LB_OK;
 }
 
-lb_status check_paths(const lb_path* paths, lb_dtype sc, int64_t d_in, int64_t d_out, int64_t r) {
+// with_l: l is read (every call but the from-latent one)
+lb_status check_paths(const lb_path* paths, lb_dtype sc, int64_t d_in, int64_t d_out, int64_t r,
+                      bool with_l = true) {
   if (!paths) return LB_ERR_NULL;
   const size_t es = dtype_size(sc);
   for (int p = 0; p < 2; ++p) {
     const lb_path& P = paths[p];
     if ((r > 0 && d_out > 0 && !P.U) || (r > 0 && d_in > 0 && !P.V) || (d_out > 0 && !P.h) ||
-        (d_in > 0 && !P.g) || (r > 0 && !P.l))
+        (d_in > 0 && !P.g) || (with_l && r > 0 && !P.l))
       return LB_ERR_NULL;
     if (!aligned(P.U, 4) || !aligned(P.V, 4) || !aligned(P.h, es) || !aligned(P.g, es) || !aligned(P.l, es))
       return LB_ERR_ALIGN;
@@ -357,6 +359,81 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
     off += sb;
   }
   return flush();
+}
+
+size_t lb_latent_workspace_bytes(int64_t T, int64_t d_in, int64_t r) {
+  if (check_sizes(T, d_in, 0, r) != LB_OK || !lb::latent_supports(T, d_in, r)) return 0;
+  return lb::latent_workspace_bytes(static_cast<int>(T), static_cast<int>(d_in), static_cast<int>(r));
+}
+
+lb_status lb_linear_latent(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t r,
+                           const lb_path* paths, lb_dtype scale_dtype, void* w, lb_dtype latent_dtype,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype) || !dtype_ok(latent_dtype)) return LB_ERR_DTYPE;
+  lb_status st = check_sizes(T, d_in, 0, r);
+  if (st != LB_OK) return st;
+  if (!lb::latent_supports(T, d_in, r)) return LB_ERR_SHAPE;
+  if (T == 0 || r == 0) return LB_OK;
+  if (!w || (d_in > 0 && !x)) return LB_ERR_NULL;
+  if (!aligned(x, dtype_size(act_dtype)) || !aligned(w, dtype_size(latent_dtype))) return LB_ERR_ALIGN;
+  if (!paths) return LB_ERR_NULL;
+  // only V, g and l are read
+  lb_path used[2];
+  for (int p = 0; p < 2; ++p) used[p] = lb_path{nullptr, paths[p].V, nullptr, paths[p].g, paths[p].l};
+  st = check_paths(used, scale_dtype, d_in, 0, r);
+  if (st != LB_OK) return st;
+  const size_t nw = static_cast<size_t>(2 * T * r) * dtype_size(latent_dtype);
+  if (overlap(w, nw, x, static_cast<size_t>(T * d_in) * dtype_size(act_dtype))) return LB_ERR_ARG;
+  const size_t need = lb_latent_workspace_bytes(T, d_in, r);
+  if (!workspace) return LB_ERR_NULL;
+  if (!aligned(workspace, 256)) return LB_ERR_ALIGN;
+  if (workspace_bytes < need) return LB_ERR_WORKSPACE;
+  hipError_t e;
+  if (d_in == 0) {
+    // empty reduction: every latent is zero
+    e = lb::launch_zero_elems(w, 2 * T * r, latent_dtype, stream);
+  } else {
+    lb::ForwardArgs a = make_args(x, act_dtype, T, d_in, 0, r, used, scale_dtype, w, workspace, workspace_bytes);
+    e = lb::launch_latent(a, latent_dtype, stream);
+  }
+  return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+}
+
+size_t lb_from_latent_workspace_bytes(int64_t T, int64_t r) {
+  if (check_sizes(T, 0, 0, r) != LB_OK || !lb::from_latent_supports(T, 0, r)) return 0;
+  return lb::from_latent_workspace_bytes(static_cast<int>(T), static_cast<int>(r));
+}
+
+lb_status lb_linear_from_latent(const void* w, lb_dtype latent_dtype, int64_t T, int64_t d_out, int64_t r,
+                                const lb_path* paths, lb_dtype scale_dtype, void* y, lb_dtype out_dtype,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(latent_dtype) || !dtype_ok(scale_dtype) || !dtype_ok(out_dtype)) return LB_ERR_DTYPE;
+  lb_status st = check_sizes(T, 0, d_out, r);
+  if (st != LB_OK) return st;
+  if (!lb::from_latent_supports(T, d_out, r)) return LB_ERR_SHAPE;
+  if (T == 0 || d_out == 0) return LB_OK;
+  if (!y || (r > 0 && !w)) return LB_ERR_NULL;
+  if (!aligned(w, dtype_size(latent_dtype)) || !aligned(y, dtype_size(out_dtype))) return LB_ERR_ALIGN;
+  if (!paths) return LB_ERR_NULL;
+  // only U and h are read
+  lb_path used[2];
+  for (int p = 0; p < 2; ++p) used[p] = lb_path{paths[p].U, nullptr, paths[p].h, nullptr, nullptr};
+  st = check_paths(used, scale_dtype, 0, d_out, r, false);
+  if (st != LB_OK) return st;
+  const size_t ny = static_cast<size_t>(T * d_out) * dtype_size(out_dtype);
+  if (overlap(y, ny, w, static_cast<size_t>(2 * T * r) * dtype_size(latent_dtype))) return LB_ERR_ARG;
+  const size_t need = lb_from_latent_workspace_bytes(T, r);
+  if (!workspace) return LB_ERR_NULL;
+  if (!aligned(workspace, 256)) return LB_ERR_ALIGN;
+  if (workspace_bytes < need) return LB_ERR_WORKSPACE;
+  hipError_t e;
+  if (r == 0) {
+    e = lb::launch_zero_elems(y, T * d_out, out_dtype, stream);
+  } else {
+    lb::ForwardArgs a = make_args(nullptr, out_dtype, T, 0, d_out, r, used, scale_dtype, y, workspace, workspace_bytes);
+    e = lb::launch_from_latent(a, w, latent_dtype, stream);
+  }
+  return e == hipSuccess ? LB_OK : LB_ERR_HIP;
 }
 
 lb_status lb_dense_reference_weight(const lb_path* paths, lb_dtype scale_dtype, int64_t d_in, int64_t d_out,

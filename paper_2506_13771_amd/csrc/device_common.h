@@ -163,6 +163,10 @@ __device__ __forceinline__ void st(void* p, int64_t i, float v) {
   } else if constexpr (DT == kDtBF16) {
     static_cast<uint16_t*>(p)[i] = static_cast<uint16_t>(f32_to_bf16_bits(v));
   } else {
+    // the fp32 value is formed first: without the pin the compiler may fold
+    // the multiply that produced it into a mixed-precision fma that rounds
+    // the exact product to f16 (a different result on fp32 ties)
+    asm volatile("" : "+v"(v));
     static_cast<__half*>(p)[i] = __float2half_rn(v);
   }
 }

@@ -199,6 +199,16 @@ hipError_t launch_decode_mma(const ForwardArgs& a, const MmaGeom& g, hipStream_t
 // dtype (T <= 64 each), each with its own workspace slice, in one launch per
 // group of equal token tiles and load form
 hipError_t launch_decode_mma_batch(const ForwardArgs* a, int n, hipStream_t stream);
+// Latent cache [T][2][r] of dtype lat_dt.  launch_latent runs stage 1 of
+// the prefill kernels on a.x and stores the cache at a.y; launch_from_latent
+// reads the cache `lat` and runs stage 2 into a.y (dtype a.act_dt).  The
+// workspaces hold the stage-1 partial sums / the w terms only.
+bool latent_supports(int64_t T, int64_t d_in, int64_t r);
+bool from_latent_supports(int64_t T, int64_t d_out, int64_t r);
+size_t latent_workspace_bytes(int T, int d_in, int r);
+size_t from_latent_workspace_bytes(int T, int r);
+hipError_t launch_latent(const ForwardArgs& a, int lat_dt, hipStream_t stream);
+hipError_t launch_from_latent(const ForwardArgs& a, const void* lat, int lat_dt, hipStream_t stream);
 hipError_t launch_dense_ref(const ForwardArgs& a, float* W, hipStream_t stream);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 hipError_t launch_zero_elems(void* p, int64_t n, int dt, hipStream_t stream);

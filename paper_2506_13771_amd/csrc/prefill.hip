@@ -86,6 +86,7 @@ struct PrefillParams {
   const void* l[2];
   float* pbuf;      // P1: [ks][token tile][path][ns16p][4 token subtiles][64 lanes][4] partial sums
   uint32_t* wterm;  // [2][NW][nkb][T][4 lane groups] x 16 B: w terms as P2 B fragments
+  void* lat;        // latent cache [T][2][r] (the latent-cache calls only)
   int T, d_in, d_out, r;
   int nkb, ns16;    // 32-latent blocks, 16-latent subtiles per path
   int n_tt, n_lt;   // P1 token tiles, latent tiles
@@ -384,25 +385,39 @@ __global__ void __launch_bounds__(kThreads1, 1) prefill_p1(PrefillParams P) {
 // ---------------------------------------------------------------------------
 // P1b: w = l (.) (sum of the ks partials, ascending) as NW bf16 terms in P2's
 // B-fragment layout wterm[p][term][kbl][t][lane group]; one thread per
-// (pair, token tile, token subtile, P2 lane), so a wave reads 1 KB runs
+// (pair, token tile, token subtile, P2 lane), so a wave reads 1 KB runs.  The
+// latent-cache kernels share its thread mapping: prefill_latent_out stores w
+// itself (the cache), prefill_latent_in cuts a stored w into the terms.
 // ---------------------------------------------------------------------------
-template <int ACT, int SC>
-__global__ void __launch_bounds__(kThreads) prefill_p1b(PrefillParams P) {
-  constexpr int NW = ACT == kDtF32 ? 3 : 2;
+struct PairItem {
+  int t, p, kbl, g4;  // token, path, 32-latent block, lane group
+  int tt, tn, ln;     // P1 token tile, its 16-token subtile, P2 lane
+};
+
+// the item of this thread; false past the last pair or token
+__device__ __forceinline__ bool pair_item(const PrefillParams& P, PairItem& it) {
   const int item = blockIdx.x * kThreads + threadIdx.x;
-  const int ln = item & 63;
-  const int tn = (item >> 6) & 3;
+  it.ln = item & 63;
+  it.tn = (item >> 6) & 3;
   const int rest = item >> 8;
-  const int tt = rest % P.n_tt;
+  it.tt = rest % P.n_tt;
   const int q = rest / P.n_tt;  // (path, 32-latent block)
-  if (q >= 2 * P.nkb) return;
-  const int t = tt * kTok1 + 16 * tn + (ln & 15);
-  if (t >= P.T) return;
-  const int g4 = ln >> 4;
-  const int p = q >= P.nkb ? 1 : 0;
-  const int kbl = q - p * P.nkb;
+  if (q >= 2 * P.nkb) return false;
+  it.t = it.tt * kTok1 + 16 * it.tn + (it.ln & 15);
+  if (it.t >= P.T) return false;
+  it.g4 = it.ln >> 4;
+  it.p = q >= P.nkb ? 1 : 0;
+  it.kbl = q - it.p * P.nkb;
+  return true;
+}
+
+// w0[v] = w of latent 32 kbl + 4 g4 + v and w1[v] of the same + 16 (0 past r):
+// the ks partial sums added in ascending split order, times l
+template <int SC>
+__device__ __forceinline__ void latent_w(const PrefillParams& P, const PairItem& it, float (&w0)[4], float (&w1)[4]) {
   // subtiles 2 kbl (latents 32 kbl + 4 g4 + v) and 2 kbl + 1 (the same + 16)
-  const float* src = P.pbuf + ((static_cast<int64_t>(tt) * 2 + p) * P.ns16p + 2 * kbl) * kPart + tn * 256 + ln * 4;
+  const float* src =
+      P.pbuf + ((static_cast<int64_t>(it.tt) * 2 + it.p) * P.ns16p + 2 * it.kbl) * kPart + it.tn * 256 + it.ln * 4;
   const int64_t kstride = static_cast<int64_t>(P.n_tt) * 2 * P.ns16p * kPart;
   floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0;
 #pragma unroll 8
@@ -412,16 +427,27 @@ __global__ void __launch_bounds__(kThreads) prefill_p1b(PrefillParams P) {
     s1 += *reinterpret_cast<const floatx4*>(sp + kPart);
   }
   const int r = P.r;
-  const rsrc_t lr = make_rsrc(p ? P.l[1] : P.l[0], P.l_bytes);
+  const rsrc_t lr = make_rsrc(it.p ? P.l[1] : P.l[0], P.l_bytes);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int k = 32 * it.kbl + 4 * it.g4 + v;
+    const float a = s0[v] * bits_to_f32<SC>(bload<SC>(lr, k, k < r));
+    const float b = s1[v] * bits_to_f32<SC>(bload<SC>(lr, k + 16, k + 16 < r));
+    w0[v] = k < r ? a : 0.0f;
+    w1[v] = k + 16 < r ? b : 0.0f;
+  }
+}
+
+// w0 / w1 (as from latent_w) cut into NW bf16 terms, stored as P2 B fragments
+template <int NW>
+__device__ __forceinline__ void store_wterm(const PrefillParams& P, const PairItem& it, const float (&w0)[4],
+                                            const float (&w1)[4]) {
   uint32_t lo[NW][4], hi[NW][4];
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
-    const int k = 32 * kbl + 4 * g4 + v;
-    const float w0 = s0[v] * bits_to_f32<SC>(bload<SC>(lr, k, k < r));
-    const float w1 = s1[v] * bits_to_f32<SC>(bload<SC>(lr, k + 16, k + 16 < r));
     uint32_t a[NW], b[NW];
-    split_round<NW>(k < r ? w0 : 0.0f, a);
-    split_round<NW>(k + 16 < r ? w1 : 0.0f, b);
+    split_round<NW>(w0[v], a);
+    split_round<NW>(w1[v], b);
 #pragma unroll
     for (int e = 0; e < NW; ++e) lo[e][v] = a[e], hi[e][v] = b[e];
   }
@@ -430,8 +456,54 @@ __global__ void __launch_bounds__(kThreads) prefill_p1b(PrefillParams P) {
     u32x4 d;
 #pragma unroll
     for (int v = 0; v < 4; ++v) d[v] = lo[e][v] | (hi[e][v] << 16);
-    reinterpret_cast<u32x4*>(P.wterm)[((static_cast<int64_t>(p * NW + e) * P.nkb + kbl) * P.T + t) * 4 + g4] = d;
+    reinterpret_cast<u32x4*>(P.wterm)[((static_cast<int64_t>(it.p * NW + e) * P.nkb + it.kbl) * P.T + it.t) * 4 +
+                                      it.g4] = d;
   }
+}
+
+template <int ACT, int SC>
+__global__ void __launch_bounds__(kThreads) prefill_p1b(PrefillParams P) {
+  constexpr int NW = ACT == kDtF32 ? 3 : 2;
+  PairItem it;
+  if (!pair_item(P, it)) return;
+  float w0[4], w1[4];
+  latent_w<SC>(P, it, w0, w1);
+  store_wterm<NW>(P, it, w0, w1);
+}
+
+// The latent cache [T][2][r] (dtype LD, rounded to nearest even when 16-bit):
+// element (t, p, k) at (2 t + p) r + k
+template <int SC, int LD>
+__global__ void __launch_bounds__(kThreads) prefill_latent_out(PrefillParams P) {
+  PairItem it;
+  if (!pair_item(P, it)) return;
+  float w0[4], w1[4];
+  latent_w<SC>(P, it, w0, w1);
+  const int r = P.r;
+  const int64_t row = (static_cast<int64_t>(it.t) * 2 + it.p) * r;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int k = 32 * it.kbl + 4 * it.g4 + v;
+    if (k < r) st<LD>(P.lat, row + k, w0[v]);
+    if (k + 16 < r) st<LD>(P.lat, row + k + 16, w1[v]);
+  }
+}
+
+template <int ACT, int LD>
+__global__ void __launch_bounds__(kThreads) prefill_latent_in(PrefillParams P) {
+  constexpr int NW = ACT == kDtF32 ? 3 : 2;
+  PairItem it;
+  if (!pair_item(P, it)) return;
+  const int r = P.r;
+  const int64_t row = (static_cast<int64_t>(it.t) * 2 + it.p) * r;
+  float w0[4], w1[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int k = 32 * it.kbl + 4 * it.g4 + v;
+    w0[v] = ld_or0<LD>(P.lat, row + k, k < r);
+    w1[v] = ld_or0<LD>(P.lat, row + k + 16, k + 16 < r);
+  }
+  store_wterm<NW>(P, it, w0, w1);
 }
 
 // ---------------------------------------------------------------------------
@@ -453,6 +525,8 @@ __host__ __device__ constexpr size_t p2_wd_bytes(int pairs, int bufs) {
 template <int DT>
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
   typedef float f2 __attribute__((ext_vector_type(2)));
+  // f16: round the fp32 values themselves (see st<>)
+  if constexpr (DT != kDtBF16) asm volatile("" : "+v"(a), "+v"(b));
   const f2 v = {a, b};
   if constexpr (DT == kDtBF16) {
     typedef __bf16 h2 __attribute__((ext_vector_type(2)));
@@ -791,21 +865,35 @@ hipError_t launch_p2(const PrefillParams& P, const PrefillGeom& g, hipStream_t s
 }
 
 template <int ACT, int SC>
-hipError_t launch_all(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
-  hipError_t e;
+hipError_t launch_p1_ms(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
   switch (g.ms) {
-    case 1: e = launch_p1<1, ACT, SC>(P, g, stream); break;
-    case 2: e = launch_p1<2, ACT, SC>(P, g, stream); break;
-    case 3: e = launch_p1<3, ACT, SC>(P, g, stream); break;
-    case 4: e = launch_p1<4, ACT, SC>(P, g, stream); break;
-    case 5: e = launch_p1<5, ACT, SC>(P, g, stream); break;
-    default: e = launch_p1<kMaxMs, ACT, SC>(P, g, stream); break;
+    case 1: return launch_p1<1, ACT, SC>(P, g, stream);
+    case 2: return launch_p1<2, ACT, SC>(P, g, stream);
+    case 3: return launch_p1<3, ACT, SC>(P, g, stream);
+    case 4: return launch_p1<4, ACT, SC>(P, g, stream);
+    case 5: return launch_p1<5, ACT, SC>(P, g, stream);
+    default: return launch_p1<kMaxMs, ACT, SC>(P, g, stream);
   }
-  if (e != hipSuccess) return e;
+}
+
+// grid of the pair kernels (P1b and the latent-cache kernels)
+dim3 pair_grid(const PrefillParams& P) {
   const int items = 2 * P.nkb * P.n_tt * 256;
-  hipLaunchKernelGGL((prefill_p1b<ACT, SC>), dim3((items + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, P);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return dim3((items + kThreads - 1) / kThreads);
+}
+
+template <int ACT, int SC>
+hipError_t launch_p2_any(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
   return P.fast ? launch_p2<ACT, SC, true>(P, g, stream) : launch_p2<ACT, SC, false>(P, g, stream);
+}
+
+template <int ACT, int SC>
+hipError_t launch_all(const PrefillParams& P, const PrefillGeom& g, hipStream_t stream) {
+  hipError_t e = launch_p1_ms<ACT, SC>(P, g, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((prefill_p1b<ACT, SC>), pair_grid(P), dim3(kThreads), 0, stream, P);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return launch_p2_any<ACT, SC>(P, g, stream);
 }
 
 template <int ACT>
@@ -814,6 +902,50 @@ hipError_t launch_act(const PrefillParams& P, int sc_dt, const PrefillGeom& g, h
     case kDtF32: return launch_all<ACT, kDtF32>(P, g, stream);
     case kDtF16: return launch_all<ACT, kDtF16>(P, g, stream);
     default: return launch_all<ACT, kDtBF16>(P, g, stream);
+  }
+}
+
+// latent call: P1, then the cache store
+template <int ACT, int SC>
+hipError_t launch_latent_typed(const PrefillParams& P, int lat_dt, const PrefillGeom& g, hipStream_t stream) {
+  hipError_t e = launch_p1_ms<ACT, SC>(P, g, stream);
+  if (e != hipSuccess) return e;
+  switch (lat_dt) {
+    case kDtF32: hipLaunchKernelGGL((prefill_latent_out<SC, kDtF32>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
+    case kDtF16: hipLaunchKernelGGL((prefill_latent_out<SC, kDtF16>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
+    default: hipLaunchKernelGGL((prefill_latent_out<SC, kDtBF16>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
+  }
+  return hipGetLastError();
+}
+template <int ACT>
+hipError_t launch_latent_act(const PrefillParams& P, int sc_dt, int lat_dt, const PrefillGeom& g,
+                             hipStream_t stream) {
+  switch (sc_dt) {
+    case kDtF32: return launch_latent_typed<ACT, kDtF32>(P, lat_dt, g, stream);
+    case kDtF16: return launch_latent_typed<ACT, kDtF16>(P, lat_dt, g, stream);
+    default: return launch_latent_typed<ACT, kDtBF16>(P, lat_dt, g, stream);
+  }
+}
+
+// from-latent call: the cache cut into w terms, then P2
+template <int ACT, int SC>
+hipError_t launch_from_latent_typed(const PrefillParams& P, int lat_dt, const PrefillGeom& g, hipStream_t stream) {
+  switch (lat_dt) {
+    case kDtF32: hipLaunchKernelGGL((prefill_latent_in<ACT, kDtF32>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
+    case kDtF16: hipLaunchKernelGGL((prefill_latent_in<ACT, kDtF16>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
+    default: hipLaunchKernelGGL((prefill_latent_in<ACT, kDtBF16>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
+  }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_p2_any<ACT, SC>(P, g, stream);
+}
+template <int ACT>
+hipError_t launch_from_latent_act(const PrefillParams& P, int sc_dt, int lat_dt, const PrefillGeom& g,
+                                  hipStream_t stream) {
+  switch (sc_dt) {
+    case kDtF32: return launch_from_latent_typed<ACT, kDtF32>(P, lat_dt, g, stream);
+    case kDtF16: return launch_from_latent_typed<ACT, kDtF16>(P, lat_dt, g, stream);
+    default: return launch_from_latent_typed<ACT, kDtBF16>(P, lat_dt, g, stream);
   }
 }
 
@@ -906,7 +1038,11 @@ bool prefill_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
          packed_bytes(r, d_in) < lim && static_cast<int64_t>(g.wterm_bytes) < lim;
 }
 
-hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g0, hipStream_t stream) {
+namespace {
+
+// The kernels' parameters for a.  The workspace holds the P1 partial sums at
+// pbuf_off and the w terms at wterm_off of g.
+PrefillParams prefill_params(const ForwardArgs& a, PrefillGeom& g) {
   const int64_t ex = a.act_dt == kDtF32 ? 4 : 2, es = a.sc_dt == kDtF32 ? 4 : 2;
   auto al = [](const void* q, int64_t n) { return reinterpret_cast<uintptr_t>(q) % n == 0; };
   // 16-byte V-word loads: whole 4-word groups per latent block row
@@ -914,7 +1050,6 @@ hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g0, hipStream
   // P2 fast path: whole 4-output groups, 16-byte aligned U words, aligned h and y
   const bool fast = a.d_out % 4 == 0 && al(a.U[0], 16) && al(a.U[1], 16) && al(a.h[0], 4 * es) &&
                     al(a.h[1], 4 * es) && al(a.y, 4 * ex);
-  PrefillGeom g = g0;
   plan_lds(g, a.act_dt, a.sc_dt, vw, fast);
   PrefillParams P{};
   P.x = a.x;
@@ -958,10 +1093,63 @@ hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g0, hipStream
   const int nw = a.act_dt == kDtF32 ? 3 : 2;
   P.wt_bytes = static_cast<uint32_t>(static_cast<int64_t>(2) * nw * g.nkb * a.T * 64);
   P.wd_off = static_cast<uint32_t>(p2_w_bytes(g.res ? 2 * g.nkb : g.kbc, nw));
+  return P;
+}
+
+// d_in that gives the smallest stage-1 plan (the from-latent call has no stage 1)
+constexpr int kNoStage1 = 32;
+
+}  // namespace
+
+hipError_t launch_prefill(const ForwardArgs& a, const PrefillGeom& g0, hipStream_t stream) {
+  PrefillGeom g = g0;
+  const PrefillParams P = prefill_params(a, g);
   switch (a.act_dt) {
     case kDtF32: return launch_act<kDtF32>(P, a.sc_dt, g, stream);
     case kDtF16: return launch_act<kDtF16>(P, a.sc_dt, g, stream);
     default: return launch_act<kDtBF16>(P, a.sc_dt, g, stream);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// latent cache
+// ---------------------------------------------------------------------------
+bool latent_supports(int64_t T, int64_t d_in, int64_t r) { return prefill_supports(T, d_in, 0, r); }
+
+bool from_latent_supports(int64_t T, int64_t d_out, int64_t r) {
+  return prefill_supports(T, kNoStage1, d_out, r);
+}
+
+size_t latent_workspace_bytes(int T, int d_in, int r) {
+  const PrefillGeom g = prefill_geometry(T, d_in, 0, r);
+  return g.pbuf_off + align256(4 * g.pbuf_floats);
+}
+
+size_t from_latent_workspace_bytes(int T, int r) {
+  const PrefillGeom g = prefill_geometry(T, kNoStage1, 0, r);
+  return kCtrlBytes + align256(g.wterm_bytes);
+}
+
+hipError_t launch_latent(const ForwardArgs& a, int lat_dt, hipStream_t stream) {
+  PrefillGeom g = prefill_geometry(a.T, a.d_in, 0, a.r);
+  PrefillParams P = prefill_params(a, g);
+  P.lat = a.y;
+  switch (a.act_dt) {
+    case kDtF32: return launch_latent_act<kDtF32>(P, a.sc_dt, lat_dt, g, stream);
+    case kDtF16: return launch_latent_act<kDtF16>(P, a.sc_dt, lat_dt, g, stream);
+    default: return launch_latent_act<kDtBF16>(P, a.sc_dt, lat_dt, g, stream);
+  }
+}
+
+hipError_t launch_from_latent(const ForwardArgs& a, const void* lat, int lat_dt, hipStream_t stream) {
+  PrefillGeom g = prefill_geometry(a.T, kNoStage1, a.d_out, a.r);
+  g.wterm_off = kCtrlBytes;  // no partial sums
+  PrefillParams P = prefill_params(a, g);
+  P.lat = const_cast<void*>(lat);
+  switch (a.act_dt) {
+    case kDtF32: return launch_from_latent_act<kDtF32>(P, a.sc_dt, lat_dt, g, stream);
+    case kDtF16: return launch_from_latent_act<kDtF16>(P, a.sc_dt, lat_dt, g, stream);
+    default: return launch_from_latent_act<kDtBF16>(P, a.sc_dt, lat_dt, g, stream);
   }
 }
 

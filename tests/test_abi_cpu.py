@@ -241,3 +241,88 @@ def test_many_validation_errors(lib):
     assert call(ok2, ws=FAKE * 64 + 128, ws_bytes=1 << 30) == lb.LB_ERR_ALIGN
     # empty linears need no work and no GPU
     assert call([_desc(T=0), _desc(d_out=0, y=y2)], ws_bytes=1 << 20) == lb.LB_OK
+
+
+# ---------------------------------------------------------------------------
+# latent cache calls (validation only; the GPU parity tests run them)
+# ---------------------------------------------------------------------------
+FAR = FAKE * 16  # a second aligned address, far from FAKE
+
+
+def _lat(lib, x=FAKE, act=lb.LB_BF16, T=4, d_in=64, r=16, paths=None, sc=lb.LB_F16, w=FAR, ld=lb.LB_F32,
+         ws=FAKE * 64, ws_bytes=None):
+    if paths is None:
+        paths = _paths(U=0, h=0)  # U and h are not read
+    if ws_bytes is None:
+        ws_bytes = lb.lb_latent_workspace_bytes(max(T, 0), max(d_in, 0), max(r, 0)) - 1
+    return lib.lb_linear_latent(x, act, T, d_in, r, paths, sc, w, ld, ws, ws_bytes, None)
+
+
+def _from(lib, w=FAKE, ld=lb.LB_F32, T=4, d_out=64, r=16, paths=None, sc=lb.LB_F16, y=FAR, out=lb.LB_BF16,
+          ws=FAKE * 64, ws_bytes=None):
+    if paths is None:
+        paths = _paths(V=0, g=0, l=0)  # V, g and l are not read
+    if ws_bytes is None:
+        ws_bytes = lb.lb_from_latent_workspace_bytes(max(T, 0), max(r, 0)) - 1
+    return lib.lb_linear_from_latent(w, ld, T, d_out, r, paths, sc, y, out, ws, ws_bytes, None)
+
+
+def test_latent_workspace_sizes(lib):
+    for T, d_in, r in [(1, 4096, 80), (2048, 5120, 96), (64, 11008, 800), (3, 33, 5)]:
+        n = lb.lb_latent_workspace_bytes(T, d_in, r)
+        # at least one fp32 partial per latent, token and path
+        assert n % 256 == 0 and n >= 2 * T * r * 4
+        m = lb.lb_from_latent_workspace_bytes(T, r)
+        # the w terms: up to three bf16 terms per latent, token and path (32-latent blocks)
+        assert m % 256 == 0 and m >= 2 * 3 * 2 * T * 32 * ((r + 31) // 32)
+    assert lb.lb_latent_workspace_bytes(-1, 4, 4) == 0
+    assert lb.lb_from_latent_workspace_bytes(4, -1) == 0
+
+
+def test_latent_validation_errors(lib):
+    assert _lat(lib) == lb.LB_ERR_WORKSPACE
+    assert _lat(lib, act=5) == lb.LB_ERR_DTYPE
+    assert _lat(lib, sc=5) == lb.LB_ERR_DTYPE
+    assert _lat(lib, ld=3) == lb.LB_ERR_DTYPE
+    assert _lat(lib, T=-1) == lb.LB_ERR_SHAPE
+    assert _lat(lib, r=-2) == lb.LB_ERR_SHAPE
+    assert _lat(lib, T=1 << 20, d_in=1 << 12) == lb.LB_ERR_SHAPE
+    assert _lat(lib, x=0) == lb.LB_ERR_NULL
+    assert _lat(lib, w=0) == lb.LB_ERR_NULL
+    assert _lat(lib, x=FAKE + 1) == lb.LB_ERR_ALIGN
+    assert _lat(lib, w=FAR + 2) == lb.LB_ERR_ALIGN
+    assert _lat(lib, w=FAR + 2, ld=lb.LB_BF16) == lb.LB_ERR_WORKSPACE
+    assert _lat(lib, paths=_paths(U=0, h=0, V=0)) == lb.LB_ERR_NULL
+    assert _lat(lib, paths=_paths(U=0, h=0, l=0)) == lb.LB_ERR_NULL
+    assert _lat(lib, paths=_paths(U=0, h=0, g=FAKE + 1)) == lb.LB_ERR_ALIGN
+    # U and h are not read, so not checked either
+    assert _lat(lib, paths=_paths(U=FAKE + 1, h=FAKE + 1)) == lb.LB_ERR_WORKSPACE
+    assert lib.lb_linear_latent(FAKE, lb.LB_BF16, 4, 64, 16, None, lb.LB_F16, FAR, lb.LB_F32, FAKE * 64, 1 << 30,
+                                None) == lb.LB_ERR_NULL
+    assert _lat(lib, w=FAKE + 256) == lb.LB_ERR_ARG  # w overlaps x
+    assert _lat(lib, ws=0) == lb.LB_ERR_NULL
+    assert _lat(lib, ws=FAKE * 64 + 16, ws_bytes=1 << 30) == lb.LB_ERR_ALIGN
+    assert _lat(lib, T=0) == lb.LB_OK
+    assert _lat(lib, r=0) == lb.LB_OK
+
+
+def test_from_latent_validation_errors(lib):
+    assert _from(lib) == lb.LB_ERR_WORKSPACE
+    assert _from(lib, ld=9) == lb.LB_ERR_DTYPE
+    assert _from(lib, out=9) == lb.LB_ERR_DTYPE
+    assert _from(lib, sc=9) == lb.LB_ERR_DTYPE
+    assert _from(lib, d_out=-1) == lb.LB_ERR_SHAPE
+    assert _from(lib, T=1 << 20, d_out=1 << 12) == lb.LB_ERR_SHAPE
+    assert _from(lib, w=0) == lb.LB_ERR_NULL
+    assert _from(lib, y=0) == lb.LB_ERR_NULL
+    assert _from(lib, w=FAKE + 2) == lb.LB_ERR_ALIGN
+    assert _from(lib, y=FAR + 1) == lb.LB_ERR_ALIGN
+    assert _from(lib, paths=_paths(V=0, g=0, l=0, U=0)) == lb.LB_ERR_NULL
+    assert _from(lib, paths=_paths(V=0, g=0, l=0, h=0)) == lb.LB_ERR_NULL
+    assert _from(lib, paths=_paths(V=0, g=0, l=0, U=FAKE + 2)) == lb.LB_ERR_ALIGN
+    # V, g and l are not read, so not checked either
+    assert _from(lib, paths=_paths(V=FAKE + 1, g=FAKE + 1, l=FAKE + 1)) == lb.LB_ERR_WORKSPACE
+    assert _from(lib, y=FAKE + 128) == lb.LB_ERR_ARG  # y overlaps w
+    assert _from(lib, ws=0) == lb.LB_ERR_NULL
+    assert _from(lib, T=0) == lb.LB_OK
+    assert _from(lib, d_out=0) == lb.LB_OK
