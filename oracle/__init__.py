@@ -20,6 +20,12 @@ Functions and the passages of arXiv 2506.13771 they follow:
   dense_weight (O2)        Eqs. (w_primary_hat), (res_approx_structure),
                            (final_weight_approx_res);
   dense_forward (O2)       Y = X W_hat^T, the left side of Proposition 1;
+  latent / from_latent     the rank-r latent cache and the output from it,
+  (O5)                     Sec. "Analysis", paragraph "KV Cache Compression";
+  backward (O6)            the chain rule through Proposition 1 with the
+                           SmoothSign surrogate for the sign's derivative,
+                           Sec. 4 "Training Details" and Appendix "SmoothSign
+                           versus Straight-Through Estimator";
   bpw / rank_real /
   rank_for_bpw             Appendix "Average Bits Per Weight Calculation",
                            Eqs. (b_calculation) and (r_calculation).
@@ -74,6 +80,9 @@ def _load():
         lib.lbo_latent.argtypes = [vp, i64, i64, i64, vp, vp, vp, i32, vp]
         lib.lbo_from_latent.restype = None
         lib.lbo_from_latent.argtypes = [vp, i64, i64, i64, vp, vp, i32, vp]
+        lib.lbo_backward.restype = None
+        lib.lbo_backward.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, i32, f64, vp, vp, vp, vp,
+                                     vp, vp]
         lib.lbo_dense_weight.restype = None
         lib.lbo_dense_weight.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, i32, vp]
         lib.lbo_dense_forward.restype = None
@@ -199,6 +208,36 @@ def from_latent(w, U, h) -> np.ndarray:
     y = np.empty((T, d_out), dtype=np.float64)
     _load().lbo_from_latent(_p(w), T, d_out, r, _ptr_array(U), _ptr_array(h), n, _p(y))
     return y
+
+
+SMOOTHSIGN_K = 100.0  # the tanh slope of SmoothSign (Sec. 4 "Training Details")
+
+
+def backward(x, dy, U_lat, V_lat, h, g, l, kappa: float = SMOOTHSIGN_K) -> dict:
+    """O6.  Gradients of a loss with upstream gradient dy [T, d_out] for x [T, d_in] through both
+    paths, the signs taken of the real latent factors U_lat [d_out, r] and V_lat [d_in, r], the
+    sign's derivative replaced by that of tanh(kappa u).  Returns dx and per-path lists dU, dV,
+    dh, dg, dl (fp64)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    dy = np.ascontiguousarray(dy, dtype=np.float64)
+    U_lat = [np.ascontiguousarray(a, dtype=np.float64) for a in U_lat]
+    V_lat = [np.ascontiguousarray(a, dtype=np.float64) for a in V_lat]
+    h = [np.ascontiguousarray(a, dtype=np.float64) for a in h]
+    g = [np.ascontiguousarray(a, dtype=np.float64) for a in g]
+    l = [np.ascontiguousarray(a, dtype=np.float64) for a in l]
+    n = len(U_lat)
+    T, d_in = x.shape
+    d_out, r = U_lat[0].shape
+    dx = np.empty((T, d_in))
+    dU = [np.empty((d_out, r)) for _ in range(n)]
+    dV = [np.empty((d_in, r)) for _ in range(n)]
+    dh = [np.empty(d_out) for _ in range(n)]
+    dg = [np.empty(d_in) for _ in range(n)]
+    dl = [np.empty(r) for _ in range(n)]
+    _load().lbo_backward(_p(x), _p(dy), T, d_in, d_out, r, _ptr_array(U_lat), _ptr_array(V_lat), _ptr_array(h),
+                         _ptr_array(g), _ptr_array(l), n, float(kappa), _p(dx), _ptr_array(dU), _ptr_array(dV),
+                         _ptr_array(dh), _ptr_array(dg), _ptr_array(dl))
+    return {"dx": dx, "dU": dU, "dV": dV, "dh": dh, "dg": dg, "dl": dl}
 
 
 def forward_sampled(x, U, V, h, g, l, ts, is_) -> np.ndarray:

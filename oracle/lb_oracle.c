@@ -18,6 +18,10 @@
  *     Sec. 3.3, Eqs. (res_approx_structure) and (final_weight_approx_res);
  *   - the rank-r latent that replaces keys and values in the cache, and the
  *     forward from it: Sec. "Analysis", paragraph "KV Cache Compression";
+ *   - the backward of the layer for quantization-aware training with the
+ *     SmoothSign surrogate (the derivative of tanh(100 u) for that of the
+ *     sign): Sec. 4 "Training Details", Appendix "SmoothSign versus
+ *     Straight-Through Estimator";
  *   - the bits-per-weight accounting and its inversion for the rank:
  *     Appendix "Average Bits Per Weight Calculation", Eqs. (b_calculation)
  *     and (r_calculation);
@@ -231,6 +235,100 @@ void lbo_from_latent(const double* w, int64_t T, int64_t d_out, int64_t r, const
       }
     }
   }
+}
+
+/* O6: the backward of one layer for quantization-aware training (Sec. 4
+   "Training Details"; Appendix "SmoothSign versus Straight-Through
+   Estimator").  For a loss L with upstream gradient dy = dL/dy [T x d_out],
+   the chain rule through the steps of Proposition 1 (Eq. proposition1), path
+   by path, token by token (ascending t), with the sign taken as in the
+   forward (R1) and its derivative replaced by that of tanh(kappa u) (the
+   paper's SmoothSign, kappa = 100):
+     a = x (.) g ; z = a V_s ; w = z (.) l ; u = w U_s^T           (forward)
+     dh     += dy (.) u
+     du      = dy (.) h
+     dU_s   += du^T w          (outer product, d_out x r)
+     dw      = du U_s
+     dl     += dw (.) z
+     dz      = dw (.) l
+     dV_s   += a^T dz          (d_in x r)
+     da      = dz V_s^T
+     dg     += da (.) x
+     dx     += da (.) g        (summed over the paths)
+   and finally dU = dU_s (.) kappa (1 - tanh^2(kappa U_latent)), likewise dV.
+   U_lat, V_lat are the real latent factors [d_out x r], [d_in x r] whose
+   signs the forward uses.  Outputs: dx [T x d_in], and per path dU [d_out x r],
+   dV [d_in x r], dh [d_out], dg [d_in], dl [r]. */
+void lbo_backward(const double* x, const double* dy, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                  const double* const* U_lat, const double* const* V_lat, const double* const* h,
+                  const double* const* g, const double* const* l, int npaths, double kappa, double* dx,
+                  double* const* dU, double* const* dV, double* const* dh, double* const* dg,
+                  double* const* dl) {
+  double* a = (double*)malloc(sizeof(double) * (size_t)(d_in > 0 ? d_in : 1));
+  double* z = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+  double* w = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+  double* du = (double*)malloc(sizeof(double) * (size_t)(d_out > 0 ? d_out : 1));
+  double* dw = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+  double* dz = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+  for (int64_t i = 0; i < T * d_in; i++) dx[i] = 0.0;
+  for (int p = 0; p < npaths; p++) {
+    const double* Ul = U_lat[p];
+    const double* Vl = V_lat[p];
+    for (int64_t i = 0; i < d_out * r; i++) dU[p][i] = 0.0;
+    for (int64_t j = 0; j < d_in * r; j++) dV[p][j] = 0.0;
+    for (int64_t i = 0; i < d_out; i++) dh[p][i] = 0.0;
+    for (int64_t j = 0; j < d_in; j++) dg[p][j] = 0.0;
+    for (int64_t k = 0; k < r; k++) dl[p][k] = 0.0;
+    for (int64_t t = 0; t < T; t++) {
+      const double* xt = x + t * d_in;
+      const double* dyt = dy + t * d_out;
+      for (int64_t j = 0; j < d_in; j++) a[j] = xt[j] * g[p][j];
+      for (int64_t k = 0; k < r; k++) {
+        double s = 0.0;
+        for (int64_t j = 0; j < d_in; j++) s += (lbo_is_negative(Vl[j * r + k]) ? -1.0 : 1.0) * a[j];
+        z[k] = s;
+        w[k] = s * l[p][k];
+      }
+      for (int64_t i = 0; i < d_out; i++) {
+        double u = 0.0;
+        for (int64_t k = 0; k < r; k++) u += (lbo_is_negative(Ul[i * r + k]) ? -1.0 : 1.0) * w[k];
+        dh[p][i] += dyt[i] * u;
+        du[i] = dyt[i] * h[p][i];
+      }
+      for (int64_t i = 0; i < d_out; i++)
+        for (int64_t k = 0; k < r; k++) dU[p][i * r + k] += du[i] * w[k];
+      for (int64_t k = 0; k < r; k++) {
+        double s = 0.0;
+        for (int64_t i = 0; i < d_out; i++) s += (lbo_is_negative(Ul[i * r + k]) ? -1.0 : 1.0) * du[i];
+        dw[k] = s;
+        dl[p][k] += s * z[k];
+        dz[k] = s * l[p][k];
+      }
+      for (int64_t j = 0; j < d_in; j++)
+        for (int64_t k = 0; k < r; k++) dV[p][j * r + k] += a[j] * dz[k];
+      for (int64_t j = 0; j < d_in; j++) {
+        double s = 0.0;
+        for (int64_t k = 0; k < r; k++) s += (lbo_is_negative(Vl[j * r + k]) ? -1.0 : 1.0) * dz[k];
+        dg[p][j] += s * xt[j];
+        dx[t * d_in + j] += s * g[p][j];
+      }
+    }
+    /* SmoothSign: the derivative of tanh(kappa u) in place of that of sign(u) */
+    for (int64_t i = 0; i < d_out * r; i++) {
+      const double th = tanh(kappa * Ul[i]);
+      dU[p][i] *= kappa * (1.0 - th * th);
+    }
+    for (int64_t j = 0; j < d_in * r; j++) {
+      const double th = tanh(kappa * Vl[j]);
+      dV[p][j] *= kappa * (1.0 - th * th);
+    }
+  }
+  free(a);
+  free(z);
+  free(w);
+  free(du);
+  free(dw);
+  free(dz);
 }
 
 /* Same as lbo_forward_factored but only for the listed (t, i) output

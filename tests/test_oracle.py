@@ -434,6 +434,140 @@ def test_to_f64_exact():
 
 
 # ---------------------------------------------------------------------------
+# the backward (O6): the dense route of the same loss, finite differences,
+# linearity, the SmoothSign factor
+# ---------------------------------------------------------------------------
+def _rand_train_layer(rs, T, d_in, d_out, r, lat_scale=0.02):
+    """Real latent factors (of the order of 1 / kappa, so the surrogate factor varies), scales of
+    both signs, x and an upstream gradient dy."""
+    U_lat = [lat_scale * rs.standard_normal((d_out, r)) for _ in range(2)]
+    V_lat = [lat_scale * rs.standard_normal((d_in, r)) for _ in range(2)]
+    h = [rs.standard_normal(d_out) for _ in range(2)]
+    g = [rs.standard_normal(d_in) for _ in range(2)]
+    l = [rs.standard_normal(r) for _ in range(2)]
+    x = rs.standard_normal((T, d_in))
+    dy = rs.standard_normal((T, d_out))
+    return x, dy, U_lat, V_lat, h, g, l
+
+
+def _signs(a):
+    return np.where(a < 0, -1, 1).astype(np.int8)
+
+
+def _tanh_slope_fd(u, kappa, eps=1e-7):
+    """d/du tanh(kappa u) by central differences of numpy's tanh."""
+    return (np.tanh(kappa * (u + eps)) - np.tanh(kappa * (u - eps))) / (2 * eps)
+
+
+def _dense_route(x, dy, U_lat, V_lat, h, g, l, kappa):
+    """Gradients of L = sum(dy * (x W_hat^T)) from the dense weight: with G = dy^T x, L = sum(G * W_hat)
+    and W_hat = sum_p diag(h_p) U_p diag(l_p) V_p^T diag(g_p), so every gradient is a contraction of G
+    with the other factors (numpy matrix products), then the SmoothSign slope from finite differences."""
+    U = [_signs(a) for a in U_lat]
+    V = [_signs(a) for a in V_lat]
+    G = dy.T @ x
+    out = {"dx": dy @ O.dense_weight(U, V, h, g, l), "dU": [], "dV": [], "dh": [], "dg": [], "dl": []}
+    for p in range(2):
+        Us, Vs = U[p].astype(np.float64), V[p].astype(np.float64)
+        core = (Us * l[p]) @ Vs.T  # U diag(l) V^T
+        out["dh"].append((G * core * g[p][None, :]).sum(axis=1))
+        out["dg"].append((G * core * h[p][:, None]).sum(axis=0))
+        out["dl"].append(np.einsum("ij,ik,jk->k", G, h[p][:, None] * Us, g[p][:, None] * Vs))
+        dUs = h[p][:, None] * ((G * g[p][None, :]) @ Vs) * l[p][None, :]
+        dVs = g[p][:, None] * ((G.T * h[p][None, :]) @ Us) * l[p][None, :]
+        out["dU"].append(dUs * _tanh_slope_fd(U_lat[p], kappa))
+        out["dV"].append(dVs * _tanh_slope_fd(V_lat[p], kappa))
+    return out
+
+
+def _close(a, b, rtol):
+    return np.allclose(a, b, rtol=rtol, atol=rtol * max(1.0, np.abs(b).max()))
+
+
+@pytest.mark.parametrize("T,d_in,d_out,r", [(3, 9, 7, 5), (1, 33, 17, 16), (4, 5, 40, 1), (2, 64, 32, 33)])
+def test_backward_matches_the_dense_route(T, d_in, d_out, r):
+    rs = np.random.default_rng(T * 1000 + d_in + r)
+    args = _rand_train_layer(rs, T, d_in, d_out, r)
+    got = O.backward(*args)
+    ref = _dense_route(*args, kappa=O.SMOOTHSIGN_K)
+    assert _close(got["dx"], ref["dx"], 1e-11)
+    for key in ("dh", "dg", "dl"):
+        for p in range(2):
+            assert _close(got[key][p], ref[key][p], 1e-11), (key, p)
+    for key in ("dU", "dV"):
+        for p in range(2):
+            assert _close(got[key][p], ref[key][p], 1e-6), (key, p)  # finite-difference slope
+
+
+def test_backward_finite_differences():
+    """L is linear in each of x, h_p, g_p, l_p, so a central difference along any direction is the
+    directional derivative up to rounding."""
+    rs = np.random.default_rng(41)
+    x, dy, U_lat, V_lat, h, g, l = _rand_train_layer(rs, 3, 12, 10, 6)
+    U, V = [_signs(a) for a in U_lat], [_signs(a) for a in V_lat]
+    got = O.backward(x, dy, U_lat, V_lat, h, g, l)
+
+    def loss(x_, h_, g_, l_):
+        return float((dy * O.forward_factored(x_, U, V, h_, g_, l_)).sum())
+
+    eps = 1e-3
+    d = rs.standard_normal(x.shape)
+    fd = (loss(x + eps * d, h, g, l) - loss(x - eps * d, h, g, l)) / (2 * eps)
+    assert abs(fd - (got["dx"] * d).sum()) <= 1e-9 * (1 + abs(fd))
+    for p in range(2):
+        for name, vecs, key in (("h", h, "dh"), ("g", g, "dg"), ("l", l, "dl")):
+            dv = rs.standard_normal(vecs[p].shape)
+            plus = [v.copy() for v in vecs]
+            minus = [v.copy() for v in vecs]
+            plus[p] += eps * dv
+            minus[p] -= eps * dv
+            argsp = {"h": h, "g": g, "l": l}
+            argsm = dict(argsp)
+            argsp[name], argsm[name] = plus, minus
+            fd = (loss(x, argsp["h"], argsp["g"], argsp["l"]) - loss(x, argsm["h"], argsm["g"], argsm["l"])) / (2 * eps)
+            assert abs(fd - (got[key][p] * dv).sum()) <= 1e-9 * (1 + abs(fd)), (name, p)
+
+
+def test_backward_linear_in_dy_and_zero_for_zero_dy():
+    rs = np.random.default_rng(42)
+    x, dy, U_lat, V_lat, h, g, l = _rand_train_layer(rs, 2, 16, 12, 8)
+    dy2 = rs.standard_normal(dy.shape)
+    a = O.backward(x, dy, U_lat, V_lat, h, g, l)
+    b = O.backward(x, dy2, U_lat, V_lat, h, g, l)
+    c = O.backward(x, dy + dy2, U_lat, V_lat, h, g, l)
+    assert _close(c["dx"], a["dx"] + b["dx"], 1e-12)
+    for key in ("dU", "dV", "dh", "dg", "dl"):
+        for p in range(2):
+            assert _close(c[key][p], a[key][p] + b[key][p], 1e-12), key
+    z = O.backward(x, np.zeros_like(dy), U_lat, V_lat, h, g, l)
+    assert not z["dx"].any() and not any(z[k][p].any() for k in ("dU", "dV", "dh", "dg", "dl") for p in range(2))
+
+
+def test_backward_smoothsign_factor():
+    """At u = 0 the surrogate slope is kappa; far from 0 it vanishes; the sign itself follows the
+    forward's convention (u = 0 counts as +1, so flipping the sign of a zero latent changes nothing)."""
+    rs = np.random.default_rng(43)
+    x, dy, U_lat, V_lat, h, g, l = _rand_train_layer(rs, 2, 10, 8, 4)
+    for A in U_lat + V_lat:
+        A[0, :] = 0.0
+        A[1, :] = 1.0  # kappa u = 100: slope below 1e-80
+    for kappa in (100.0, 7.0):
+        got = O.backward(x, dy, U_lat, V_lat, h, g, l, kappa=kappa)
+        ref = _dense_route(x, dy, U_lat, V_lat, h, g, l, kappa=1.0)  # slope(0) = 1 for kappa = 1 ...
+        for p in range(2):
+            # ... so at u = 0 the dense-route value is the sign gradient itself
+            assert _close(got["dU"][p][0], kappa * ref["dU"][p][0], 1e-6)
+            assert _close(got["dV"][p][0], kappa * ref["dV"][p][0], 1e-6)
+        if kappa == 100.0:
+            assert all(np.abs(got[k][p][1]).max() < 1e-60 for k in ("dU", "dV") for p in range(2))
+    U2 = [a.copy() for a in U_lat]
+    U2[0][0, :] = -0.0
+    a = O.backward(x, dy, U_lat, V_lat, h, g, l)
+    b = O.backward(x, dy, U2, V_lat, h, g, l)
+    assert np.array_equal(a["dx"], b["dx"])
+
+
+# ---------------------------------------------------------------------------
 # the pins catch planted mistakes (mutations are applied to a copy of the oracle
 # source on the CPU; the real oracle is never modified)
 # ---------------------------------------------------------------------------
@@ -452,6 +586,13 @@ MUTANTS = [
     ("from latent: wrong path", "U[p][i * r + k] * w[(p * T + t) * r + k];", "U[p][i * r + k] * w[(0 * T + t) * r + k];"),
     ("from latent: dropped row scale", "        y[t * d_out + i] += s * h[p][i];\n      }\n    }\n  }\n}",
      "        y[t * d_out + i] += s;\n      }\n    }\n  }\n}"),
+    ("backward: dropped row scale", "du[i] = dyt[i] * h[p][i];", "du[i] = dyt[i];"),
+    ("backward: dropped latent scale in dz", "dz[k] = s * l[p][k];", "dz[k] = s;"),
+    ("backward: dl from w", "dl[p][k] += s * z[k];", "dl[p][k] += s * w[k];"),
+    ("backward: dg from a", "dg[p][j] += s * xt[j];", "dg[p][j] += s * a[j];"),
+    ("backward: surrogate sign", "dU[p][i] *= kappa * (1.0 - th * th);", "dU[p][i] *= kappa * (1.0 + th * th);"),
+    ("backward: transposed dV", "dV[p][j * r + k] += a[j] * dz[k];", "dV[p][j * r + k] += a[j] * dz[(k + 1) % r];"),
+    ("backward: dx misses g", "dx[t * d_in + j] += s * g[p][j];", "dx[t * d_in + j] += s;"),
 ]
 
 
@@ -495,7 +636,26 @@ def _checks_fail_for(lib_path):
     y2 = np.empty((T, d_out))
     lib.lbo_from_latent(w.ctypes.data, T, d_out, r, pU, ph, 2, y2.ctypes.data)
     ok_latent = np.allclose(y2, O.dense_forward(x, O.dense_weight(U, V, h, g, l)), rtol=1e-12, atol=1e-12)
-    return not (ok_dense and ok_tiny and ok_latent)
+    # the backward against the dense route
+    lib.lbo_backward.argtypes = [vp, vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, ctypes.c_int, ctypes.c_double,
+                                 vp, vp, vp, vp, vp, vp]
+    lib.lbo_backward.restype = None
+    args = _rand_train_layer(np.random.default_rng(98), 3, 9, 7, 5)
+    xb, dyb, Ul, Vl, hb, gb, lb_ = [a if isinstance(a, list) else np.ascontiguousarray(a) for a in args]
+    T, d_in = xb.shape
+    d_out, r = Ul[0].shape
+    outs = {"dU": [np.empty((d_out, r)) for _ in range(2)], "dV": [np.empty((d_in, r)) for _ in range(2)],
+            "dh": [np.empty(d_out) for _ in range(2)], "dg": [np.empty(d_in) for _ in range(2)],
+            "dl": [np.empty(r) for _ in range(2)]}
+    dxb = np.empty((T, d_in))
+    pp = lambda A: (ctypes.c_void_p * len(A))(*[np.ascontiguousarray(a).ctypes.data for a in A])
+    lib.lbo_backward(xb.ctypes.data, dyb.ctypes.data, T, d_in, d_out, r, pp(Ul), pp(Vl), pp(hb), pp(gb), pp(lb_),
+                     2, O.SMOOTHSIGN_K, dxb.ctypes.data, pp(outs["dU"]), pp(outs["dV"]), pp(outs["dh"]),
+                     pp(outs["dg"]), pp(outs["dl"]))
+    ref = _dense_route(*args, kappa=O.SMOOTHSIGN_K)
+    ok_bwd = _close(dxb, ref["dx"], 1e-11) and all(
+        _close(outs[k][p], ref[k][p], 1e-6) for k in outs for p in range(2))
+    return not (ok_dense and ok_tiny and ok_latent and ok_bwd)
 
 
 @pytest.mark.parametrize("desc,orig,repl", MUTANTS, ids=[m[0] for m in MUTANTS])
