@@ -192,6 +192,49 @@ class LatentCall:
             raise RuntimeError(f"latent-cache call ({self.mode}) failed with status {st}")
 
 
+class BackwardCall:
+    """A layer's backward (lb_linear_backward, dx included) for x and a random upstream gradient,
+    pre-marshalled; times like a Layer."""
+
+    def __init__(self, layer, kappa=100.0):
+        import torch
+        import paper_2506_13771_amd as lb
+        L = layer
+        self.layer = L
+        self.lib = lb.load_library()
+        g = torch.Generator(device=L.x.device).manual_seed(7)
+        self.dy = torch.randn((L.T, L.d_out), generator=g, device=L.x.device).to(L.x.dtype)
+        self.dx = torch.empty_like(L.x)
+        self.train = []
+        tarr = (lb.lb_path_train * 2)()
+        for p in range(2):
+            U_lat = torch.randn((L.d_out, L.r), generator=g, device=L.x.device) / kappa
+            V_lat = torch.randn((L.d_in, L.r), generator=g, device=L.x.device) / kappa
+            q = lb.LittleBitPathTrain(U_latent=U_lat, V_latent=V_lat,
+                                      Ut=lb.lb_pack_signs(U_lat, lb.LB_ROLE_V), Vt=lb.lb_pack_signs(V_lat, lb.LB_ROLE_U))
+            for name, shape in (("dU", (L.d_out, L.r)), ("dV", (L.d_in, L.r)), ("dh", (L.d_out,)),
+                                ("dg", (L.d_in,)), ("dl", (L.r,))):
+                setattr(q, name, torch.empty(shape, dtype=torch.float32, device=L.x.device))
+            tarr[p] = lb.lb_path_train(*[getattr(q, f).data_ptr() for f in ("U_latent", "V_latent", "Ut", "Vt", "dU",
+                                                                            "dV", "dh", "dg", "dl")])
+            self.train.append(q)
+        self._tarr = tarr
+        n = lb.lb_backward_workspace_bytes(L.T, L.d_in, L.d_out, L.r)
+        self.ws = torch.empty(max(n, 256), dtype=torch.uint8, device=L.x.device)
+        self.argv = (ctypes.c_void_p(L.x.data_ptr()), ctypes.c_void_p(self.dy.data_ptr()), lb._dtype_code(L.x), L.T,
+                     L.d_in, L.d_out, L.r, L._arr, lb._dtype_code(L.paths[0].h), tarr, ctypes.c_float(kappa),
+                     ctypes.c_void_p(self.dx.data_ptr()), ctypes.c_void_p(self.ws.data_ptr()), self.ws.numel(),
+                     ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+
+    def set_stream(self, handle):
+        self.argv = self.argv[:-1] + (ctypes.c_void_p(handle),)
+
+    def call(self):
+        st = self.lib.lb_linear_backward(*self.argv)
+        if st != 0:
+            raise RuntimeError(f"lb_linear_backward failed with status {st}")
+
+
 def time_calls(layers, steps, warmup, use_graph=True, per_graph=None):
     """Run every layer's forward `steps` times (after `warmup`) on the current stream, timed
     with HIP events recorded on that stream.  With use_graph the launches of `per_graph`
@@ -386,7 +429,7 @@ def cpu_baseline(li, seconds):
 # ----------------------------------------------------------------------------
 # sweep of the other configurations (diagnostic lines written to a file)
 # ----------------------------------------------------------------------------
-def run_sweep(path, steps, warmup, only=("7b", "13b", "kv", "70b")):
+def run_sweep(path, steps, warmup, only=("7b", "13b", "kv", "train", "70b")):
     import torch
     from paper_2506_13771_amd import synth
     out = open(path, "w")
@@ -444,6 +487,24 @@ def run_sweep(path, steps, warmup, only=("7b", "13b", "kv", "70b")):
                   "latent_tflops": 4 * T * d_in * r / (ms_l * 1e-3) / 1e12,
                   "from_latent_tflops": 4 * T * r * d_out / (ms_u * 1e-3) / 1e12})
             del L, lat, frm
+    # training step of one layer (QAT backward with SmoothSign) on the Llama2-7B block shapes at
+    # 0.1 BPW, 2048 tokens (the paper's training sequence length), beside the forward
+    for idx, (name, d_in, d_out) in enumerate(synth.LLAMA2_7B if "train" in only else ()):
+        if name not in ("q", "gate", "down"):
+            continue
+        r = ranks_7b[0.1][max(d_in, d_out)]
+        T = 2048
+        L = Layer(synth.make_linear(d_in, d_out, r, T, cfg=6, linear=idx), "cuda")
+        n_st, n_wu = max(10, steps // 20), max(3, warmup // 20)
+        ms_f, _ = time_calls([L], n_st, n_wu)
+        B = BackwardCall(L)
+        ms_b, _ = time_calls([B], n_st, n_wu)
+        fl = 2.0 * 2 * T * r * (2 * d_out + 3 * d_in)
+        emit({"config": "llama2-7b-train-step", "linear": name, "bpw": 0.1, "T": T, "d_in": d_in, "d_out": d_out,
+              "r": r, "us_backward": ms_b * 1e3, "us_forward": ms_f * 1e3, "backward_flops": fl,
+              "backward_tflops": fl / (ms_b * 1e-3) / 1e12,
+              "backward_mfma_frac": fl / (ms_b * 1e-3) / 1e12 / PEAK_BF16_TFLOPS})
+        del L, B
     # 70B sweep: 80 layers x 7 linears resident, back-to-back on one stream
     ranks_70b = {(8192, 8192): 176, (8192, 1024): 16, (8192, 28672): 288, (28672, 8192): 288}
     for T in ((1, 8, 64) if "70b" in only else ()):
@@ -481,9 +542,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", default=None, help="write per-configuration JSON lines to this file")
-    ap.add_argument("--sweep-only", default="7b,13b,kv,70b",
+    ap.add_argument("--sweep-only", default="7b,13b,kv,train,70b",
                     help="comma list of the sweep's parts to run (7b block, 13b prefill, 7b latent K/V cache, "
-                         "70b decode sweep)")
+                         "7b training-step backward, 70b decode sweep)")
     ap.add_argument("--no-warm", action="store_true",
                     help="skip the warm-cache measurements (counter runs: every decode dispatch is then a "
                          "cold-rotation one)")

@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define LB_ABI_VERSION 3
+#define LB_ABI_VERSION 4
 
 typedef enum lb_status {
   LB_OK = 0,
@@ -247,6 +247,54 @@ size_t lb_from_latent_workspace_bytes(int64_t T, int64_t r);
 lb_status lb_linear_from_latent(const void* w, lb_dtype latent_dtype, int64_t T, int64_t d_out, int64_t r,
                                 const lb_path* paths, lb_dtype scale_dtype, void* y, lb_dtype out_dtype,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Training-time inputs and gradient outputs of one path for
+   lb_linear_backward.  All float arrays are fp32, row-major, 4-byte aligned,
+   owned by the caller; gradients are written, not accumulated. */
+typedef struct lb_path_train {
+  const float* U_latent;  /* [d_out x r] real latent factor whose signs are U_p */
+  const float* V_latent;  /* [d_in x r] real latent factor whose signs are V_p */
+  const void* Ut;         /* U_p's signs packed with LB_ROLE_V (rows = d_out):
+                             lb_pack_signs(U_latent, LB_F32, d_out, r, LB_ROLE_V, ...) */
+  const void* Vt;         /* V_p's signs packed with LB_ROLE_U (rows = d_in):
+                             lb_pack_signs(V_latent, LB_F32, d_in, r, LB_ROLE_U, ...) */
+  float* dU;              /* out [d_out x r]: dL/dU_latent */
+  float* dV;              /* out [d_in x r]:  dL/dV_latent */
+  float* dh;              /* out [d_out] */
+  float* dg;              /* out [d_in] */
+  float* dl;              /* out [r] */
+} lb_path_train;
+
+/* Host, pure.  Workspace bytes lb_linear_backward needs (0 for invalid sizes);
+   no zero-fill needed. */
+size_t lb_backward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
+
+/* Backward of one LittleBit linear for quantization-aware training (Sec. 4
+   "Training Details"; Appendix "SmoothSign versus Straight-Through
+   Estimator").  Given x [T x d_in] and the upstream gradient dy = dL/dy
+   [T x d_out] (both act_dtype), the chain rule through Proposition 1 for both
+   paths, with a = g (.) x, z = a V, w = l (.) z, dw = (h (.) dy) U, dz = l (.) dw:
+     dx      = sum_p g_p (.) (dz_p V_p^T)                (act_dtype, one rounding;
+                                                          skipped if dx is NULL)
+     dh_p    = rowsum(U_p (.) (dy^T w_p)),   dg_p = rowsum(V_p (.) (x^T dz_p))
+     dl_p    = sum_t dw_p (.) z_p
+     dU_p    = h_p (.) (dy^T w_p) (.) s'(U_latent),  dV_p = g_p (.) (x^T dz_p) (.) s'(V_latent)
+   where the signs U_p, V_p are those of the latent factors (a value < 0 is
+   -1) and s'(u) = kappa sech^2(kappa u), the derivative of tanh(kappa u) that
+   SmoothSign uses in place of the sign's (the paper uses kappa = 100).
+   paths: V (packed with LB_ROLE_V, as for the forward), h, g and l are read;
+   U may be NULL.  train[2]: the latent factors, their signs packed in the
+   other orientation, and the gradient outputs.  The binary contractions run
+   on the prefill kernels (exact bf16 term products, fp32 accumulation); the
+   two contractions over tokens run on the matrix cores with exact bf16 terms
+   (three for w and dz) and fp32 accumulation.  Any size may be 0 (the
+   non-empty gradients are then zero).  dx must not overlap x or dy
+   (LB_ERR_ARG).  kappa must be finite and > 0 (LB_ERR_ARG).  workspace:
+   256-byte aligned, >= lb_backward_workspace_bytes(T, d_in, d_out, r). */
+lb_status lb_linear_backward(const void* x, const void* dy, lb_dtype act_dtype, int64_t T, int64_t d_in,
+                             int64_t d_out, int64_t r, const lb_path* paths, lb_dtype scale_dtype,
+                             const lb_path_train* train, float kappa, void* dx, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
 
 /* Checking path: the dense effective weight of both paths,
      W[i][j] = sum_p h_p[i] g_p[j] sum_k U_p[i][k] l_p[k] V_p[j][k]

@@ -12,7 +12,8 @@ The names follow the C ABI:
   lb_forward_workspace_bytes, lb_workspace_init, lb_decode_max_tokens,
   lb_linear_forward_many, lb_forward_many_workspace_bytes,
   lb_linear_latent, lb_latent_workspace_bytes,
-  lb_linear_from_latent, lb_from_latent_workspace_bytes.
+  lb_linear_from_latent, lb_from_latent_workspace_bytes,
+  lb_linear_backward, lb_backward_workspace_bytes.
 """
 from __future__ import annotations
 
@@ -28,7 +29,7 @@ LB_OK, LB_ERR_NULL, LB_ERR_SHAPE, LB_ERR_DTYPE, LB_ERR_ALIGN, LB_ERR_WORKSPACE, 
 LB_F32, LB_F16, LB_BF16 = 0, 1, 2
 LB_ROLE_U, LB_ROLE_V = 0, 1
 LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL, LB_KERNEL_DECODE_MFMA = 0, 1, 2, 3
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 
 class LittleBitError(RuntimeError):
@@ -46,6 +47,12 @@ class lb_linear_desc(ctypes.Structure):
     _fields_ = [("x", ctypes.c_void_p), ("act_dtype", ctypes.c_int), ("T", ctypes.c_int64),
                 ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64), ("r", ctypes.c_int64),
                 ("paths", lb_path * 2), ("scale_dtype", ctypes.c_int), ("y", ctypes.c_void_p)]
+
+
+class lb_path_train(ctypes.Structure):
+    _fields_ = [("U_latent", ctypes.c_void_p), ("V_latent", ctypes.c_void_p), ("Ut", ctypes.c_void_p),
+                ("Vt", ctypes.c_void_p), ("dU", ctypes.c_void_p), ("dV", ctypes.c_void_p), ("dh", ctypes.c_void_p),
+                ("dg", ctypes.c_void_p), ("dl", ctypes.c_void_p)]
 
 
 _lib = None
@@ -97,6 +104,11 @@ def load_library(path: str = LIB_PATH):
     lib.lb_linear_from_latent.restype = i32
     lib.lb_linear_from_latent.argtypes = [vp, i32, i64, i64, i64, ctypes.POINTER(lb_path), i32, vp, i32, vp, sz,
                                           vp]
+    lib.lb_backward_workspace_bytes.restype = sz
+    lib.lb_backward_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.lb_linear_backward.restype = i32
+    lib.lb_linear_backward.argtypes = [vp, vp, i32, i64, i64, i64, i64, ctypes.POINTER(lb_path), i32,
+                                       ctypes.POINTER(lb_path_train), ctypes.c_float, vp, vp, sz, vp]
     lib.lb_dense_reference_weight.restype = i32
     lib.lb_dense_reference_weight.argtypes = [ctypes.POINTER(lb_path), i32, i64, i64, i64, vp, vp]
     if lib.lb_abi_version() != ABI_VERSION:
@@ -336,6 +348,59 @@ def lb_linear_from_latent(w, paths: Sequence[LittleBitPath], y=None, out_dtype=N
     return y
 
 
+def lb_backward_workspace_bytes(T: int, d_in: int, d_out: int, r: int) -> int:
+    return int(load_library().lb_backward_workspace_bytes(T, d_in, d_out, r))
+
+
+@dataclass
+class LittleBitPathTrain:
+    """One path's fp32 latent factors, their signs packed in the backward's orientation (Ut: U packed
+    with LB_ROLE_V, Vt: V packed with LB_ROLE_U) and, after lb_linear_backward, the gradients."""
+    U_latent: object
+    V_latent: object
+    Ut: object = None
+    Vt: object = None
+    dU: object = None
+    dV: object = None
+    dh: object = None
+    dg: object = None
+    dl: object = None
+
+
+def lb_linear_backward(x, dy, paths: Sequence[LittleBitPath], train: Sequence[LittleBitPathTrain],
+                       kappa: float = 100.0, dx=None, need_dx: bool = True, workspace=None, stream=None):
+    """Gradients of one layer for x [T, d_in] and dy [T, d_out]: fills (allocating when None) Ut, Vt (packed
+    from the latents), dU, dV, dh, dg, dl of each train entry; returns dx (None when need_dx is False)."""
+    torch = _torch()
+    lib = load_library()
+    T, d_in = x.shape
+    d_out = dy.shape[1]
+    r = train[0].U_latent.shape[1]
+    arr, sc = _paths_struct(paths)
+    tarr = (lb_path_train * 2)()
+    dev = x.device
+    for i, q in enumerate(train):
+        if q.Ut is None:
+            q.Ut = lb_pack_signs(q.U_latent, LB_ROLE_V, stream=stream)
+        if q.Vt is None:
+            q.Vt = lb_pack_signs(q.V_latent, LB_ROLE_U, stream=stream)
+        for name, shape in (("dU", (d_out, r)), ("dV", (d_in, r)), ("dh", (d_out,)), ("dg", (d_in,)), ("dl", (r,))):
+            if getattr(q, name) is None:
+                setattr(q, name, torch.empty(shape, dtype=torch.float32, device=dev))
+        tarr[i] = lb_path_train(*[_dev_ptr(getattr(q, f), f) for f in ("U_latent", "V_latent", "Ut", "Vt", "dU",
+                                                                         "dV", "dh", "dg", "dl")])
+    if need_dx and dx is None:
+        dx = torch.empty((T, d_in), dtype=x.dtype, device=dev)
+    if workspace is None:
+        workspace = _scratch(lb_backward_workspace_bytes(T, d_in, d_out, r), dev)
+    st = lib.lb_linear_backward(_dev_ptr(x, "x"), _dev_ptr(dy, "dy"), _dtype_code(x), T, d_in, d_out, r, arr, sc,
+                                tarr, float(kappa), _dev_ptr(dx, "dx") if need_dx else 0,
+                                _dev_ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+                                _stream(stream))
+    _check(st, "lb_linear_backward")
+    return dx if need_dx else None
+
+
 def lb_dense_reference_weight(paths: Sequence[LittleBitPath], d_in: int, d_out: int, r: int, W=None, stream=None):
     """Dense fp32 W_hat [d_out, d_in] from the packed buffers (checking path)."""
     torch = _torch()
@@ -356,5 +421,6 @@ __all__ = [
     "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "alloc_workspace", "lb_linear_forward",
     "lb_dense_reference_weight", "lb_linear_desc", "make_descs", "lb_forward_many_workspace_bytes",
     "lb_linear_forward_many", "lb_latent_workspace_bytes", "lb_from_latent_workspace_bytes", "lb_linear_latent",
-    "lb_linear_from_latent",
+    "lb_linear_from_latent", "lb_path_train", "LittleBitPathTrain", "lb_backward_workspace_bytes",
+    "lb_linear_backward",
 ]

@@ -5,7 +5,7 @@
 #include <cstdint>
 #include <cstring>
 
-#include "lb_internal.h"
+#include "lb_backward.h"
 
 namespace {
 
@@ -30,14 +30,15 @@ lb_status check_sizes(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
   return LB_OK;
 }
 
-// with_l: l is read (every call but the from-latent one)
+// with_l / with_u: l / U are read (l by every call but the from-latent one,
+// U by every call but the backward)
 lb_status check_paths(const lb_path* paths, lb_dtype sc, int64_t d_in, int64_t d_out, int64_t r,
-                      bool with_l = true) {
+                      bool with_l = true, bool with_u = true) {
   if (!paths) return LB_ERR_NULL;
   const size_t es = dtype_size(sc);
   for (int p = 0; p < 2; ++p) {
     const lb_path& P = paths[p];
-    if ((r > 0 && d_out > 0 && !P.U) || (r > 0 && d_in > 0 && !P.V) || (d_out > 0 && !P.h) ||
+    if ((with_u && r > 0 && d_out > 0 && !P.U) || (r > 0 && d_in > 0 && !P.V) || (d_out > 0 && !P.h) ||
         (d_in > 0 && !P.g) || (with_l && r > 0 && !P.l))
       return LB_ERR_NULL;
     if (!aligned(P.U, 4) || !aligned(P.V, 4) || !aligned(P.h, es) || !aligned(P.g, es) || !aligned(P.l, es))
@@ -433,6 +434,92 @@ lb_status lb_linear_from_latent(const void* w, lb_dtype latent_dtype, int64_t T,
     lb::ForwardArgs a = make_args(nullptr, out_dtype, T, 0, d_out, r, used, scale_dtype, y, workspace, workspace_bytes);
     e = lb::launch_from_latent(a, w, latent_dtype, stream);
   }
+  return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+}
+
+size_t lb_backward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
+  if (check_sizes(T, d_in, d_out, r) != LB_OK || !lb::backward_supports(T, d_in, d_out, r)) return 0;
+  return lb::backward_workspace_bytes(static_cast<int>(T), static_cast<int>(d_in), static_cast<int>(d_out),
+                                      static_cast<int>(r));
+}
+
+lb_status lb_linear_backward(const void* x, const void* dy, lb_dtype act_dtype, int64_t T, int64_t d_in,
+                             int64_t d_out, int64_t r, const lb_path* paths, lb_dtype scale_dtype,
+                             const lb_path_train* train, float kappa, void* dx, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype)) return LB_ERR_DTYPE;
+  lb_status st = check_sizes(T, d_in, d_out, r);
+  if (st != LB_OK) return st;
+  if (!lb::backward_supports(T, d_in, d_out, r)) return LB_ERR_SHAPE;
+  if (!(kappa > 0.0f) || !std::isfinite(kappa)) return LB_ERR_ARG;
+  if (!paths || !train) return LB_ERR_NULL;
+  const size_t ea = dtype_size(act_dtype);
+  if ((T * d_in > 0 && !x) || (T * d_out > 0 && !dy)) return LB_ERR_NULL;
+  if (!aligned(x, ea) || !aligned(dy, ea) || !aligned(dx, ea)) return LB_ERR_ALIGN;
+  // forward parameters read: V, h, g, l
+  lb_path used[2];
+  for (int p = 0; p < 2; ++p) used[p] = lb_path{nullptr, paths[p].V, paths[p].h, paths[p].g, paths[p].l};
+  st = check_paths(used, scale_dtype, d_in, d_out, r, true, false);
+  if (st != LB_OK) return st;
+  for (int p = 0; p < 2; ++p) {
+    const lb_path_train& q = train[p];
+    if ((d_out * r > 0 && (!q.U_latent || !q.Ut || !q.dU)) || (d_in * r > 0 && (!q.V_latent || !q.Vt || !q.dV)) ||
+        (d_out > 0 && !q.dh) || (d_in > 0 && !q.dg) || (r > 0 && !q.dl))
+      return LB_ERR_NULL;
+    if (!aligned(q.U_latent, 4) || !aligned(q.V_latent, 4) || !aligned(q.Ut, 4) || !aligned(q.Vt, 4) ||
+        !aligned(q.dU, 4) || !aligned(q.dV, 4) || !aligned(q.dh, 4) || !aligned(q.dg, 4) || !aligned(q.dl, 4))
+      return LB_ERR_ALIGN;
+  }
+  const size_t ndx = static_cast<size_t>(T * d_in) * ea;
+  if (dx && (overlap(dx, ndx, x, ndx) || overlap(dx, ndx, dy, static_cast<size_t>(T * d_out) * ea)))
+    return LB_ERR_ARG;
+  const size_t need = lb_backward_workspace_bytes(T, d_in, d_out, r);
+  if (!workspace) return LB_ERR_NULL;
+  if (!aligned(workspace, 256)) return LB_ERR_ALIGN;
+  if (workspace_bytes < need) return LB_ERR_WORKSPACE;
+  hipError_t e = hipSuccess;
+  if (T == 0 || d_in == 0 || d_out == 0 || r == 0) {
+    // an empty sum somewhere in every gradient: the non-empty ones are zero
+    for (int p = 0; p < 2 && e == hipSuccess; ++p) {
+      const lb_path_train& q = train[p];
+      if ((e = lb::launch_zero_elems(q.dU, d_out * r, LB_F32, stream)) != hipSuccess) break;
+      if ((e = lb::launch_zero_elems(q.dV, d_in * r, LB_F32, stream)) != hipSuccess) break;
+      if ((e = lb::launch_zero_elems(q.dh, d_out, LB_F32, stream)) != hipSuccess) break;
+      if ((e = lb::launch_zero_elems(q.dg, d_in, LB_F32, stream)) != hipSuccess) break;
+      e = lb::launch_zero_elems(q.dl, r, LB_F32, stream);
+    }
+    if (e == hipSuccess && dx) e = lb::launch_zero_elems(dx, T * d_in, act_dtype, stream);
+    return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+  }
+  lb::BackwardArgs b{};
+  b.x = x;
+  b.dy = dy;
+  b.act_dt = act_dtype;
+  b.sc_dt = scale_dtype;
+  b.T = static_cast<int>(T);
+  b.d_in = static_cast<int>(d_in);
+  b.d_out = static_cast<int>(d_out);
+  b.r = static_cast<int>(r);
+  for (int p = 0; p < 2; ++p) {
+    b.V[p] = paths[p].V;
+    b.h[p] = paths[p].h;
+    b.g[p] = paths[p].g;
+    b.l[p] = paths[p].l;
+    b.Ut[p] = train[p].Ut;
+    b.Vt[p] = train[p].Vt;
+    b.U_lat[p] = train[p].U_latent;
+    b.V_lat[p] = train[p].V_latent;
+    b.dU[p] = train[p].dU;
+    b.dV[p] = train[p].dV;
+    b.dh[p] = train[p].dh;
+    b.dg[p] = train[p].dg;
+    b.dl[p] = train[p].dl;
+  }
+  b.dx = dx;
+  b.kappa = kappa;
+  b.ws = workspace;
+  b.ws_bytes = workspace_bytes;
+  e = lb::launch_backward(b, stream);
   return e == hipSuccess ? LB_OK : LB_ERR_HIP;
 }
 

@@ -1,0 +1,451 @@
+// Backward of one LittleBit linear for quantization-aware training (Sec. 4
+// "Training Details": QAT of the latent factors and scales, with SmoothSign,
+// Appendix "SmoothSign versus Straight-Through Estimator": the sign in the
+// forward, the derivative of tanh(kappa u), kappa = 100, in the backward).
+//
+// The chain rule through Proposition 1 (Eq. proposition1), per path p, with
+// a = g (.) x, z = a V_s, w = l (.) z, u = w U_s^T and an upstream gradient dy:
+//   dw   = (h (.) dy) U_s          binary contraction over outputs   (prefill stage 1 on dy,
+//                                                                      U_s packed with role V)
+//   dz   = l (.) dw
+//   dx   = sum_p g_p (.) (dz_p V_s^T)  binary contraction over latents (prefill stage 2 from dz,
+//                                                                      V_s packed with role U)
+//   C_U  = dy^T w                  dense, over tokens:  dU = h (.) C_U (.) slope(U_lat),
+//                                                       dh = rowsum(U_s (.) C_U)
+//   C_V  = x^T dz                  dense, over tokens:  dV = g (.) C_V (.) slope(V_lat),
+//                                                       dg = rowsum(V_s (.) C_V)
+//   dl   = sum_t dw (.) z
+// with slope(u) = kappa sech^2(kappa u).  z (of x) and dw (of dy) are kept in
+// fp32 [T][2][r] in the workspace.
+//
+// The two token contractions run on the matrix cores (tgemm): a workgroup of
+// 4 waves owns 64 rows (outputs or inputs) and up to 128 latents of one path
+// and a run of 32-token steps; each step stages the tile of A (dy or x, cut
+// into its exact bf16 terms) and of B (w or dz, fp32, cut into three exact
+// bf16 terms) in LDS with tokens contiguous, so that both operands read their
+// 8 reduction slots as one 16-byte LDS load.  Every product is exact and the
+// matrix cores accumulate in fp32; token splits are added in ascending order
+// by the epilogue.
+#include "device_common.h"
+#include "lb_backward.h"
+
+namespace lb {
+
+namespace {
+
+constexpr int kGThreads = 256;  // 4 waves
+constexpr int kGM = 64;         // rows per workgroup (16 per wave)
+constexpr int kGTok = 32;       // tokens per step
+constexpr int kGMaxNk = 8;      // 16-latent subtiles per workgroup
+constexpr int kRow = 40;        // LDS row stride in bf16 (32 tokens + 8 pad)
+constexpr int kGWantWg = 1024;  // workgroups aimed at by the token splits
+constexpr int kGMinSteps = 2;   // fewest steps per token split
+constexpr int kDlChunk = 16;    // tokens per partial sum of dl
+
+struct GemmParams {
+  const void* A;   // [T][M] act dtype
+  const float* B;  // [T][2][r]
+  const void* l[2];
+  float* part;     // [ks][2][M][r]
+  int T, M, r;
+  int n_mt, n_kt, ks, steps_per;
+  int sc_dt;
+};
+
+struct GemmGeom {
+  int nk, n_mt, n_kt, ks, steps_per;
+  size_t part_floats;
+};
+
+GemmGeom gemm_geom(int T, int M, int r) {
+  GemmGeom g{};
+  // empty sizes plan as size 1 (their calls launch nothing)
+  if (M < 1) M = 1;
+  if (r < 1) r = 1;
+  const int ns16 = (r + 15) / 16;
+  g.nk = ns16 < kGMaxNk ? ns16 : kGMaxNk;
+  g.n_kt = (ns16 + g.nk - 1) / g.nk;
+  g.n_mt = (M + kGM - 1) / kGM;
+  const int steps = T > kGTok ? (T + kGTok - 1) / kGTok : 1;
+  const int tiles = g.n_mt * g.n_kt * 2;
+  int ks = (kGWantWg + tiles - 1) / tiles;
+  const int ks_max = steps / kGMinSteps > 1 ? steps / kGMinSteps : 1;
+  if (ks > ks_max) ks = ks_max;
+  if (ks < 1) ks = 1;
+  g.steps_per = (steps + ks - 1) / ks;
+  g.ks = (steps + g.steps_per - 1) / g.steps_per;
+  g.part_floats = static_cast<size_t>(g.ks) * 2 * r * M;
+  return g;
+}
+
+__device__ __forceinline__ float load_scale(const void* p, int i, int dt) { return load_as_f32(p, i, dt); }
+
+template <int ADT, int NK>
+__global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
+  constexpr int E = nterms<ADT>();
+  constexpr int KT = 16 * NK;
+  constexpr int NBI = (KT * 4 + kGThreads - 1) / kGThreads;  // B items per thread
+  __shared__ __attribute__((aligned(16))) uint16_t As[E][kGM][kRow];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[3][KT][kRow];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int bid = blockIdx.x;
+  const int mt = bid % P.n_mt;
+  bid /= P.n_mt;
+  const int kt = bid % P.n_kt;
+  bid /= P.n_kt;
+  const int p = bid & 1, sp = bid >> 1;
+  const int m0 = mt * kGM, k0 = kt * KT;
+  const int T = P.T, M = P.M, r = P.r;
+  const int steps = (T + kGTok - 1) / kGTok;
+  const int st0 = sp * P.steps_per;
+  int nst = steps - st0;
+  if (nst > P.steps_per) nst = P.steps_per;
+
+  // A loader: row am, tokens 8 aq .. 8 aq + 7 of a step
+  const int am = tid & 63, aq = tid >> 6;
+  const bool a_ok = m0 + am < M;
+  // B loader items: latent bk, tokens 8 bq .. 8 bq + 7
+  int bk[NBI], bq[NBI];
+  bool b_ok[NBI];
+  float lv[NBI];
+#pragma unroll
+  for (int i = 0; i < NBI; ++i) {
+    const int idx = tid + kGThreads * i;
+    bk[i] = idx % KT;
+    bq[i] = idx / KT;
+    b_ok[i] = bq[i] < 4 && k0 + bk[i] < r;
+    lv[i] = b_ok[i] ? load_scale(P.l[p], k0 + bk[i], P.sc_dt) : 0.0f;
+  }
+  uint32_t ra[8];
+  float rb[NBI][8];
+  auto load = [&](int st) {
+    const int tb = (st0 + st) * kGTok;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const int t = tb + 8 * aq + s;
+      const bool ok = a_ok && t < T;
+      const uint32_t u = ld_bits<ADT>(P.A, ok ? static_cast<int64_t>(t) * M + m0 + am : 0);
+      ra[s] = ok ? u : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < NBI; ++i) {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int t = tb + 8 * bq[i] + s;
+        const bool ok = b_ok[i] && t < T;
+        const float v = P.B[ok ? (static_cast<int64_t>(t) * 2 + p) * r + k0 + bk[i] : 0];
+        rb[i][s] = ok ? v : 0.0f;
+      }
+    }
+  };
+  auto store = [&]() {
+    uint32_t at[8][E];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      if constexpr (ADT == kDtBF16)
+        at[s][0] = ra[s];
+      else
+        split_exact<E>(bits_to_f32<ADT>(ra[s]), at[s]);
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      u32x4 d;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) d[v] = at[2 * v][e] | (at[2 * v + 1][e] << 16);
+      *reinterpret_cast<u32x4*>(&As[e][am][8 * aq]) = d;
+    }
+#pragma unroll
+    for (int i = 0; i < NBI; ++i) {
+      if (bq[i] >= 4) continue;
+      uint32_t bt[8][3];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) split_exact<3>(rb[i][s] * lv[i], bt[s]);
+#pragma unroll
+      for (int f = 0; f < 3; ++f) {
+        u32x4 d;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) d[v] = bt[2 * v][f] | (bt[2 * v + 1][f] << 16);
+        *reinterpret_cast<u32x4*>(&Bs[f][bk[i]][8 * bq[i]]) = d;
+      }
+    }
+  };
+
+  floatx4 acc[NK];
+#pragma unroll
+  for (int j = 0; j < NK; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int fr = lane & 15, fq = lane >> 4;
+  if (nst > 0) {
+    load(0);
+    store();
+    __syncthreads();
+    for (int st = 0; st < nst; ++st) {
+      if (st + 1 < nst) load(st + 1);
+      u32x4 a[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) a[e] = *reinterpret_cast<const u32x4*>(&As[e][16 * wave + fr][8 * fq]);
+#pragma unroll
+      for (int f = 0; f < 3; ++f) {
+#pragma unroll
+        for (int j = 0; j < NK; ++j) {
+          const u32x4 b = *reinterpret_cast<const u32x4*>(&Bs[f][16 * j + fr][8 * fq]);
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[j] = mfma(a[e], b, acc[j]);
+        }
+      }
+      __syncthreads();
+      if (st + 1 < nst) {
+        store();
+        __syncthreads();
+      }
+    }
+  }
+  // partial sums [m][k]: rows 16 wave + 4 fq + e of latent 16 j + fr
+  float* out = P.part + (static_cast<int64_t>(sp) * 2 + p) * r * static_cast<int64_t>(M);
+#pragma unroll
+  for (int j = 0; j < NK; ++j) {
+    const int k = k0 + 16 * j + fr;
+    if (k >= r) continue;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int m = m0 + 16 * wave + 4 * fq + e;
+      if (m < M) out[static_cast<int64_t>(m) * r + k] = acc[j][e];
+    }
+  }
+}
+
+struct EpiParams {
+  const float* part;  // [ks][2][M][r]
+  const float* lat[2];
+  const void* s[2];   // row scales (h or g)
+  float* dlat[2];
+  float* drow[2];
+  int M, r, ks, sc_dt;
+  float kappa;
+};
+
+// d/du tanh(kappa u) = kappa sech^2(kappa u) = 4 kappa e / (1 + e)^2 with
+// e = exp(-2 |kappa u|): no cancellation for large |u|
+__device__ __forceinline__ float smooth_slope(float kappa, float u) {
+  const float e = expf(-2.0f * fabsf(kappa * u));
+  const float d = 1.0f + e;
+  return 4.0f * kappa * e / (d * d);
+}
+
+// one wave per (path, row), lanes over latents: sums the token splits in
+// ascending order, writes the latent-factor gradient, and the row-scale
+// gradient through a fixed butterfly over the wave
+__global__ void __launch_bounds__(256) tgemm_epilogue(EpiParams P) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= 2 * P.M) return;  // whole waves leave together
+  const int p = row >= P.M ? 1 : 0;
+  const int m = row - p * P.M;
+  const int M = P.M, r = P.r;
+  const float sc = load_scale(P.s[p], m, P.sc_dt);
+  const float* lat = P.lat[p] + static_cast<int64_t>(m) * r;
+  float* dlat = P.dlat[p] + static_cast<int64_t>(m) * r;
+  const float* src = P.part + (static_cast<int64_t>(p) * M + m) * r;
+  const int64_t sstride = static_cast<int64_t>(2) * M * r;
+  float acc = 0.0f;
+  for (int k = lane; k < r; k += 64) {
+    float c = 0.0f;
+    for (int s = 0; s < P.ks; ++s) c += src[s * sstride + k];
+    const float u = lat[k];
+    acc += u < 0.0f ? -c : c;
+    dlat[k] = sc * c * smooth_slope(P.kappa, u);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  if (lane == 0) P.drow[p][m] = acc;
+}
+
+// dl partials: part[ch][c] = sum over the chunk's tokens of dw * z at column
+// c = p r + k of the [T][2][r] arrays
+__global__ void __launch_bounds__(256) dl_partial(const float* dw, const float* z, float* part, int T, int cols) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int ch = blockIdx.y;
+  if (c >= cols) return;
+  const int t1 = (ch + 1) * kDlChunk < T ? (ch + 1) * kDlChunk : T;
+  float s = 0.0f;
+  for (int t = ch * kDlChunk; t < t1; ++t) {
+    const int64_t i = static_cast<int64_t>(t) * cols + c;
+    s += dw[i] * z[i];
+  }
+  part[static_cast<int64_t>(ch) * cols + c] = s;
+}
+
+__global__ void __launch_bounds__(256) dl_final(const float* part, int nch, int r, float* dl0, float* dl1) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= 2 * r) return;
+  float s = 0.0f;
+#pragma unroll 8
+  for (int ch = 0; ch < nch; ++ch) s += part[static_cast<int64_t>(ch) * 2 * r + c];
+  if (c < r)
+    dl0[c] = s;
+  else
+    dl1[c - r] = s;
+}
+
+template <int ADT>
+hipError_t launch_tgemm_nk(const GemmParams& P, int nk, hipStream_t stream) {
+  const dim3 grid(P.n_mt * P.n_kt * 2 * P.ks), block(kGThreads);
+  switch (nk) {
+    case 1: hipLaunchKernelGGL((tgemm<ADT, 1>), grid, block, 0, stream, P); break;
+    case 2: hipLaunchKernelGGL((tgemm<ADT, 2>), grid, block, 0, stream, P); break;
+    case 3: hipLaunchKernelGGL((tgemm<ADT, 3>), grid, block, 0, stream, P); break;
+    case 4: hipLaunchKernelGGL((tgemm<ADT, 4>), grid, block, 0, stream, P); break;
+    case 5: hipLaunchKernelGGL((tgemm<ADT, 5>), grid, block, 0, stream, P); break;
+    case 6: hipLaunchKernelGGL((tgemm<ADT, 6>), grid, block, 0, stream, P); break;
+    case 7: hipLaunchKernelGGL((tgemm<ADT, 7>), grid, block, 0, stream, P); break;
+    default: hipLaunchKernelGGL((tgemm<ADT, kGMaxNk>), grid, block, 0, stream, P); break;
+  }
+  return hipGetLastError();
+}
+
+// C = A^T (l (.) B) over tokens, then the epilogue into dlat / drow
+hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const float* B, float* part,
+                          const float* const* lat, const void* const* s, float* const* dlat, float* const* drow,
+                          hipStream_t stream) {
+  const GemmGeom g = gemm_geom(b.T, M, b.r);
+  GemmParams P{};
+  P.A = A;
+  P.B = B;
+  P.l[0] = b.l[0];
+  P.l[1] = b.l[1];
+  P.part = part;
+  P.T = b.T;
+  P.M = M;
+  P.r = b.r;
+  P.n_mt = g.n_mt;
+  P.n_kt = g.n_kt;
+  P.ks = g.ks;
+  P.steps_per = g.steps_per;
+  P.sc_dt = b.sc_dt;
+  hipError_t e;
+  switch (b.act_dt) {
+    case kDtF32: e = launch_tgemm_nk<kDtF32>(P, g.nk, stream); break;
+    case kDtF16: e = launch_tgemm_nk<kDtF16>(P, g.nk, stream); break;
+    default: e = launch_tgemm_nk<kDtBF16>(P, g.nk, stream); break;
+  }
+  if (e != hipSuccess) return e;
+  EpiParams Q{};
+  Q.part = part;
+  for (int p = 0; p < 2; ++p) {
+    Q.lat[p] = lat[p];
+    Q.s[p] = s[p];
+    Q.dlat[p] = dlat[p];
+    Q.drow[p] = drow[p];
+  }
+  Q.M = M;
+  Q.r = b.r;
+  Q.ks = g.ks;
+  Q.sc_dt = b.sc_dt;
+  Q.kappa = b.kappa;
+  hipLaunchKernelGGL(tgemm_epilogue, dim3((2 * M + 3) / 4), dim3(256), 0, stream, Q);
+  return hipGetLastError();
+}
+
+size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+
+struct BackwardLayout {
+  size_t z_off, dw_off, stage_off, part_off, dl_off, total;
+};
+
+BackwardLayout backward_layout(int T, int d_in, int d_out, int r) {
+  BackwardLayout L{};
+  const size_t lat = align256(static_cast<size_t>(T) * 2 * r * 4);
+  size_t stage = latent_workspace_bytes(T, d_in, r);
+  const size_t s2 = latent_workspace_bytes(T, d_out, r);
+  const size_t s3 = from_latent_workspace_bytes(T, r);
+  if (s2 > stage) stage = s2;
+  if (s3 > stage) stage = s3;
+  const GemmGeom gu = gemm_geom(T, d_out, r), gv = gemm_geom(T, d_in, r);
+  const size_t part = align256(4 * (gu.part_floats > gv.part_floats ? gu.part_floats : gv.part_floats));
+  const int nch = (T + kDlChunk - 1) / kDlChunk;
+  L.z_off = kCtrlBytes;
+  L.dw_off = L.z_off + lat;
+  L.stage_off = L.dw_off + lat;
+  L.part_off = L.stage_off + align256(stage);
+  L.dl_off = L.part_off + part;
+  L.total = L.dl_off + align256(static_cast<size_t>(nch) * 2 * r * 4);
+  return L;
+}
+
+}  // namespace
+
+bool backward_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r) {
+  const int64_t lim = int64_t(1) << 31;
+  if (!latent_supports(T, d_in, r) || !latent_supports(T, d_out, r) || !from_latent_supports(T, d_in, r))
+    return false;
+  const int64_t m = d_in > d_out ? d_in : d_out;
+  const int64_t steps = (T + kGTok - 1) / kGTok;
+  // token-split partial sums, [T][2][r] arrays and the row offsets of the token tiles
+  return steps * 2 * r * m < lim && 2 * T * r < lim && (T + kGTok) * m < lim;
+}
+
+size_t backward_workspace_bytes(int T, int d_in, int d_out, int r) { return backward_layout(T, d_in, d_out, r).total; }
+
+hipError_t launch_backward(const BackwardArgs& b, hipStream_t stream) {
+  const BackwardLayout L = backward_layout(b.T, b.d_in, b.d_out, b.r);
+  char* ws = static_cast<char*>(b.ws);
+  float* z = reinterpret_cast<float*>(ws + L.z_off);
+  float* dw = reinterpret_cast<float*>(ws + L.dw_off);
+  float* part = reinterpret_cast<float*>(ws + L.part_off);
+  float* dlp = reinterpret_cast<float*>(ws + L.dl_off);
+  void* stage = ws + L.stage_off;
+  const size_t stage_bytes = L.part_off - L.stage_off;
+  hipError_t e;
+  // z of x: stage 1 through V and g
+  {
+    ForwardArgs a{};
+    a.x = b.x;
+    a.act_dt = b.act_dt;
+    a.T = b.T;
+    a.d_in = b.d_in;
+    a.r = b.r;
+    for (int p = 0; p < 2; ++p) a.V[p] = b.V[p], a.g[p] = b.g[p], a.l[p] = b.l[p];
+    a.sc_dt = b.sc_dt;
+    a.ws = stage;
+    a.ws_bytes = stage_bytes;
+    if ((e = launch_stage1_sums(a, z, stream)) != hipSuccess) return e;
+  }
+  // dw of dy: stage 1 through U (role V packing) and h
+  {
+    ForwardArgs a{};
+    a.x = b.dy;
+    a.act_dt = b.act_dt;
+    a.T = b.T;
+    a.d_in = b.d_out;
+    a.r = b.r;
+    for (int p = 0; p < 2; ++p) a.V[p] = b.Ut[p], a.g[p] = b.h[p], a.l[p] = b.l[p];
+    a.sc_dt = b.sc_dt;
+    a.ws = stage;
+    a.ws_bytes = stage_bytes;
+    if ((e = launch_stage1_sums(a, dw, stream)) != hipSuccess) return e;
+  }
+  // dx from dz = l (.) dw: stage 2 through V (role U packing) and g
+  if (b.dx) {
+    ForwardArgs a{};
+    a.act_dt = b.act_dt;
+    a.T = b.T;
+    a.d_out = b.d_in;
+    a.r = b.r;
+    for (int p = 0; p < 2; ++p) a.U[p] = b.Vt[p], a.h[p] = b.g[p], a.l[p] = b.l[p];
+    a.sc_dt = b.sc_dt;
+    a.y = b.dx;
+    a.ws = stage;
+    a.ws_bytes = stage_bytes;
+    if ((e = launch_stage2_scaled(a, dw, stream)) != hipSuccess) return e;
+  }
+  // dU, dh from C_U = dy^T (l (.) z); dV, dg from C_V = x^T (l (.) dw)
+  if ((e = run_token_gemm(b, b.dy, b.d_out, z, part, b.U_lat, b.h, b.dU, b.dh, stream)) != hipSuccess) return e;
+  if ((e = run_token_gemm(b, b.x, b.d_in, dw, part, b.V_lat, b.g, b.dV, b.dg, stream)) != hipSuccess) return e;
+  // dl = sum_t dw (.) z
+  const int nch = (b.T + kDlChunk - 1) / kDlChunk, cols = 2 * b.r;
+  hipLaunchKernelGGL(dl_partial, dim3((cols + 255) / 256, nch), dim3(256), 0, stream, dw, z, dlp, b.T, cols);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(dl_final, dim3((cols + 255) / 256), dim3(256), 0, stream, dlp, nch, b.r, b.dl[0], b.dl[1]);
+  return hipGetLastError();
+}
+
+}  // namespace lb

@@ -47,6 +47,7 @@
 #include <atomic>
 
 #include "device_common.h"
+#include "lb_backward.h"
 
 namespace lb {
 
@@ -412,8 +413,8 @@ __device__ __forceinline__ bool pair_item(const PrefillParams& P, PairItem& it) 
 }
 
 // w0[v] = w of latent 32 kbl + 4 g4 + v and w1[v] of the same + 16 (0 past r):
-// the ks partial sums added in ascending split order, times l
-template <int SC>
+// the ks partial sums added in ascending split order, times l (SCALE) or not
+template <int SC, bool SCALE = true>
 __device__ __forceinline__ void latent_w(const PrefillParams& P, const PairItem& it, float (&w0)[4], float (&w1)[4]) {
   // subtiles 2 kbl (latents 32 kbl + 4 g4 + v) and 2 kbl + 1 (the same + 16)
   const float* src =
@@ -431,8 +432,8 @@ __device__ __forceinline__ void latent_w(const PrefillParams& P, const PairItem&
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const int k = 32 * it.kbl + 4 * it.g4 + v;
-    const float a = s0[v] * bits_to_f32<SC>(bload<SC>(lr, k, k < r));
-    const float b = s1[v] * bits_to_f32<SC>(bload<SC>(lr, k + 16, k + 16 < r));
+    const float a = SCALE ? s0[v] * bits_to_f32<SC>(bload<SC>(lr, k, k < r)) : s0[v];
+    const float b = SCALE ? s1[v] * bits_to_f32<SC>(bload<SC>(lr, k + 16, k + 16 < r)) : s1[v];
     w0[v] = k < r ? a : 0.0f;
     w1[v] = k + 16 < r ? b : 0.0f;
   }
@@ -472,13 +473,14 @@ __global__ void __launch_bounds__(kThreads) prefill_p1b(PrefillParams P) {
 }
 
 // The latent cache [T][2][r] (dtype LD, rounded to nearest even when 16-bit):
-// element (t, p, k) at (2 t + p) r + k
-template <int SC, int LD>
+// element (t, p, k) at (2 t + p) r + k.  SCALE: l (.) z (the cache); else z
+// itself (the backward keeps it in fp32)
+template <int SC, int LD, bool SCALE = true>
 __global__ void __launch_bounds__(kThreads) prefill_latent_out(PrefillParams P) {
   PairItem it;
   if (!pair_item(P, it)) return;
   float w0[4], w1[4];
-  latent_w<SC>(P, it, w0, w1);
+  latent_w<SC, SCALE>(P, it, w0, w1);
   const int r = P.r;
   const int64_t row = (static_cast<int64_t>(it.t) * 2 + it.p) * r;
 #pragma unroll
@@ -489,7 +491,9 @@ __global__ void __launch_bounds__(kThreads) prefill_latent_out(PrefillParams P) 
   }
 }
 
-template <int ACT, int LD>
+// w terms of P2 from a stored [T][2][r] array: the cache itself, or (SC >= 0)
+// its product with l (the backward's dz = l (.) dw)
+template <int ACT, int LD, int SC = -1>
 __global__ void __launch_bounds__(kThreads) prefill_latent_in(PrefillParams P) {
   constexpr int NW = ACT == kDtF32 ? 3 : 2;
   PairItem it;
@@ -502,6 +506,15 @@ __global__ void __launch_bounds__(kThreads) prefill_latent_in(PrefillParams P) {
     const int k = 32 * it.kbl + 4 * it.g4 + v;
     w0[v] = ld_or0<LD>(P.lat, row + k, k < r);
     w1[v] = ld_or0<LD>(P.lat, row + k + 16, k + 16 < r);
+  }
+  if constexpr (SC >= 0) {
+    const rsrc_t lr = make_rsrc(it.p ? P.l[1] : P.l[0], P.l_bytes);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int k = 32 * it.kbl + 4 * it.g4 + v;
+      w0[v] *= bits_to_f32<SC>(bload<SC>(lr, k, k < r));
+      w1[v] *= bits_to_f32<SC>(bload<SC>(lr, k + 16, k + 16 < r));
+    }
   }
   store_wterm<NW>(P, it, w0, w1);
 }
@@ -905,12 +918,15 @@ hipError_t launch_act(const PrefillParams& P, int sc_dt, const PrefillGeom& g, h
   }
 }
 
-// latent call: P1, then the cache store
+// latent call: P1, then the cache store (lat_dt < 0: fp32 sums without l)
 template <int ACT, int SC>
 hipError_t launch_latent_typed(const PrefillParams& P, int lat_dt, const PrefillGeom& g, hipStream_t stream) {
   hipError_t e = launch_p1_ms<ACT, SC>(P, g, stream);
   if (e != hipSuccess) return e;
   switch (lat_dt) {
+    case -1:
+      hipLaunchKernelGGL((prefill_latent_out<SC, kDtF32, false>), pair_grid(P), dim3(kThreads), 0, stream, P);
+      break;
     case kDtF32: hipLaunchKernelGGL((prefill_latent_out<SC, kDtF32>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
     case kDtF16: hipLaunchKernelGGL((prefill_latent_out<SC, kDtF16>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
     default: hipLaunchKernelGGL((prefill_latent_out<SC, kDtBF16>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
@@ -927,10 +943,14 @@ hipError_t launch_latent_act(const PrefillParams& P, int sc_dt, int lat_dt, cons
   }
 }
 
-// from-latent call: the cache cut into w terms, then P2
+// from-latent call: the cache cut into w terms, then P2 (lat_dt < 0: an fp32
+// array times l)
 template <int ACT, int SC>
 hipError_t launch_from_latent_typed(const PrefillParams& P, int lat_dt, const PrefillGeom& g, hipStream_t stream) {
   switch (lat_dt) {
+    case -1:
+      hipLaunchKernelGGL((prefill_latent_in<ACT, kDtF32, SC>), pair_grid(P), dim3(kThreads), 0, stream, P);
+      break;
     case kDtF32: hipLaunchKernelGGL((prefill_latent_in<ACT, kDtF32>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
     case kDtF16: hipLaunchKernelGGL((prefill_latent_in<ACT, kDtF16>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
     default: hipLaunchKernelGGL((prefill_latent_in<ACT, kDtBF16>), pair_grid(P), dim3(kThreads), 0, stream, P); break;
@@ -1139,6 +1159,16 @@ hipError_t launch_latent(const ForwardArgs& a, int lat_dt, hipStream_t stream) {
     case kDtF16: return launch_latent_act<kDtF16>(P, a.sc_dt, lat_dt, g, stream);
     default: return launch_latent_act<kDtBF16>(P, a.sc_dt, lat_dt, g, stream);
   }
+}
+
+hipError_t launch_stage1_sums(const ForwardArgs& a, float* z, hipStream_t stream) {
+  ForwardArgs b = a;
+  b.y = z;
+  return launch_latent(b, -1, stream);
+}
+
+hipError_t launch_stage2_scaled(const ForwardArgs& a, const float* w, hipStream_t stream) {
+  return launch_from_latent(a, w, -1, stream);
 }
 
 hipError_t launch_from_latent(const ForwardArgs& a, const void* lat, int lat_dt, hipStream_t stream) {

@@ -326,3 +326,69 @@ def test_from_latent_validation_errors(lib):
     assert _from(lib, ws=0) == lb.LB_ERR_NULL
     assert _from(lib, T=0) == lb.LB_OK
     assert _from(lib, d_out=0) == lb.LB_OK
+
+
+# ---------------------------------------------------------------------------
+# backward (validation only)
+# ---------------------------------------------------------------------------
+def _train(**kw):
+    arr = (lb.lb_path_train * 2)()
+    base = dict(U_latent=FAKE, V_latent=FAKE, Ut=FAKE, Vt=FAKE, dU=FAR, dV=FAR, dh=FAR, dg=FAR, dl=FAR)
+    base.update(kw)
+    for i in range(2):
+        arr[i] = lb.lb_path_train(*[base[f] for f in ("U_latent", "V_latent", "Ut", "Vt", "dU", "dV", "dh", "dg",
+                                                      "dl")])
+    return arr
+
+
+def _bwd(lib, x=FAKE, dy=FAKE * 2, act=lb.LB_BF16, T=4, d_in=64, d_out=48, r=16, paths=None, sc=lb.LB_F16,
+         train=None, kappa=100.0, dx=FAR * 4, ws=FAKE * 64, ws_bytes=None):
+    if paths is None:
+        paths = _paths(U=0)  # U is not read
+    if train is None:
+        train = _train()
+    if ws_bytes is None:
+        ws_bytes = lb.lb_backward_workspace_bytes(max(T, 0), max(d_in, 0), max(d_out, 0), max(r, 0)) - 1
+    return lib.lb_linear_backward(x, dy, act, T, d_in, d_out, r, paths, sc, train, kappa, dx, ws, ws_bytes, None)
+
+
+def test_backward_workspace_sizes(lib):
+    for T, d_in, d_out, r in [(2048, 4096, 4096, 80), (64, 11008, 4096, 128), (3, 33, 17, 5), (1, 64, 64, 300)]:
+        n = lb.lb_backward_workspace_bytes(T, d_in, d_out, r)
+        # z and dw of both paths in fp32, plus the stage and split buffers
+        assert n % 256 == 0 and n >= 2 * (2 * T * r * 4)
+    assert lb.lb_backward_workspace_bytes(-1, 4, 4, 4) == 0
+    # empty sizes plan without dividing by zero (regression) and still reserve the control block
+    for T, d_in, d_out, r in [(0, 64, 48, 16), (8, 0, 48, 16), (8, 64, 0, 16), (8, 64, 48, 0), (0, 0, 0, 0)]:
+        assert lb.lb_backward_workspace_bytes(T, d_in, d_out, r) >= 256
+
+
+def test_backward_validation_errors(lib):
+    assert _bwd(lib) == lb.LB_ERR_WORKSPACE
+    assert _bwd(lib, act=3) == lb.LB_ERR_DTYPE
+    assert _bwd(lib, sc=3) == lb.LB_ERR_DTYPE
+    assert _bwd(lib, T=-1) == lb.LB_ERR_SHAPE
+    assert _bwd(lib, T=1 << 20, d_in=1 << 12) == lb.LB_ERR_SHAPE
+    assert _bwd(lib, kappa=0.0) == lb.LB_ERR_ARG
+    assert _bwd(lib, kappa=float("inf")) == lb.LB_ERR_ARG
+    assert _bwd(lib, kappa=float("nan")) == lb.LB_ERR_ARG
+    assert _bwd(lib, x=0) == lb.LB_ERR_NULL
+    assert _bwd(lib, dy=0) == lb.LB_ERR_NULL
+    assert _bwd(lib, x=FAKE + 1) == lb.LB_ERR_ALIGN
+    assert _bwd(lib, dx=FAR * 4 + 1) == lb.LB_ERR_ALIGN
+    assert _bwd(lib, paths=_paths(U=0, V=0)) == lb.LB_ERR_NULL
+    assert _bwd(lib, paths=_paths(U=0, h=FAKE + 1)) == lb.LB_ERR_ALIGN
+    assert lib.lb_linear_backward(FAKE, FAKE * 2, lb.LB_BF16, 4, 64, 48, 16, None, lb.LB_F16, _train(), 100.0,
+                                  FAR * 4, FAKE * 64, 1 << 30, None) == lb.LB_ERR_NULL
+    assert lib.lb_linear_backward(FAKE, FAKE * 2, lb.LB_BF16, 4, 64, 48, 16, _paths(U=0), lb.LB_F16, None, 100.0,
+                                  FAR * 4, FAKE * 64, 1 << 30, None) == lb.LB_ERR_NULL
+    for f in ("U_latent", "V_latent", "Ut", "Vt", "dU", "dV", "dh", "dg", "dl"):
+        assert _bwd(lib, train=_train(**{f: 0})) == lb.LB_ERR_NULL, f
+        assert _bwd(lib, train=_train(**{f: FAR + 2})) == lb.LB_ERR_ALIGN, f
+    assert _bwd(lib, dx=FAKE + 64) == lb.LB_ERR_ARG  # dx overlaps x
+    assert _bwd(lib, dx=FAKE * 2 + 64) == lb.LB_ERR_ARG  # dx overlaps dy
+    assert _bwd(lib, ws=0) == lb.LB_ERR_NULL
+    assert _bwd(lib, ws=FAKE * 64 + 8, ws_bytes=1 << 30) == lb.LB_ERR_ALIGN
+    # dx may be NULL (not computed); U of the paths is never read
+    assert _bwd(lib, dx=0) == lb.LB_ERR_WORKSPACE
+    assert _bwd(lib, paths=_paths(U=FAKE + 1)) == lb.LB_ERR_WORKSPACE

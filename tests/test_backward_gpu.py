@@ -1,0 +1,159 @@
+"""GPU parity of the layer backward (lb_linear_backward) against the oracle's
+backward (O6) on the same seeded inputs.
+
+Bars: dx meets the forward's bar for its dtype (fp32: relative L2 <= 1e-5;
+bf16 / f16: max relative error <= 1e-2 per token row); every fp32 gradient
+(dU, dV, dh, dg, dl of both paths) relative L2 <= 1e-5 over the tensor (all
+products exact, fp32 accumulation).  The latent factors are drawn at a scale
+of 1 / kappa so that the SmoothSign slope varies over its range.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2506_13771_amd import synth
+import lbtest_utils as U
+from conftest import gpu_available
+
+pytestmark = pytest.mark.gpu
+
+if gpu_available():
+    import torch
+    import paper_2506_13771_amd as lb
+
+KAPPA = 100.0
+
+# (T, d_in, d_out, r, act dtype, scale dtype)
+SHAPES = [
+    (64, 256, 192, 48, "bf16", "f16"),
+    (33, 100, 70, 17, "f32", "f32"),
+    (130, 512, 384, 80, "bf16", "bf16"),
+    (5, 96, 64, 31, "f16", "f16"),
+    (200, 1024, 768, 64, "bf16", "f16"),
+    (96, 300, 500, 160, "bf16", "f16"),   # two latent tiles of the token contraction
+    (3, 40, 24, 1, "f32", "bf16"),
+]
+
+
+def _setup(shape, cfg):
+    T, d_in, d_out, r, act, sc = shape
+    li = synth.make_linear(d_in, d_out, r, T, act_dtype=act, scale_dtype=sc, cfg=cfg)
+    rs = np.random.default_rng(cfg * 7919 + T)
+    # latents of the order of 1 / kappa (their signs are the layer's signs)
+    U_lat = [(li.U_latent[p] / KAPPA).astype(np.float32) for p in range(2)]
+    V_lat = [(li.V_latent[p] / KAPPA).astype(np.float32) for p in range(2)]
+    dy_raw = synth.quantize(rs.standard_normal((T, d_out)), act)
+    x, paths, _ = U.to_device(li)
+    dy = U.raw_to_torch(dy_raw, act)
+    train = [lb.LittleBitPathTrain(U_latent=torch.from_numpy(U_lat[p]).cuda(),
+                                   V_latent=torch.from_numpy(V_lat[p]).cuda()) for p in range(2)]
+    return li, x, dy, dy_raw, paths, train, U_lat, V_lat
+
+
+def _oracle(li, dy_raw, U_lat, V_lat):
+    h, g, l = U.oracle_scales(li)
+    x = O.to_f64(li.x, li.act_dtype)
+    dy = O.to_f64(dy_raw, li.act_dtype)
+    return O.backward(x, dy, [u.astype(np.float64) for u in U_lat], [v.astype(np.float64) for v in V_lat],
+                      h, g, l, kappa=KAPPA)
+
+
+def _check_grads(li, dx, train, ref, label):
+    if dx is not None:
+        got = O.to_f64(U.torch_to_raw(dx, li.act_dtype), li.act_dtype)
+        if li.act_dtype == "f32":
+            assert U.rel_l2(got, ref["dx"]) <= U.TOL_F32_REL_L2, (label, U.rel_l2(got, ref["dx"]))
+        else:
+            assert U.row_inf_rel(got, ref["dx"]) <= U.TOL_BF16_ROW_INF, (label, U.row_inf_rel(got, ref["dx"]))
+    for key, attr in (("dU", "dU"), ("dV", "dV"), ("dh", "dh"), ("dg", "dg"), ("dl", "dl")):
+        for p in range(2):
+            got = getattr(train[p], attr).cpu().numpy().astype(np.float64)
+            err = U.rel_l2(got, ref[key][p])
+            assert np.all(np.isfinite(got)) and err <= U.TOL_F32_REL_L2, (label, key, p, err)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_backward_matches_oracle(shape):
+    li, x, dy, dy_raw, paths, train, U_lat, V_lat = _setup(shape, cfg=41)
+    dx = lb.lb_linear_backward(x, dy, paths, train, kappa=KAPPA)
+    torch.cuda.synchronize()
+    _check_grads(li, dx, train, _oracle(li, dy_raw, U_lat, V_lat), str(shape))
+
+
+def test_backward_full_width():
+    # the Llama2-7B q_proj shape at 0.1 BPW (r = 80 per path), 512 tokens
+    shape = (512, 4096, 4096, 80, "bf16", "f16")
+    li, x, dy, dy_raw, paths, train, U_lat, V_lat = _setup(shape, cfg=42)
+    dx = lb.lb_linear_backward(x, dy, paths, train, kappa=KAPPA)
+    torch.cuda.synchronize()
+    _check_grads(li, dx, train, _oracle(li, dy_raw, U_lat, V_lat), "q_proj")
+
+
+def test_backward_without_dx_and_repeated():
+    shape = (100, 320, 256, 48, "bf16", "f16")
+    li, x, dy, dy_raw, paths, train, U_lat, V_lat = _setup(shape, cfg=43)
+    dx = lb.lb_linear_backward(x, dy, paths, train, kappa=KAPPA)
+    torch.cuda.synchronize()
+    first = {k: [getattr(q, k).clone() for q in train] for k in ("dU", "dV", "dh", "dg", "dl")}
+    for rep in range(2):
+        for q in train:
+            for k in first:
+                getattr(q, k).fill_(float("nan"))
+        out = lb.lb_linear_backward(x, dy, paths, train, kappa=KAPPA, need_dx=(rep == 0))
+        torch.cuda.synchronize()
+        if rep == 0:
+            assert torch.equal(out, dx)
+        else:
+            assert out is None
+        for k in first:
+            for p in range(2):
+                assert torch.equal(getattr(train[p], k), first[k][p]), (rep, k, p)
+
+
+def test_backward_empty_sizes():
+    # T = 0, d_in = 0 or r = 0: every non-empty gradient is zero
+    for T, d_in, d_out, r in [(0, 64, 48, 16), (8, 0, 48, 16), (8, 64, 48, 0)]:
+        li = synth.make_linear(64, 48, 16, 8, cfg=44)
+        _, paths, _ = U.to_device(li)
+        x = torch.zeros((T, d_in), dtype=torch.bfloat16, device="cuda")
+        dy = torch.ones((T, d_out), dtype=torch.bfloat16, device="cuda")
+        train = [lb.LittleBitPathTrain(U_latent=torch.randn(d_out, r, device="cuda"),
+                                       V_latent=torch.randn(d_in, r, device="cuda"),
+                                       Ut=torch.zeros(4, dtype=torch.uint8, device="cuda"),
+                                       Vt=torch.zeros(4, dtype=torch.uint8, device="cuda")) for _ in range(2)]
+        for q in train:
+            for k, n in (("dU", (d_out, r)), ("dV", (d_in, r)), ("dh", (d_out,)), ("dg", (d_in,)), ("dl", (r,))):
+                setattr(q, k, torch.full(n, 5.0, device="cuda"))
+        dx = torch.full((T, d_in), 5.0, dtype=torch.bfloat16, device="cuda")
+        lb.lb_linear_backward(x, dy, paths, train, kappa=KAPPA, dx=dx)
+        torch.cuda.synchronize()
+        assert bool((dx == 0).all())
+        for q in train:
+            for k in ("dU", "dV", "dh", "dg", "dl"):
+                assert bool((getattr(q, k) == 0).all()), (T, d_in, r, k)
+
+
+def test_backward_in_a_graph():
+    shape = (64, 512, 384, 48, "bf16", "f16")
+    li, x, dy, dy_raw, paths, train, U_lat, V_lat = _setup(shape, cfg=45)
+    ws = torch.empty(lb.lb_backward_workspace_bytes(64, 512, 384, 48), dtype=torch.uint8, device="cuda")
+    dx = lb.lb_linear_backward(x, dy, paths, train, kappa=KAPPA, workspace=ws)
+    torch.cuda.synchronize()
+    ref = {k: [getattr(q, k).clone() for q in train] for k in ("dU", "dV", "dh", "dg", "dl")}
+    dx_ref = dx.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        lb.lb_linear_backward(x, dy, paths, train, kappa=KAPPA, dx=dx, workspace=ws)
+    for _ in range(3):
+        dx.zero_()
+        for q in train:
+            for k in ref:
+                getattr(q, k).zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dx, dx_ref)
+        for k in ref:
+            for p in range(2):
+                assert torch.equal(getattr(train[p], k), ref[k][p]), k
+        lb.lb_linear_forward(x, paths, li.r)  # eager work between replays
+        torch.cuda.synchronize()
