@@ -14,16 +14,17 @@
 //                                                       dh = rowsum(U_s (.) C_U)
 //   C_V  = x^T dz                  dense, over tokens:  dV = g (.) C_V (.) slope(V_lat),
 //                                                       dg = rowsum(V_s (.) C_V)
-//   dl   = sum_t dw (.) z
+//   dl   = sum_t dw (.) z           (partial sums in the B-term pass of the V side)
 // with slope(u) = kappa sech^2(kappa u).  z (of x) and dw (of dy) are kept in
 // fp32 [T][2][r] in the workspace.
 //
 // The two token contractions run on the matrix cores (tgemm): a workgroup of
 // 4 waves owns 64 rows (outputs or inputs) and up to 128 latents of one path
 // and a run of 32-token steps; each step stages the tile of A (dy or x, cut
-// into its exact bf16 terms) and of B (w or dz, fp32, cut into three exact
-// bf16 terms) in LDS with tokens contiguous, so that both operands read their
-// 8 reduction slots as one 16-byte LDS load.  Every product is exact and the
+// into its exact bf16 terms) and of B (w or dz: fp32, cut into three exact
+// bf16 terms once by a pre-pass, bterms, which writes them with the tokens of
+// a step contiguous) in LDS with tokens contiguous, so that both operands read
+// their 8 reduction slots as one 16-byte LDS load.  Every product is exact and the
 // matrix cores accumulate in fp32; token splits are added in ascending order
 // by the epilogue.
 #include "device_common.h"
@@ -40,20 +41,17 @@ constexpr int kGMaxNk = 8;      // 16-latent subtiles per workgroup
 constexpr int kRow = 40;        // LDS row stride in bf16 (32 tokens + 8 pad)
 constexpr int kGWantWg = 1024;  // workgroups aimed at by the token splits
 constexpr int kGMinSteps = 2;   // fewest steps per token split
-constexpr int kDlChunk = 16;    // tokens per partial sum of dl
 
 struct GemmParams {
-  const void* A;   // [T][M] act dtype
-  const float* B;  // [T][2][r]
-  const void* l[2];
-  float* part;     // [ks][2][M][r]
-  int T, M, r;
+  const void* A;        // [T][M] act dtype
+  const uint16_t* Bt;   // [steps][2][3][kpad][32]: bf16 terms of l (.) B, tokens contiguous
+  float* part;          // [ks][2][M][r]
+  int T, M, r, kpad;
   int n_mt, n_kt, ks, steps_per;
-  int sc_dt;
 };
 
 struct GemmGeom {
-  int nk, n_mt, n_kt, ks, steps_per;
+  int nk, n_mt, n_kt, ks, steps_per, kpad;
   size_t part_floats;
 };
 
@@ -75,16 +73,66 @@ GemmGeom gemm_geom(int T, int M, int r) {
   g.steps_per = (steps + ks - 1) / ks;
   g.ks = (steps + g.steps_per - 1) / g.steps_per;
   g.part_floats = static_cast<size_t>(g.ks) * 2 * r * M;
+  g.kpad = g.n_kt * 16 * g.nk;
   return g;
 }
 
+// partial sums of dl: one per 8-token group
+int dl_parts(int T) { return 4 * (T > kGTok ? (T + kGTok - 1) / kGTok : 1); }
+
+// bytes of the B terms [steps][2][3][kpad][32] bf16
+size_t bterm_bytes(int T, int r) {
+  const GemmGeom g = gemm_geom(T, 1, r);
+  const int steps = T > kGTok ? (T + kGTok - 1) / kGTok : 1;
+  return static_cast<size_t>(steps) * 2 * 3 * g.kpad * kGTok * 2;
+}
+
 __device__ __forceinline__ float load_scale(const void* p, int i, int dt) { return load_as_f32(p, i, dt); }
+
+// B terms: one thread per (step, path, latent, 8-token group) cuts
+// l[k] B[t][p][k] (fp32 product) into its three exact bf16 terms and writes
+// them with the 32 tokens of a step contiguous (zero past T and past r)
+// With zz (the V side, B = dw): also the partial sums of dl over the thread's
+// 8 tokens, dlp[step][oct][p r + k] = sum_s dw z
+__global__ void __launch_bounds__(256) bterms(const float* B, const void* l0, const void* l1, int sc_dt, int T,
+                                              int r, int kpad, uint16_t* Bt, const float* zz, float* dlp) {
+  const int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int oct = static_cast<int>(item & 3);
+  int64_t rest = item >> 2;
+  const int k = static_cast<int>(rest % kpad);
+  rest /= kpad;
+  const int p = static_cast<int>(rest & 1);
+  const int64_t step = rest >> 1;
+  const int steps = T > kGTok ? (T + kGTok - 1) / kGTok : 1;
+  if (step >= steps) return;
+  const bool kok = k < r;
+  const float lv = kok ? load_scale(p ? l1 : l0, k, sc_dt) : 0.0f;
+  uint32_t t3[8][3];
+  float dls = 0.0f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const int64_t t = step * kGTok + 8 * oct + s;
+    const bool ok = kok && t < T;
+    const int64_t i = ok ? (t * 2 + p) * r + k : 0;
+    const float v = B[i];
+    split_exact<3>(ok ? v * lv : 0.0f, t3[s]);
+    if (zz) dls += ok ? v * zz[i] : 0.0f;
+  }
+  if (zz && kok) dlp[(step * 4 + oct) * 2 * r + p * r + k] = dls;
+#pragma unroll
+  for (int f = 0; f < 3; ++f) {
+    u32x4 d;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) d[v] = t3[2 * v][f] | (t3[2 * v + 1][f] << 16);
+    *reinterpret_cast<u32x4*>(Bt + (((step * 2 + p) * 3 + f) * kpad + k) * kGTok + 8 * oct) = d;
+  }
+}
 
 template <int ADT, int NK>
 __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
   constexpr int E = nterms<ADT>();
   constexpr int KT = 16 * NK;
-  constexpr int NBI = (KT * 4 + kGThreads - 1) / kGThreads;  // B items per thread
+  constexpr int NBI = (3 * KT * 4 + kGThreads - 1) / kGThreads;  // 16-byte B pieces per thread
   __shared__ __attribute__((aligned(16))) uint16_t As[E][kGM][kRow];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[3][KT][kRow];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -104,20 +152,9 @@ __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
   // A loader: row am, tokens 8 aq .. 8 aq + 7 of a step
   const int am = tid & 63, aq = tid >> 6;
   const bool a_ok = m0 + am < M;
-  // B loader items: latent bk, tokens 8 bq .. 8 bq + 7
-  int bk[NBI], bq[NBI];
-  bool b_ok[NBI];
-  float lv[NBI];
-#pragma unroll
-  for (int i = 0; i < NBI; ++i) {
-    const int idx = tid + kGThreads * i;
-    bk[i] = idx % KT;
-    bq[i] = idx / KT;
-    b_ok[i] = bq[i] < 4 && k0 + bk[i] < r;
-    lv[i] = b_ok[i] ? load_scale(P.l[p], k0 + bk[i], P.sc_dt) : 0.0f;
-  }
+  // B loader pieces: 16 bytes (8 tokens) of term f of latent k0 + bk
   uint32_t ra[8];
-  float rb[NBI][8];
+  u32x4 rb[NBI];
   auto load = [&](int st) {
     const int tb = (st0 + st) * kGTok;
 #pragma unroll
@@ -127,14 +164,14 @@ __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
       const uint32_t u = ld_bits<ADT>(P.A, ok ? static_cast<int64_t>(t) * M + m0 + am : 0);
       ra[s] = ok ? u : 0u;
     }
+    const uint16_t* bsrc = P.Bt + ((static_cast<int64_t>(st0 + st) * 2 + p) * 3 * P.kpad + k0) * kGTok;
 #pragma unroll
     for (int i = 0; i < NBI; ++i) {
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const int t = tb + 8 * bq[i] + s;
-        const bool ok = b_ok[i] && t < T;
-        const float v = P.B[ok ? (static_cast<int64_t>(t) * 2 + p) * r + k0 + bk[i] : 0];
-        rb[i][s] = ok ? v : 0.0f;
+      const int idx = tid + kGThreads * i;  // (f, bk, oct) with oct fastest
+      if (idx < 3 * KT * 4) {
+        const int f = idx / (KT * 4), rem = idx - f * KT * 4;
+        rb[i] = *reinterpret_cast<const u32x4*>(bsrc + (static_cast<int64_t>(f) * P.kpad + (rem >> 2)) * kGTok +
+                                                8 * (rem & 3));
       }
     }
   };
@@ -156,16 +193,10 @@ __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
     }
 #pragma unroll
     for (int i = 0; i < NBI; ++i) {
-      if (bq[i] >= 4) continue;
-      uint32_t bt[8][3];
-#pragma unroll
-      for (int s = 0; s < 8; ++s) split_exact<3>(rb[i][s] * lv[i], bt[s]);
-#pragma unroll
-      for (int f = 0; f < 3; ++f) {
-        u32x4 d;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) d[v] = bt[2 * v][f] | (bt[2 * v + 1][f] << 16);
-        *reinterpret_cast<u32x4*>(&Bs[f][bk[i]][8 * bq[i]]) = d;
+      const int idx = tid + kGThreads * i;
+      if (idx < 3 * KT * 4) {
+        const int f = idx / (KT * 4), rem = idx - f * KT * 4;
+        *reinterpret_cast<u32x4*>(&Bs[f][rem >> 2][8 * (rem & 3)]) = rb[i];
       }
     }
   };
@@ -259,31 +290,22 @@ __global__ void __launch_bounds__(256) tgemm_epilogue(EpiParams P) {
   if (lane == 0) P.drow[p][m] = acc;
 }
 
-// dl partials: part[ch][c] = sum over the chunk's tokens of dw * z at column
-// c = p r + k of the [T][2][r] arrays
-__global__ void __launch_bounds__(256) dl_partial(const float* dw, const float* z, float* part, int T, int cols) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  const int ch = blockIdx.y;
-  if (c >= cols) return;
-  const int t1 = (ch + 1) * kDlChunk < T ? (ch + 1) * kDlChunk : T;
+// dl[p][k] = sum of the partials of column c = p r + k: one wave per column,
+// lanes over the partials in a fixed order, then a fixed butterfly
+__global__ void __launch_bounds__(256) dl_final(const float* part, int n, int r, float* dl0, float* dl1) {
+  const int lane = threadIdx.x & 63;
+  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (c >= 2 * r) return;  // whole waves
   float s = 0.0f;
-  for (int t = ch * kDlChunk; t < t1; ++t) {
-    const int64_t i = static_cast<int64_t>(t) * cols + c;
-    s += dw[i] * z[i];
+  for (int i = lane; i < n; i += 64) s += part[static_cast<int64_t>(i) * 2 * r + c];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (lane == 0) {
+    if (c < r)
+      dl0[c] = s;
+    else
+      dl1[c - r] = s;
   }
-  part[static_cast<int64_t>(ch) * cols + c] = s;
-}
-
-__global__ void __launch_bounds__(256) dl_final(const float* part, int nch, int r, float* dl0, float* dl1) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= 2 * r) return;
-  float s = 0.0f;
-#pragma unroll 8
-  for (int ch = 0; ch < nch; ++ch) s += part[static_cast<int64_t>(ch) * 2 * r + c];
-  if (c < r)
-    dl0[c] = s;
-  else
-    dl1[c - r] = s;
 }
 
 template <int ADT>
@@ -303,25 +325,28 @@ hipError_t launch_tgemm_nk(const GemmParams& P, int nk, hipStream_t stream) {
 }
 
 // C = A^T (l (.) B) over tokens, then the epilogue into dlat / drow
-hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const float* B, float* part,
+hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const float* B, uint16_t* Bt, float* part,
                           const float* const* lat, const void* const* s, float* const* dlat, float* const* drow,
-                          hipStream_t stream) {
+                          const float* zz, float* dlp, hipStream_t stream) {
   const GemmGeom g = gemm_geom(b.T, M, b.r);
+  const int steps = b.T > kGTok ? (b.T + kGTok - 1) / kGTok : 1;
+  const int64_t items = static_cast<int64_t>(steps) * 2 * g.kpad * 4;
+  hipLaunchKernelGGL(bterms, dim3(static_cast<unsigned>((items + 255) / 256)), dim3(256), 0, stream, B, b.l[0],
+                     b.l[1], b.sc_dt, b.T, b.r, g.kpad, Bt, zz, dlp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   GemmParams P{};
   P.A = A;
-  P.B = B;
-  P.l[0] = b.l[0];
-  P.l[1] = b.l[1];
+  P.Bt = Bt;
   P.part = part;
   P.T = b.T;
   P.M = M;
   P.r = b.r;
+  P.kpad = g.kpad;
   P.n_mt = g.n_mt;
   P.n_kt = g.n_kt;
   P.ks = g.ks;
   P.steps_per = g.steps_per;
-  P.sc_dt = b.sc_dt;
-  hipError_t e;
   switch (b.act_dt) {
     case kDtF32: e = launch_tgemm_nk<kDtF32>(P, g.nk, stream); break;
     case kDtF16: e = launch_tgemm_nk<kDtF16>(P, g.nk, stream); break;
@@ -348,7 +373,7 @@ hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const flo
 size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct BackwardLayout {
-  size_t z_off, dw_off, stage_off, part_off, dl_off, total;
+  size_t z_off, dw_off, stage_off, part_off, bt_off, dl_off, total;
 };
 
 BackwardLayout backward_layout(int T, int d_in, int d_out, int r) {
@@ -361,13 +386,13 @@ BackwardLayout backward_layout(int T, int d_in, int d_out, int r) {
   if (s3 > stage) stage = s3;
   const GemmGeom gu = gemm_geom(T, d_out, r), gv = gemm_geom(T, d_in, r);
   const size_t part = align256(4 * (gu.part_floats > gv.part_floats ? gu.part_floats : gv.part_floats));
-  const int nch = (T + kDlChunk - 1) / kDlChunk;
   L.z_off = kCtrlBytes;
   L.dw_off = L.z_off + lat;
   L.stage_off = L.dw_off + lat;
   L.part_off = L.stage_off + align256(stage);
-  L.dl_off = L.part_off + part;
-  L.total = L.dl_off + align256(static_cast<size_t>(nch) * 2 * r * 4);
+  L.bt_off = L.part_off + part;
+  L.dl_off = L.bt_off + align256(bterm_bytes(T, r));
+  L.total = L.dl_off + align256(static_cast<size_t>(dl_parts(T)) * 2 * r * 4);
   return L;
 }
 
@@ -392,6 +417,7 @@ hipError_t launch_backward(const BackwardArgs& b, hipStream_t stream) {
   float* dw = reinterpret_cast<float*>(ws + L.dw_off);
   float* part = reinterpret_cast<float*>(ws + L.part_off);
   float* dlp = reinterpret_cast<float*>(ws + L.dl_off);
+  uint16_t* bt = reinterpret_cast<uint16_t*>(ws + L.bt_off);
   void* stage = ws + L.stage_off;
   const size_t stage_bytes = L.part_off - L.stage_off;
   hipError_t e;
@@ -438,13 +464,14 @@ hipError_t launch_backward(const BackwardArgs& b, hipStream_t stream) {
     if ((e = launch_stage2_scaled(a, dw, stream)) != hipSuccess) return e;
   }
   // dU, dh from C_U = dy^T (l (.) z); dV, dg from C_V = x^T (l (.) dw)
-  if ((e = run_token_gemm(b, b.dy, b.d_out, z, part, b.U_lat, b.h, b.dU, b.dh, stream)) != hipSuccess) return e;
-  if ((e = run_token_gemm(b, b.x, b.d_in, dw, part, b.V_lat, b.g, b.dV, b.dg, stream)) != hipSuccess) return e;
-  // dl = sum_t dw (.) z
-  const int nch = (b.T + kDlChunk - 1) / kDlChunk, cols = 2 * b.r;
-  hipLaunchKernelGGL(dl_partial, dim3((cols + 255) / 256, nch), dim3(256), 0, stream, dw, z, dlp, b.T, cols);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(dl_final, dim3((cols + 255) / 256), dim3(256), 0, stream, dlp, nch, b.r, b.dl[0], b.dl[1]);
+  if ((e = run_token_gemm(b, b.dy, b.d_out, z, bt, part, b.U_lat, b.h, b.dU, b.dh, nullptr, nullptr, stream)) !=
+      hipSuccess)
+    return e;
+  // the V side's B pass also forms the partial sums of dl = sum_t dw (.) z
+  if ((e = run_token_gemm(b, b.x, b.d_in, dw, bt, part, b.V_lat, b.g, b.dV, b.dg, z, dlp, stream)) != hipSuccess)
+    return e;
+  hipLaunchKernelGGL(dl_final, dim3((2 * b.r + 3) / 4), dim3(256), 0, stream, dlp, dl_parts(b.T), b.r, b.dl[0],
+                     b.dl[1]);
   return hipGetLastError();
 }
 
