@@ -218,16 +218,18 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
    stored token-major: w [T x 2 x r] in latent_dtype (F32, F16 or BF16),
    element (t, p, k) at (2 t + p) r + k, so that the latents of new tokens are
    appended to a cache as one contiguous run.  16-bit latents are rounded to
-   nearest even from fp32; an F32 cache holds the fp32 values the prefill
-   kernels compute, and lb_linear_from_latent on it gives bit for bit what
-   lb_linear_forward_kernel(..., LB_KERNEL_PREFILL) gives for the same x.
+   nearest even from fp32.  For T >= 5 an F32 cache holds the fp32 values the
+   prefill kernels compute, and lb_linear_from_latent on it gives bit for bit
+   what lb_linear_forward_kernel(..., LB_KERNEL_PREFILL) gives for the same x.
 
    lb_linear_latent: w of x [T x d_in] (act_dtype).  Only V, g and l of the
-   paths are read (U and h may be NULL).  Stage 1 of the prefill kernels
-   (exact bf16 term products, fp32 accumulation), then one pass that sums its
-   partial results, scales by l and stores w.  d_in == 0 zero-fills w.  w must
-   not overlap x (LB_ERR_ARG).  workspace: 256-byte aligned, >=
-   lb_latent_workspace_bytes(T, d_in, r) bytes (no zero-fill needed). */
+   paths are read (U and h may be NULL).  T <= 4 (a decoding step): one launch
+   that forms g (.) x in fp32 and adds it with the signs of V in fp32; larger
+   T: stage 1 of the prefill kernels (exact bf16 term products, fp32
+   accumulation), then one pass that sums its partial results, scales by l and
+   stores w.  d_in == 0 zero-fills w.  w must not overlap x (LB_ERR_ARG).
+   workspace: 256-byte aligned, >= lb_latent_workspace_bytes(T, d_in, r) bytes
+   (no zero-fill needed). */
 size_t lb_latent_workspace_bytes(int64_t T, int64_t d_in, int64_t r);
 lb_status lb_linear_latent(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t r,
                            const lb_path* paths, lb_dtype scale_dtype, void* w, lb_dtype latent_dtype,

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblittlebit.so")
-SOURCES = ["api.cpp", "pack.hip", "decode.hip", "decode_mma.hip", "prefill.hip", "backward.hip", "dense_ref.hip"]
+SOURCES = ["api.cpp", "pack.hip", "decode.hip", "decode_mma.hip", "prefill.hip", "latent_small.hip", "backward.hip", "dense_ref.hip"]
 ARCH = os.environ.get("LB_OFFLOAD_ARCH", "gfx950")
 
 

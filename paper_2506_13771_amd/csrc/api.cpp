@@ -6,6 +6,7 @@
 #include <cstring>
 
 #include "lb_backward.h"
+#include "lb_latent.h"
 
 namespace {
 
@@ -395,7 +396,9 @@ lb_status lb_linear_latent(const void* x, lb_dtype act_dtype, int64_t T, int64_t
     e = lb::launch_zero_elems(w, 2 * T * r, latent_dtype, stream);
   } else {
     lb::ForwardArgs a = make_args(x, act_dtype, T, d_in, 0, r, used, scale_dtype, w, workspace, workspace_bytes);
-    e = lb::launch_latent(a, latent_dtype, stream);
+    // a decoding step's few tokens: one launch; otherwise the prefill stage 1
+    e = lb::latent_small_supports(T, d_in, r) ? lb::launch_latent_small(a, latent_dtype, stream)
+                                              : lb::launch_latent(a, latent_dtype, stream);
   }
   return e == hipSuccess ? LB_OK : LB_ERR_HIP;
 }
