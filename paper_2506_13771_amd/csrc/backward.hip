@@ -19,7 +19,8 @@
 // fp32 [T][2][r] in the workspace.
 //
 // The two token contractions run on the matrix cores (tgemm): a workgroup of
-// 4 waves owns 64 rows (outputs or inputs) and up to 128 latents of one path
+// 4 waves owns 128 rows (outputs or inputs; two 16-row blocks per wave, which
+// share each B fragment) and up to 128 latents of one path
 // and a run of 32-token steps; each step stages the tile of A (dy or x, cut
 // into its exact bf16 terms) and of B (w or dz: fp32, cut into three exact
 // bf16 terms once by a pre-pass, bterms, which writes them with the tokens of
@@ -35,11 +36,12 @@ namespace lb {
 namespace {
 
 constexpr int kGThreads = 256;  // 4 waves
-constexpr int kGM = 64;         // rows per workgroup (16 per wave)
+constexpr int kGRB = 2;         // 16-row blocks per wave
+constexpr int kGM = 64 * kGRB;  // rows per workgroup
 constexpr int kGTok = 32;       // tokens per step
 constexpr int kGMaxNk = 8;      // 16-latent subtiles per workgroup
 constexpr int kRow = 40;        // LDS row stride in bf16 (32 tokens + 8 pad)
-constexpr int kGWantWg = 1024;  // workgroups aimed at by the token splits
+constexpr int kGWantWg = 512;   // workgroups aimed at by the token splits
 constexpr int kGMinSteps = 2;   // fewest steps per token split
 
 struct GemmParams {
@@ -149,20 +151,23 @@ __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
   int nst = steps - st0;
   if (nst > P.steps_per) nst = P.steps_per;
 
-  // A loader: row am, tokens 8 aq .. 8 aq + 7 of a step
+  // A loader: rows am + 64 i, tokens 8 aq .. 8 aq + 7 of a step
   const int am = tid & 63, aq = tid >> 6;
-  const bool a_ok = m0 + am < M;
   // B loader pieces: 16 bytes (8 tokens) of term f of latent k0 + bk
-  uint32_t ra[8];
+  uint32_t ra[kGRB][8];
   u32x4 rb[NBI];
   auto load = [&](int st) {
     const int tb = (st0 + st) * kGTok;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const int t = tb + 8 * aq + s;
-      const bool ok = a_ok && t < T;
-      const uint32_t u = ld_bits<ADT>(P.A, ok ? static_cast<int64_t>(t) * M + m0 + am : 0);
-      ra[s] = ok ? u : 0u;
+    for (int i = 0; i < kGRB; ++i) {
+      const bool a_ok = m0 + am + 64 * i < M;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int t = tb + 8 * aq + s;
+        const bool ok = a_ok && t < T;
+        const uint32_t u = ld_bits<ADT>(P.A, ok ? static_cast<int64_t>(t) * M + m0 + am + 64 * i : 0);
+        ra[i][s] = ok ? u : 0u;
+      }
     }
     const uint16_t* bsrc = P.Bt + ((static_cast<int64_t>(st0 + st) * 2 + p) * 3 * P.kpad + k0) * kGTok;
 #pragma unroll
@@ -176,20 +181,23 @@ __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
     }
   };
   auto store = [&]() {
-    uint32_t at[8][E];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      if constexpr (ADT == kDtBF16)
-        at[s][0] = ra[s];
-      else
-        split_exact<E>(bits_to_f32<ADT>(ra[s]), at[s]);
-    }
+    for (int i = 0; i < kGRB; ++i) {
+      uint32_t at[8][E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      u32x4 d;
+      for (int s = 0; s < 8; ++s) {
+        if constexpr (ADT == kDtBF16)
+          at[s][0] = ra[i][s];
+        else
+          split_exact<E>(bits_to_f32<ADT>(ra[i][s]), at[s]);
+      }
 #pragma unroll
-      for (int v = 0; v < 4; ++v) d[v] = at[2 * v][e] | (at[2 * v + 1][e] << 16);
-      *reinterpret_cast<u32x4*>(&As[e][am][8 * aq]) = d;
+      for (int e = 0; e < E; ++e) {
+        u32x4 d;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) d[v] = at[2 * v][e] | (at[2 * v + 1][e] << 16);
+        *reinterpret_cast<u32x4*>(&As[e][am + 64 * i][8 * aq]) = d;
+      }
     }
 #pragma unroll
     for (int i = 0; i < NBI; ++i) {
@@ -201,9 +209,11 @@ __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
     }
   };
 
-  floatx4 acc[NK];
+  floatx4 acc[kGRB][NK];
 #pragma unroll
-  for (int j = 0; j < NK; ++j) acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < kGRB; ++i)
+#pragma unroll
+    for (int j = 0; j < NK; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
   const int fr = lane & 15, fq = lane >> 4;
   if (nst > 0) {
     load(0);
@@ -211,16 +221,21 @@ __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
     __syncthreads();
     for (int st = 0; st < nst; ++st) {
       if (st + 1 < nst) load(st + 1);
-      u32x4 a[E];
+      u32x4 a[kGRB][E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) a[e] = *reinterpret_cast<const u32x4*>(&As[e][16 * wave + fr][8 * fq]);
+      for (int i = 0; i < kGRB; ++i)
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          a[i][e] = *reinterpret_cast<const u32x4*>(&As[e][16 * (wave + 4 * i) + fr][8 * fq]);
 #pragma unroll
       for (int f = 0; f < 3; ++f) {
 #pragma unroll
         for (int j = 0; j < NK; ++j) {
           const u32x4 b = *reinterpret_cast<const u32x4*>(&Bs[f][16 * j + fr][8 * fq]);
 #pragma unroll
-          for (int e = 0; e < E; ++e) acc[j] = mfma(a[e], b, acc[j]);
+          for (int i = 0; i < kGRB; ++i)
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[i][j] = mfma(a[i][e], b, acc[i][j]);
         }
       }
       __syncthreads();
@@ -230,17 +245,19 @@ __global__ void __launch_bounds__(kGThreads) tgemm(GemmParams P) {
       }
     }
   }
-  // partial sums [m][k]: rows 16 wave + 4 fq + e of latent 16 j + fr
+  // partial sums [m][k]: rows 16 (wave + 4 i) + 4 fq + e of latent 16 j + fr
   float* out = P.part + (static_cast<int64_t>(sp) * 2 + p) * r * static_cast<int64_t>(M);
 #pragma unroll
   for (int j = 0; j < NK; ++j) {
     const int k = k0 + 16 * j + fr;
     if (k >= r) continue;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int m = m0 + 16 * wave + 4 * fq + e;
-      if (m < M) out[static_cast<int64_t>(m) * r + k] = acc[j][e];
-    }
+    for (int i = 0; i < kGRB; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + 16 * (wave + 4 * i) + 4 * fq + e;
+        if (m < M) out[static_cast<int64_t>(m) * r + k] = acc[i][j][e];
+      }
   }
 }
 
