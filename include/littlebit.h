@@ -252,7 +252,8 @@ lb_status lb_linear_from_latent(const void* w, lb_dtype latent_dtype, int64_t T,
 
 /* Training-time inputs and gradient outputs of one path for
    lb_linear_backward.  All float arrays are fp32, row-major, 4-byte aligned,
-   owned by the caller; gradients are written, not accumulated. */
+   owned by the caller; gradients are written, not accumulated, and no
+   gradient array may overlap an input or another output (not checked). */
 typedef struct lb_path_train {
   const float* U_latent;  /* [d_out x r] real latent factor whose signs are U_p */
   const float* V_latent;  /* [d_in x r] real latent factor whose signs are V_p */

@@ -157,3 +157,13 @@ def test_backward_in_a_graph():
                 assert torch.equal(getattr(train[p], k), ref[k][p]), k
         lb.lb_linear_forward(x, paths, li.r)  # eager work between replays
         torch.cuda.synchronize()
+
+
+def test_backward_13b_gate_width():
+    # the Llama2-13B gate shape at 0.1 BPW (5120 -> 13824, r = 160 per path: two latent tiles of the
+    # token contraction), 64 tokens
+    shape = (64, 5120, 13824, 160, "bf16", "f16")
+    li, x, dy, dy_raw, paths, train, U_lat, V_lat = _setup(shape, cfg=46)
+    dx = lb.lb_linear_backward(x, dy, paths, train, kappa=KAPPA)
+    torch.cuda.synchronize()
+    _check_grads(li, dx, train, _oracle(li, dy_raw, U_lat, V_lat), "13b gate")

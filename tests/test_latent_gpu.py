@@ -202,3 +202,22 @@ def test_latent_calls_in_a_graph():
         assert torch.equal(w_g, w) and torch.equal(y_g.view(torch.int16), y_eager.view(torch.int16))
         lb.lb_linear_forward(x, paths, 48)  # eager work between replays
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("T", [2, 64])
+def test_latent_cache_at_the_70b_gate_width(T):
+    # 8192 -> 28672 at 0.1 BPW (r = 288 per path): the widest linear of the 70B sweep
+    shape = (T, 8192, 28672, 288, "bf16", "f16")
+    li, x, paths = _setup(shape, cfg=38)
+    w = lb.lb_linear_latent(x, paths, li.r, latent_dtype=torch.bfloat16)
+    y = lb.lb_linear_from_latent(w, paths, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    ref_w = _oracle_latent(li)
+    got_w = O.to_f64(U.torch_to_raw(w, "bf16"), "bf16")
+    scale = np.abs(ref_w).max(axis=2, keepdims=True)
+    assert np.all(np.abs(got_w - ref_w) <= 2.0 ** -8 * np.abs(ref_w) + 1e-5 * scale)
+    # the output from the bf16 cache, on a sample of tokens, against the oracle forward
+    tokens = np.arange(0, T, max(1, T // 8))
+    ref_y = U.oracle_forward(li, tokens)
+    got_y = O.to_f64(U.torch_to_raw(y, "bf16"), "bf16")[tokens]
+    assert U.row_inf_rel(got_y, ref_y) <= U.TOL_BF16_ROW_INF
