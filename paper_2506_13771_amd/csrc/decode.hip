@@ -246,13 +246,20 @@ __device__ __forceinline__ float quad_sum(float v) {
   return v;
 }
 
-template <int TM, int ACT, int SC, int WPL>
+// RB blocks of kRows2 output rows per workgroup (list launches take several:
+// the gathered partials and their tables serve every block)
+template <int TM, int ACT, int SC, int WPL, int RB>
 __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
   const int tid = threadIdx.x;
   const int kq = tid & (kKQ - 1);
-  const int i = q2 * kRows2 + (tid >> 2);  // output row
   const int T = P.T, r = P.r, d_out = P.d_out;
-  const bool iok = i < d_out;
+  int ir[RB];  // output row of each block
+  bool iokr[RB];
+#pragma unroll
+  for (int b = 0; b < RB; ++b) {
+    ir[b] = (q2 * RB + b) * kRows2 + (tid >> 2);
+    iokr[b] = ir[b] < d_out;
+  }
   const int nw = nblocks32(r), nbu = r >> 5, tailu = r & 31;
   const int nsrc = P.direct ? P.s1d : 1;
   const int R4 = (r + 3) & ~3;  // LDS row of the gathered partials (padded to 16 bytes)
@@ -262,21 +269,27 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
 
   // prefetch: this lane's U words (words kq, kq + 4, ... of row i, as two 16-bit
   // halves so that full words and the tail word are the same loads) and h
-  uint32_t wlo[2][WPL], whi[2][WPL], hb[2];
+  uint32_t wlo[RB][2][WPL], whi[RB][2][WPL], hb[RB][2];
   const uint32_t plane = 4u * nbu * d_out;
-  const uint32_t toff = plane + (tailu <= 16 ? 2u : 4u) * i;
 #pragma unroll
-  for (int pp = 0; pp < 2; ++pp) {
-    const rsrc_t ur = make_rsrc(pp ? P.U[1] : P.U[0], P.u_bytes);
+  for (int b = 0; b < RB; ++b) {
+    const int i = ir[b];
+    const bool iok = iokr[b];
+    const uint32_t toff = plane + (tailu <= 16 ? 2u : 4u) * i;
 #pragma unroll
-    for (int e = 0; e < WPL; ++e) {
-      const int kb = kq + kKQ * e;
-      const bool full = iok && kb < nbu, tl = iok && kb == nbu && tailu != 0;
-      const uint32_t off = full ? static_cast<uint32_t>(kb * d_out + i) * 4u : (tl ? toff : kOob);
-      wlo[pp][e] = __builtin_amdgcn_raw_buffer_load_b16(ur, off, 0, 0);
-      whi[pp][e] = __builtin_amdgcn_raw_buffer_load_b16(ur, full || (tl && tailu > 16) ? off + 2 : kOob, 0, 0);
+    for (int pp = 0; pp < 2; ++pp) {
+      const rsrc_t ur = make_rsrc(pp ? P.U[1] : P.U[0], P.u_bytes);
+#pragma unroll
+      for (int e = 0; e < WPL; ++e) {
+        const int kb = kq + kKQ * e;
+        const bool full = iok && kb < nbu, tl = iok && kb == nbu && tailu != 0;
+        const uint32_t off = full ? static_cast<uint32_t>(kb * d_out + i) * 4u : (tl ? toff : kOob);
+        wlo[b][pp][e] = __builtin_amdgcn_raw_buffer_load_b16(ur, off, 0, 0);
+        whi[b][pp][e] =
+            __builtin_amdgcn_raw_buffer_load_b16(ur, full || (tl && tailu > 16) ? off + 2 : kOob, 0, 0);
+      }
+      hb[b][pp] = bload<SC>(make_rsrc(pp ? P.h[1] : P.h[0], P.h_bytes), i, iok);
     }
-    hb[pp] = bload<SC>(make_rsrc(pp ? P.h[1] : P.h[0], P.h_bytes), i, iok);
   }
   uint32_t epoch = load_epoch<2>(P.ctrl);
   uint32_t tag = 0u, done_before = 0u;
@@ -360,28 +373,31 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
     }
     __syncthreads();
     // contraction of row i with both paths; lane kq covers words kq, kq + 4, ...
-    float acc[2][TM];
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
+    for (int b = 0; b < RB; ++b) {
+      float acc[2][TM];
 #pragma unroll
-      for (int t = 0; t < TM; ++t) acc[pp][t] = 0.0f;
+      for (int pp = 0; pp < 2; ++pp)
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
+        for (int t = 0; t < TM; ++t) acc[pp][t] = 0.0f;
 #pragma unroll
-      for (int e = 0; e < WPL; ++e) {
-        const int kb = kq + kKQ * e;
-        if (kb < nw) {
-          const uint32_t wk = ((wlo[pp][e] & 0xffffu) | (whi[pp][e] << 16)) ^ kKey;
+      for (int pp = 0; pp < 2; ++pp)
 #pragma unroll
-          for (int t = 0; t < TM; ++t)
-            if (t < tn) acc[pp][t] += word_sum(tb2 + ((pp * tch + t) * nw + kb) * kBlk, wk);
+        for (int e = 0; e < WPL; ++e) {
+          const int kb = kq + kKQ * e;
+          if (kb < nw) {
+            const uint32_t wk = ((wlo[b][pp][e] & 0xffffu) | (whi[b][pp][e] << 16)) ^ kKey;
+#pragma unroll
+            for (int t = 0; t < TM; ++t)
+              if (t < tn) acc[pp][t] += word_sum(tb2 + ((pp * tch + t) * nw + kb) * kBlk, wk);
+          }
         }
-      }
-    const float h0 = bits_to_f32<SC>(hb[0]), h1 = bits_to_f32<SC>(hb[1]);
+      const float h0 = bits_to_f32<SC>(hb[b][0]), h1 = bits_to_f32<SC>(hb[b][1]);
 #pragma unroll
-    for (int t = 0; t < TM; ++t) {
-      const float v = h0 * quad_sum(acc[0][t]) + h1 * quad_sum(acc[1][t]);
-      if (iok && t < tn && kq == t) st<ACT>(P.y, static_cast<int64_t>(t0 + t) * d_out + i, v);
+      for (int t = 0; t < TM; ++t) {
+        const float v = h0 * quad_sum(acc[0][t]) + h1 * quad_sum(acc[1][t]);
+        if (iokr[b] && t < tn && kq == t) st<ACT>(P.y, static_cast<int64_t>(t0 + t) * d_out + ir[b], v);
+      }
     }
     __syncthreads();  // the next token chunk reuses the LDS
   }
@@ -405,7 +421,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_kernel(DecodeParams P) {
   if (wg < P.n_s1)
     stage1<TM, ACT, SC, VEC>(P, wg, smem);
   else
-    stage2<TM, ACT, SC, WPL>(P, wg - P.n_s1, smem);
+    stage2<TM, ACT, SC, WPL, 1>(P, wg - P.n_s1, smem);
 }
 
 // A list of independent linears in one launch: the stage-1 workgroups of
@@ -415,6 +431,12 @@ __global__ void __launch_bounds__(kThreads, 2) decode_kernel(DecodeParams P) {
 // instantiation serves all of them (TM, WPL: the largest of the list; VEC:
 // only when every member is aligned; stage 2 masks the words a rank does
 // not have).
+// stage 2 of a list launch: blocks of kRows2 rows per workgroup (fewer for
+// wide ranks, whose U words of several blocks would not stay in registers)
+__host__ __device__ constexpr int batch_rows(int wpl) { return wpl <= 2 ? 4 : (wpl <= 4 ? 2 : 1); }
+// ... for one-token lists only (the tables of more tokens leave no registers)
+__host__ __device__ constexpr int list_rows(int tm, int wpl) { return tm == 1 ? batch_rows(wpl) : 1; }
+
 struct DecodeBatch {
   int n;
   int s1_end[kDecodeMaxBatch];  // one past each linear's last stage-1 workgroup
@@ -437,7 +459,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_batch_kernel(DecodeBatch B
     int i = 0;
     while (w2 >= B.s2_end[i]) ++i;
     const DecodeParams P = B.p[i];
-    stage2<TM, ACT, SC, WPL>(P, w2 - (i ? B.s2_end[i - 1] : 0), smem);
+    stage2<TM, ACT, SC, WPL, list_rows(TM, WPL)>(P, w2 - (i ? B.s2_end[i - 1] : 0), smem);
   }
 }
 
@@ -631,8 +653,16 @@ hipError_t launch_decode_batch(const ForwardArgs* a, int n, hipStream_t stream) 
     smem_vec = g.smem_bytes > smem_vec ? g.smem_bytes : smem_vec;
     smem_elem = g.smem_bytes_elem > smem_elem ? g.smem_bytes_elem : smem_elem;
     s1 += g.n_s1;
-    s2 += g.n_s2;
     B.s1_end[i] = s1;
+  }
+  // batch_rows row blocks per stage-2 workgroup (the list's widest rank
+  // decides); the call protocol counts that many workgroups
+  // the token count the launch instantiates (as launch_typed chooses it)
+  const int tm = !vec ? kDecodeMaxTokens : (T <= 1 ? 1 : (T <= 2 ? 2 : 4));
+  const int rb = list_rows(tm, wpl);
+  for (int i = 0; i < n; ++i) {
+    B.p[i].n_s2 = (B.p[i].n_s2 + rb - 1) / rb;
+    s2 += B.p[i].n_s2;
     B.s2_end[i] = s2;
   }
   return launch_any(B, a[0].act_dt, T, a[0].sc_dt, vec, wpl, dim3(s1 + s2), vec ? smem_vec : smem_elem, stream);
