@@ -151,3 +151,18 @@ def test_many_graph_replays_match_eager():
         for i in range(len(lins)):
             assert _same_bits(y_graph[i], y_eager[i]), (rep, i)
             assert _same_bits(y_mid[i], y_eager[i]), (rep, i)
+
+
+def test_many_one_token_lists_of_every_row_block_count():
+    # one-token list launches give each stage-2 workgroup 4, 2 or 1 blocks of 64 rows by the U
+    # words a lane holds (ranks up to 256, up to 512, above); ragged row counts leave the last
+    # workgroup's blocks partly or wholly past d_out
+    for specs in ([(1, 640, 900, 200, "bf16", "f16"), (1, 512, 70, 64, "bf16", "f16"), (1, 300, 1000, 96, "bf16", "f16")],
+                  [(1, 1024, 700, 300, "bf16", "f16"), (1, 512, 65, 200, "bf16", "f16"), (1, 2048, 2112, 288, "bf16", "f16")],
+                  [(1, 1024, 777, 600, "bf16", "f16"), (1, 640, 130, 40, "bf16", "f16")]):
+        lins = _linears(specs, cfg=26)
+        ys, _ = _many(lins)
+        ref = _singles(lins)
+        for i, ((li, _, _), y, r) in enumerate(zip(lins, ys, ref)):
+            assert _same_bits(y, r), (i, specs[i])
+            _check(li, U.torch_to_raw(y, "bf16"), label=f"row blocks {specs[i]}")
