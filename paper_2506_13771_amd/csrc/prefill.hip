@@ -550,6 +550,18 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
   }
 }
 
+// sign_terms for +-1.0 pairs with one bitfield insert per register: M (the
+// two bf16 sign bits) and B (two bf16 1.0) are kept in registers by the
+// caller, opaque to constant folding, so that (x & M) | (B & ~M) becomes
+// v_bfi_b32 instead of an and and an or with literals
+__device__ __forceinline__ u32x4 sign_ones(uint32_t word, int gq, uint32_t M, uint32_t B) {
+  const uint32_t ws = word >> (4 * gq);
+  u32x4 a;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) a[v] = ((ws << (15 - v)) & M) | (B & ~M);
+  return a;
+}
+
 // FAST: d_out % 4 == 0 and aligned U, h and y, so the U words of a unit come
 // in 16-byte global-to-LDS loads (4 blocks of 64 outputs a load), its scales
 // and 16-bit tail words in dword ones (all prefetched a unit ahead) and y in
@@ -680,7 +692,8 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
   };
 
   floatx4 acc[2][kIm2][kTn2];
-  const uint32_t ones[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+  uint32_t sgn_m = 0x80008000u, one_b = 0x3F803F80u;
+  asm volatile("" : "+v"(sgn_m), "+v"(one_b));
   // products of one held pair: w from held slot hs, the U words from LDS
   // (full) or the 16-bit tail words (W16)
   auto pair = [&](auto pc, auto w16, int hs, const uint32_t* words, int buf, const uint32_t (&tw)[kIm2]) {
@@ -701,7 +714,7 @@ __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
         word = *reinterpret_cast<const uint16_t*>(region(buf) + wdp * 256 + 512 + p * 256 + (16 * im + n16) * 2);
       else
         word = tw[im] & 0xffffu;
-      const u32x4 A = sign_terms(word, gq, ones);
+      const u32x4 A = sign_ones(word, gq, sgn_m, one_b);
 #pragma unroll
       for (int e = 0; e < NW; ++e)
 #pragma unroll
