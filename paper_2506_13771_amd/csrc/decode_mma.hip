@@ -274,7 +274,7 @@ __device__ __forceinline__ void mma_stage1(const MmaParams& P, int wg, float* sm
 // ---------------------------------------------------------------------------
 // stage 2
 // ---------------------------------------------------------------------------
-template <int ACT, int SC>
+template <int ACT, int SC, int RB>
 __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* smem) {
   constexpr int NW = ACT == kDtF32 ? 3 : 2;  // bf16 terms of w
   const int T = P.T, r = P.r, d_out = P.d_out;
@@ -286,26 +286,27 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
   const int nsrc = P.direct ? P.s1d : 1;
   const int tch = min(16, T);  // tokens per chunk
   const int R32 = 32 * nkb;    // row stride of the summed w (zero past r)
-  const int qrow0 = q * kWaves * 16;
+  constexpr int RW = 64 * RB;  // rows of this workgroup: RB blocks of 64 (list launches take several)
+  const int qrow0 = q * RW;
 
-  // LDS: U words [2][nkb][64 rows] (block nbu holds the tail word), summed w
+  // LDS: U words [2][nkb][RW rows] (block nbu holds the tail word), summed w
   // [2][tch][R32], and (when there are several partials per value) the
   // gathered partials [2][tch][nsrc][r]
   uint32_t* uwl = reinterpret_cast<uint32_t*>(smem);
-  float* wsum = smem + 2 * nkb * 64;
+  float* wsum = smem + 2 * nkb * RW;
   float* raw = wsum + 2 * tch * R32;
 
-  // prefetch (cooperative, raw): the U words of this workgroup's 64 rows, and
+  // prefetch (cooperative, raw): the U words of this workgroup's rows, and
   // the row scales of this lane's output rows; then the epoch
-  constexpr int kUPer = (kMaxUWords + 1) * 64 / kThreads + 1;  // entries per thread and path
+  constexpr int kUPer = (kMaxUWords + 1) * RW / kThreads + 1;  // entries per thread and path
   uint32_t ulo[2][kUPer], uhi[2][kUPer];
 #pragma unroll
   for (int pp = 0; pp < 2; ++pp) {
     const rsrc_t ur = make_rsrc(pp ? P.U[1] : P.U[0], P.u_bytes);
 #pragma unroll
     for (int j = 0; j < kUPer; ++j) {
-      const int e = tid + kThreads * j;  // (kb, row) = (e >> 6, e & 63)
-      const int kb = e >> 6, row = qrow0 + (e & 63);
+      const int e = tid + kThreads * j;  // (kb, row) = (e / RW, e % RW)
+      const int kb = e / RW, row = qrow0 + (e % RW);
       const bool full = kb < nbu, tl = kb == nbu && tailu != 0;
       const uint32_t plane = 4u * nbu * d_out;
       const uint32_t toff = tailu <= 16 ? plane + 2u * row : plane + 4u * row;
@@ -316,13 +317,15 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
           __builtin_amdgcn_raw_buffer_load_b16(ur, full || (tl && tailu > 16) ? off + 2 : kOob, 0, 0));
     }
   }
-  uint32_t hb[2][4];
+  uint32_t hb[RB][2][4];
 #pragma unroll
-  for (int pp = 0; pp < 2; ++pp) {
-    const rsrc_t hr = make_rsrc(pp ? P.h[1] : P.h[0], P.h_bytes);
+  for (int b = 0; b < RB; ++b)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) hb[pp][e] = bload<SC>(hr, qrow0 + wave * 16 + 4 * gq + e);
-  }
+    for (int pp = 0; pp < 2; ++pp) {
+      const rsrc_t hr = make_rsrc(pp ? P.h[1] : P.h[0], P.h_bytes);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) hb[b][pp][e] = bload<SC>(hr, qrow0 + 64 * b + wave * 16 + 4 * gq + e);
+    }
   uint32_t epoch = load_epoch<4>(P.ctrl);
   pin(epoch);
   const uint32_t tag = epoch + 1u;
@@ -334,7 +337,7 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
 #pragma unroll
     for (int j = 0; j < kUPer; ++j) {
       const int e = tid + kThreads * j;
-      if (e < nkb * 64) uwl[pp * nkb * 64 + e] = ulo[pp][j] | (uhi[pp][j] << 16);
+      if (e < nkb * RW) uwl[pp * nkb * RW + e] = ulo[pp][j] | (uhi[pp][j] << 16);
     }
 
   bool ok = true;
@@ -406,15 +409,15 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
     __syncthreads();
     // contraction: A = the signs of U row qrow0 + wave * 16 + n16 (+-1), B = w
     // of token column n16 at latents 32 kb + 4 gq + v (+16), as NW bf16 terms
-    floatx4 acc[2];
-    acc[0] = acc[1] = floatx4{0.f, 0.f, 0.f, 0.f};
+    floatx4 acc[RB][2];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) acc[b][0] = acc[b][1] = floatx4{0.f, 0.f, 0.f, 0.f};
     const uint32_t ones[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
 #pragma unroll
     for (int pp = 0; pp < 2; ++pp) {
       const float* wrow = wsum + (pp * tch + (n16 < tch ? n16 : 0)) * R32 + 4 * gq;
-      const uint32_t* ucol = uwl + pp * nkb * 64 + wave * 16 + n16;
+      const uint32_t* ucol = uwl + pp * nkb * RW + wave * 16 + n16;
       for (int kb = 0; kb < nkb; ++kb) {
-        const u32x4 A = sign_terms(ucol[kb * 64], gq, ones);
         const float4 w0 = *reinterpret_cast<const float4*>(wrow + 32 * kb);
         const float4 w1 = *reinterpret_cast<const float4*>(wrow + 32 * kb + 16);
         const float wl[4] = {w0.x, w0.y, w0.z, w0.w}, wh[4] = {w1.x, w1.y, w1.z, w1.w};
@@ -424,24 +427,31 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
           split_round<NW>(wl[v], lo[v]);
           split_round<NW>(wh[v], hi[v]);
         }
+        u32x4 B[NW];
 #pragma unroll
-        for (int a = 0; a < NW; ++a) {
-          u32x4 B;
+        for (int a = 0; a < NW; ++a)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) B[v] = lo[v][a] | (hi[v][a] << 16);
-          acc[pp] = mfma(A, B, acc[pp]);
+          for (int v = 0; v < 4; ++v) B[a][v] = lo[v][a] | (hi[v][a] << 16);
+        // the w terms of this block serve every row block
+#pragma unroll
+        for (int b = 0; b < RB; ++b) {
+          const u32x4 A = sign_terms(ucol[kb * RW + 64 * b], gq, ones);
+#pragma unroll
+          for (int a = 0; a < NW; ++a) acc[b][pp] = mfma(A, B[a], acc[b][pp]);
         }
       }
     }
-    // y[t][i] = h_0[i] acc_0 + h_1[i] acc_1 for rows i = qrow0 + wave * 16 + 4 gq + e
+    // y[t][i] = h_0[i] acc_0 + h_1[i] acc_1 for rows i = qrow0 + 64 b + wave * 16 + 4 gq + e
     const int t = t0 + n16;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int i = qrow0 + wave * 16 + 4 * gq + e;
-      if (t < T && i < d_out)
-        st<ACT>(P.y, static_cast<int64_t>(t) * d_out + i,
-                bits_to_f32<SC>(hb[0][e]) * acc[0][e] + bits_to_f32<SC>(hb[1][e]) * acc[1][e]);
-    }
+    for (int b = 0; b < RB; ++b)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = qrow0 + 64 * b + wave * 16 + 4 * gq + e;
+        if (t < T && i < d_out)
+          st<ACT>(P.y, static_cast<int64_t>(t) * d_out + i,
+                  bits_to_f32<SC>(hb[b][0][e]) * acc[b][0][e] + bits_to_f32<SC>(hb[b][1][e]) * acc[b][1][e]);
+      }
     __syncthreads();  // the next chunk reuses the LDS
   }
   if (!ok) atomic_store_relaxed(P.ctrl + kCtrlError, 1u);
@@ -463,7 +473,7 @@ __global__ void __launch_bounds__(kThreads, 1) decode_mma_kernel(MmaParams P) {
   if (wg < P.n_s1)
     mma_stage1<TT, ACT, SC, VEC>(P, wg, smem);
   else
-    mma_stage2<ACT, SC>(P, wg - P.n_s1, smem);
+    mma_stage2<ACT, SC, 1>(P, wg - P.n_s1, smem);
 }
 
 // A list of independent linears in one launch (the stage-1 workgroups of
@@ -476,6 +486,8 @@ struct MmaBatch {
   int s2_end[kDecodeMaxBatch];  // the same for stage 2, counted from the first stage-2 workgroup
   MmaParams p[kDecodeMaxBatch];
 };
+
+constexpr int kMmaListRows = 2;  // stage 2 of a list launch: blocks of 64 rows per workgroup
 
 template <int TT, int ACT, int SC, bool VEC>
 __global__ void __launch_bounds__(kThreads, 1) decode_mma_batch_kernel(MmaBatch B) {
@@ -492,7 +504,7 @@ __global__ void __launch_bounds__(kThreads, 1) decode_mma_batch_kernel(MmaBatch 
     int i = 0;
     while (w2 >= B.s2_end[i]) ++i;
     const MmaParams P = B.p[i];
-    mma_stage2<ACT, SC>(P, w2 - (i ? B.s2_end[i - 1] : 0), smem);
+    mma_stage2<ACT, SC, kMmaListRows>(P, w2 - (i ? B.s2_end[i - 1] : 0), smem);
   }
 }
 
@@ -675,16 +687,30 @@ hipError_t launch_decode_mma_batch(const ForwardArgs* a, int n, hipStream_t stre
     MmaBatch B{};
     int s1 = 0, s2 = 0, T = 0;
     size_t smem = 0;
+    // LDS of a member in a list launch (U words of kMmaListRows x 64 rows)
+    auto list_smem = [&](int j) {
+      return G[j].smem_bytes + static_cast<size_t>(4) * 2 * nblocks32(a[j].r) * 64 * (kMmaListRows - 1);
+    };
+    constexpr size_t kMaxLds = 160 * 1024;
     for (int j = i; j < n; ++j) {
       if (done[j] || (a[j].T + 15) / 16 != tt || (P[j].vec != 0) != vec) continue;
+      if (list_smem(j) > kMaxLds && B.n > 0) continue;  // a launch of its own later
       done[j] = true;
+      if (list_smem(j) > kMaxLds) {  // j == i: alone, as a single call
+        B.p[0] = P[j];
+        B.n = 1;
+        break;
+      }
       B.p[B.n] = P[j];
+      // kMmaListRows row blocks per stage-2 workgroup: that many fewer
+      // workgroups, U words of that many rows in LDS
+      B.p[B.n].n_s2 = (G[j].n_s2 + kMmaListRows - 1) / kMmaListRows;
       s1 += G[j].n_s1;
-      s2 += G[j].n_s2;
+      s2 += B.p[B.n].n_s2;
       B.s1_end[B.n] = s1;
       B.s2_end[B.n] = s2;
       T = a[j].T > T ? a[j].T : T;
-      smem = G[j].smem_bytes > smem ? G[j].smem_bytes : smem;
+      smem = list_smem(j) > smem ? list_smem(j) : smem;
       ++B.n;
     }
     const hipError_t e = B.n == 1 ? launch_any(P[i], a[i].act_dt, a[i].T, vec, a[i].sc_dt,
