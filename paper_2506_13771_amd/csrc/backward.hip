@@ -14,7 +14,7 @@
 //                                                       dh = rowsum(U_s (.) C_U)
 //   C_V  = x^T dz                  dense, over tokens:  dV = g (.) C_V (.) slope(V_lat),
 //                                                       dg = rowsum(V_s (.) C_V)
-//   dl   = sum_t dw (.) z           (partial sums in the B-term pass of the V side)
+//   dl   = sum_t dw (.) z           (partial sums in the B-term pass of the V side, added by its epilogue)
 // with slope(u) = kappa sech^2(kappa u).  z (of x) and dw (of dy) are kept in
 // fp32 [T][2][r] in the workspace.
 //
@@ -269,6 +269,10 @@ struct EpiParams {
   float* drow[2];
   int M, r, ks, sc_dt;
   float kappa;
+  // with dlp: the workgroups past the rows' also add dl's partial sums
+  const float* dlp;
+  int n_dl;  // partials per column
+  float* dl[2];
 };
 
 // d/du tanh(kappa u) = kappa sech^2(kappa u) = 4 kappa e / (1 + e)^2 with
@@ -282,8 +286,29 @@ __device__ __forceinline__ float smooth_slope(float kappa, float u) {
 // one wave per (path, row), lanes over latents: sums the token splits in
 // ascending order, writes the latent-factor gradient, and the row-scale
 // gradient through a fixed butterfly over the wave
+// dl[p][k] = sum of the partials of column c = p r + k, by one wave: lanes
+// over the partials in a fixed order, then a fixed butterfly
+__device__ void dl_column(const float* part, int n, int r, int c, int lane, float* dl0, float* dl1) {
+  float s = 0.0f;
+  for (int i = lane; i < n; i += 64) s += part[static_cast<int64_t>(i) * 2 * r + c];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (lane == 0) {
+    if (c < r)
+      dl0[c] = s;
+    else
+      dl1[c - r] = s;
+  }
+}
+
 __global__ void __launch_bounds__(256) tgemm_epilogue(EpiParams P) {
   const int lane = threadIdx.x & 63;
+  const int nrow_wg = (2 * P.M + 3) / 4;
+  if (static_cast<int>(blockIdx.x) >= nrow_wg) {  // dl: one wave per column
+    const int c = (blockIdx.x - nrow_wg) * 4 + (threadIdx.x >> 6);
+    if (c < 2 * P.r) dl_column(P.dlp, P.n_dl, P.r, c, lane, P.dl[0], P.dl[1]);
+    return;
+  }
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= 2 * P.M) return;  // whole waves leave together
   const int p = row >= P.M ? 1 : 0;
@@ -307,24 +332,6 @@ __global__ void __launch_bounds__(256) tgemm_epilogue(EpiParams P) {
   if (lane == 0) P.drow[p][m] = acc;
 }
 
-// dl[p][k] = sum of the partials of column c = p r + k: one wave per column,
-// lanes over the partials in a fixed order, then a fixed butterfly
-__global__ void __launch_bounds__(256) dl_final(const float* part, int n, int r, float* dl0, float* dl1) {
-  const int lane = threadIdx.x & 63;
-  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (c >= 2 * r) return;  // whole waves
-  float s = 0.0f;
-  for (int i = lane; i < n; i += 64) s += part[static_cast<int64_t>(i) * 2 * r + c];
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
-  if (lane == 0) {
-    if (c < r)
-      dl0[c] = s;
-    else
-      dl1[c - r] = s;
-  }
-}
-
 template <int ADT>
 hipError_t launch_tgemm_nk(const GemmParams& P, int nk, hipStream_t stream) {
   const dim3 grid(P.n_mt * P.n_kt * 2 * P.ks), block(kGThreads);
@@ -344,7 +351,7 @@ hipError_t launch_tgemm_nk(const GemmParams& P, int nk, hipStream_t stream) {
 // C = A^T (l (.) B) over tokens, then the epilogue into dlat / drow
 hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const float* B, uint16_t* Bt, float* part,
                           const float* const* lat, const void* const* s, float* const* dlat, float* const* drow,
-                          const float* zz, float* dlp, hipStream_t stream) {
+                          const float* zz, float* dlp, bool with_dl, hipStream_t stream) {
   const GemmGeom g = gemm_geom(b.T, M, b.r);
   const int steps = b.T > kGTok ? (b.T + kGTok - 1) / kGTok : 1;
   const int64_t items = static_cast<int64_t>(steps) * 2 * g.kpad * 4;
@@ -383,7 +390,16 @@ hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const flo
   Q.ks = g.ks;
   Q.sc_dt = b.sc_dt;
   Q.kappa = b.kappa;
-  hipLaunchKernelGGL(tgemm_epilogue, dim3((2 * M + 3) / 4), dim3(256), 0, stream, Q);
+  // the V side's epilogue also adds dl's partial sums (formed by its B-term
+  // pass), in workgroups of their own after the rows'
+  const int n_dl_wg = with_dl ? (2 * b.r + 3) / 4 : 0;
+  if (with_dl) {
+    Q.dlp = dlp;
+    Q.n_dl = dl_parts(b.T);
+    Q.dl[0] = b.dl[0];
+    Q.dl[1] = b.dl[1];
+  }
+  hipLaunchKernelGGL(tgemm_epilogue, dim3((2 * M + 3) / 4 + n_dl_wg), dim3(256), 0, stream, Q);
   return hipGetLastError();
 }
 
@@ -481,15 +497,12 @@ hipError_t launch_backward(const BackwardArgs& b, hipStream_t stream) {
     if ((e = launch_stage2_scaled(a, dw, stream)) != hipSuccess) return e;
   }
   // dU, dh from C_U = dy^T (l (.) z); dV, dg from C_V = x^T (l (.) dw)
-  if ((e = run_token_gemm(b, b.dy, b.d_out, z, bt, part, b.U_lat, b.h, b.dU, b.dh, nullptr, nullptr, stream)) !=
-      hipSuccess)
+  if ((e = run_token_gemm(b, b.dy, b.d_out, z, bt, part, b.U_lat, b.h, b.dU, b.dh, nullptr, nullptr, false,
+                          stream)) != hipSuccess)
     return e;
-  // the V side's B pass also forms the partial sums of dl = sum_t dw (.) z
-  if ((e = run_token_gemm(b, b.x, b.d_in, dw, bt, part, b.V_lat, b.g, b.dV, b.dg, z, dlp, stream)) != hipSuccess)
-    return e;
-  hipLaunchKernelGGL(dl_final, dim3((2 * b.r + 3) / 4), dim3(256), 0, stream, dlp, dl_parts(b.T), b.r, b.dl[0],
-                     b.dl[1]);
-  return hipGetLastError();
+  // the V side's B pass forms the partial sums of dl = sum_t dw (.) z and its
+  // epilogue adds them
+  return run_token_gemm(b, b.x, b.d_in, dw, bt, part, b.V_lat, b.g, b.dV, b.dg, z, dlp, true, stream);
 }
 
 }  // namespace lb
