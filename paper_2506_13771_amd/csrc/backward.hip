@@ -96,9 +96,23 @@ __device__ __forceinline__ float load_scale(const void* p, int i, int dt) { retu
 // them with the 32 tokens of a step contiguous (zero past T and past r)
 // With zz (the V side, B = dw): also the partial sums of dl over the thread's
 // 8 tokens, dlp[step][oct][p r + k] = sum_s dw z
-__global__ void __launch_bounds__(256) bterms(const float* B, const void* l0, const void* l1, int sc_dt, int T,
-                                              int r, int kpad, uint16_t* Bt, const float* zz, float* dlp) {
-  const int64_t item = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+// Both sides in one launch: the first nb1 workgroups take job 0 (U side:
+// B = z), the rest job 1 (V side: B = dw, with zz = z and the dl partials).
+struct BtermJob {
+  const float* B;
+  uint16_t* Bt;
+  const float* zz;
+  float* dlp;
+};
+__global__ void __launch_bounds__(256) bterms(BtermJob j0, BtermJob j1, int nb1, const void* l0, const void* l1,
+                                              int sc_dt, int T, int r, int kpad) {
+  const bool second = static_cast<int>(blockIdx.x) >= nb1;
+  const BtermJob& J = second ? j1 : j0;
+  const float* B = J.B;
+  uint16_t* Bt = J.Bt;
+  const float* zz = J.zz;
+  float* dlp = J.dlp;
+  const int64_t item = static_cast<int64_t>(second ? blockIdx.x - nb1 : blockIdx.x) * 256 + threadIdx.x;
   const int oct = static_cast<int>(item & 3);
   int64_t rest = item >> 2;
   const int k = static_cast<int>(rest % kpad);
@@ -348,17 +362,25 @@ hipError_t launch_tgemm_nk(const GemmParams& P, int nk, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// C = A^T (l (.) B) over tokens, then the epilogue into dlat / drow
-hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const float* B, uint16_t* Bt, float* part,
-                          const float* const* lat, const void* const* s, float* const* dlat, float* const* drow,
-                          const float* zz, float* dlp, bool with_dl, hipStream_t stream) {
-  const GemmGeom g = gemm_geom(b.T, M, b.r);
+// the B terms of both sides (z for U, dw for V) and dl's partial sums
+hipError_t run_bterms(const BackwardArgs& b, const float* z, const float* dw, uint16_t* bt_u, uint16_t* bt_v,
+                      float* dlp, hipStream_t stream) {
+  const GemmGeom g = gemm_geom(b.T, 1, b.r);
   const int steps = b.T > kGTok ? (b.T + kGTok - 1) / kGTok : 1;
   const int64_t items = static_cast<int64_t>(steps) * 2 * g.kpad * 4;
-  hipLaunchKernelGGL(bterms, dim3(static_cast<unsigned>((items + 255) / 256)), dim3(256), 0, stream, B, b.l[0],
-                     b.l[1], b.sc_dt, b.T, b.r, g.kpad, Bt, zz, dlp);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  const int nb1 = static_cast<int>((items + 255) / 256);
+  const BtermJob ju{z, bt_u, nullptr, nullptr}, jv{dw, bt_v, z, dlp};
+  hipLaunchKernelGGL(bterms, dim3(2 * nb1), dim3(256), 0, stream, ju, jv, nb1, b.l[0], b.l[1], b.sc_dt, b.T, b.r,
+                     g.kpad);
+  return hipGetLastError();
+}
+
+// C = A^T Bt (the terms of l (.) B) over tokens, then the epilogue into dlat / drow
+hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const uint16_t* Bt, float* part,
+                          const float* const* lat, const void* const* s, float* const* dlat, float* const* drow,
+                          float* dlp, bool with_dl, hipStream_t stream) {
+  const GemmGeom g = gemm_geom(b.T, M, b.r);
+  hipError_t e;
   GemmParams P{};
   P.A = A;
   P.Bt = Bt;
@@ -406,7 +428,7 @@ hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const flo
 size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct BackwardLayout {
-  size_t z_off, dw_off, stage_off, part_off, bt_off, dl_off, total;
+  size_t z_off, dw_off, stage_off, part_off, bt_off, bt2_off, dl_off, total;
 };
 
 BackwardLayout backward_layout(int T, int d_in, int d_out, int r) {
@@ -424,7 +446,8 @@ BackwardLayout backward_layout(int T, int d_in, int d_out, int r) {
   L.stage_off = L.dw_off + lat;
   L.part_off = L.stage_off + align256(stage);
   L.bt_off = L.part_off + part;
-  L.dl_off = L.bt_off + align256(bterm_bytes(T, r));
+  L.bt2_off = L.bt_off + align256(bterm_bytes(T, r));
+  L.dl_off = L.bt2_off + align256(bterm_bytes(T, r));
   L.total = L.dl_off + align256(static_cast<size_t>(dl_parts(T)) * 2 * r * 4);
   return L;
 }
@@ -451,6 +474,7 @@ hipError_t launch_backward(const BackwardArgs& b, hipStream_t stream) {
   float* part = reinterpret_cast<float*>(ws + L.part_off);
   float* dlp = reinterpret_cast<float*>(ws + L.dl_off);
   uint16_t* bt = reinterpret_cast<uint16_t*>(ws + L.bt_off);
+  uint16_t* bt2 = reinterpret_cast<uint16_t*>(ws + L.bt2_off);
   void* stage = ws + L.stage_off;
   const size_t stage_bytes = L.part_off - L.stage_off;
   hipError_t e;
@@ -497,12 +521,13 @@ hipError_t launch_backward(const BackwardArgs& b, hipStream_t stream) {
     if ((e = launch_stage2_scaled(a, dw, stream)) != hipSuccess) return e;
   }
   // dU, dh from C_U = dy^T (l (.) z); dV, dg from C_V = x^T (l (.) dw)
-  if ((e = run_token_gemm(b, b.dy, b.d_out, z, bt, part, b.U_lat, b.h, b.dU, b.dh, nullptr, nullptr, false,
-                          stream)) != hipSuccess)
+  // B terms of both sides in one launch (the V side's pass also forms the
+  // partial sums of dl = sum_t dw (.) z, which its epilogue adds)
+  if ((e = run_bterms(b, z, dw, bt, bt2, dlp, stream)) != hipSuccess) return e;
+  if ((e = run_token_gemm(b, b.dy, b.d_out, bt, part, b.U_lat, b.h, b.dU, b.dh, nullptr, false, stream)) !=
+      hipSuccess)
     return e;
-  // the V side's B pass forms the partial sums of dl = sum_t dw (.) z and its
-  // epilogue adds them
-  return run_token_gemm(b, b.x, b.d_in, dw, bt, part, b.V_lat, b.g, b.dV, b.dg, z, dlp, true, stream);
+  return run_token_gemm(b, b.x, b.d_in, bt2, part, b.V_lat, b.g, b.dV, b.dg, dlp, true, stream);
 }
 
 }  // namespace lb
