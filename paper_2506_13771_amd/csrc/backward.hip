@@ -428,23 +428,25 @@ hipError_t run_token_gemm(const BackwardArgs& b, const void* A, int M, const uin
 size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct BackwardLayout {
-  size_t z_off, dw_off, stage_off, part_off, bt_off, bt2_off, dl_off, total;
+  size_t z_off, dw_off, stage_off, stage2_off, part_off, bt_off, bt2_off, dl_off, total;
 };
 
 BackwardLayout backward_layout(int T, int d_in, int d_out, int r) {
   BackwardLayout L{};
   const size_t lat = align256(static_cast<size_t>(T) * 2 * r * 4);
+  // stage areas: x's stage 1 then dx's stage 2 in the first, dy's stage 1 in
+  // the second (both stage-1 runs' partials are alive at once)
   size_t stage = latent_workspace_bytes(T, d_in, r);
   const size_t s2 = latent_workspace_bytes(T, d_out, r);
   const size_t s3 = from_latent_workspace_bytes(T, r);
-  if (s2 > stage) stage = s2;
   if (s3 > stage) stage = s3;
   const GemmGeom gu = gemm_geom(T, d_out, r), gv = gemm_geom(T, d_in, r);
   const size_t part = align256(4 * (gu.part_floats > gv.part_floats ? gu.part_floats : gv.part_floats));
   L.z_off = kCtrlBytes;
   L.dw_off = L.z_off + lat;
   L.stage_off = L.dw_off + lat;
-  L.part_off = L.stage_off + align256(stage);
+  L.stage2_off = L.stage_off + align256(stage);
+  L.part_off = L.stage2_off + align256(s2);
   L.bt_off = L.part_off + part;
   L.bt2_off = L.bt_off + align256(bterm_bytes(T, r));
   L.dl_off = L.bt2_off + align256(bterm_bytes(T, r));
@@ -476,35 +478,28 @@ hipError_t launch_backward(const BackwardArgs& b, hipStream_t stream) {
   uint16_t* bt = reinterpret_cast<uint16_t*>(ws + L.bt_off);
   uint16_t* bt2 = reinterpret_cast<uint16_t*>(ws + L.bt2_off);
   void* stage = ws + L.stage_off;
-  const size_t stage_bytes = L.part_off - L.stage_off;
+  const size_t stage_bytes = L.stage2_off - L.stage_off;
   hipError_t e;
-  // z of x: stage 1 through V and g
+  // z of x (stage 1 through V and g) and dw of dy (stage 1 through U, role V
+  // packing, and h): two stage-1 launches, one launch for both split sums
   {
-    ForwardArgs a{};
-    a.x = b.x;
-    a.act_dt = b.act_dt;
-    a.T = b.T;
-    a.d_in = b.d_in;
-    a.r = b.r;
-    for (int p = 0; p < 2; ++p) a.V[p] = b.V[p], a.g[p] = b.g[p], a.l[p] = b.l[p];
-    a.sc_dt = b.sc_dt;
-    a.ws = stage;
-    a.ws_bytes = stage_bytes;
-    if ((e = launch_stage1_sums(a, z, stream)) != hipSuccess) return e;
-  }
-  // dw of dy: stage 1 through U (role V packing) and h
-  {
-    ForwardArgs a{};
-    a.x = b.dy;
-    a.act_dt = b.act_dt;
-    a.T = b.T;
-    a.d_in = b.d_out;
-    a.r = b.r;
-    for (int p = 0; p < 2; ++p) a.V[p] = b.Ut[p], a.g[p] = b.h[p], a.l[p] = b.l[p];
-    a.sc_dt = b.sc_dt;
-    a.ws = stage;
-    a.ws_bytes = stage_bytes;
-    if ((e = launch_stage1_sums(a, dw, stream)) != hipSuccess) return e;
+    ForwardArgs ax{}, ay{};
+    ax.x = b.x;
+    ax.act_dt = b.act_dt;
+    ax.T = b.T;
+    ax.d_in = b.d_in;
+    ax.r = b.r;
+    for (int p = 0; p < 2; ++p) ax.V[p] = b.V[p], ax.g[p] = b.g[p], ax.l[p] = b.l[p];
+    ax.sc_dt = b.sc_dt;
+    ax.ws = stage;
+    ax.ws_bytes = stage_bytes;
+    ay = ax;
+    ay.x = b.dy;
+    ay.d_in = b.d_out;
+    for (int p = 0; p < 2; ++p) ay.V[p] = b.Ut[p], ay.g[p] = b.h[p];
+    ay.ws = ws + L.stage2_off;
+    ay.ws_bytes = L.part_off - L.stage2_off;
+    if ((e = launch_stage1_sums2(ax, z, ay, dw, stream)) != hipSuccess) return e;
   }
   // dx from dz = l (.) dw: stage 2 through V (role U packing) and g
   if (b.dx) {

@@ -10,6 +10,10 @@ namespace lb {
 // of a.x through a.V and a.g (a.d_in inputs); a.ws holds the split partial
 // sums (>= latent_workspace_bytes(T, d_in, r)).
 hipError_t launch_stage1_sums(const ForwardArgs& a, float* z, hipStream_t stream);
+// launch_stage1_sums of two inputs of one token count, rank and dtypes
+// (a0.ws and a1.ws distinct), with one launch for both split sums.
+hipError_t launch_stage1_sums2(const ForwardArgs& a0, float* z0, const ForwardArgs& a1, float* z1,
+                               hipStream_t stream);
 // Prefill stage 2 from w = l (.) src, src [T][2][r] fp32, through a.U, a.h
 // and a.l into a.y (dtype a.act_dt, a.d_out outputs); a.ws holds the w terms
 // (>= from_latent_workspace_bytes(T, r)).

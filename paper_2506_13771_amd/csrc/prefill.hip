@@ -396,8 +396,8 @@ struct PairItem {
 };
 
 // the item of this thread; false past the last pair or token
-__device__ __forceinline__ bool pair_item(const PrefillParams& P, PairItem& it) {
-  const int item = blockIdx.x * kThreads + threadIdx.x;
+__device__ __forceinline__ bool pair_item(const PrefillParams& P, PairItem& it, int bid = -1) {
+  const int item = (bid < 0 ? static_cast<int>(blockIdx.x) : bid) * kThreads + threadIdx.x;
   it.ln = item & 63;
   it.tn = (item >> 6) & 3;
   const int rest = item >> 8;
@@ -493,6 +493,27 @@ __global__ void __launch_bounds__(kThreads) prefill_latent_out(PrefillParams P) 
 
 // w terms of P2 from a stored [T][2][r] array: the cache itself, or (SC >= 0)
 // its product with l (the backward's dz = l (.) dw)
+// fp32 stage-1 sums (no l) of two linears in one launch: the first nb0
+// workgroups for Q0, the rest for Q1
+template <int SC>
+__global__ void __launch_bounds__(kThreads) prefill_sums2(PrefillParams Q0, PrefillParams Q1, int nb0) {
+  const bool second = static_cast<int>(blockIdx.x) >= nb0;
+  const PrefillParams& P = second ? Q1 : Q0;
+  PairItem it;
+  if (!pair_item(P, it, second ? static_cast<int>(blockIdx.x) - nb0 : static_cast<int>(blockIdx.x))) return;
+  float w0[4], w1[4];
+  latent_w<SC, false>(P, it, w0, w1);
+  const int r = P.r;
+  const int64_t row = (static_cast<int64_t>(it.t) * 2 + it.p) * r;
+  float* z = static_cast<float*>(P.lat);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int k = 32 * it.kbl + 4 * it.g4 + v;
+    if (k < r) z[row + k] = w0[v];
+    if (k + 16 < r) z[row + k + 16] = w1[v];
+  }
+}
+
 template <int ACT, int LD, int SC = -1>
 __global__ void __launch_bounds__(kThreads) prefill_latent_in(PrefillParams P) {
   constexpr int NW = ACT == kDtF32 ? 3 : 2;
@@ -1178,6 +1199,38 @@ hipError_t launch_stage1_sums(const ForwardArgs& a, float* z, hipStream_t stream
   ForwardArgs b = a;
   b.y = z;
   return launch_latent(b, -1, stream);
+}
+
+hipError_t launch_stage1_sums2(const ForwardArgs& a0, float* z0, const ForwardArgs& a1, float* z1,
+                               hipStream_t stream) {
+  if (a0.act_dt != a1.act_dt || a0.sc_dt != a1.sc_dt || a0.T != a1.T || a0.r != a1.r) return hipErrorInvalidValue;
+  PrefillGeom g0 = prefill_geometry(a0.T, a0.d_in, 0, a0.r), g1 = prefill_geometry(a1.T, a1.d_in, 0, a1.r);
+  PrefillParams Q0 = prefill_params(a0, g0), Q1 = prefill_params(a1, g1);
+  Q0.lat = z0;
+  Q1.lat = z1;
+  hipError_t e;
+  auto p1 = [&](const PrefillParams& Q, const PrefillGeom& g) -> hipError_t {
+    switch (a0.act_dt * 3 + a0.sc_dt) {
+      case kDtF32 * 3 + kDtF32: return launch_p1_ms<kDtF32, kDtF32>(Q, g, stream);
+      case kDtF32 * 3 + kDtF16: return launch_p1_ms<kDtF32, kDtF16>(Q, g, stream);
+      case kDtF32 * 3 + kDtBF16: return launch_p1_ms<kDtF32, kDtBF16>(Q, g, stream);
+      case kDtF16 * 3 + kDtF32: return launch_p1_ms<kDtF16, kDtF32>(Q, g, stream);
+      case kDtF16 * 3 + kDtF16: return launch_p1_ms<kDtF16, kDtF16>(Q, g, stream);
+      case kDtF16 * 3 + kDtBF16: return launch_p1_ms<kDtF16, kDtBF16>(Q, g, stream);
+      case kDtBF16 * 3 + kDtF32: return launch_p1_ms<kDtBF16, kDtF32>(Q, g, stream);
+      case kDtBF16 * 3 + kDtF16: return launch_p1_ms<kDtBF16, kDtF16>(Q, g, stream);
+      default: return launch_p1_ms<kDtBF16, kDtBF16>(Q, g, stream);
+    }
+  };
+  if ((e = p1(Q0, g0)) != hipSuccess) return e;
+  if ((e = p1(Q1, g1)) != hipSuccess) return e;
+  const int nb0 = static_cast<int>(pair_grid(Q0).x), nb1 = static_cast<int>(pair_grid(Q1).x);
+  switch (a0.sc_dt) {
+    case kDtF32: hipLaunchKernelGGL((prefill_sums2<kDtF32>), dim3(nb0 + nb1), dim3(kThreads), 0, stream, Q0, Q1, nb0); break;
+    case kDtF16: hipLaunchKernelGGL((prefill_sums2<kDtF16>), dim3(nb0 + nb1), dim3(kThreads), 0, stream, Q0, Q1, nb0); break;
+    default: hipLaunchKernelGGL((prefill_sums2<kDtBF16>), dim3(nb0 + nb1), dim3(kThreads), 0, stream, Q0, Q1, nb0); break;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_stage2_scaled(const ForwardArgs& a, const float* w, hipStream_t stream) {
