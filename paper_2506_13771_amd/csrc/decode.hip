@@ -437,8 +437,17 @@ __host__ __device__ constexpr int batch_rows(int wpl) { return wpl <= 2 ? 4 : (w
 // ... for one-token lists only (the tables of more tokens leave no registers)
 __host__ __device__ constexpr int list_rows(int tm, int wpl) { return tm == 1 ? batch_rows(wpl) : 1; }
 
+// A list launch with more stage-1 workgroups than this goes out as two
+// launches: every stage-1 workgroup first, in a kernel of its own, which needs
+// far fewer registers than stage 2 (204 for a one-token list at four words per
+// lane: 2 workgroups per CU), so that several times the workgroups per CU
+// overlap their load latencies; then the stage-2 workgroups, whose waits then
+// find every partial already published.
+constexpr int kSplitMinS1 = 1024;
+
 struct DecodeBatch {
   int n;
+  int wg0;                      // list block id of this launch's first workgroup
   int s1_end[kDecodeMaxBatch];  // one past each linear's last stage-1 workgroup
   int s2_end[kDecodeMaxBatch];  // the same for stage 2, counted from the first stage-2 workgroup
   DecodeParams p[kDecodeMaxBatch];
@@ -447,7 +456,7 @@ struct DecodeBatch {
 template <int TM, int ACT, int SC, bool VEC, int WPL>
 __global__ void __launch_bounds__(kThreads, 2) decode_batch_kernel(DecodeBatch B) {
   extern __shared__ __attribute__((aligned(16))) float smem[];
-  const int wg = blockIdx.x;
+  const int wg = blockIdx.x + B.wg0;
   const int s1tot = B.s1_end[B.n - 1];
   if (wg < s1tot) {
     int i = 0;
@@ -461,6 +470,17 @@ __global__ void __launch_bounds__(kThreads, 2) decode_batch_kernel(DecodeBatch B
     const DecodeParams P = B.p[i];
     stage2<TM, ACT, SC, WPL, list_rows(TM, WPL)>(P, w2 - (i ? B.s2_end[i - 1] : 0), smem);
   }
+}
+
+// the stage-1 workgroups of a list alone (grid: the list's stage-1 total)
+template <int TM, int ACT, int SC, bool VEC>
+__global__ void __launch_bounds__(kThreads) decode_batch_s1_kernel(DecodeBatch B) {
+  extern __shared__ __attribute__((aligned(16))) float smem[];
+  const int wg = blockIdx.x;
+  int i = 0;
+  while (wg >= B.s1_end[i]) ++i;
+  const DecodeParams P = B.p[i];
+  stage1<TM, ACT, SC, VEC>(P, wg - (i ? B.s1_end[i - 1] : 0), smem);
 }
 
 // one launch of the single-linear (DecodeParams) or list (DecodeBatch) kernel
@@ -478,10 +498,32 @@ hipError_t launch_one(const A& args, dim3 grid, size_t smem, hipStream_t stream)
     if (e != hipSuccess) return e;
     limit.store(smem);
   }
-  if constexpr (kOne)
+  if constexpr (kOne) {
     hipLaunchKernelGGL((decode_kernel<TM, ACT, SC, VEC, WPL>), grid, dim3(kThreads), smem, stream, args);
-  else
-    hipLaunchKernelGGL((decode_batch_kernel<TM, ACT, SC, VEC, WPL>), grid, dim3(kThreads), smem, stream, args);
+  } else {
+    const int s1 = args.s1_end[args.n - 1];
+    if (s1 <= kSplitMinS1) {
+      hipLaunchKernelGGL((decode_batch_kernel<TM, ACT, SC, VEC, WPL>), grid, dim3(kThreads), smem, stream, args);
+    } else {
+      // stage 1 alone: its tables of TM tokens are all the LDS it needs
+      constexpr size_t smem1 = sizeof(float) * TM * kChunk * kBlk;
+      static std::atomic<size_t> limit1{65536};
+      if (smem1 > limit1.load()) {
+        const hipError_t e =
+            hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_batch_s1_kernel<TM, ACT, SC, VEC>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem1));
+        if (e != hipSuccess) return e;
+        limit1.store(smem1);
+      }
+      hipLaunchKernelGGL((decode_batch_s1_kernel<TM, ACT, SC, VEC>), dim3(s1), dim3(kThreads), smem1, stream, args);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess || static_cast<int>(grid.x) <= s1) return e;
+      DecodeBatch b2 = args;
+      b2.wg0 = s1;
+      hipLaunchKernelGGL((decode_batch_kernel<TM, ACT, SC, VEC, WPL>), dim3(grid.x - s1), dim3(kThreads), smem, stream,
+                         b2);
+    }
+  }
   return hipGetLastError();
 }
 

@@ -166,3 +166,22 @@ def test_many_one_token_lists_of_every_row_block_count():
         for i, ((li, _, _), y, r) in enumerate(zip(lins, ys, ref)):
             assert _same_bits(y, r), (i, specs[i])
             _check(li, U.torch_to_raw(y, "bf16"), label=f"row blocks {specs[i]}")
+
+
+def test_many_large_lists_launch_stage_one_apart():
+    # lists with more than 1024 stage-1 workgroups go out as a stage-1 launch and a stage-2 launch;
+    # the second list has an unaligned member (element-wise loads, four-token tables whose LDS
+    # exceeds the default limit) and mixed token counts
+    for specs in ([(1, 8192, 2048, 176, "bf16", "f16")] * 5 + [(1, 4096, 3000, 288, "bf16", "f16"),
+                                                                (1, 7000, 1100, 100, "bf16", "f16")],
+                  [(2, 8192, 1024, 176, "bf16", "f16")] * 4 + [(2, 8190, 700, 160, "bf16", "f16"),
+                                                               (1, 6000, 900, 300, "bf16", "f16")]):
+        lins = _linears(specs, cfg=27)
+        ys, ws = _many(lins)
+        ref = _singles(lins)
+        for i, ((li, _, _), y, r) in enumerate(zip(lins, ys, ref)):
+            assert _same_bits(y, r), (i, specs[i])
+            _check(li, U.torch_to_raw(y, "bf16"), label=f"split list {specs[i]}")
+        again, _ = _many(lins, ws=ws)  # the same workspace again: the call protocol's next epoch
+        for i in range(len(lins)):
+            assert _same_bits(again[i], ys[i]), i
