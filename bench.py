@@ -282,35 +282,55 @@ def time_calls(layers, steps, warmup, use_graph=True, per_graph=None):
     return e0.elapsed_time(e1) / steps, steps
 
 
-def time_rotation(copies, steps, warmup):
-    """Cold-cache timing: `steps` calls cycling through `copies` (distinct weight buffers of
-    one layer, together larger than the caches), captured into one HIP graph and replayed.
-    Returns (ms per call, calls timed)."""
+def cache_flush(nbytes=1 << 30):
+    """Evict the caches (every L2 and the 256 MB Infinity Cache): read and write a buffer of
+    `nbytes` on the current stream.  Also keeps the GPU busy while the host submits whatever
+    is enqueued next, so that a timed region that starts after it has no submission gap."""
     import torch
+    buf = getattr(cache_flush, "_buf", None)
+    if buf is None or buf.numel() != nbytes // 4:
+        buf = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+        buf.zero_()
+        cache_flush._buf = buf
+    buf.add_(1.0)
+
+
+def time_rotation(copies, steps, warmup):
+    """Cold-cache timing: `steps` calls on distinct weight buffers of one layer (the
+    `copies`, together larger than twice the Infinity Cache), captured into one HIP graph.
+    The timed calls start at copy len(copies) // 2 and cycle; the untimed warm-up calls use
+    copies 0, 1, ...; before the timed replay the caches are flushed (cache_flush), so no
+    timed call finds its weights in a cache.  Returns (ms per call, calls timed, distinct
+    copies the timed calls touched)."""
+    import torch
+    n = len(copies)
+    c0 = n // 2
+    order = [copies[(c0 + i) % n] for i in range(steps)]
     stream = torch.cuda.current_stream()
     for L in copies:
         L.set_stream(stream.cuda_stream)
     for i in range(warmup):
-        copies[i % len(copies)].call()
+        copies[i % max(1, c0)].call()
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         cap = torch.cuda.current_stream().cuda_stream
-        for L in copies:
+        for L in order:
             L.set_stream(cap)
-        for i in range(steps):
-            copies[i % len(copies)].call()
+        for L in order:
+            L.call()
     for L in copies:
         L.set_stream(stream.cuda_stream)
-    graph.replay()  # untimed: first replay
+    graph.replay()  # untimed: first replay (graph upload)
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
+    cache_flush()
     e0.record(stream)
     graph.replay()
     e1.record(stream)
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / steps, steps
+    return e0.elapsed_time(e1) / steps, steps, len({id(L) for L in order})
 
 
 def source_digest(files):
@@ -400,7 +420,31 @@ def measured_traffic(workload_key):
 # ----------------------------------------------------------------------------
 # CPU baseline: the oracle as it stands, on this host
 # ----------------------------------------------------------------------------
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def host_threads() -> int:
+    """Threads for the all-core oracle: the cores this process may run on, capped by
+    OMP_NUM_THREADS when that is set."""
+    n = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        n = min(n, int(env))
+    return max(1, n)
+
+
 def cpu_baseline(li, seconds):
+    """The fp64 oracle O1 (as it stands) on this host, on the headline layer and inputs:
+    single-threaded, and the same loops on every available core (OpenMP over (path, token,
+    latent) and (token, row)).  Each variant runs for about `seconds`."""
     import oracle as O
     Us, Vs = [], []
     for p in range(2):
@@ -412,18 +456,30 @@ def cpu_baseline(li, seconds):
     h = [O.to_f64(a, li.scale_dtype) for a in li.h]
     g = [O.to_f64(a, li.scale_dtype) for a in li.g]
     l = [O.to_f64(a, li.scale_dtype) for a in li.l]
-    O.forward_factored(x, Us, Vs, h, g, l)
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        O.forward_factored(x, Us, Vs, h, g, l)
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    return {"value": n * li.T / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n} full fp64 oracle forwards of the same layer and inputs "
-                      f"({li.d_in}x{li.d_out}, r={li.r}, T={li.T}), single thread, {el:.1f} s"}
+    nthr = host_threads()
+
+    def timed(fn):
+        fn()
+        n = 0
+        t0 = time.perf_counter()
+        while True:
+            fn()
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                return n, el
+
+    n1, el1 = timed(lambda: O.forward_factored(x, Us, Vs, h, g, l))
+    nm, elm = timed(lambda: O.forward_factored_par(x, Us, Vs, h, g, l, nthr))
+    y1 = O.forward_factored(x, Us, Vs, h, g, l)
+    ym = O.forward_factored_par(x, Us, Vs, h, g, l, nthr)
+    return {"value": nm * li.T / elm, "unit": "tokens/s", "cores": nthr, "kind": "oracle",
+            "cpu_model": cpu_model(), "omp_threads": nthr,
+            "single_thread_value": n1 * li.T / el1,
+            "identical_results": bool(np.array_equal(y1, ym)),
+            "sample": f"full fp64 oracle forwards of the headline layer and inputs ({li.d_in}x{li.d_out}, "
+                      f"r={li.r}, T={li.T}): {nm} on {nthr} threads in {elm:.1f} s (value), "
+                      f"{n1} on one thread in {el1:.1f} s (single_thread_value)"}
 
 
 # ----------------------------------------------------------------------------
@@ -533,14 +589,153 @@ def run_sweep(path, steps, warmup, only=("7b", "13b", "kv", "train", "70b")):
     out.close()
 
 
+class ListCall:
+    """One lb_linear_forward_many call over pre-marshalled descriptors, timed like a Layer."""
+
+    def __init__(self, descs, n, device="cuda"):
+        import torch
+        import paper_2506_13771_amd as lb
+        self.arr, self.n = descs, n
+        need = lb.lb_forward_many_workspace_bytes(descs, n)
+        self.ws = lb.lb_workspace_init(torch.empty(max(need, 256), dtype=torch.uint8, device=device))
+        self.lib = lb.load_library()
+        self.argv = (self.arr, n, ctypes.c_void_p(self.ws.data_ptr()), self.ws.numel(),
+                     ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+
+    def set_stream(self, handle):
+        self.argv = self.argv[:-1] + (ctypes.c_void_p(handle),)
+
+    def call(self):
+        st = self.lib.lb_linear_forward_many(*self.argv)
+        if st != 0:
+            raise RuntimeError(f"lb_linear_forward_many failed with status {st}")
+
+
+class ResidentLinears:
+    """Linears resident on the GPU (packed signs, fp16 scales) with bf16 inputs of up to
+    t_max tokens each; desc(T) gives lb_linear_desc entries over the first T tokens."""
+
+    def __init__(self, shapes, t_max, cfg, direct_words, device="cuda"):
+        import torch
+        import paper_2506_13771_amd as lb
+        from paper_2506_13771_amd import synth
+        self.shapes = shapes
+        self.items = []
+        self.alg = {}
+        for idx, (name, d_in, d_out, r) in enumerate(shapes):
+            li = synth.make_linear(d_in, d_out, r, t_max, cfg=cfg, linear=idx, direct_words=direct_words)
+            L = Layer(li, device, pack_on_gpu=not direct_words)
+            del L.ws
+            self.items.append(L)
+        self.lb = lb
+
+    def descs(self, T):
+        arr, ys = self.lb.make_descs([(L.x[:T], L.paths, L.r, L.y[:T]) for L in self.items])
+        return arr
+
+    def bytes_and_flops(self, T):
+        b = w = f = 0.0
+        for L in self.items:
+            bb, ww = alg_bytes(T, L.d_in, L.d_out, L.r, L.e_act, L.e_scale)
+            b += bb
+            w += ww
+            f += alg_flops(T, L.d_in, L.d_out, L.r)
+        return b, w, f
+
+
+def list_timing(res, T, steps, warmup):
+    """ms per lb_linear_forward_many call over every linear of `res` at T tokens, graph-replayed,
+    with the derived rates."""
+    import torch
+    n = len(res.items)
+    call = ListCall(res.descs(T), n)
+    ms, k = time_calls([call], steps, warmup, use_graph=True, per_graph=1)
+    b, w, f = res.bytes_and_flops(T)
+    t_att = max(b / (PEAK_HBM_GBS * 1e9), f / (PEAK_BF16_TFLOPS * 1e12))
+    del call
+    torch.cuda.synchronize()
+    return {"T": T, "ms_per_call": ms, "calls_timed": k, "us_per_linear": ms * 1e3 / n,
+            "tokens_per_s": T / (ms * 1e-3), "alg_bytes": b, "weights_bytes": w,
+            "GBps": b / (ms * 1e-3) / 1e9, "hbm_frac": b / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "weights_GBps": w / (ms * 1e-3) / 1e9, "alg_flops": f,
+            "attainable_us": t_att * 1e6, "attainable_frac": t_att / (ms * 1e-3)}
+
+
+RANKS_70B = {(8192, 8192): 176, (8192, 1024): 16, (8192, 28672): 288, (28672, 8192): 288}
+RANKS_7B = {0.1: {4096: 80, 11008: 128}, 0.55: {4096: 544, 11008: 800}}
+
+
+def run_sweep70b(ts, steps, warmup):
+    """The Llama2-70B-shaped decode sweep: 80 layers x 7 linears at 0.1 BPW resident in HBM
+    (about 0.81 GB of packed signs and scales, more than three times the Infinity Cache, so
+    every call streams its weights from HBM), all 560 linears in one lb_linear_forward_many
+    call, T tokens per linear."""
+    import torch
+    from paper_2506_13771_amd import synth
+    t0 = time.perf_counter()
+    shapes = [(f"L{layer}.{name}", d_in, d_out, RANKS_70B[(d_in, d_out)])
+              for layer in range(80) for (name, d_in, d_out) in synth.LLAMA2_70B]
+    res = ResidentLinears(shapes, max(ts), cfg=4, direct_words=True)
+    setup_s = time.perf_counter() - t0
+    out = {"workload": "Llama2-70B shapes, 80 layers x (q,k,v,o,gate,up,down) at 0.1 BPW, bf16 x, fp16 scales, "
+                       "one lb_linear_forward_many call per sweep",
+           "linears": len(shapes), "weights_bytes": res.bytes_and_flops(1)[1], "setup_s": setup_s, "per_T": []}
+    for T in ts:
+        rec = list_timing(res, T, steps, warmup)
+        out["per_T"].append(rec)
+        log(f"sweep70b T={T}: {rec['ms_per_call']:.3f} ms, {rec['GBps']:.0f} GB/s ({100 * rec['hbm_frac']:.1f}% of HBM peak)")
+    del res
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_block7b(ts, steps, warmup, bpw=0.1):
+    """The 7 linears of one Llama2-7B block (q,k,v,o 4096x4096; gate, up 4096->11008; down
+    11008->4096) in one lb_linear_forward_many call (weights warm: one block is about 2 MB)."""
+    import torch
+    from paper_2506_13771_amd import synth
+    shapes = [(name, d_in, d_out, RANKS_7B[bpw][max(d_in, d_out)]) for (name, d_in, d_out) in synth.LLAMA2_7B]
+    res = ResidentLinears(shapes, max(ts), cfg=2, direct_words=False)
+    out = {"workload": f"Llama2-7B block, 7 linears at {bpw} BPW, bf16 x, fp16 scales, one lb_linear_forward_many "
+                       "call (weights warm in the caches)", "bpw": bpw, "per_T": []}
+    for T in ts:
+        rec = list_timing(res, T, max(steps, 50), max(warmup, 10))
+        out["per_T"].append(rec)
+        log(f"block7b T={T}: {rec['us_per_linear']:.2f} us per linear")
+    del res
+    torch.cuda.empty_cache()
+    return out
+
+
+# The paper's kernel-level latencies of one linear at batch 1 (Appendix "Inference Efficiency
+# Analysis", Table tab:latency_appendix_full): NVIDIA A100, FP16 inputs and FP16 accumulation,
+# cuBLAS FP16 torch.matmul as the baseline.  Context only: other hardware, other precision.
+PAPER_CONTEXT = {
+    "source": "Appendix Inference Efficiency Analysis, Table tab:latency_appendix_full",
+    "hardware": "NVIDIA A100, FP16 activations and accumulation, batch size 1",
+    "rows": [
+        {"shape": "Llama2-7B MLP-like, out 4096 x in 11008", "bpw": 0.1, "littlebit_ms": 0.0190, "fp16_ms": 0.0620,
+         "speedup_vs_fp16": 3.26},
+        {"shape": "Llama2-70B ATTN-like, 8192 x 8192", "bpw": 0.1, "littlebit_ms": 0.0207, "fp16_ms": 0.0896,
+         "speedup_vs_fp16": 4.33},
+        {"shape": "Llama2-70B MLP-like, out 8192 x in 28672", "bpw": 0.1, "littlebit_ms": 0.0249, "fp16_ms": 0.2882,
+         "speedup_vs_fp16": 11.57},
+    ],
+    "note": "no row has the 4096x4096 headline shape; the closest is the 7B MLP-like row",
+}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5000)
     ap.add_argument("--warmup", type=int, default=500)
     ap.add_argument("--launch", choices=["graph", "stream"], default="graph")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=8.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep70b", action="store_true", help="skip the 70B 560-linear list sweep")
+    ap.add_argument("--sweep70b-tokens", default="1,8,64", help="token counts of the 70B list sweep")
+    ap.add_argument("--no-block7b", action="store_true", help="skip the 7B block list timing")
     ap.add_argument("--sweep", default=None, help="write per-configuration JSON lines to this file")
     ap.add_argument("--sweep-only", default="7b,13b,kv,train,70b",
                     help="comma list of the sweep's parts to run (7b block, 13b prefill, 7b latent K/V cache, "
@@ -591,12 +786,14 @@ def main():
     copies[-1].call()
     torch.cuda.synchronize()
     assert torch.equal(y0, L.y), "a weight copy of the rotation differs from the original layer"
+    distinct = None
     if args.launch == "graph":
-        ms, steps = time_rotation(copies, args.steps, args.warmup)
+        ms, steps, distinct = time_rotation(copies, args.steps, args.warmup)
     else:
         ms, steps = time_calls(copies, max(1, args.steps // ncopies), max(1, args.warmup // ncopies),
                                use_graph=False)
         ms, steps = ms / ncopies, steps * ncopies
+        distinct = ncopies
     # the same layer called repeatedly (weights warm in the caches), graph-replayed and stream-issued
     ms_warm = ms_stream = None
     if not args.no_warm:
@@ -622,7 +819,9 @@ def main():
                                "path, 2 paths), T=1 decode, bf16 x, fp16 scales, Bernoulli(1/2) signs",
                    "d_in": d_in, "d_out": d_out, "r": r, "T": T, "bpw": round(lb.lb_bits_per_weight(d_in, d_out, r), 5),
                    "kernel": "decode", "launch": args.launch,
-                   "weights": f"cold: {ncopies} copies rotated ({ncopies * bw / 1e6:.0f} MB)"},
+                   "weights": f"cold: {ncopies} copies ({ncopies * bw / 1e6:.0f} MB), the timed calls on copies "
+                              f"the warm-up did not touch, caches flushed before the timed replay",
+                   "distinct_copies_touched": distinct},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
                      "alg_bytes_per_launch": b, "weights_bytes_per_launch": bw,
@@ -630,6 +829,12 @@ def main():
                      "avg_launch_us_warm": ms_warm * 1e3 if ms_warm is not None else None,
                      "avg_launch_us_warm_stream_issued": ms_stream * 1e3 if ms_stream is not None else None},
     }
+    if not args.no_sweep70b:
+        ts = tuple(int(t) for t in args.sweep70b_tokens.split(","))
+        rec["sweep70b"] = run_sweep70b(ts, args.steps, args.warmup)
+    if not args.no_block7b:
+        rec["block7b"] = run_block7b((1, 16, 64), args.steps, args.warmup)
+    rec["paper_context"] = PAPER_CONTEXT
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(li, args.cpu_seconds)
     print(json.dumps(rec), flush=True)

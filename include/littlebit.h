@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define LB_ABI_VERSION 4
+#define LB_ABI_VERSION 5
 
 typedef enum lb_status {
   LB_OK = 0,
@@ -146,6 +146,20 @@ size_t lb_forward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64_
 /* Zero-fill a workspace of `bytes` bytes on `stream`. */
 lb_status lb_workspace_init(void* workspace, size_t bytes, hipStream_t stream);
 
+/* Read and clear the error word of a workspace used by lb_linear_forward,
+   lb_linear_forward_kernel or lb_linear_forward_many (the word sits in the
+   control block at the start of the workspace; one word per workspace, shared
+   by every call that used it).  Enqueued on `stream`: *status (a DEVICE int32,
+   4-byte aligned) receives the word and the word is reset to 0.  0 means no
+   bounded wait of the single-launch decode kernels expired since the last
+   clear.  Nonzero (bit 0) means one did: a workgroup gave up waiting for
+   partial sums of another workgroup of the same call, took the values it
+   never saw as NaN (so the affected outputs are NaN, never stale values of an
+   earlier call) and set the word; the outputs of the calls since the last
+   clear are then not to be trusted.  workspace_bytes must be at least the 256
+   bytes of the control block (LB_ERR_WORKSPACE). */
+lb_status lb_workspace_status(void* workspace, size_t workspace_bytes, int32_t* status, hipStream_t stream);
+
 /* Largest token count LB_KERNEL_DECODE accepts. */
 int64_t lb_decode_max_tokens(void);
 
@@ -187,8 +201,11 @@ typedef struct lb_linear_desc {
 /* Host, pure.  Workspace bytes lb_linear_forward_many needs for this list:
    the sum of lb_forward_workspace_bytes of its linears, each rounded up to
    256 bytes (0 if n <= 0, descs is NULL or a size is invalid).  Linear i uses
-   the slice after those of linears 0 .. i-1, with the same zero-fill-once and
-   reuse rules as lb_forward_workspace_bytes. */
+   the slice after those of linears 0 .. i-1 for its intermediate values; the
+   control block of the decode kernels' call protocol is the one at the start
+   of the workspace for every linear, so the zero-fill-once and reuse rules of
+   lb_forward_workspace_bytes hold for the whole workspace, across lists of
+   any layout and single calls on the same buffer. */
 size_t lb_forward_many_workspace_bytes(const lb_linear_desc* descs, int64_t n);
 
 /* Forward of n independent LittleBit linears (each as lb_linear_forward

@@ -43,6 +43,9 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 /* ---------------------------------------------------------------------- */
 /* Sign convention (Eq. uv_sign): the codomain is {-1,+1}.                 */
@@ -197,6 +200,54 @@ void lbo_forward_factored(const double* x, int64_t T, int64_t d_in, int64_t d_ou
   }
   free(a);
   free(z);
+}
+
+/* O1 on several host threads (OpenMP), for timing the oracle on every core:
+   the same operations as lbo_forward_factored, each output summed in the
+   same order (ascending j for z, ascending k for u, paths in order), so the
+   result is bit-identical; only independent outputs run concurrently:
+   stage 1 over (path, token, latent), stage 2 over (token, output row).
+   nthreads <= 0 leaves the OpenMP default. */
+void lbo_forward_factored_par(const double* x, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                              const int8_t* const* U, const int8_t* const* V,
+                              const double* const* h, const double* const* g, const double* const* l,
+                              int npaths, int nthreads, double* y) {
+  double* z = (double*)malloc(sizeof(double) * (size_t)(npaths * T * r > 0 ? npaths * T * r : 1));
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+  const int64_t n1 = (int64_t)npaths * T * r;
+#pragma omp parallel for schedule(static)
+  for (int64_t e = 0; e < n1; e++) {
+    const int64_t p = e / (T * r), t = (e / r) % T, k = e % r;
+    double s = 0.0;
+    for (int64_t j = 0; j < d_in; j++) s += (double)V[p][j * r + k] * (x[t * d_in + j] * g[p][j]);
+    z[e] = s * l[p][k];
+  }
+  const int64_t n2 = T * d_out;
+#pragma omp parallel for schedule(static)
+  for (int64_t e = 0; e < n2; e++) {
+    const int64_t t = e / d_out, i = e % d_out;
+    double acc = 0.0;
+    for (int p = 0; p < npaths; p++) {
+      const double* zp = z + ((int64_t)p * T + t) * r;
+      double s = 0.0;
+      for (int64_t k = 0; k < r; k++) s += (double)U[p][i * r + k] * zp[k];
+      acc += s * h[p][i];
+    }
+    y[e] = acc;
+  }
+  free(z);
+}
+
+int lbo_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
 }
 
 /* O5: the latent cache of Sec. "Analysis", paragraph "KV Cache Compression"

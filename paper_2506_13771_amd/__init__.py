@@ -9,7 +9,7 @@ falling back to anything else.
 The names follow the C ABI:
   lb_pack_signs, lb_linear_forward, lb_dense_reference_weight,
   lb_packed_bytes, lb_bits_per_weight, lb_rank_for_bpw,
-  lb_forward_workspace_bytes, lb_workspace_init, lb_decode_max_tokens,
+  lb_forward_workspace_bytes, lb_workspace_init, lb_workspace_status, lb_decode_max_tokens,
   lb_linear_forward_many, lb_forward_many_workspace_bytes,
   lb_linear_latent, lb_latent_workspace_bytes,
   lb_linear_from_latent, lb_from_latent_workspace_bytes,
@@ -29,7 +29,7 @@ LB_OK, LB_ERR_NULL, LB_ERR_SHAPE, LB_ERR_DTYPE, LB_ERR_ALIGN, LB_ERR_WORKSPACE, 
 LB_F32, LB_F16, LB_BF16 = 0, 1, 2
 LB_ROLE_U, LB_ROLE_V = 0, 1
 LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL, LB_KERNEL_DECODE_MFMA = 0, 1, 2, 3
-ABI_VERSION = 4
+ABI_VERSION = 5
 
 
 class LittleBitError(RuntimeError):
@@ -84,6 +84,8 @@ def load_library(path: str = LIB_PATH):
     lib.lb_forward_workspace_bytes.argtypes = [i64, i64, i64, i64]
     lib.lb_workspace_init.restype = i32
     lib.lb_workspace_init.argtypes = [vp, sz, vp]
+    lib.lb_workspace_status.restype = i32
+    lib.lb_workspace_status.argtypes = [vp, sz, vp, vp]
     lib.lb_decode_max_tokens.restype = i64
     lib.lb_decode_max_tokens.argtypes = []
     lib.lb_linear_forward.restype = i32
@@ -229,6 +231,17 @@ def lb_workspace_init(ws, stream=None):
     st = load_library().lb_workspace_init(_dev_ptr(ws, "workspace"), ws.numel() * ws.element_size(), _stream(stream))
     _check(st, "lb_workspace_init")
     return ws
+
+
+def lb_workspace_status(ws, stream=None) -> int:
+    """Read and clear the workspace's error word (0: no bounded wait expired since the last clear);
+    synchronises the stream to return the value."""
+    torch = _torch()
+    out = torch.full((1,), -1, dtype=torch.int32, device=ws.device)
+    st = load_library().lb_workspace_status(_dev_ptr(ws, "workspace"), ws.numel() * ws.element_size(),
+                                            _dev_ptr(out, "status"), _stream(stream))
+    _check(st, "lb_workspace_status")
+    return int(out.item())
 
 
 def alloc_workspace(T: int, d_in: int, d_out: int, r: int, device="cuda"):
@@ -418,7 +431,7 @@ __all__ = [
     "LB_ERR_ARG", "LB_F32", "LB_F16", "LB_BF16", "LB_ROLE_U", "LB_ROLE_V", "LB_KERNEL_AUTO", "LB_KERNEL_DECODE",
     "LB_KERNEL_PREFILL", "LB_KERNEL_DECODE_MFMA", "LittleBitError", "LittleBitPath", "lb_path", "load_library", "lb_status_str",
     "lb_packed_bytes", "lb_bits_per_weight", "lb_rank_for_bpw", "lb_forward_workspace_bytes",
-    "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "alloc_workspace", "lb_linear_forward",
+    "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "lb_workspace_status", "alloc_workspace", "lb_linear_forward",
     "lb_dense_reference_weight", "lb_linear_desc", "make_descs", "lb_forward_many_workspace_bytes",
     "lb_linear_forward_many", "lb_latent_workspace_bytes", "lb_from_latent_workspace_bytes", "lb_linear_latent",
     "lb_linear_from_latent", "lb_path_train", "LittleBitPathTrain", "lb_backward_workspace_bytes",

@@ -12,7 +12,29 @@ namespace {
 
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
 
-bool dtype_ok(lb_dtype d) { return d == LB_F32 || d == LB_F16 || d == LB_BF16; }
+// The value of an enum argument as an int, read without an enum-typed load: C
+// callers may pass any int, and a value outside an enum's range must reach
+// the range checks below, not be read as the enum first.
+template <typename E>
+int enum_value(const E& e) {
+  static_assert(sizeof(E) == sizeof(int), "enums of the ABI are int-sized");
+  int v;
+  std::memcpy(&v, &e, sizeof v);
+  return v;
+}
+
+bool dtype_ok(const lb_dtype& d) {
+  const int v = enum_value(d);
+  return v == LB_F32 || v == LB_F16 || v == LB_BF16;
+}
+bool role_ok(const lb_role& r) {
+  const int v = enum_value(r);
+  return v == LB_ROLE_U || v == LB_ROLE_V;
+}
+bool kernel_ok(const lb_kernel& k) {
+  const int v = enum_value(k);
+  return v == LB_KERNEL_AUTO || v == LB_KERNEL_DECODE || v == LB_KERNEL_PREFILL || v == LB_KERNEL_DECODE_MFMA;
+}
 size_t dtype_size(lb_dtype d) { return d == LB_F32 ? 4 : 2; }
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -100,7 +122,7 @@ extern "C" {
 int lb_abi_version(void) { return LB_ABI_VERSION; }
 
 const char* lb_status_str(lb_status s) {
-  switch (s) {
+  switch (enum_value(s)) {
     case LB_OK: return "LB_OK";
     case LB_ERR_NULL: return "LB_ERR_NULL";
     case LB_ERR_SHAPE: return "LB_ERR_SHAPE";
@@ -114,7 +136,7 @@ const char* lb_status_str(lb_status s) {
 }
 
 size_t lb_packed_bytes(lb_role role, int64_t rows, int64_t r) {
-  if (rows < 0 || r < 0 || (role != LB_ROLE_U && role != LB_ROLE_V)) return 0;
+  if (rows < 0 || r < 0 || !role_ok(role)) return 0;
   return role == LB_ROLE_U ? packed_bytes(rows, r) : packed_bytes(r, rows);
 }
 
@@ -142,7 +164,7 @@ int64_t lb_rank_for_bpw(int64_t d_in, int64_t d_out, double bpw, int64_t mult) {
 
 lb_status lb_pack_signs(const void* src, lb_dtype src_dtype, int64_t rows, int64_t r, lb_role role, void* dst,
                         int32_t* nan_count, hipStream_t stream) {
-  if (role != LB_ROLE_U && role != LB_ROLE_V) return LB_ERR_ARG;
+  if (!role_ok(role)) return LB_ERR_ARG;
   if (!dtype_ok(src_dtype)) return LB_ERR_DTYPE;
   if (rows < 0 || r < 0 || !fits(rows, r)) return LB_ERR_SHAPE;
   if (rows == 0 || r == 0) return LB_OK;
@@ -188,12 +210,18 @@ lb_status lb_workspace_init(void* workspace, size_t bytes, hipStream_t stream) {
   return lb::launch_fill_zero(workspace, bytes, stream) == hipSuccess ? LB_OK : LB_ERR_HIP;
 }
 
+lb_status lb_workspace_status(void* workspace, size_t workspace_bytes, int32_t* status, hipStream_t stream) {
+  if (!workspace || !status) return LB_ERR_NULL;
+  if (!aligned(workspace, 256) || !aligned(status, 4)) return LB_ERR_ALIGN;
+  if (workspace_bytes < lb::kCtrlBytes) return LB_ERR_WORKSPACE;
+  const hipError_t e = lb::launch_take_status(static_cast<uint32_t*>(workspace), status, stream);
+  return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+}
+
 lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out,
                                    int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y, void* workspace,
                                    size_t workspace_bytes, lb_kernel kernel, hipStream_t stream) {
-  if (kernel != LB_KERNEL_AUTO && kernel != LB_KERNEL_DECODE && kernel != LB_KERNEL_PREFILL &&
-      kernel != LB_KERNEL_DECODE_MFMA)
-    return LB_ERR_ARG;
+  if (!kernel_ok(kernel)) return LB_ERR_ARG;
   if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype)) return LB_ERR_DTYPE;
   lb_status st = check_sizes(T, d_in, d_out, r);
   if (st != LB_OK) return st;
@@ -234,6 +262,7 @@ lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T,
 lb_status lb_linear_forward(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
                             const lb_path* paths, lb_dtype scale_dtype, void* y, void* workspace,
                             size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype)) return LB_ERR_DTYPE;  // before passing them on
   return lb_linear_forward_kernel(x, act_dtype, T, d_in, d_out, r, paths, scale_dtype, y, workspace,
                                   workspace_bytes, LB_KERNEL_AUTO, stream);
 }
@@ -352,7 +381,9 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
         if (st != LB_OK) return st;
       }
       bk = k;
-      batch[nb++] = make_args(d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.paths, d.scale_dtype, d.y, ws + off, sb);
+      batch[nb] = make_args(d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.paths, d.scale_dtype, d.y, ws + off, sb);
+      // one control block for the whole list: the start of its workspace
+      batch[nb++].ctrl = workspace;
     } else {
       const lb_status st = lb_linear_forward_kernel(d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.paths,
                                                     d.scale_dtype, d.y, ws + off, sb, LB_KERNEL_AUTO, stream);

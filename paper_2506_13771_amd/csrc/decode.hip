@@ -95,6 +95,7 @@ struct DecodeParams {
   int bpr;     // 32-input blocks per run
   int n_s1;    // stage-1 workgroups (2 * nkt * s1d)
   int n_s2;    // stage-2 workgroups
+  int n_done;  // stage-2 workgroups of the launch that count on ctrl (the last one ends the call)
   int direct;  // stage 2 reads every run's partial (else the two-level sums)
   int tch;     // tokens per stage-2 chunk
   uint32_t magic_r;  // fast_div multiplier for r
@@ -353,7 +354,9 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
           const int pp = e >= per_path ? 1 : 0;
           const int el = e - pp * per_path;
           const int row = static_cast<int>(fast_div(static_cast<uint32_t>(el), P.magic_r));  // tl * nsrc + run
-          raw[(pp * tch * nsrc + row) * R4 + (el - row * r)] = slot_value(sv[j]);
+          // a slot a timed-out wait never saw carrying this call's tag is NaN
+          raw[(pp * tch * nsrc + row) * R4 + (el - row * r)] =
+              slot_ready(sv[j], tag) ? slot_value(sv[j]) : __builtin_nanf("");
         }
       }
     }
@@ -408,7 +411,7 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
   // then: stage-2 workgroups counted themselves after reading it, and every
   // stage-1 workgroup published values carrying the tag, which this
   // workgroup has gathered (directly, or through the two-level reducers).
-  if (tid == 0 && done_before == static_cast<uint32_t>(P.n_s2 - 1)) {
+  if (tid == 0 && done_before == static_cast<uint32_t>(P.n_done - 1)) {
     atomic_store_relaxed(P.ctrl + kCtrlDone, 0u);
     atomic_store_relaxed(P.ctrl + kCtrlEpoch, tag);
   }
@@ -642,7 +645,7 @@ bool decode_params(const ForwardArgs& a, const DecodeGeom& g, DecodeParams& P) {
     P.l[p] = a.l[p];
   }
   char* ws = static_cast<char*>(a.ws);
-  P.ctrl = reinterpret_cast<uint32_t*>(ws);
+  P.ctrl = reinterpret_cast<uint32_t*>(a.ctrl ? a.ctrl : a.ws);
   P.partial = reinterpret_cast<uint64_t*>(ws + g.partial_off);
   P.wbuf = reinterpret_cast<uint64_t*>(ws + g.wbuf_off);
   P.T = a.T;
@@ -654,6 +657,7 @@ bool decode_params(const ForwardArgs& a, const DecodeGeom& g, DecodeParams& P) {
   P.bpr = g.bpr;
   P.n_s1 = g.n_s1;
   P.n_s2 = g.n_s2;
+  P.n_done = g.n_s2;
   P.direct = g.direct;
   P.tch = g.tch;
   P.magic_r = a.r > 1 ? static_cast<uint32_t>(((uint64_t(1) << 32) + a.r - 1) / a.r) : 0u;
@@ -706,6 +710,14 @@ hipError_t launch_decode_batch(const ForwardArgs* a, int n, hipStream_t stream) 
     B.p[i].n_s2 = (B.p[i].n_s2 + rb - 1) / rb;
     s2 += B.p[i].n_s2;
     B.s2_end[i] = s2;
+  }
+  // members that share a control block end the call together: the last of
+  // all their stage-2 workgroups stores the epoch
+  for (int i = 0; i < n; ++i) {
+    int cnt = 0;
+    for (int j = 0; j < n; ++j)
+      if (B.p[j].ctrl == B.p[i].ctrl) cnt += B.p[j].n_s2;
+    B.p[i].n_done = cnt;
   }
   return launch_any(B, a[0].act_dt, T, a[0].sc_dt, vec, wpl, dim3(s1 + s2), vec ? smem_vec : smem_elem, stream);
 }

@@ -78,6 +78,7 @@ struct MmaParams {
   int bpr;     // 32-wide input blocks per run
   int n_s1;    // stage-1 workgroups (2 * nmf * s1d)
   int n_s2;    // stage-2 workgroups
+  int n_done;  // stage-2 workgroups of the launch that count on ctrl (the last one ends the call)
   int direct;  // stage 2 reads every run's partial (else the two-level sums)
   int vec;     // x and g may be read as aligned 4-element vectors
   uint32_t x_bytes, g_bytes, v_bytes, u_bytes, h_bytes, l_bytes;
@@ -382,11 +383,13 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
         for (int j = 0; j < kGather; ++j) {
           const int e = e0 + tid + kThreads * j;
           if (e < n1) {
+            // a slot a timed-out wait never saw carrying this call's tag is NaN
+            const float v = slot_ready(sv[j], tag) ? slot_value(sv[j]) : __builtin_nanf("");
             if (nsrc > 1) {
-              raw[pp * tch * nsrc * r + e] = slot_value(sv[j]);
+              raw[pp * tch * nsrc * r + e] = v;
             } else {
               const int tl = static_cast<int>(fast_div(e, P.magic_r));
-              wsum[(pp * tch + tl) * R32 + (e - tl * r)] = slot_value(sv[j]);
+              wsum[(pp * tch + tl) * R32 + (e - tl * r)] = v;
             }
           }
         }
@@ -460,7 +463,7 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
   // workgroups counted themselves after reading it, and every stage-1
   // workgroup published values carrying the tag, which this workgroup has
   // gathered (directly, or through the two-level reducers).
-  if (tid == 0 && done_before == static_cast<uint32_t>(P.n_s2 - 1)) {
+  if (tid == 0 && done_before == static_cast<uint32_t>(P.n_done - 1)) {
     atomic_store_relaxed(P.ctrl + kCtrlDone, 0u);
     atomic_store_relaxed(P.ctrl + kCtrlEpoch, tag);
   }
@@ -633,7 +636,7 @@ void mma_params(const ForwardArgs& a, const MmaGeom& g, MmaParams& P) {
     P.l[p] = a.l[p];
   }
   char* ws = static_cast<char*>(a.ws);
-  P.ctrl = reinterpret_cast<uint32_t*>(ws);
+  P.ctrl = reinterpret_cast<uint32_t*>(a.ctrl ? a.ctrl : a.ws);
   P.partial = reinterpret_cast<uint64_t*>(ws + g.partial_off);
   P.wbuf = reinterpret_cast<uint64_t*>(ws + g.wbuf_off);
   P.T = a.T;
@@ -645,6 +648,7 @@ void mma_params(const ForwardArgs& a, const MmaGeom& g, MmaParams& P) {
   P.bpr = g.bpr;
   P.n_s1 = g.n_s1;
   P.n_s2 = g.n_s2;
+  P.n_done = g.n_s2;
   P.direct = g.direct;
   const int64_t ex = a.act_dt == kDtF32 ? 4 : 2, es = a.sc_dt == kDtF32 ? 4 : 2;
   const uintptr_t xa = 4 * ex, ga = 4 * es;
@@ -712,6 +716,14 @@ hipError_t launch_decode_mma_batch(const ForwardArgs* a, int n, hipStream_t stre
       T = a[j].T > T ? a[j].T : T;
       smem = list_smem(j) > smem ? list_smem(j) : smem;
       ++B.n;
+    }
+    // members that share a control block end the call together: the last of
+    // all their stage-2 workgroups stores the epoch
+    for (int k = 0; k < B.n; ++k) {
+      int cnt = 0;
+      for (int m = 0; m < B.n; ++m)
+        if (B.p[m].ctrl == B.p[k].ctrl) cnt += B.p[m].n_s2;
+      B.p[k].n_done = cnt;
     }
     const hipError_t e = B.n == 1 ? launch_any(P[i], a[i].act_dt, a[i].T, vec, a[i].sc_dt,
                                                dim3(G[i].n_s1 + G[i].n_s2), G[i].smem_bytes, stream)

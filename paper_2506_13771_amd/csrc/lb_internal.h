@@ -126,6 +126,11 @@ struct ForwardArgs {
   void* y;
   void* ws;
   size_t ws_bytes;
+  // control block (epoch, done counter, error word) of the decode kernels'
+  // call protocol; nullptr: the start of ws.  Every linear of a list launch
+  // shares the control block at the start of the list's workspace, so that
+  // tags stay unique per workspace whatever the list's layout.
+  void* ctrl = nullptr;
 };
 
 // Look-up-table decode kernel geometry (pure function of the sizes; also sizes
@@ -211,6 +216,8 @@ hipError_t launch_latent(const ForwardArgs& a, int lat_dt, hipStream_t stream);
 hipError_t launch_from_latent(const ForwardArgs& a, const void* lat, int lat_dt, hipStream_t stream);
 hipError_t launch_dense_ref(const ForwardArgs& a, float* W, hipStream_t stream);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
+// *out = the error word of the control block at ctrl, which is then cleared
+hipError_t launch_take_status(uint32_t* ctrl, int32_t* out, hipStream_t stream);
 hipError_t launch_zero_elems(void* p, int64_t n, int dt, hipStream_t stream);
 
 }  // namespace lb

@@ -99,4 +99,16 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream) {
   return hipGetLastError();
 }
 
+namespace {
+__global__ void take_status_kernel(uint32_t* ctrl, int32_t* out) {
+  const uint32_t v = __hip_atomic_exchange(ctrl + kCtrlError, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  *out = static_cast<int32_t>(v);
+}
+}  // namespace
+
+hipError_t launch_take_status(uint32_t* ctrl, int32_t* out, hipStream_t stream) {
+  hipLaunchKernelGGL(take_status_kernel, dim3(1), dim3(1), 0, stream, ctrl, out);
+  return hipGetLastError();
+}
+
 }  // namespace lb

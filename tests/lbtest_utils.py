@@ -58,12 +58,24 @@ def oracle_scales(li: synth.LinearInputs):
 
 
 def oracle_forward(li: synth.LinearInputs, tokens=None):
+    """O1 on the layer's inputs (every token, or the given ones).  Runs the OpenMP form of
+    O1, which performs the same operations per output in the same order as the serial one
+    (bit-identical, pinned in test_oracle.py), on the host's cores."""
     U, V, _, _ = oracle_signs(li)
     h, g, l = oracle_scales(li)
     x = O.to_f64(li.x, li.act_dtype)
     if tokens is not None:
         x = x[tokens]
-    return O.forward_factored(x, U, V, h, g, l)
+    return O.forward_factored_par(x, U, V, h, g, l, host_threads())
+
+
+def host_threads() -> int:
+    import os
+    n = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        n = min(n, int(env))
+    return max(1, min(n, 16))
 
 
 def to_device(li: synth.LinearInputs, pack_on_gpu: bool = True):

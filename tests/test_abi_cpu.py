@@ -177,6 +177,14 @@ def test_workspace_init_validation(lib):
     assert lib.lb_workspace_init(0, 0, None) == lb.LB_OK
 
 
+def test_workspace_status_validation(lib):
+    assert lib.lb_workspace_status(0, 256, FAKE, None) == lb.LB_ERR_NULL
+    assert lib.lb_workspace_status(FAKE, 256, 0, None) == lb.LB_ERR_NULL
+    assert lib.lb_workspace_status(FAKE + 4, 256, FAKE, None) == lb.LB_ERR_ALIGN
+    assert lib.lb_workspace_status(FAKE, 256, FAKE + 2, None) == lb.LB_ERR_ALIGN
+    assert lib.lb_workspace_status(FAKE, 255, FAKE, None) == lb.LB_ERR_WORKSPACE
+
+
 def test_binding_refuses_cpu_tensors(lib):
     import torch
     x = torch.zeros(2, 64, dtype=torch.bfloat16)

@@ -185,3 +185,42 @@ def test_many_large_lists_launch_stage_one_apart():
         again, _ = _many(lins, ws=ws)  # the same workspace again: the call protocol's next epoch
         for i in range(len(lins)):
             assert _same_bits(again[i], ys[i]), i
+
+
+def test_many_layouts_change_on_one_workspace():
+    """One workspace serves lists of different layouts in turn ([A], then [B, A], then [A]
+    again, several times): linear A's intermediate values move between calls while the control
+    block stays at the start of the workspace, so every result must still be bit-identical to
+    A's (and B's) single call, and the workspace's error word must stay clear."""
+    lins = _linears([(1, 8192, 2048, 176, "bf16", "f16"), (1, 512, 512, 32, "bf16", "f16"),
+                     (8, 1024, 1024, 80, "bf16", "f16")], cfg=28)
+    ref = _singles(lins)
+    layouts = ([0], [1, 0], [2, 1, 0], [0], [0, 2])
+    need = 0
+    for idx in layouts:
+        arr, _ = lb.make_descs([(lins[i][1], lins[i][2], lins[i][0].r, None) for i in idx])
+        need = max(need, lb.lb_forward_many_workspace_bytes(arr, len(idx)))
+    ws = lb.lb_workspace_init(torch.empty(need, dtype=torch.uint8, device="cuda"))
+    for rep in range(3):
+        for idx in layouts:
+            ys, _ = _many([lins[i] for i in idx], ws=ws)
+            for i, y in zip(idx, ys):
+                assert _same_bits(y, ref[i]), (rep, idx, i)
+    assert lb.lb_workspace_status(ws) == 0
+
+
+def test_workspace_status_after_calls():
+    """The error word of a workspace reads 0 after calls of every decode kernel and a list on
+    it (no bounded wait expired), and reading it clears it."""
+    lins = _linears([(1, 4096, 4096, 80, "bf16", "f16"), (3, 1024, 2048, 48, "bf16", "f16"),
+                     (2, 8192, 1024, 16, "bf16", "f16")], cfg=29)
+    need = max(lb.lb_forward_workspace_bytes(li.T, li.d_in, li.d_out, li.r) for li, _, _ in lins)
+    ws = lb.lb_workspace_init(torch.empty(need, dtype=torch.uint8, device="cuda"))
+    for li, x, paths in lins:
+        for k in (lb.LB_KERNEL_AUTO, lb.LB_KERNEL_DECODE, lb.LB_KERNEL_DECODE_MFMA):
+            lb.lb_linear_forward(x, paths, li.r, workspace=ws, kernel=k)
+    torch.cuda.synchronize()
+    assert lb.lb_workspace_status(ws) == 0
+    _, ws2 = _many(lins)
+    assert lb.lb_workspace_status(ws2) == 0
+    assert lb.lb_workspace_status(ws2) == 0

@@ -140,6 +140,21 @@ def test_factored_equals_dense(d_in, d_out, r, T):
     assert np.abs(y1 - y2).max() / scale < 1e-12
 
 
+@pytest.mark.parametrize("d_in,d_out,r,T", [(1, 1, 1, 1), (33, 31, 32, 3), (100, 77, 19, 5), (64, 300, 40, 2)])
+@pytest.mark.parametrize("nthreads", [1, 3, 8])
+def test_parallel_forward_is_bit_identical(d_in, d_out, r, T, nthreads):
+    """The OpenMP form of O1 computes every output with the same operations in the same
+    order as the serial one, so it must agree bit for bit, at any thread count; and it
+    meets the brute-force dense route like the serial one."""
+    rs = np.random.default_rng(7000 + d_in + d_out + r + T)
+    x, U, V, h, g, l = _rand_layer(rs, T, d_in, d_out, r)
+    y1 = O.forward_factored(x, U, V, h, g, l)
+    yp = O.forward_factored_par(x, U, V, h, g, l, nthreads)
+    assert np.array_equal(y1, yp)
+    y2 = O.dense_forward(x, O.dense_weight(U, V, h, g, l))
+    assert np.abs(yp - y2).max() / (np.abs(y2).max() + 1e-300) < 1e-12
+
+
 def test_brute_force_python_loops():
     """Independent brute force: enumerate every W_hat entry with Python loops, from the
     definition diag(h) U diag(l) V^T diag(g), for both paths."""
