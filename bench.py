@@ -643,18 +643,60 @@ class ResidentLinears:
         return b, w, f
 
 
+class StreamListCall:
+    """The streaming list forward (lb_list_init once, then lb_list_forward: three launches for the
+    whole list) over pre-marshalled descriptors, timed like a Layer."""
+
+    def __init__(self, descs, n, device="cuda"):
+        import torch
+        import paper_2506_13771_amd as lb
+        self.arr, self.n = descs, n
+        self.lib = lb.load_library()
+        need = lb.lb_list_workspace_bytes(descs, n)
+        if need == 0:
+            raise RuntimeError("list out of the streaming forward's scope")
+        self.ws = torch.empty(need, dtype=torch.uint8, device=device)
+        st = self.lib.lb_list_init(descs, n, ctypes.c_void_p(self.ws.data_ptr()), need,
+                                   ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        if st != 0:
+            raise RuntimeError(f"lb_list_init failed with status {st}")
+        self.argv = (self.arr, n, ctypes.c_void_p(self.ws.data_ptr()), need,
+                     ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+
+    def set_stream(self, handle):
+        self.argv = self.argv[:-1] + (ctypes.c_void_p(handle),)
+
+    def call(self):
+        st = self.lib.lb_list_forward(*self.argv)
+        if st != 0:
+            raise RuntimeError(f"lb_list_forward failed with status {st}")
+
+
 def list_timing(res, T, steps, warmup):
-    """ms per lb_linear_forward_many call over every linear of `res` at T tokens, graph-replayed,
-    with the derived rates."""
+    """ms per list call over every linear of `res` at T tokens, graph-replayed, with the derived
+    rates: the streaming list forward (lb_list_forward) where the list is in its scope (T <= 2),
+    else lb_linear_forward_many; for T <= 2 lb_linear_forward_many is timed beside it."""
     import torch
+    import paper_2506_13771_amd as lb
     n = len(res.items)
-    call = ListCall(res.descs(T), n)
+    descs = res.descs(T)
+    extra = {}
+    if lb.lb_list_workspace_bytes(descs, n) > 0:
+        call = StreamListCall(descs, n)
+        api = "lb_list_forward"
+        many = ListCall(descs, n)
+        ms_many, _ = time_calls([many], steps, warmup, use_graph=True, per_graph=1)
+        extra["ms_per_call_forward_many"] = ms_many
+        del many
+    else:
+        call = ListCall(descs, n)
+        api = "lb_linear_forward_many"
     ms, k = time_calls([call], steps, warmup, use_graph=True, per_graph=1)
     b, w, f = res.bytes_and_flops(T)
     t_att = max(b / (PEAK_HBM_GBS * 1e9), f / (PEAK_BF16_TFLOPS * 1e12))
     del call
     torch.cuda.synchronize()
-    return {"T": T, "ms_per_call": ms, "calls_timed": k, "us_per_linear": ms * 1e3 / n,
+    return {"T": T, "api": api, "ms_per_call": ms, "calls_timed": k, "us_per_linear": ms * 1e3 / n, **extra,
             "tokens_per_s": T / (ms * 1e-3), "alg_bytes": b, "weights_bytes": w,
             "GBps": b / (ms * 1e-3) / 1e9, "hbm_frac": b / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
             "weights_GBps": w / (ms * 1e-3) / 1e9, "alg_flops": f,
@@ -678,7 +720,7 @@ def run_sweep70b(ts, steps, warmup):
     res = ResidentLinears(shapes, max(ts), cfg=4, direct_words=True)
     setup_s = time.perf_counter() - t0
     out = {"workload": "Llama2-70B shapes, 80 layers x (q,k,v,o,gate,up,down) at 0.1 BPW, bf16 x, fp16 scales, "
-                       "one lb_linear_forward_many call per sweep",
+                       "one list call per sweep (lb_list_forward for T <= 2, else lb_linear_forward_many)",
            "linears": len(shapes), "weights_bytes": res.bytes_and_flops(1)[1], "setup_s": setup_s, "per_T": []}
     for T in ts:
         rec = list_timing(res, T, steps, warmup)
@@ -696,8 +738,9 @@ def run_block7b(ts, steps, warmup, bpw=0.1):
     from paper_2506_13771_amd import synth
     shapes = [(name, d_in, d_out, RANKS_7B[bpw][max(d_in, d_out)]) for (name, d_in, d_out) in synth.LLAMA2_7B]
     res = ResidentLinears(shapes, max(ts), cfg=2, direct_words=False)
-    out = {"workload": f"Llama2-7B block, 7 linears at {bpw} BPW, bf16 x, fp16 scales, one lb_linear_forward_many "
-                       "call (weights warm in the caches)", "bpw": bpw, "per_T": []}
+    out = {"workload": f"Llama2-7B block, 7 linears at {bpw} BPW, bf16 x, fp16 scales, one list call "
+                       "(lb_list_forward for T <= 2, else lb_linear_forward_many; weights warm in the caches)",
+           "bpw": bpw, "per_T": []}
     for T in ts:
         rec = list_timing(res, T, max(steps, 50), max(warmup, 10))
         out["per_T"].append(rec)

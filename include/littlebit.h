@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define LB_ABI_VERSION 5
+#define LB_ABI_VERSION 6
 
 typedef enum lb_status {
   LB_OK = 0,
@@ -156,8 +156,10 @@ lb_status lb_workspace_init(void* workspace, size_t bytes, hipStream_t stream);
    partial sums of another workgroup of the same call, took the values it
    never saw as NaN (so the affected outputs are NaN, never stale values of an
    earlier call) and set the word; the outputs of the calls since the last
-   clear are then not to be trusted.  workspace_bytes must be at least the 256
-   bytes of the control block (LB_ERR_WORKSPACE). */
+   clear are then not to be trusted.  Bit 1: lb_list_forward found a plan that
+   does not match its descriptors and computed nothing.  workspace_bytes must
+   be at least the 256 bytes of the control block (LB_ERR_WORKSPACE).  For a
+   workspace of lb_list_* the word is part of the plan's header. */
 lb_status lb_workspace_status(void* workspace, size_t workspace_bytes, int32_t* status, hipStream_t stream);
 
 /* Largest token count LB_KERNEL_DECODE accepts. */
@@ -225,6 +227,44 @@ size_t lb_forward_many_workspace_bytes(const lb_linear_desc* descs, int64_t n);
    aligned, >= lb_forward_many_workspace_bytes(descs, n) bytes. */
 lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/* Streaming list forward of decode-sized linears: the decoding step of a
+   model in which every nn.Linear is a LittleBit linear (appendix "End-to-End
+   Decoding Throughput"), e.g. all linears of all layers of a model for a
+   batch of independent inputs, or the q/k/v or gate/up projections of one
+   layer.  Each linear is computed as lb_linear_forward computes it
+   (Proposition 1, Eq. proposition1, both paths, Eq. final_weight_approx_res)
+   and the result is bit-identical to lb_linear_forward_kernel(...,
+   LB_KERNEL_DECODE) for that linear; the whole list takes three launches
+   (latent partial sums of every linear, their sums times l, every output),
+   with no workgroup waiting for another.
+
+   Scope: every linear with work has 1 <= T <= 2 tokens, r <= 1024, a d_in
+   whose runs fit the look-up-table kernel (d_in <= 32768 at r <= 1024 is
+   always accepted), and the list shares one activation and one scale dtype
+   (LB_ERR_SHAPE / LB_ERR_DTYPE otherwise); linears with T == 0 or d_out == 0
+   are skipped, those with d_in == 0 or r == 0 get y = 0.  n <= 65535.  No y
+   may overlap another linear's x or y (LB_ERR_ARG); other checks as for
+   lb_linear_forward.
+
+   The list's descriptors live in the workspace (the "plan"):
+   lb_list_workspace_bytes: host, pure; bytes of a workspace for this list
+     (0 if the list is invalid or out of scope).
+   lb_list_init: writes the plan for descs into workspace (256-byte aligned,
+     >= lb_list_workspace_bytes bytes) and waits for the copy on `stream`
+     (it synchronises the stream, so it cannot be captured in a graph); call
+     it again whenever any field of any descriptor changes (pointers
+     included).
+   lb_list_forward: the forward of the list whose plan is in workspace;
+     asynchronous and capturable.  descs must be the array lb_list_init saw
+     (same values): the kernels compare a fingerprint of descs with the plan's
+     and, if they differ, write nothing but bit 1 of the workspace's error
+     word (lb_workspace_status). */
+size_t lb_list_workspace_bytes(const lb_linear_desc* descs, int64_t n);
+lb_status lb_list_init(const lb_linear_desc* descs, int64_t n, void* workspace, size_t workspace_bytes,
+                       hipStream_t stream);
+lb_status lb_list_forward(const lb_linear_desc* descs, int64_t n, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
 
 /* Latent K/V cache (paragraph "KV Cache Compression", Fig. kv_cache_viz,
    Table kv_cache_reduction: applied to the key and value projections, the

@@ -11,6 +11,7 @@ The names follow the C ABI:
   lb_packed_bytes, lb_bits_per_weight, lb_rank_for_bpw,
   lb_forward_workspace_bytes, lb_workspace_init, lb_workspace_status, lb_decode_max_tokens,
   lb_linear_forward_many, lb_forward_many_workspace_bytes,
+  lb_list_workspace_bytes, lb_list_init, lb_list_forward (class LittleBitList),
   lb_linear_latent, lb_latent_workspace_bytes,
   lb_linear_from_latent, lb_from_latent_workspace_bytes,
   lb_linear_backward, lb_backward_workspace_bytes.
@@ -29,7 +30,7 @@ LB_OK, LB_ERR_NULL, LB_ERR_SHAPE, LB_ERR_DTYPE, LB_ERR_ALIGN, LB_ERR_WORKSPACE, 
 LB_F32, LB_F16, LB_BF16 = 0, 1, 2
 LB_ROLE_U, LB_ROLE_V = 0, 1
 LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL, LB_KERNEL_DECODE_MFMA = 0, 1, 2, 3
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 
 class LittleBitError(RuntimeError):
@@ -97,6 +98,12 @@ def load_library(path: str = LIB_PATH):
     lib.lb_forward_many_workspace_bytes.argtypes = [ctypes.POINTER(lb_linear_desc), i64]
     lib.lb_linear_forward_many.restype = i32
     lib.lb_linear_forward_many.argtypes = [ctypes.POINTER(lb_linear_desc), i64, vp, sz, vp]
+    lib.lb_list_workspace_bytes.restype = sz
+    lib.lb_list_workspace_bytes.argtypes = [ctypes.POINTER(lb_linear_desc), i64]
+    lib.lb_list_init.restype = i32
+    lib.lb_list_init.argtypes = [ctypes.POINTER(lb_linear_desc), i64, vp, sz, vp]
+    lib.lb_list_forward.restype = i32
+    lib.lb_list_forward.argtypes = [ctypes.POINTER(lb_linear_desc), i64, vp, sz, vp]
     lib.lb_latent_workspace_bytes.restype = sz
     lib.lb_latent_workspace_bytes.argtypes = [i64, i64, i64]
     lib.lb_linear_latent.restype = i32
@@ -308,6 +315,37 @@ def lb_linear_forward_many(items, workspace=None, stream=None):
     return ys
 
 
+def lb_list_workspace_bytes(descs, n: int) -> int:
+    return int(load_library().lb_list_workspace_bytes(descs, n))
+
+
+class LittleBitList:
+    """A fixed list of decode-sized linears (items (x, paths, r, y), y allocated when None) run by the
+    streaming list forward: the plan is written once into the list's workspace (lb_list_init) and every
+    forward() is three launches (lb_list_forward).  The tensors must outlive the object and keep their
+    storage (the plan holds their addresses)."""
+
+    def __init__(self, items, stream=None):
+        torch = _torch()
+        self.items = items
+        self.descs, self.ys = make_descs(items)
+        self.n = len(items)
+        lib = load_library()
+        need = lb_list_workspace_bytes(self.descs, self.n)
+        if need == 0:
+            raise LittleBitError(LB_ERR_SHAPE, "lb_list_workspace_bytes (list out of scope or invalid)")
+        dev = self.ys[0].device if self.ys else "cuda"
+        self.workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        st = lib.lb_list_init(self.descs, self.n, _dev_ptr(self.workspace, "workspace"), need, _stream(stream))
+        _check(st, "lb_list_init")
+
+    def forward(self, stream=None):
+        st = load_library().lb_list_forward(self.descs, self.n, _dev_ptr(self.workspace, "workspace"),
+                                            self.workspace.numel(), _stream(stream))
+        _check(st, "lb_list_forward")
+        return self.ys
+
+
 def lb_latent_workspace_bytes(T: int, d_in: int, r: int) -> int:
     return int(load_library().lb_latent_workspace_bytes(T, d_in, r))
 
@@ -433,7 +471,7 @@ __all__ = [
     "lb_packed_bytes", "lb_bits_per_weight", "lb_rank_for_bpw", "lb_forward_workspace_bytes",
     "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "lb_workspace_status", "alloc_workspace", "lb_linear_forward",
     "lb_dense_reference_weight", "lb_linear_desc", "make_descs", "lb_forward_many_workspace_bytes",
-    "lb_linear_forward_many", "lb_latent_workspace_bytes", "lb_from_latent_workspace_bytes", "lb_linear_latent",
+    "lb_linear_forward_many", "lb_list_workspace_bytes", "LittleBitList", "lb_latent_workspace_bytes", "lb_from_latent_workspace_bytes", "lb_linear_latent",
     "lb_linear_from_latent", "lb_path_train", "LittleBitPathTrain", "lb_backward_workspace_bytes",
     "lb_linear_backward",
 ]

@@ -16,7 +16,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblittlebit.so")
-SOURCES = ["api.cpp", "pack.hip", "decode.hip", "decode_mma.hip", "prefill.hip", "latent_small.hip", "backward.hip", "dense_ref.hip"]
+SOURCES = ["api.cpp", "pack.hip", "decode.hip", "decode_mma.hip", "prefill.hip", "latent_small.hip", "backward.hip",
+           "dense_ref.hip", "stream.hip"]
+# the look-up-table kernels of decode.hip and stream.hip give bit-identical
+# results only if neither contracts a multiply and an add into one fma
+EXTRA_FLAGS = {"decode.hip": ["-ffp-contract=off"], "stream.hip": ["-ffp-contract=off"]}
 ARCH = os.environ.get("LB_OFFLOAD_ARCH", "gfx950")
 
 
@@ -35,7 +39,7 @@ def common_flags():
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj] + common_flags()
+    cmd = [hipcc(), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj] + common_flags() + EXTRA_FLAGS.get(src, [])
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{res.stdout}\n{res.stderr}")

@@ -1,9 +1,11 @@
 // C ABI of the LittleBit library: host-side validation, dispatch and launch.
 // Every argument is checked before anything touches HIP, so every error path
 // is testable without a GPU; nothing here allocates device memory.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <vector>
 
 #include "lb_backward.h"
 #include "lb_latent.h"
@@ -392,6 +394,141 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
     off += sb;
   }
   return flush();
+}
+
+namespace {
+
+// FNV-1a over the fields of the descriptors (not their bytes: padding is not
+// part of a descriptor's value)
+struct Fnv {
+  uint64_t h = 1469598103934665603ull;
+  void add(uint64_t v) {
+    for (int i = 0; i < 8; ++i) {
+      h ^= (v >> (8 * i)) & 0xffu;
+      h *= 1099511628211ull;
+    }
+  }
+  void add(const void* p) { add(static_cast<uint64_t>(reinterpret_cast<uintptr_t>(p))); }
+};
+
+uint64_t list_fingerprint(const lb_linear_desc* descs, int64_t n) {
+  Fnv f;
+  f.add(static_cast<uint64_t>(n));
+  for (int64_t i = 0; i < n; ++i) {
+    const lb_linear_desc& d = descs[i];
+    f.add(d.x);
+    f.add(d.y);
+    f.add(static_cast<uint64_t>(enum_value(d.act_dtype)));
+    f.add(static_cast<uint64_t>(enum_value(d.scale_dtype)));
+    f.add(static_cast<uint64_t>(d.T));
+    f.add(static_cast<uint64_t>(d.d_in));
+    f.add(static_cast<uint64_t>(d.d_out));
+    f.add(static_cast<uint64_t>(d.r));
+    for (int p = 0; p < 2; ++p) {
+      f.add(d.paths[p].U);
+      f.add(d.paths[p].V);
+      f.add(d.paths[p].h);
+      f.add(d.paths[p].g);
+      f.add(d.paths[p].l);
+    }
+  }
+  return f.h;
+}
+
+// Outputs of a list overlap nothing the list reads or writes, in O(n log n):
+// the y ranges sorted by start must be disjoint, and no x range may meet one.
+bool list_outputs_disjoint(const lb_linear_desc* descs, int64_t n) {
+  struct Range {
+    uintptr_t lo, hi;
+    int64_t who;
+  };
+  std::vector<Range> ys, xs;
+  for (int64_t i = 0; i < n; ++i) {
+    const lb_linear_desc& d = descs[i];
+    const size_t es = dtype_size(d.act_dtype);
+    const size_t ny = static_cast<size_t>(d.T * d.d_out) * es, nx = static_cast<size_t>(d.T * d.d_in) * es;
+    if (ny > 0) ys.push_back({reinterpret_cast<uintptr_t>(d.y), reinterpret_cast<uintptr_t>(d.y) + ny, i});
+    if (nx > 0) xs.push_back({reinterpret_cast<uintptr_t>(d.x), reinterpret_cast<uintptr_t>(d.x) + nx, i});
+  }
+  std::sort(ys.begin(), ys.end(), [](const Range& a, const Range& b) { return a.lo < b.lo; });
+  for (size_t k = 1; k < ys.size(); ++k)
+    if (ys[k].lo < ys[k - 1].hi) return false;
+  for (const Range& x : xs) {
+    // the first y starting at or after x.lo, and the one before it
+    // (a linear's y may overlap its own x: its output is written after its
+    // input has been read; the ys are disjoint, so the walk below stops at
+    // the first other y inside x)
+    auto it = std::lower_bound(ys.begin(), ys.end(), x.lo, [](const Range& a, uintptr_t v) { return a.lo < v; });
+    if (it != ys.begin() && (it - 1)->hi > x.lo && (it - 1)->who != x.who) return false;
+    for (; it != ys.end() && it->lo < x.hi; ++it)
+      if (it->who != x.who) return false;
+  }
+  return true;
+}
+
+// the validation lb_list_* share; on success fills args (one per descriptor)
+lb_status list_check(const lb_linear_desc* descs, int64_t n, std::vector<lb::ForwardArgs>& args) {
+  if (n < 0 || n > 65535) return LB_ERR_ARG;
+  if (n > 0 && !descs) return LB_ERR_NULL;
+  int act = -1, sc = -1;
+  args.clear();
+  for (int64_t i = 0; i < n; ++i) {
+    const lb_linear_desc& d = descs[i];
+    const lb_status st = check_forward(d);
+    if (st != LB_OK) return st;
+    lb::ForwardArgs a = make_args(d.x, d.act_dtype, d.T, d.d_in, d.d_out, d.r, d.paths, d.scale_dtype, d.y, nullptr, 0);
+    if (d.T > 0 && d.d_out > 0 && d.d_in > 0 && d.r > 0) {
+      if (!lb::stream_supports(a)) return LB_ERR_SHAPE;
+      if (act < 0) act = a.act_dt, sc = a.sc_dt;
+      if (a.act_dt != act || a.sc_dt != sc) return LB_ERR_DTYPE;
+    }
+    args.push_back(a);
+  }
+  if (!list_outputs_disjoint(descs, n)) return LB_ERR_ARG;
+  return LB_OK;
+}
+
+}  // namespace
+
+size_t lb_list_workspace_bytes(const lb_linear_desc* descs, int64_t n) {
+  std::vector<lb::ForwardArgs> args;
+  if (list_check(descs, n, args) != LB_OK) return 0;
+  return lb::stream_workspace_bytes(args.data(), static_cast<int>(n));
+}
+
+lb_status lb_list_init(const lb_linear_desc* descs, int64_t n, void* workspace, size_t workspace_bytes,
+                       hipStream_t stream) {
+  std::vector<lb::ForwardArgs> args;
+  lb_status st = list_check(descs, n, args);
+  if (st != LB_OK) return st;
+  const size_t need = lb::stream_workspace_bytes(args.data(), static_cast<int>(n));
+  if (!workspace) return LB_ERR_NULL;
+  if (!aligned(workspace, 256)) return LB_ERR_ALIGN;
+  if (workspace_bytes < need) return LB_ERR_WORKSPACE;
+  const hipError_t e =
+      lb::stream_init(args.data(), static_cast<int>(n), list_fingerprint(descs, n), workspace, stream);
+  return e == hipSuccess ? LB_OK : LB_ERR_HIP;
+}
+
+lb_status lb_list_forward(const lb_linear_desc* descs, int64_t n, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+  std::vector<lb::ForwardArgs> args;
+  lb_status st = list_check(descs, n, args);
+  if (st != LB_OK) return st;
+  const size_t need = lb::stream_workspace_bytes(args.data(), static_cast<int>(n));
+  if (!workspace) return LB_ERR_NULL;
+  if (!aligned(workspace, 256)) return LB_ERR_ALIGN;
+  if (workspace_bytes < need) return LB_ERR_WORKSPACE;
+  hipError_t e = hipSuccess;
+  // linears with an empty reduction: y = 0
+  for (int64_t i = 0; i < n && e == hipSuccess; ++i) {
+    const lb_linear_desc& d = descs[i];
+    if (d.T > 0 && d.d_out > 0 && (d.d_in == 0 || d.r == 0))
+      e = lb::launch_zero_elems(d.y, d.T * d.d_out, d.act_dtype, stream);
+  }
+  if (e == hipSuccess)
+    e = lb::stream_forward(args.data(), static_cast<int>(n), list_fingerprint(descs, n), workspace, stream);
+  return e == hipSuccess ? LB_OK : LB_ERR_HIP;
 }
 
 size_t lb_latent_workspace_bytes(int64_t T, int64_t d_in, int64_t r) {

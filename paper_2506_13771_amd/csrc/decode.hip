@@ -51,32 +51,28 @@
 #include <atomic>
 #include <type_traits>
 
-#include "device_common.h"
+#include "lut_common.h"
 
 namespace lb {
 
 namespace {
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
+using lut::build_table;
+using lut::f32x4;
+using lut::kBlk;
+using lut::kChunk;
+using lut::kKey;
+using lut::kMaxRuns;
+using lut::tsw;
+using lut::word_sum;
 
 constexpr int kThreads = 256;
 constexpr int kKc = 16;                 // latent columns per stage-1 tile
-constexpr int kChunk = 32;              // blocks of 32 inputs per stage-1 chunk (one table per thread)
-constexpr int kMaxRuns = 16;            // d_in runs per latent tile (partials per z value)
-constexpr int kBlk = 8 * 16 + 16;       // floats of one block's 8 nibble tables, padded (bank spread)
 constexpr int kKQ = 4;                  // stage 2: lanes per output row
 constexpr int kRows2 = kThreads / kKQ;  // stage 2: output rows per workgroup
 constexpr int kGather = 8;              // stage 2: slots a thread gathers per round
 constexpr int kDirectMaxSlots = kThreads * kGather;  // stage 2 reads every partial up to this many
 constexpr size_t kLds2Max = 64 * 1024;  // stage-2 LDS budget per token chunk (bytes)
-
-// Table swizzle: entry m of nibble table q of a block sits at m ^ tsw(q).
-// tsw keeps 4-entry groups contiguous (128-bit writes) and spreads the writes
-// of a wave's 64 builders over all LDS banks.  XORing a packed word with kKey
-// applies tsw(q) to each nibble q at once.
-__host__ __device__ constexpr int tsw(int q) { return (q & 6) << 1; }
-constexpr uint32_t kKey = 0xCC884400u;
-static_assert(((kKey >> 8) & 15) == tsw(2) && ((kKey >> 28) & 15) == tsw(7), "swizzle key");
 
 struct DecodeParams {
   const void* x;
@@ -95,34 +91,13 @@ struct DecodeParams {
   int bpr;     // 32-input blocks per run
   int n_s1;    // stage-1 workgroups (2 * nkt * s1d)
   int n_s2;    // stage-2 workgroups
-  int n_done;  // stage-2 workgroups of the launch that count on ctrl (the last one ends the call)
+  int ctr_word;   // control-block word counting this linear's finished stage-2 workgroups
+  int n_members;  // linears of the launch sharing the control block (1: a single call)
   int direct;  // stage 2 reads every run's partial (else the two-level sums)
   int tch;     // tokens per stage-2 chunk
   uint32_t magic_r;  // fast_div multiplier for r
   uint32_t x_bytes, g_bytes, l_bytes, h_bytes, v_bytes, u_bytes;
 };
-
-// The 16 entries of one nibble table over a0..a3 (entry m = sum_i (bit i of m
-// ? -a_i : a_i)), written as 4 groups of 4 at their swizzled positions.
-__device__ __forceinline__ void build_table(float* t16, int q, float a0, float a1, float a2, float a3) {
-  const float s01[4] = {a0 + a1, a1 - a0, a0 - a1, -a0 - a1};
-  const float s23[4] = {a2 + a3, a3 - a2, a2 - a3, -a2 - a3};
-  const int gs = tsw(q) >> 2;
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const f32x4 v = {s01[0] + s23[c], s01[1] + s23[c], s01[2] + s23[c], s01[3] + s23[c]};
-    *reinterpret_cast<f32x4*>(t16 + 4 * (c ^ gs)) = v;
-  }
-}
-
-// Signed sum of one packed word against the 8 tables of a block (tb8 points
-// at the block's first table; wk is the word XORed with kKey).
-__device__ __forceinline__ float word_sum(const float* tb8, uint32_t wk) {
-  float v[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) v[q] = tb8[16 * q + ((wk >> (4 * q)) & 15)];
-  return ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
-}
 
 // ---------------------------------------------------------------------------
 // stage 1
@@ -184,11 +159,7 @@ __device__ void stage1(const DecodeParams& P, int wg, float* smem) {
 #pragma unroll
     for (int t = 0; t < TM; ++t) {
       float a[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        a[i] = raw4_elem<ACT, VEC>(xb[t], i) * raw4_elem<SC, VEC>(gb, i);
-        if (tailv != 0 && jb + i >= d_in) a[i] = 0.0f;  // x past d_in belongs to the next row
-      }
+      lut::table_inputs<ACT, SC, VEC>(xb[t], gb, jb, d_in, tailv, a);
       build_table(tbl + (t * kChunk + tb) * kBlk + 16 * tq, tq, a[0], a[1], a[2], a[3]);
     }
     __syncthreads();
@@ -218,8 +189,8 @@ __device__ void stage1(const DecodeParams& P, int wg, float* smem) {
   __syncthreads();
   if (tid < 16 * TM) {
     const int t = tid >> 4;  // tid & 15 == kk: this thread loaded l of its own column
-    const float s = ((red[(0 * TM + t) * 16 + kk] + red[(1 * TM + t) * 16 + kk]) +
-                     (red[(2 * TM + t) * 16 + kk] + red[(3 * TM + t) * 16 + kk])) *
+    const float s = lut::tree4(red[(0 * TM + t) * 16 + kk], red[(1 * TM + t) * 16 + kk],
+                               red[(2 * TM + t) * 16 + kk], red[(3 * TM + t) * 16 + kk]) *
                     bits_to_f32<SC>(lbits);
     if (t < T && kok) {
       uint64_t* slots = P.partial + static_cast<int64_t>(p * T + t) * P.s1d * r + k;  // [p][t][run][k]
@@ -331,7 +302,7 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
         tag = epoch + 1u;
         // count this workgroup as one that has read the epoch (the returned
         // count is used at the end)
-        if (tid == 0) done_before = atomic_add_relaxed(P.ctrl + kCtrlDone, 1u);
+        if (tid == 0) done_before = atomic_add_relaxed(P.ctrl + P.ctr_word, 1u);
       }
       for (uint32_t it = 0;; ++it) {
         bool ready = true;
@@ -398,7 +369,7 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
       const float h0 = bits_to_f32<SC>(hb[b][0]), h1 = bits_to_f32<SC>(hb[b][1]);
 #pragma unroll
       for (int t = 0; t < TM; ++t) {
-        const float v = h0 * quad_sum(acc[0][t]) + h1 * quad_sum(acc[1][t]);
+        const float v = lut::row_value(h0, quad_sum(acc[0][t]), h1, quad_sum(acc[1][t]));
         if (iokr[b] && t < tn && kq == t) st<ACT>(P.y, static_cast<int64_t>(t0 + t) * d_out + ir[b], v);
       }
     }
@@ -411,9 +382,17 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
   // then: stage-2 workgroups counted themselves after reading it, and every
   // stage-1 workgroup published values carrying the tag, which this
   // workgroup has gathered (directly, or through the two-level reducers).
-  if (tid == 0 && done_before == static_cast<uint32_t>(P.n_done - 1)) {
-    atomic_store_relaxed(P.ctrl + kCtrlDone, 0u);
-    atomic_store_relaxed(P.ctrl + kCtrlEpoch, tag);
+  // In a list launch each linear counts its workgroups on a word of its own
+  // (one contended word for all of them would serialise the atomics), and the
+  // last workgroup of each linear counts that linear on the shared word.
+  if (tid == 0 && done_before == static_cast<uint32_t>(P.n_s2 - 1)) {
+    atomic_store_relaxed(P.ctrl + P.ctr_word, 0u);
+    const bool last = P.n_members <= 1 ||
+                      atomic_add_relaxed(P.ctrl + kCtrlDone, 1u) == static_cast<uint32_t>(P.n_members - 1);
+    if (last) {
+      if (P.n_members > 1) atomic_store_relaxed(P.ctrl + kCtrlDone, 0u);
+      atomic_store_relaxed(P.ctrl + kCtrlEpoch, tag);
+    }
   }
 }
 
@@ -657,7 +636,8 @@ bool decode_params(const ForwardArgs& a, const DecodeGeom& g, DecodeParams& P) {
   P.bpr = g.bpr;
   P.n_s1 = g.n_s1;
   P.n_s2 = g.n_s2;
-  P.n_done = g.n_s2;
+  P.ctr_word = kCtrlDone;
+  P.n_members = 1;
   P.direct = g.direct;
   P.tch = g.tch;
   P.magic_r = a.r > 1 ? static_cast<uint32_t>(((uint64_t(1) << 32) + a.r - 1) / a.r) : 0u;
@@ -711,13 +691,16 @@ hipError_t launch_decode_batch(const ForwardArgs* a, int n, hipStream_t stream) 
     s2 += B.p[i].n_s2;
     B.s2_end[i] = s2;
   }
-  // members that share a control block end the call together: the last of
-  // all their stage-2 workgroups stores the epoch
+  // members that share a control block end the call together: each counts
+  // its stage-2 workgroups on word kCtrlMember + i, the last member to finish
+  // stores the epoch
   for (int i = 0; i < n; ++i) {
     int cnt = 0;
-    for (int j = 0; j < n; ++j)
-      if (B.p[j].ctrl == B.p[i].ctrl) cnt += B.p[j].n_s2;
-    B.p[i].n_done = cnt;
+    for (int j = 0; j < n; ++j) cnt += B.p[j].ctrl == B.p[i].ctrl ? 1 : 0;
+    if (cnt > 1) {
+      B.p[i].ctr_word = kCtrlMember + i;
+      B.p[i].n_members = cnt;
+    }
   }
   return launch_any(B, a[0].act_dt, T, a[0].sc_dt, vec, wpl, dim3(s1 + s2), vec ? smem_vec : smem_elem, stream);
 }

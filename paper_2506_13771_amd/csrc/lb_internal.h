@@ -107,6 +107,7 @@ __device__ __forceinline__ bool spin_until_at_least(const uint32_t* p, uint32_t 
 constexpr int kCtrlEpoch = 0;      // decode: tag of the last completed call
 constexpr int kCtrlDone = 1;       // decode: finished stage-2 workgroups of the running call
 constexpr int kCtrlError = 2;      // set to nonzero if a bounded wait expired
+constexpr int kCtrlMember = 16;    // list launches: finished stage-2 workgroups of member m at word 16 + m
 constexpr int kCtrlWords = 64;
 constexpr size_t kCtrlBytes = ((kCtrlWords * 4 + 255) / 256) * 256;
 
@@ -215,6 +216,12 @@ size_t from_latent_workspace_bytes(int T, int r);
 hipError_t launch_latent(const ForwardArgs& a, int lat_dt, hipStream_t stream);
 hipError_t launch_from_latent(const ForwardArgs& a, const void* lat, int lat_dt, hipStream_t stream);
 hipError_t launch_dense_ref(const ForwardArgs& a, float* W, hipStream_t stream);
+// Streaming list of decode-sized linears (stream.hip): three launches for the
+// whole list, the plan (descriptors and work maps) in the workspace.
+bool stream_supports(const ForwardArgs& a);
+size_t stream_workspace_bytes(const ForwardArgs* a, int n);
+hipError_t stream_init(const ForwardArgs* a, int n, uint64_t fingerprint, void* ws, hipStream_t stream);
+hipError_t stream_forward(const ForwardArgs* a, int n, uint64_t fingerprint, void* ws, hipStream_t stream);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 // *out = the error word of the control block at ctrl, which is then cleared
 hipError_t launch_take_status(uint32_t* ctrl, int32_t* out, hipStream_t stream);

@@ -400,3 +400,43 @@ def test_backward_validation_errors(lib):
     # dx may be NULL (not computed); U of the paths is never read
     assert _bwd(lib, dx=0) == lb.LB_ERR_WORKSPACE
     assert _bwd(lib, paths=_paths(U=FAKE + 1)) == lb.LB_ERR_WORKSPACE
+
+
+def _list_descs(n, T=1, d_in=64, d_out=64, r=16, act=lb.LB_BF16, sc=lb.LB_F16, ystep=4096):
+    arr = (lb.lb_linear_desc * n)()
+    for i in range(n):
+        arr[i] = lb.lb_linear_desc(FAKE, act, T, d_in, d_out, r, _paths(), sc, FAKE * 4 + i * ystep)
+    return arr
+
+
+def test_list_validation(lib):
+    arr = _list_descs(3)
+    need = lib.lb_list_workspace_bytes(arr, 3)
+    assert need > 0
+    # out of scope: three tokens, a rank above 1024, mixed dtypes
+    assert lib.lb_list_workspace_bytes(_list_descs(2, T=3), 2) == 0
+    assert lib.lb_list_workspace_bytes(_list_descs(2, r=1040), 2) == 0
+    assert lib.lb_list_init(_list_descs(2, T=3), 2, FAKE, 1 << 30, None) == lb.LB_ERR_SHAPE
+    mixed = _list_descs(2)
+    mixed[1].act_dtype = lb.LB_F32
+    assert lib.lb_list_init(mixed, 2, FAKE, 1 << 30, None) == lb.LB_ERR_DTYPE
+    assert lib.lb_list_forward(mixed, 2, FAKE, 1 << 30, None) == lb.LB_ERR_DTYPE
+    # overlapping outputs, and an output over another linear's input
+    assert lib.lb_list_init(_list_descs(2, ystep=2), 2, FAKE, 1 << 30, None) == lb.LB_ERR_ARG
+    over = _list_descs(2)
+    over[1].x = over[0].y
+    assert lib.lb_list_forward(over, 2, FAKE, 1 << 30, None) == lb.LB_ERR_ARG
+    # a linear's output may overlap its own input
+    own = _list_descs(1)
+    own[0].y = own[0].x
+    assert lib.lb_list_workspace_bytes(own, 1) > 0
+    # workspace checks
+    assert lib.lb_list_init(arr, 3, 0, need, None) == lb.LB_ERR_NULL
+    assert lib.lb_list_init(arr, 3, FAKE + 16, need, None) == lb.LB_ERR_ALIGN
+    assert lib.lb_list_init(arr, 3, FAKE, need - 1, None) == lb.LB_ERR_WORKSPACE
+    assert lib.lb_list_forward(arr, 3, FAKE, need - 1, None) == lb.LB_ERR_WORKSPACE
+    assert lib.lb_list_forward(None, 3, FAKE, need, None) == lb.LB_ERR_NULL
+    assert lib.lb_list_forward(arr, -1, FAKE, need, None) == lb.LB_ERR_ARG
+    assert lib.lb_list_forward(arr, 70000, FAKE, need, None) == lb.LB_ERR_ARG
+    # the workspace grows with the list
+    assert lib.lb_list_workspace_bytes(_list_descs(600), 600) > need
