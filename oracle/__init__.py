@@ -26,6 +26,11 @@ Functions and the passages of arXiv 2506.13771 they follow:
                            SmoothSign surrogate for the sign's derivative,
                            Sec. 4 "Training Details" and Appendix "SmoothSign
                            versus Straight-Through Estimator";
+  svd / rank1 /            Dual-SVID initialisation, Sec. 3.2 "Dual-SVID
+  svid_path / dual_svid    Initialization" (Eqs. sign_init_concise,
+  (O7)                     scale_init_rank1_concise, latent_scale_init_concise_0),
+                           and the residual path from the primary path's
+                           error, Sec. 3.3 "Residual Compensation";
   bpw / rank_real /
   rank_for_bpw             Appendix "Average Bits Per Weight Calculation",
                            Eqs. (b_calculation) and (r_calculation).
@@ -76,6 +81,16 @@ def _load():
         lib.lbo_forward_factored.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, i32, vp]
         lib.lbo_forward_factored_par.restype = None
         lib.lbo_forward_factored_par.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, i32, i32, vp]
+        lib.lbo_svd.restype = None
+        lib.lbo_svd.argtypes = [vp, i64, i64, vp, vp, vp]
+        lib.lbo_rank1.restype = None
+        lib.lbo_rank1.argtypes = [vp, i64, i64, vp, vp]
+        lib.lbo_svid_path.restype = None
+        lib.lbo_svid_path.argtypes = [vp, i64, i64, i64, vp, vp, vp, vp, vp]
+        lib.lbo_path_weight.restype = None
+        lib.lbo_path_weight.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
+        lib.lbo_dual_svid.restype = None
+        lib.lbo_dual_svid.argtypes = [vp, i64, i64, i64, vp, vp, vp, vp, vp, vp]
         lib.lbo_max_threads.restype = i32
         lib.lbo_max_threads.argtypes = []
         lib.lbo_forward_sampled.restype = None
@@ -318,3 +333,73 @@ def rank_real(d_in: int, d_out: int, b: float) -> float:
 def rank_for_bpw(d_in: int, d_out: int, b: float, mult: int = 16, mode: int = 1) -> int:
     """mode 0: nearest integer (paper's examples); mode 1: largest multiple of mult within budget."""
     return int(_load().lbo_rank_for_bpw(d_in, d_out, b, mult, mode))
+
+
+# ----------------------------------------------------------------------------
+# O7: Dual-SVID initialisation
+# ----------------------------------------------------------------------------
+def svd(A):
+    """Thin SVD by one-sided Jacobi: A [m, n] = U diag(s) V^T, U [m, k], V [n, k], k = min(m, n),
+    s descending, each left vector's entry of largest magnitude positive."""
+    A = np.ascontiguousarray(A, dtype=np.float64)
+    m, n = A.shape
+    k = min(m, n)
+    U = np.zeros((m, k))
+    V = np.zeros((n, k))
+    s = np.zeros(k)
+    _load().lbo_svd(_p(A), m, n, _p(U), _p(s), _p(V))
+    return U, s, V
+
+
+def rank1(M):
+    """Best rank-1 approximation M ~ a b^T of a nonnegative matrix M [d, r], the top singular value
+    split evenly between a and b."""
+    M = np.ascontiguousarray(M, dtype=np.float64)
+    d, r = M.shape
+    a = np.zeros(d)
+    b = np.zeros(r)
+    _load().lbo_rank1(_p(M), d, r, _p(a), _p(b))
+    return a, b
+
+
+def svid_path(W, r):
+    """One path of Dual-SVID: (U_latent [d_out, r], V_latent [d_in, r], h0, g0, l0)."""
+    W = np.ascontiguousarray(W, dtype=np.float64)
+    d_out, d_in = W.shape
+    if not 1 <= r <= min(d_out, d_in):
+        raise ValueError("rank out of range")
+    Ul = np.zeros((d_out, r))
+    Vl = np.zeros((d_in, r))
+    h, g, l = np.zeros(d_out), np.zeros(d_in), np.zeros(r)
+    _load().lbo_svid_path(_p(W), d_out, d_in, r, _p(Ul), _p(Vl), _p(h), _p(g), _p(l))
+    return Ul, Vl, h, g, l
+
+
+def path_weight(Ul, Vl, h, g, l):
+    """diag(h) sign(U_latent) diag(l) sign(V_latent)^T diag(g) of one path."""
+    Ul = np.ascontiguousarray(Ul, dtype=np.float64)
+    Vl = np.ascontiguousarray(Vl, dtype=np.float64)
+    h, g, l = (np.ascontiguousarray(a, dtype=np.float64) for a in (h, g, l))
+    d_out, r = Ul.shape
+    d_in = Vl.shape[0]
+    W = np.zeros((d_out, d_in))
+    _load().lbo_path_weight(_p(Ul), _p(Vl), _p(h), _p(g), _p(l), d_out, d_in, r, _p(W))
+    return W
+
+
+def dual_svid(W, r) -> dict:
+    """Dual-SVID of both paths: the primary from W, the residual from W - W_hat_pri,0.  Returns
+    {"U": [2 x U_latent], "V": [...], "h": [...], "g": [...], "l": [...], "Wres": W - W_hat_pri,0}."""
+    W = np.ascontiguousarray(W, dtype=np.float64)
+    d_out, d_in = W.shape
+    if not 1 <= r <= min(d_out, d_in):
+        raise ValueError("rank out of range")
+    U = [np.zeros((d_out, r)) for _ in range(2)]
+    V = [np.zeros((d_in, r)) for _ in range(2)]
+    h = [np.zeros(d_out) for _ in range(2)]
+    g = [np.zeros(d_in) for _ in range(2)]
+    l = [np.zeros(r) for _ in range(2)]
+    Wres = np.zeros((d_out, d_in))
+    _load().lbo_dual_svid(_p(W), d_out, d_in, r, _ptr_array(U), _ptr_array(V), _ptr_array(h), _ptr_array(g),
+                          _ptr_array(l), _p(Wres))
+    return {"U": U, "V": V, "h": h, "g": g, "l": l, "Wres": Wres}

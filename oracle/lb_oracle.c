@@ -472,3 +472,198 @@ int64_t lbo_rank_for_bpw(int64_t d_in, int64_t d_out, double b, int64_t mult, in
   while (lbo_total_bits(d_in, d_out, r + mult, 2) <= budget) r += mult;
   return r;
 }
+
+/* ---------------------------------------------------------------------- */
+/* O7: Dual-SVID initialisation (Sec. 3.2 "Dual-SVID Initialization",      */
+/* Eqs. sign_init_concise, scale_init_rank1_concise,                       */
+/* latent_scale_init_concise_0) and the residual path's initialisation     */
+/* from the primary path's error (Sec. 3.3 "Residual Compensation").       */
+/*                                                                         */
+/* Readings where the section is silent (listed in the design notes):      */
+/*   - the truncated SVD W ~ U' V'^T splits each singular value evenly:    */
+/*     U' = U_r diag(sqrt(sigma)), V' = V_r diag(sqrt(sigma));             */
+/*   - a singular pair's sign is fixed by making the entry of largest      */
+/*     magnitude of its left vector positive (the first one on a tie);     */
+/*   - the rank-1 factors of a magnitude matrix M ~ s l^T split the top    */
+/*     singular value evenly, s = sqrt(s1) u1, l = sqrt(s1) v1, with the   */
+/*     sign that makes sum(u1) >= 0 (M is nonnegative, so u1, v1 are);     */
+/*   - sign() of a latent factor as everywhere else: -1 iff < 0.           */
+/* The effective weight diag(h0) sign(U') diag(l0) sign(V')^T diag(g0) is  */
+/* the same under either even split (any split moves a factor between h0   */
+/* and l_u0, or g0 and l_v0) and under any choice of singular-pair signs   */
+/* (a pair flips a column of both sign matrices).                          */
+/* ---------------------------------------------------------------------- */
+
+/* Thin SVD of A [m x n] (row-major): A = U diag(s) V^T, U [m x k], V [n x k],
+   k = min(m, n), s descending, by one-sided Jacobi rotations (Hestenes):
+   rotate pairs of columns of a working copy until every pair is orthogonal;
+   the column norms are then the singular values and the accumulated rotations
+   the right vectors.  Works on the columns of A if m >= n, else of A^T. */
+void lbo_svd(const double* A, int64_t m, int64_t n, double* U, double* s, double* V) {
+  const int tall = m >= n;
+  const int64_t rows = tall ? m : n, cols = tall ? n : m;  /* G = A or A^T, rows x cols */
+  double* G = (double*)malloc(sizeof(double) * (size_t)(rows * cols > 0 ? rows * cols : 1));
+  double* R = (double*)malloc(sizeof(double) * (size_t)(cols * cols > 0 ? cols * cols : 1));
+  for (int64_t i = 0; i < rows; i++)
+    for (int64_t j = 0; j < cols; j++) G[i * cols + j] = tall ? A[i * n + j] : A[j * n + i];
+  for (int64_t i = 0; i < cols; i++)
+    for (int64_t j = 0; j < cols; j++) R[i * cols + j] = i == j ? 1.0 : 0.0;
+  for (int sweep = 0; sweep < 100; sweep++) {
+    int rotated = 0;
+    for (int64_t p = 0; p < cols; p++)
+      for (int64_t q = p + 1; q < cols; q++) {
+        double a = 0.0, b = 0.0, c = 0.0;
+        for (int64_t i = 0; i < rows; i++) {
+          a += G[i * cols + p] * G[i * cols + p];
+          b += G[i * cols + q] * G[i * cols + q];
+          c += G[i * cols + p] * G[i * cols + q];
+        }
+        if (c == 0.0 || fabs(c) <= 1e-14 * sqrt(a * b)) continue;
+        rotated = 1;
+        /* the rotation that zeroes the (p, q) entry of G^T G */
+        const double zeta = (b - a) / (2.0 * c);
+        const double t = (zeta >= 0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+        const double cs = 1.0 / sqrt(1.0 + t * t), sn = cs * t;
+        for (int64_t i = 0; i < rows; i++) {
+          const double gp = G[i * cols + p], gq = G[i * cols + q];
+          G[i * cols + p] = cs * gp - sn * gq;
+          G[i * cols + q] = sn * gp + cs * gq;
+        }
+        for (int64_t i = 0; i < cols; i++) {
+          const double rp = R[i * cols + p], rq = R[i * cols + q];
+          R[i * cols + p] = cs * rp - sn * rq;
+          R[i * cols + q] = sn * rp + cs * rq;
+        }
+      }
+    if (!rotated) break;
+  }
+  /* singular values = column norms; order them descending */
+  int64_t* ord = (int64_t*)malloc(sizeof(int64_t) * (size_t)(cols > 0 ? cols : 1));
+  double* nrm = (double*)malloc(sizeof(double) * (size_t)(cols > 0 ? cols : 1));
+  for (int64_t j = 0; j < cols; j++) {
+    double a = 0.0;
+    for (int64_t i = 0; i < rows; i++) a += G[i * cols + j] * G[i * cols + j];
+    nrm[j] = sqrt(a);
+    ord[j] = j;
+  }
+  for (int64_t j = 1; j < cols; j++) /* insertion sort, stable */
+    for (int64_t i = j; i > 0 && nrm[ord[i]] > nrm[ord[i - 1]]; i--) {
+      const int64_t tmp = ord[i];
+      ord[i] = ord[i - 1];
+      ord[i - 1] = tmp;
+    }
+  /* G's columns / sigma are the vectors along `rows`, R's along `cols` */
+  for (int64_t k = 0; k < cols; k++) {
+    const int64_t j = ord[k];
+    const double sg = nrm[j];
+    s[k] = sg;
+    double* L = tall ? U : V; /* vectors of length rows */
+    double* Rv = tall ? V : U; /* vectors of length cols */
+    for (int64_t i = 0; i < rows; i++) L[i * cols + k] = sg > 0.0 ? G[i * cols + j] / sg : 0.0;
+    for (int64_t i = 0; i < cols; i++) Rv[i * cols + k] = R[i * cols + j];
+  }
+  /* sign convention: the left vector's entry of largest magnitude is positive */
+  for (int64_t k = 0; k < cols; k++) {
+    int64_t best = 0;
+    double bv = -1.0;
+    for (int64_t i = 0; i < m; i++) {
+      const double v = fabs(U[i * cols + k]);
+      if (v > bv) {
+        bv = v;
+        best = i;
+      }
+    }
+    if (U[best * cols + k] < 0.0) {
+      for (int64_t i = 0; i < m; i++) U[i * cols + k] = -U[i * cols + k];
+      for (int64_t i = 0; i < n; i++) V[i * cols + k] = -V[i * cols + k];
+    }
+  }
+  free(ord);
+  free(nrm);
+  free(G);
+  free(R);
+}
+
+/* Best rank-1 approximation M ~ a b^T of a nonnegative matrix M [d x r]
+   (Eq. scale_init_rank1_concise): the top singular triplet, its value split
+   evenly, a = sqrt(s1) u1, b = sqrt(s1) v1, signed so that sum(u1) >= 0. */
+void lbo_rank1(const double* M, int64_t d, int64_t r, double* a, double* b) {
+  const int64_t k = d < r ? d : r;
+  double* Us = (double*)malloc(sizeof(double) * (size_t)(d * k > 0 ? d * k : 1));
+  double* Vs = (double*)malloc(sizeof(double) * (size_t)(r * k > 0 ? r * k : 1));
+  double* sv = (double*)malloc(sizeof(double) * (size_t)(k > 0 ? k : 1));
+  lbo_svd(M, d, r, Us, sv, Vs);
+  double sum = 0.0;
+  for (int64_t i = 0; i < d; i++) sum += Us[i * k];
+  const double sg = k > 0 ? sqrt(sv[0]) : 0.0, f = sum >= 0.0 ? 1.0 : -1.0;
+  for (int64_t i = 0; i < d; i++) a[i] = k > 0 ? f * sg * Us[i * k] : 0.0;
+  for (int64_t j = 0; j < r; j++) b[j] = k > 0 ? f * sg * Vs[j * k] : 0.0;
+  free(Us);
+  free(Vs);
+  free(sv);
+}
+
+/* One path of Dual-SVID for a weight W [d_out x d_in] and rank r
+   (1 <= r <= min(d_out, d_in)):
+     (1) truncated SVD, U' = U_r diag(sqrt(sigma)), V' = V_r diag(sqrt(sigma));
+     (2) U_sign = sign(U'), V_sign = sign(V')            (Eq. sign_init_concise);
+     (3) |U'| ~ h0 l_u^T, |V'| ~ g0 l_v^T               (Eq. scale_init_rank1_concise),
+         l0 = l_u (.) l_v                                (Eq. latent_scale_init_concise_0).
+   Outputs: the latent factors U' [d_out x r] and V' [d_in x r] (the QAT latent
+   initialisation, whose signs are U_sign and V_sign), h0 [d_out], g0 [d_in],
+   l0 [r]. */
+void lbo_svid_path(const double* W, int64_t d_out, int64_t d_in, int64_t r, double* Ulat, double* Vlat, double* h,
+                   double* g, double* l) {
+  const int64_t k = d_out < d_in ? d_out : d_in;
+  double* Us = (double*)malloc(sizeof(double) * (size_t)(d_out * k));
+  double* Vs = (double*)malloc(sizeof(double) * (size_t)(d_in * k));
+  double* sv = (double*)malloc(sizeof(double) * (size_t)k);
+  double* M = (double*)malloc(sizeof(double) * (size_t)((d_out > d_in ? d_out : d_in) * r));
+  double* lu = (double*)malloc(sizeof(double) * (size_t)r);
+  double* lv = (double*)malloc(sizeof(double) * (size_t)r);
+  lbo_svd(W, d_out, d_in, Us, sv, Vs);
+  for (int64_t i = 0; i < d_out; i++)
+    for (int64_t c = 0; c < r; c++) Ulat[i * r + c] = Us[i * k + c] * sqrt(sv[c]);
+  for (int64_t j = 0; j < d_in; j++)
+    for (int64_t c = 0; c < r; c++) Vlat[j * r + c] = Vs[j * k + c] * sqrt(sv[c]);
+  for (int64_t i = 0; i < d_out * r; i++) M[i] = fabs(Ulat[i]);
+  lbo_rank1(M, d_out, r, h, lu);
+  for (int64_t i = 0; i < d_in * r; i++) M[i] = fabs(Vlat[i]);
+  lbo_rank1(M, d_in, r, g, lv);
+  for (int64_t c = 0; c < r; c++) l[c] = lu[c] * lv[c];
+  free(Us);
+  free(Vs);
+  free(sv);
+  free(M);
+  free(lu);
+  free(lv);
+}
+
+/* Effective weight of one path from its latent factors and scales:
+   W[i][j] = h[i] g[j] sum_k sign(Ulat[i][k]) l[k] sign(Vlat[j][k])   (Eq. w_primary_hat),
+   ascending k. */
+void lbo_path_weight(const double* Ulat, const double* Vlat, const double* h, const double* g, const double* l,
+                     int64_t d_out, int64_t d_in, int64_t r, double* W) {
+  for (int64_t i = 0; i < d_out; i++)
+    for (int64_t j = 0; j < d_in; j++) {
+      double acc = 0.0;
+      for (int64_t c = 0; c < r; c++) {
+        const double su = lbo_is_negative(Ulat[i * r + c]) ? -1.0 : 1.0;
+        const double sv = lbo_is_negative(Vlat[j * r + c]) ? -1.0 : 1.0;
+        acc += su * l[c] * sv;
+      }
+      W[i * d_in + j] = h[i] * acc * g[j];
+    }
+}
+
+/* Dual-SVID of both paths: the primary path from W, the residual path from the
+   primary path's error W_res,0 = W - W_hat_pri,0 (Sec. 3.3).  Outputs per path
+   p (arrays [2][...]): Ulat[p] [d_out x r], Vlat[p] [d_in x r], h[p] [d_out],
+   g[p] [d_in], l[p] [r]; and Wres [d_out x d_in] = W - W_hat_pri,0. */
+void lbo_dual_svid(const double* W, int64_t d_out, int64_t d_in, int64_t r, double* const* Ulat,
+                   double* const* Vlat, double* const* h, double* const* g, double* const* l, double* Wres) {
+  lbo_svid_path(W, d_out, d_in, r, Ulat[0], Vlat[0], h[0], g[0], l[0]);
+  lbo_path_weight(Ulat[0], Vlat[0], h[0], g[0], l[0], d_out, d_in, r, Wres);
+  for (int64_t e = 0; e < d_out * d_in; e++) Wres[e] = W[e] - Wres[e];
+  lbo_svid_path(Wres, d_out, d_in, r, Ulat[1], Vlat[1], h[1], g[1], l[1]);
+}
