@@ -40,12 +40,47 @@ __device__ __forceinline__ void build_table(float* t16, int q, float a0, float a
   }
 }
 
+// build_table without the swizzle (entry m at position m): for kernels whose
+// 64 lanes always read one table at a time (the same entries, so a look-up
+// is the same value whatever the layout), the word then needs no XOR.
+__device__ __forceinline__ void build_table_plain(float* t16, float a0, float a1, float a2, float a3) {
+  const float s01[4] = {a0 + a1, a1 - a0, a0 - a1, -a0 - a1};
+  const float s23[4] = {a2 + a3, a3 - a2, a2 - a3, -a2 - a3};
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const f32x4 v = {s01[0] + s23[c], s01[1] + s23[c], s01[2] + s23[c], s01[3] + s23[c]};
+    *reinterpret_cast<f32x4*>(t16 + 4 * c) = v;
+  }
+}
+
 // Signed sum of one packed word against the 8 tables of a block (tb8 points
 // at the block's first table; wk is the word XORed with kKey).
 __device__ __forceinline__ float word_sum(const float* tb8, uint32_t wk) {
   float v[8];
 #pragma unroll
   for (int q = 0; q < 8; ++q) v[q] = tb8[16 * q + ((wk >> (4 * q)) & 15)];
+  return ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+}
+
+// word_sum with the look-up addresses taken from two pre-shifted copies of
+// the word: byte j of e = (wk << 2) & 0x3C3C3C3C is 4 x nibble 2j, byte j of
+// o = (wk >> 2) & 0x3C3C3C3C is 4 x nibble 2j + 1, so each address is one
+// byte extract (plus the table's base) instead of a shift, a mask and a
+// scale.  The same entries are read and added in the same order as word_sum.
+// (The byte goes to the low byte of an address by one v_perm_b32: selector
+// byte j takes byte j of the second operand, 0x0c gives zero.)
+__device__ __forceinline__ uint32_t byte_of(uint32_t v, int j) {
+  return __builtin_amdgcn_perm(0u, v, 0x0c0c0c00u | static_cast<uint32_t>(j));
+}
+__device__ __forceinline__ float word_sum_b(const float* tb8, uint32_t wk) {
+  const uint32_t e = (wk << 2) & 0x3C3C3C3Cu, o = (wk >> 2) & 0x3C3C3C3Cu;
+  const char* b = reinterpret_cast<const char*>(tb8);
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = *reinterpret_cast<const float*>(b + 64 * (2 * j) + byte_of(e, j));
+    v[2 * j + 1] = *reinterpret_cast<const float*>(b + 64 * (2 * j + 1) + byte_of(o, j));
+  }
   return ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
 }
 
