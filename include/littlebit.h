@@ -200,14 +200,16 @@ typedef struct lb_linear_desc {
   void* y;
 } lb_linear_desc;
 
-/* Host, pure.  Workspace bytes lb_linear_forward_many needs for this list:
-   the sum of lb_forward_workspace_bytes of its linears, each rounded up to
-   256 bytes (0 if n <= 0, descs is NULL or a size is invalid).  Linear i uses
-   the slice after those of linears 0 .. i-1 for its intermediate values; the
-   control block of the decode kernels' call protocol is the one at the start
-   of the workspace for every linear, so the zero-fill-once and reuse rules of
-   lb_forward_workspace_bytes hold for the whole workspace, across lists of
-   any layout and single calls on the same buffer. */
+/* Host, pure.  Workspace bytes lb_linear_forward_many needs for this list: a
+   4352-byte list header (the control block of the decode kernels' call
+   protocol, shared by every linear, and 16 counter lines of the linears of a
+   list launch) plus the sum of lb_forward_workspace_bytes of its linears, each
+   rounded up to 256 bytes (0 if n <= 0, descs is NULL or a size is invalid).
+   Linear i uses the slice after the header and those of linears 0 .. i-1 for
+   its intermediate values.  The zero-fill-once and reuse rules of
+   lb_forward_workspace_bytes hold for the whole workspace, across lists of any
+   layout and single calls on the same buffer (the call tags live in the
+   shared control block, so they never repeat). */
 size_t lb_forward_many_workspace_bytes(const lb_linear_desc* descs, int64_t n);
 
 /* Forward of n independent LittleBit linears (each as lb_linear_forward

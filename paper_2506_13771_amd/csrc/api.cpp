@@ -313,7 +313,7 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
 
 size_t lb_forward_many_workspace_bytes(const lb_linear_desc* descs, int64_t n) {
   if (n <= 0 || !descs) return 0;
-  size_t need = 0;
+  size_t need = lb::kListHdrBytes;
   for (int64_t i = 0; i < n; ++i) {
     if (check_sizes(descs[i].T, descs[i].d_in, descs[i].d_out, descs[i].r) != LB_OK) return 0;
     need += slice_bytes(descs[i]);
@@ -371,7 +371,7 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
     return e == hipSuccess ? LB_OK : LB_ERR_HIP;
   };
   char* ws = static_cast<char*>(workspace);
-  size_t off = 0;
+  size_t off = lb::kListHdrBytes;
   for (int64_t i = 0; i < n; ++i) {
     const lb_linear_desc& d = descs[i];
     const size_t sb = slice_bytes(d);

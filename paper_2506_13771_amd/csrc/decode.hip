@@ -91,7 +91,8 @@ struct DecodeParams {
   int bpr;     // 32-input blocks per run
   int n_s1;    // stage-1 workgroups (2 * nkt * s1d)
   int n_s2;    // stage-2 workgroups
-  int ctr_word;   // control-block word counting this linear's finished stage-2 workgroups
+  uint32_t* ctr;  // counter of this linear's finished stage-2 workgroups (in the control block, or a
+                  // list launch's line of its own)
   int n_members;  // linears of the launch sharing the control block (1: a single call)
   int direct;  // stage 2 reads every run's partial (else the two-level sums)
   int tch;     // tokens per stage-2 chunk
@@ -302,7 +303,7 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
         tag = epoch + 1u;
         // count this workgroup as one that has read the epoch (the returned
         // count is used at the end)
-        if (tid == 0) done_before = atomic_add_relaxed(P.ctrl + P.ctr_word, 1u);
+        if (tid == 0) done_before = atomic_add_relaxed(P.ctr, 1u);
       }
       for (uint32_t it = 0;; ++it) {
         bool ready = true;
@@ -386,7 +387,7 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
   // (one contended word for all of them would serialise the atomics), and the
   // last workgroup of each linear counts that linear on the shared word.
   if (tid == 0 && done_before == static_cast<uint32_t>(P.n_s2 - 1)) {
-    atomic_store_relaxed(P.ctrl + P.ctr_word, 0u);
+    atomic_store_relaxed(P.ctr, 0u);
     const bool last = P.n_members <= 1 ||
                       atomic_add_relaxed(P.ctrl + kCtrlDone, 1u) == static_cast<uint32_t>(P.n_members - 1);
     if (last) {
@@ -636,7 +637,7 @@ bool decode_params(const ForwardArgs& a, const DecodeGeom& g, DecodeParams& P) {
   P.bpr = g.bpr;
   P.n_s1 = g.n_s1;
   P.n_s2 = g.n_s2;
-  P.ctr_word = kCtrlDone;
+  P.ctr = P.ctrl + kCtrlDone;
   P.n_members = 1;
   P.direct = g.direct;
   P.tch = g.tch;
@@ -692,13 +693,14 @@ hipError_t launch_decode_batch(const ForwardArgs* a, int n, hipStream_t stream) 
     B.s2_end[i] = s2;
   }
   // members that share a control block end the call together: each counts
-  // its stage-2 workgroups on word kCtrlMember + i, the last member to finish
-  // stores the epoch
+  // its stage-2 workgroups on a line of its own after the control block, the
+  // last member to finish stores the epoch
   for (int i = 0; i < n; ++i) {
     int cnt = 0;
     for (int j = 0; j < n; ++j) cnt += B.p[j].ctrl == B.p[i].ctrl ? 1 : 0;
     if (cnt > 1) {
-      B.p[i].ctr_word = kCtrlMember + i;
+      B.p[i].ctr = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(B.p[i].ctrl) + kCtrlBytes +
+                                               kListCtrStride * static_cast<size_t>(i));
       B.p[i].n_members = cnt;
     }
   }

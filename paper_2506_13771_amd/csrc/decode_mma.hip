@@ -78,7 +78,8 @@ struct MmaParams {
   int bpr;     // 32-wide input blocks per run
   int n_s1;    // stage-1 workgroups (2 * nmf * s1d)
   int n_s2;    // stage-2 workgroups
-  int ctr_word;   // control-block word counting this linear's finished stage-2 workgroups
+  uint32_t* ctr;  // counter of this linear's finished stage-2 workgroups (in the control block, or a
+                  // list launch's line of its own)
   int n_members;  // linears of the launch sharing the control block (1: a single call)
   int direct;  // stage 2 reads every run's partial (else the two-level sums)
   int vec;     // x and g may be read as aligned 4-element vectors
@@ -333,7 +334,7 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
   const uint32_t tag = epoch + 1u;
   // count this workgroup as one that has read the epoch (used at the end)
   uint32_t done_before = 0u;
-  if (tid == 0) done_before = atomic_add_relaxed(P.ctrl + P.ctr_word, 1u);
+  if (tid == 0) done_before = atomic_add_relaxed(P.ctr, 1u);
 #pragma unroll
   for (int pp = 0; pp < 2; ++pp)
 #pragma unroll
@@ -468,7 +469,7 @@ __device__ __forceinline__ void mma_stage2(const MmaParams& P, int q, float* sme
   // (one contended word for all of them would serialise the atomics), and the
   // last workgroup of each linear counts that linear on the shared word.
   if (tid == 0 && done_before == static_cast<uint32_t>(P.n_s2 - 1)) {
-    atomic_store_relaxed(P.ctrl + P.ctr_word, 0u);
+    atomic_store_relaxed(P.ctr, 0u);
     const bool last = P.n_members <= 1 ||
                       atomic_add_relaxed(P.ctrl + kCtrlDone, 1u) == static_cast<uint32_t>(P.n_members - 1);
     if (last) {
@@ -657,7 +658,7 @@ void mma_params(const ForwardArgs& a, const MmaGeom& g, MmaParams& P) {
   P.bpr = g.bpr;
   P.n_s1 = g.n_s1;
   P.n_s2 = g.n_s2;
-  P.ctr_word = kCtrlDone;
+  P.ctr = P.ctrl + kCtrlDone;
   P.n_members = 1;
   P.direct = g.direct;
   const int64_t ex = a.act_dt == kDtF32 ? 4 : 2, es = a.sc_dt == kDtF32 ? 4 : 2;
@@ -728,13 +729,14 @@ hipError_t launch_decode_mma_batch(const ForwardArgs* a, int n, hipStream_t stre
       ++B.n;
     }
     // members that share a control block end the call together: each counts
-    // its stage-2 workgroups on word kCtrlMember + k, the last member to
-    // finish stores the epoch
+    // its stage-2 workgroups on a line of its own after the control block,
+    // the last member to finish stores the epoch
     for (int k = 0; k < B.n; ++k) {
       int cnt = 0;
       for (int m = 0; m < B.n; ++m) cnt += B.p[m].ctrl == B.p[k].ctrl ? 1 : 0;
       if (cnt > 1) {
-        B.p[k].ctr_word = kCtrlMember + k;
+        B.p[k].ctr = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(B.p[k].ctrl) + kCtrlBytes +
+                                                 kListCtrStride * static_cast<size_t>(k));
         B.p[k].n_members = cnt;
       }
     }

@@ -107,7 +107,6 @@ __device__ __forceinline__ bool spin_until_at_least(const uint32_t* p, uint32_t 
 constexpr int kCtrlEpoch = 0;      // decode: tag of the last completed call
 constexpr int kCtrlDone = 1;       // decode: finished stage-2 workgroups of the running call
 constexpr int kCtrlError = 2;      // set to nonzero if a bounded wait expired
-constexpr int kCtrlMember = 16;    // list launches: finished stage-2 workgroups of member m at word 16 + m
 constexpr int kCtrlWords = 64;
 constexpr size_t kCtrlBytes = ((kCtrlWords * 4 + 255) / 256) * 256;
 
@@ -155,6 +154,11 @@ bool decode_supports(int64_t T, int64_t d_in, int64_t d_out, int64_t r);
 constexpr int kDecodeMaxTokens = 4;
 constexpr int kDecodeMaxBatch = 16;  // linears per list launch of the look-up-table decode kernel
 constexpr int kDecodeMaxRank = 1024;  // stage-2 tables of one token fit in LDS
+// Workspace of lb_linear_forward_many: the list's control block, then one
+// counter of finished stage-2 workgroups per member of a list launch, each in
+// a 256-byte line of its own (atomics on one line serialise), then the slices.
+constexpr size_t kListCtrStride = 256;
+constexpr size_t kListHdrBytes = kCtrlBytes + kDecodeMaxBatch * kListCtrStride;
 
 // Matrix-core decode kernel geometry.
 struct MmaGeom {

@@ -213,7 +213,8 @@ def _descs(*ds):
 def test_many_workspace_bytes_is_the_sum_of_rounded_slices(lib):
     shapes = [(1, 4096, 4096, 80), (2, 512, 1000, 17), (16, 64, 64, 16), (0, 5, 5, 5), (300, 100, 77, 48)]
     arr = _descs(*[_desc(T=T, d_in=a, d_out=b, r=r) for T, a, b, r in shapes])
-    want = sum((lb.lb_forward_workspace_bytes(*s) + 255) // 256 * 256 for s in shapes)
+    # the list header (control block + 16 counter lines of 256 bytes) and the rounded slices
+    want = 256 + 16 * 256 + sum((lb.lb_forward_workspace_bytes(*s) + 255) // 256 * 256 for s in shapes)
     assert lb.lb_forward_many_workspace_bytes(arr, len(shapes)) == want
     assert lb.lb_forward_many_workspace_bytes(arr, 0) == 0
     assert lb.lb_forward_many_workspace_bytes(None, 3) == 0
