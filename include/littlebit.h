@@ -182,6 +182,25 @@ lb_status lb_linear_forward(const void* x, lb_dtype act_dtype, int64_t T, int64_
                             int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y,
                             void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+   serving loops, harnesses that forbid allocation): lb_linear_forward with no
+   workspace argument.  The workspace is a static scratch array of the library,
+   lb_noalloc_scratch_bytes() = 32 MiB per GPU, one copy per device, held until
+   the process ends; the call allocates nothing (no hipMalloc, no allocating
+   library routine).  Sizes whose lb_forward_workspace_bytes exceed the
+   scratch return LB_ERR_WORKSPACE; other checks and results as for
+   lb_linear_forward (bit-identical to it).  The first call on a device
+   resolves that device's copy and enqueues its zero fill on `stream`; that
+   first call must not be captured in a graph (LB_ERR_ARG), later ones may be.
+   Every call on one GPU shares its scratch (the decode kernels keep their
+   call counter there, so consecutive calls on one device need no clearing):
+   calls that may overlap on one GPU (other streams, other host threads)
+   race and must not be issued. */
+size_t lb_noalloc_scratch_bytes(void);
+lb_status lb_linear_forward_noalloc(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out,
+                                    int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y,
+                                    hipStream_t stream);
+
 /* lb_linear_forward with an explicit kernel choice (any kernel accepts any
    valid input; AUTO is what lb_linear_forward uses). */
 lb_status lb_linear_forward_kernel(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in,

@@ -94,6 +94,10 @@ def load_library(path: str = LIB_PATH):
     lib.lb_linear_forward_kernel.restype = i32
     lib.lb_linear_forward_kernel.argtypes = [vp, i32, i64, i64, i64, i64, ctypes.POINTER(lb_path), i32, vp, vp,
                                              sz, i32, vp]
+    lib.lb_noalloc_scratch_bytes.restype = sz
+    lib.lb_noalloc_scratch_bytes.argtypes = []
+    lib.lb_linear_forward_noalloc.restype = i32
+    lib.lb_linear_forward_noalloc.argtypes = [vp, i32, i64, i64, i64, i64, ctypes.POINTER(lb_path), i32, vp, vp]
     lib.lb_forward_many_workspace_bytes.restype = sz
     lib.lb_forward_many_workspace_bytes.argtypes = [ctypes.POINTER(lb_linear_desc), i64]
     lib.lb_linear_forward_many.restype = i32
@@ -275,6 +279,22 @@ def lb_linear_forward(x, paths: Sequence[LittleBitPath], r: int, y=None, workspa
                                       _dev_ptr(y, "y"), _dev_ptr(workspace, "workspace"),
                                       workspace.numel() * workspace.element_size(), kernel, _stream(stream))
     _check(st, "lb_linear_forward")
+    return y
+
+
+def lb_linear_forward_noalloc(x, paths: Sequence[LittleBitPath], r: int, y=None, stream=None):
+    """lb_linear_forward with the library's static per-GPU scratch as workspace (no workspace argument,
+    nothing allocated by the call); y is allocated here when None."""
+    torch = _torch()
+    lib = load_library()
+    T, d_in = x.shape
+    d_out = paths[0].h.shape[0]
+    arr, sc = _paths_struct(paths)
+    if y is None:
+        y = torch.empty((T, d_out), dtype=x.dtype, device=x.device)
+    st = lib.lb_linear_forward_noalloc(_dev_ptr(x, "x"), _dtype_code(x), T, d_in, d_out, r, arr, sc,
+                                       _dev_ptr(y, "y"), _stream(stream))
+    _check(st, "lb_linear_forward_noalloc")
     return y
 
 
@@ -470,7 +490,7 @@ __all__ = [
     "LB_KERNEL_PREFILL", "LB_KERNEL_DECODE_MFMA", "LittleBitError", "LittleBitPath", "lb_path", "load_library", "lb_status_str",
     "lb_packed_bytes", "lb_bits_per_weight", "lb_rank_for_bpw", "lb_forward_workspace_bytes",
     "lb_decode_max_tokens", "lb_pack_signs", "lb_workspace_init", "lb_workspace_status", "alloc_workspace", "lb_linear_forward",
-    "lb_dense_reference_weight", "lb_linear_desc", "make_descs", "lb_forward_many_workspace_bytes",
+    "lb_dense_reference_weight", "lb_linear_forward_noalloc", "lb_linear_desc", "make_descs", "lb_forward_many_workspace_bytes",
     "lb_linear_forward_many", "lb_list_workspace_bytes", "LittleBitList", "lb_latent_workspace_bytes", "lb_from_latent_workspace_bytes", "lb_linear_latent",
     "lb_linear_from_latent", "lb_path_train", "LittleBitPathTrain", "lb_backward_workspace_bytes",
     "lb_linear_backward",

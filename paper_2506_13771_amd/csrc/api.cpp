@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "lb_backward.h"
@@ -267,6 +268,74 @@ lb_status lb_linear_forward(const void* x, lb_dtype act_dtype, int64_t T, int64_
   if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype)) return LB_ERR_DTYPE;  // before passing them on
   return lb_linear_forward_kernel(x, act_dtype, T, d_in, d_out, r, paths, scale_dtype, y, workspace,
                                   workspace_bytes, LB_KERNEL_AUTO, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Workspace of lb_linear_forward_noalloc: a file-scope device array, one copy
+// per GPU, held until the process ends.  Host code never uses the array's
+// name as an address: each device's copy is resolved once with
+// hipGetSymbolAddress (that device current) and that pointer is what the
+// kernels get.
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+struct ScratchSlot {
+  std::mutex mu;
+  bool ready = false;
+  void* ptr = nullptr;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// The current device's scratch, resolved and zero-filled (by a fill kernel on
+// `stream`, before the call that needs it) on its first use.  The first use
+// on a device must not be captured in a graph (LB_ERR_ARG): its zero fill
+// must run before every later call, captured or not.
+lb_status scratch_for_current_device(hipStream_t stream, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LB_ERR_HIP;
+  ScratchSlot& s = g_scratch[dev];
+  std::lock_guard<std::mutex> lock(s.mu);
+  if (!s.ready) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess) return LB_ERR_HIP;
+    if (cs != hipStreamCaptureStatusNone) return LB_ERR_ARG;
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return LB_ERR_HIP;
+    if (lb::launch_fill_zero(ptr, kNoAllocScratchBytes, stream) != hipSuccess) return LB_ERR_HIP;
+    s.ptr = ptr;
+    s.ready = true;
+  }
+  *out = s.ptr;
+  return LB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lb_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+lb_status lb_linear_forward_noalloc(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out,
+                                    int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y,
+                                    hipStream_t stream) {
+  if (!dtype_ok(act_dtype) || !dtype_ok(scale_dtype)) return LB_ERR_DTYPE;
+  const lb_status st = check_sizes(T, d_in, d_out, r);
+  if (st != LB_OK) return st;
+  if (lb_forward_workspace_bytes(T, d_in, d_out, r) > kNoAllocScratchBytes) return LB_ERR_WORKSPACE;
+  if (T == 0 || d_out == 0) return LB_OK;
+  if (!y || (d_in > 0 && !x)) return LB_ERR_NULL;
+  if (!aligned(x, dtype_size(act_dtype)) || !aligned(y, dtype_size(act_dtype))) return LB_ERR_ALIGN;
+  const lb_status sp = check_paths(paths, scale_dtype, d_in, d_out, r);
+  if (sp != LB_OK) return sp;
+  void* ws = nullptr;
+  const lb_status ss = scratch_for_current_device(stream, &ws);
+  if (ss != LB_OK) return ss;
+  return lb_linear_forward_kernel(x, act_dtype, T, d_in, d_out, r, paths, scale_dtype, y, ws, kNoAllocScratchBytes,
+                                  LB_KERNEL_AUTO, stream);
 }
 
 namespace {

@@ -146,6 +146,30 @@ def test_forward_validation_errors(lib):
         lb.LB_ERR_DTYPE
 
 
+def test_noalloc_validation_errors(lib):
+    # every check runs before the scratch is touched, so none of these calls reaches the GPU
+    assert lib.lb_noalloc_scratch_bytes() == 32 << 20
+
+    def na(x=FAKE, act=lb.LB_BF16, T=4, d_in=64, d_out=64, r=16, paths=None, sc=lb.LB_F16, y=FAKE):
+        return lib.lb_linear_forward_noalloc(x, act, T, d_in, d_out, r, _paths() if paths is None else paths, sc,
+                                             y, None)
+
+    assert na(act=9) == lb.LB_ERR_DTYPE
+    assert na(sc=-1) == lb.LB_ERR_DTYPE
+    assert na(T=-1) == lb.LB_ERR_SHAPE
+    assert na(r=-1) == lb.LB_ERR_SHAPE
+    # a workspace need beyond the 32 MiB scratch: a long prefill of a wide layer
+    assert lb.lb_forward_workspace_bytes(4096, 8192, 8192, 256) > 32 << 20
+    assert na(T=4096, d_in=8192, d_out=8192, r=256) == lb.LB_ERR_WORKSPACE
+    assert na(x=0) == lb.LB_ERR_NULL
+    assert na(y=0) == lb.LB_ERR_NULL
+    assert na(x=FAKE + 1) == lb.LB_ERR_ALIGN
+    assert na(paths=_paths(U=0)) == lb.LB_ERR_NULL
+    assert na(paths=_paths(h=FAKE + 1)) == lb.LB_ERR_ALIGN
+    assert na(T=0) == lb.LB_OK
+    assert na(d_out=0) == lb.LB_OK
+
+
 def test_pack_validation_errors(lib):
     assert lib.lb_pack_signs(FAKE, lb.LB_F32, 64, 16, 5, FAKE * 2, None, None) == lb.LB_ERR_ARG
     assert lib.lb_pack_signs(FAKE, 3, 64, 16, lb.LB_ROLE_U, FAKE * 2, None, None) == lb.LB_ERR_DTYPE

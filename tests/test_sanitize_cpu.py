@@ -30,12 +30,17 @@ def _run(cmd, **kw):
 def test_abi_and_oracle_under_sanitizers(tmp_path):
     inc = os.path.join(ROOT, "include")
     common = ["-x", "hip", "--offload-host-only", "-O1", "-g", "-std=c++17", "-fno-omit-frame-pointer", "-I", inc]
+    # api.cpp holds a device array (the no-allocation entry point's scratch): its device side is
+    # compiled too (no kernels, so it is quick), the sanitizers apply to the host side only
+    full = ["-x", "hip", "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-O1",
+            "-g", "-std=c++17", "-fno-omit-frame-pointer", "-I", inc]
     api_o, drv_o, orc_o, exe = (str(tmp_path / n) for n in ("api.o", "driver.o", "oracle.o", "driver"))
-    _run([HIPCC] + common + SAN + ["-c", os.path.join(PKG, "csrc", "api.cpp"), "-o", api_o])
+    _run([HIPCC] + full + SAN + ["-c", os.path.join(PKG, "csrc", "api.cpp"), "-o", api_o])
     _run([HIPCC] + common + SAN + ["-c", os.path.join(ROOT, "tests", "sanitize", "abi_driver.cpp"), "-o", drv_o])
     _run(["gcc", "-c", "-O1", "-g", "-std=c99", "-fsanitize=address,undefined", "-fno-omit-frame-pointer",
           "-ffp-contract=off", "-fopenmp", os.path.join(ROOT, "oracle", "lb_oracle.c"), "-o", orc_o])
-    _run([HIPCC] + SAN + ["-fopenmp", drv_o, api_o, orc_o, "-L" + PKG, "-llittlebit", "-Wl,-rpath," + PKG,
+    _run([HIPCC] + SAN + ["--offload-arch=gfx950", "-fopenmp", drv_o, api_o, orc_o, "-L" + PKG, "-llittlebit",
+                          "-Wl,-rpath," + PKG,
                           "-o", exe])
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=0",
                UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
