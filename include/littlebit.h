@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define LB_ABI_VERSION 6
+#define LB_ABI_VERSION 7
 
 typedef enum lb_status {
   LB_OK = 0,
@@ -376,6 +376,55 @@ lb_status lb_linear_backward(const void* x, const void* dy, lb_dtype act_dtype, 
                              int64_t d_out, int64_t r, const lb_path* paths, lb_dtype scale_dtype,
                              const lb_path_train* train, float kappa, void* dx, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
+
+/* ---- Dual-SVID conversion of a dense weight ------------------------------ */
+
+/* Outputs of one path of lb_dual_svid (device, fp32, row-major, caller-owned):
+   the latent factors whose signs are the path's sign matrices (pack them with
+   lb_pack_signs: U_latent with LB_ROLE_U, V_latent with LB_ROLE_V) and the
+   scales. */
+typedef struct lb_svid_out {
+  float* U_latent; /* [d_out x r]: U' = U_r diag(sqrt(sigma)), signed */
+  float* V_latent; /* [d_in x r]:  V' = V_r diag(sqrt(sigma)) */
+  float* h;        /* [d_out]: h0 */
+  float* g;        /* [d_in]:  g0 */
+  float* l;        /* [r]:     l0 = l_u (.) l_v */
+  float* sigma;    /* [r] or NULL: the path's top r singular values, descending */
+} lb_svid_out;
+
+/* Host, pure.  Workspace bytes lb_dual_svid needs (0 if the sizes are not
+   accepted): 8 * d_out * d_in bytes for the residual weight plus
+   O((d_out + d_in) * (r + oversample) + 64 (r + oversample)^2) doubles. */
+size_t lb_dual_svid_workspace_bytes(int64_t d_out, int64_t d_in, int64_t r, int64_t oversample);
+
+/* Dual-SVID initialisation of a LittleBit linear from a dense weight W
+   [d_out x d_in] (row-major, device, w_dtype f32 / f16 / bf16) at rank r
+   (Sec. 3.2 "Dual-SVID Initialization", Eqs. sign_init_concise,
+   scale_init_rank1_concise, latent_scale_init_concise_0; Sec. 3.3 "Residual
+   Compensation").  Path 0 from W, path 1 from W_res = W - W_hat_pri,0 with
+   W_hat_pri,0 = diag(h0) sign(U') diag(l0) sign(V')^T diag(g0).  Per path:
+     - the top-r singular triplets of the path's weight, by block subspace
+       iteration in fp64 (block b = min(r + oversample, d_out, d_in), `iters`
+       rounds of multiplication by W^T and W, each followed by
+       orthonormalisation, then a Rayleigh-Ritz step), the start block drawn
+       from SplitMix64 at `seed`; the error of singular pair k decays like
+       (sigma_{b+1} / sigma_k)^(2 iters + 1);
+     - each pair signed so that the left vector's entry of largest magnitude
+       is positive (the first on a tie); U' and V' split each singular value
+       evenly;
+     - h0, l_u from the best rank-1 approximation of |U'| and g0, l_v from
+       that of |V'| (top singular value split evenly, signed so that h0 and g0
+       sum to >= 0); l0 = l_u (.) l_v.
+   sign() is -1 iff a value is < 0.  Outputs per path in out[0], out[1] (host
+   array of two; every pointer but sigma required, fp32, 4-byte aligned);
+   W_res [d_out x d_in] fp32 is written when not NULL.  Sizes: 1 <= r <=
+   min(d_out, d_in), oversample >= 0, min(r + oversample, d_out, d_in) <= 1024,
+   0 <= iters <= 1000 (LB_ERR_SHAPE / LB_ERR_ARG otherwise).  workspace:
+   256-byte aligned, lb_dual_svid_workspace_bytes bytes, no zero-fill needed.
+   Deterministic: the same inputs and seed give the same bits. */
+lb_status lb_dual_svid(const void* W, lb_dtype w_dtype, int64_t d_out, int64_t d_in, int64_t r, int64_t oversample,
+                       int32_t iters, uint64_t seed, const lb_svid_out* out, float* W_res, void* workspace,
+                       size_t workspace_bytes, hipStream_t stream);
 
 /* Checking path: the dense effective weight of both paths,
      W[i][j] = sum_p h_p[i] g_p[j] sum_k U_p[i][k] l_p[k] V_p[j][k]

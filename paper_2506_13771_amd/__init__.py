@@ -30,7 +30,7 @@ LB_OK, LB_ERR_NULL, LB_ERR_SHAPE, LB_ERR_DTYPE, LB_ERR_ALIGN, LB_ERR_WORKSPACE, 
 LB_F32, LB_F16, LB_BF16 = 0, 1, 2
 LB_ROLE_U, LB_ROLE_V = 0, 1
 LB_KERNEL_AUTO, LB_KERNEL_DECODE, LB_KERNEL_PREFILL, LB_KERNEL_DECODE_MFMA = 0, 1, 2, 3
-ABI_VERSION = 6
+ABI_VERSION = 7
 
 
 class LittleBitError(RuntimeError):
@@ -54,6 +54,11 @@ class lb_path_train(ctypes.Structure):
     _fields_ = [("U_latent", ctypes.c_void_p), ("V_latent", ctypes.c_void_p), ("Ut", ctypes.c_void_p),
                 ("Vt", ctypes.c_void_p), ("dU", ctypes.c_void_p), ("dV", ctypes.c_void_p), ("dh", ctypes.c_void_p),
                 ("dg", ctypes.c_void_p), ("dl", ctypes.c_void_p)]
+
+
+class lb_svid_out(ctypes.Structure):
+    _fields_ = [("U_latent", ctypes.c_void_p), ("V_latent", ctypes.c_void_p), ("h", ctypes.c_void_p),
+                ("g", ctypes.c_void_p), ("l", ctypes.c_void_p), ("sigma", ctypes.c_void_p)]
 
 
 _lib = None
@@ -124,6 +129,11 @@ def load_library(path: str = LIB_PATH):
                                        ctypes.POINTER(lb_path_train), ctypes.c_float, vp, vp, sz, vp]
     lib.lb_dense_reference_weight.restype = i32
     lib.lb_dense_reference_weight.argtypes = [ctypes.POINTER(lb_path), i32, i64, i64, i64, vp, vp]
+    lib.lb_dual_svid_workspace_bytes.restype = sz
+    lib.lb_dual_svid_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    lib.lb_dual_svid.restype = i32
+    lib.lb_dual_svid.argtypes = [vp, i32, i64, i64, i64, i64, i32, ctypes.c_uint64, ctypes.POINTER(lb_svid_out), vp,
+                                 vp, sz, vp]
     if lib.lb_abi_version() != ABI_VERSION:
         raise RuntimeError("liblittlebit.so ABI version mismatch")
     _lib = lib
@@ -484,6 +494,62 @@ def lb_dense_reference_weight(paths: Sequence[LittleBitPath], d_in: int, d_out: 
     return W
 
 
+def lb_dual_svid_workspace_bytes(d_out: int, d_in: int, r: int, oversample: int) -> int:
+    return int(load_library().lb_dual_svid_workspace_bytes(d_out, d_in, r, oversample))
+
+
+def svid_defaults(r: int, d_out: int, d_in: int):
+    """(oversample, iters) used when lb_dual_svid is not given them: a block of about 1.5 r vectors
+    (at least r + 16) and 12 rounds of subspace iteration."""
+    return max(16, r // 2), 12
+
+
+def lb_dual_svid(W, r: int, oversample=None, iters=None, seed: int = 0, residual: bool = False, workspace=None,
+                 stream=None) -> dict:
+    """Dual-SVID of a dense weight W [d_out, d_in] (device, f32 / f16 / bf16) at rank r.  Returns
+    {"U": [U'_0, U'_1], "V": [...], "h": [...], "g": [...], "l": [...], "sigma": [...]} (fp32 device
+    tensors; U' [d_out, r], V' [d_in, r]) and, with residual=True, "W_res" = W - W_hat_pri,0 (fp32)."""
+    torch = _torch()
+    lib = load_library()
+    d_out, d_in = W.shape
+    ov, it = svid_defaults(r, d_out, d_in)
+    oversample = ov if oversample is None else oversample
+    iters = it if iters is None else iters
+    dev = W.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = {"U": [torch.empty((d_out, r), **f32) for _ in range(2)],
+           "V": [torch.empty((d_in, r), **f32) for _ in range(2)],
+           "h": [torch.empty(d_out, **f32) for _ in range(2)], "g": [torch.empty(d_in, **f32) for _ in range(2)],
+           "l": [torch.empty(r, **f32) for _ in range(2)], "sigma": [torch.empty(r, **f32) for _ in range(2)]}
+    arr = (lb_svid_out * 2)()
+    for p in range(2):
+        arr[p] = lb_svid_out(*(_dev_ptr(out[k][p], k) for k in ("U", "V", "h", "g", "l", "sigma")))
+    W_res = torch.empty((d_out, d_in), **f32) if residual else None
+    need = lb_dual_svid_workspace_bytes(d_out, d_in, r, oversample)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    st = lib.lb_dual_svid(_dev_ptr(W, "W"), _dtype_code(W), d_out, d_in, r, oversample, iters,
+                          ctypes.c_uint64(seed), arr, _dev_ptr(W_res, "W_res"), _dev_ptr(workspace, "workspace"),
+                          workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "lb_dual_svid")
+    if residual:
+        out["W_res"] = W_res
+    return out
+
+
+def littlebit_from_dense(W, r: int, scale_dtype=None, **kw):
+    """A LittleBit linear initialised from the dense W [d_out, d_in] by Dual-SVID: the two paths with
+    packed signs (LB layout v1) and scales in scale_dtype (default fp16), ready for lb_linear_forward."""
+    torch = _torch()
+    sd = torch.float16 if scale_dtype is None else scale_dtype
+    s = lb_dual_svid(W, r, **kw)
+    paths = []
+    for p in range(2):
+        paths.append(LittleBitPath(U=lb_pack_signs(s["U"][p], LB_ROLE_U), V=lb_pack_signs(s["V"][p], LB_ROLE_V),
+                                   h=s["h"][p].to(sd), g=s["g"][p].to(sd), l=s["l"][p].to(sd)))
+    return paths
+
+
 __all__ = [
     "LB_OK", "LB_ERR_NULL", "LB_ERR_SHAPE", "LB_ERR_DTYPE", "LB_ERR_ALIGN", "LB_ERR_WORKSPACE", "LB_ERR_HIP",
     "LB_ERR_ARG", "LB_F32", "LB_F16", "LB_BF16", "LB_ROLE_U", "LB_ROLE_V", "LB_KERNEL_AUTO", "LB_KERNEL_DECODE",
@@ -493,5 +559,6 @@ __all__ = [
     "lb_dense_reference_weight", "lb_linear_forward_noalloc", "lb_linear_desc", "make_descs", "lb_forward_many_workspace_bytes",
     "lb_linear_forward_many", "lb_list_workspace_bytes", "LittleBitList", "lb_latent_workspace_bytes", "lb_from_latent_workspace_bytes", "lb_linear_latent",
     "lb_linear_from_latent", "lb_path_train", "LittleBitPathTrain", "lb_backward_workspace_bytes",
-    "lb_linear_backward",
+    "lb_linear_backward", "lb_svid_out", "lb_dual_svid_workspace_bytes", "svid_defaults", "lb_dual_svid",
+    "littlebit_from_dense",
 ]

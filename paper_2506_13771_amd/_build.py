@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblittlebit.so")
 SOURCES = ["api.cpp", "pack.hip", "decode.hip", "decode_mma.hip", "prefill.hip", "latent_small.hip", "backward.hip",
-           "dense_ref.hip", "stream.hip"]
+           "dense_ref.hip", "stream.hip", "svid.hip"]
 # the look-up-table kernels of decode.hip and stream.hip give bit-identical
 # results only if neither contracts a multiply and an add into one fma
 EXTRA_FLAGS = {"decode.hip": ["-ffp-contract=off"], "stream.hip": ["-ffp-contract=off"]}

@@ -763,6 +763,38 @@ lb_status lb_linear_backward(const void* x, const void* dy, lb_dtype act_dtype, 
   return e == hipSuccess ? LB_OK : LB_ERR_HIP;
 }
 
+size_t lb_dual_svid_workspace_bytes(int64_t d_out, int64_t d_in, int64_t r, int64_t oversample) {
+  if (!fits(d_out, d_in) || check_sizes(1, d_in, d_out, r) != LB_OK) return 0;
+  if (!lb::svid_supports(d_out, d_in, r, oversample)) return 0;
+  return lb::svid_workspace_bytes(static_cast<int>(d_out), static_cast<int>(d_in), static_cast<int>(r),
+                                  static_cast<int>(std::min<int64_t>(oversample, 1 << 20)));
+}
+
+lb_status lb_dual_svid(const void* W, lb_dtype w_dtype, int64_t d_out, int64_t d_in, int64_t r, int64_t oversample,
+                       int32_t iters, uint64_t seed, const lb_svid_out* out, float* W_res, void* workspace,
+                       size_t workspace_bytes, hipStream_t stream) {
+  if (!dtype_ok(w_dtype)) return LB_ERR_DTYPE;
+  if (d_out <= 0 || d_in <= 0 || r <= 0 || oversample < 0 || !fits(d_out, d_in) ||
+      check_sizes(1, d_in, d_out, r) != LB_OK || !lb::svid_supports(d_out, d_in, r, oversample))
+    return LB_ERR_SHAPE;
+  if (iters < 0 || iters > 1000) return LB_ERR_ARG;
+  if (!W || !out || !workspace) return LB_ERR_NULL;
+  for (int p = 0; p < 2; ++p) {
+    const lb_svid_out& o = out[p];
+    if (!o.U_latent || !o.V_latent || !o.h || !o.g || !o.l) return LB_ERR_NULL;
+    if (!aligned(o.U_latent, 4) || !aligned(o.V_latent, 4) || !aligned(o.h, 4) || !aligned(o.g, 4) ||
+        !aligned(o.l, 4) || !aligned(o.sigma, 4))
+      return LB_ERR_ALIGN;
+  }
+  if (!aligned(W, dtype_size(w_dtype)) || !aligned(W_res, 4) || !aligned(workspace, 256)) return LB_ERR_ALIGN;
+  if (workspace_bytes < lb_dual_svid_workspace_bytes(d_out, d_in, r, oversample)) return LB_ERR_WORKSPACE;
+  const int over = static_cast<int>(std::min<int64_t>(oversample, 1 << 20));
+  return lb::launch_dual_svid(W, w_dtype, static_cast<int>(d_out), static_cast<int>(d_in), static_cast<int>(r), over,
+                              iters, seed, out, W_res, workspace, stream) == hipSuccess
+             ? LB_OK
+             : LB_ERR_HIP;
+}
+
 lb_status lb_dense_reference_weight(const lb_path* paths, lb_dtype scale_dtype, int64_t d_in, int64_t d_out,
                                     int64_t r, float* W, hipStream_t stream) {
   if (!dtype_ok(scale_dtype)) return LB_ERR_DTYPE;

@@ -226,6 +226,11 @@ bool stream_supports(const ForwardArgs& a);
 size_t stream_workspace_bytes(const ForwardArgs* a, int n);
 hipError_t stream_init(const ForwardArgs* a, int n, uint64_t fingerprint, void* ws, hipStream_t stream);
 hipError_t stream_forward(const ForwardArgs* a, int n, uint64_t fingerprint, void* ws, hipStream_t stream);
+// Dual-SVID conversion (svid.hip)
+bool svid_supports(int64_t d_out, int64_t d_in, int64_t r, int64_t over);
+size_t svid_workspace_bytes(int d_out, int d_in, int r, int over);
+hipError_t launch_dual_svid(const void* W, int wdt, int d_out, int d_in, int r, int over, int iters, uint64_t seed,
+                            const lb_svid_out* out, float* W_res, void* ws, hipStream_t stream);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t stream);
 // *out = the error word of the control block at ctrl, which is then cleared
 hipError_t launch_take_status(uint32_t* ctrl, int32_t* out, hipStream_t stream);

@@ -1,0 +1,661 @@
+// Dual-SVID conversion of a dense weight into the two LittleBit paths
+// (Sec. 3.2 "Dual-SVID Initialization", Eqs. sign_init_concise,
+// scale_init_rank1_concise, latent_scale_init_concise_0; the residual path from
+// the primary path's error, Sec. 3.3 "Residual Compensation"), on the GPU in
+// fp64.
+//
+// Per path, for a weight W [m x n] and rank r:
+//   1. the top-r singular triplets of W by block subspace iteration: a block of
+//      b = min(r + oversample, m, n) vectors, alternately multiplied by W and
+//      W^T and orthonormalised each time, then a Rayleigh-Ritz step on the
+//      final block (eigenvectors of Z^T Z with Z = W^T Q);
+//   2. each singular pair signed so that the left vector's entry of largest
+//      magnitude is positive (first such index on a tie), U' = U_r sqrt(S),
+//      V' = V_r sqrt(S);
+//   3. the best rank-1 approximations |U'| ~ h l_u^T and |V'| ~ g l_v^T, the
+//      top singular value split evenly and signed so that the left factor sums
+//      to >= 0; l = l_u (.) l_v;
+//   4. for the primary path, W_res = W - diag(h) sign(U') diag(l) sign(V')^T diag(g),
+//      the weight the residual path starts from.
+// The contractions (W and W^T times a block, Gram matrices, basis changes, the
+// effective weight) run on the fp64 matrix cores; the small symmetric
+// eigenproblems (b x b and r x r) run as a parallel cyclic Jacobi method on one
+// workgroup.  Orthonormalisation is by the Gram matrix's eigenvectors
+// (Q = Y E diag(lambda)^-1/2, directions with lambda <= 1e-14 lambda_max
+// dropped), so a rank-deficient block needs no special case.  Sums are in a
+// fixed order (split-K partial sums added in slab order), so a call is
+// deterministic.
+#include <algorithm>
+#include <cmath>
+
+#include "lb_internal.h"
+
+namespace lb {
+namespace {
+
+typedef double d4 __attribute__((ext_vector_type(4)));
+
+constexpr int kDtF64 = 100;  // operand code of the internal fp64 arrays
+constexpr int kGT = 64;      // GEMM output tile (rows and columns)
+constexpr int kGK = 16;      // GEMM K per LDS stage
+constexpr int kEigThreads = 1024;
+constexpr int kMaxBlock = 1024;     // largest eigenproblem: one workgroup, one pair per thread
+constexpr int kEigLdsMax = 128;     // b <= 128: the matrix stays in LDS during the sweeps
+constexpr int kEigMaxSweeps = 80;
+constexpr double kDropRel = 1e-14;  // orthonormalisation: dropped Gram eigenvalues, relative to the largest
+
+__device__ __forceinline__ double load_op(const void* p, int64_t idx, int dt) {
+  if (dt == kDtF64) return static_cast<const double*>(p)[idx];
+  return static_cast<double>(load_as_f32(p, idx, dt));
+}
+
+enum { kEpiStore = 0, kEpiResid = 1 };
+
+struct GemmArgs {
+  const void* A;  // op(A)(i, k) = A[i * sai + k * sak]
+  int a_dt, a_abs;
+  int64_t sai, sak;
+  const void* B;  // B(k, j) = B[k * sbk + j * sbj]
+  int b_dt, b_abs;
+  int64_t sbk, sbj;
+  double* C;      // C[i * ldc + j]; with ksplit > 1 the partial slab z at C + z * pstride
+  int64_t ldc, pstride;
+  int M, N, K, kchunk, ksplit;
+  int epi;        // kEpiResid: C = W(i, j) - h[i] g[j] acc
+  const void* W;
+  int w_dt;
+  int64_t ldw;
+  const double* h;
+  const double* g;
+};
+
+__device__ __forceinline__ void gemm_store(const GemmArgs& g, int i, int j, double acc) {
+  if (g.epi == kEpiResid) {
+    const double w = load_op(g.W, static_cast<int64_t>(i) * g.ldw + j, g.w_dt);
+    g.C[static_cast<int64_t>(i) * g.ldc + j] = w - g.h[i] * g.g[j] * acc;
+  } else {
+    g.C[static_cast<int64_t>(i) * g.ldc + j] = acc;
+  }
+}
+
+// C = op(A) [M x K] * B [K x N] on the fp64 matrix cores (16x16x4 per
+// instruction).  A 64 x 64 output tile per workgroup of four waves (32 x 32
+// each), K staged through LDS 16 at a time; blockIdx.z takes K range
+// [z * kchunk, (z + 1) * kchunk) and, when ksplit > 1, writes its own slab.
+// AK: A's k stride is 1 (else its i stride is); BJ: B's j stride is 1 (else
+// its k stride is) -- the tile loads walk the contiguous index.
+template <bool AK, bool BJ>
+__global__ __launch_bounds__(256) void gemm64_kernel(GemmArgs g) {
+  __shared__ double As[kGK][kGT + 1];
+  __shared__ double Bs[kGK][kGT + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int i0 = blockIdx.x * kGT, j0 = blockIdx.y * kGT;
+  const int kz0 = blockIdx.z * g.kchunk;
+  const int kz1 = min(g.K, kz0 + g.kchunk);
+  const int wi = (wv >> 1) * 32, wj = (wv & 1) * 32;
+  d4 acc[2][2];
+  for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 2; ++b) acc[a][b] = d4{0.0, 0.0, 0.0, 0.0};
+  for (int k0 = kz0; k0 < kz1; k0 += kGK) {
+    for (int e = tid; e < kGT * kGK; e += 256) {
+      const int ii = AK ? e / kGK : e % kGT;
+      const int kk = AK ? e % kGK : e / kGT;
+      const int i = i0 + ii, k = k0 + kk;
+      double v = 0.0;
+      if (i < g.M && k < kz1) {
+        v = load_op(g.A, static_cast<int64_t>(i) * g.sai + static_cast<int64_t>(k) * g.sak, g.a_dt);
+        if (g.a_abs) v = fabs(v);
+      }
+      As[kk][ii] = v;
+    }
+    for (int e = tid; e < kGT * kGK; e += 256) {
+      const int jj = BJ ? e % kGT : e / kGK;
+      const int kk = BJ ? e / kGT : e % kGK;
+      const int j = j0 + jj, k = k0 + kk;
+      double v = 0.0;
+      if (j < g.N && k < kz1) {
+        v = load_op(g.B, static_cast<int64_t>(k) * g.sbk + static_cast<int64_t>(j) * g.sbj, g.b_dt);
+        if (g.b_abs) v = fabs(v);
+      }
+      Bs[kk][jj] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kGK; kk += 4) {
+      double av[2], bv[2];
+#pragma unroll
+      for (int a = 0; a < 2; ++a) av[a] = As[kk + (lane >> 4)][wi + a * 16 + (lane & 15)];
+#pragma unroll
+      for (int b = 0; b < 2; ++b) bv[b] = Bs[kk + (lane >> 4)][wj + b * 16 + (lane & 15)];
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[a], bv[b], acc[a][b], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  // D register v of lane l holds row (l / 16) + 4 v, column l % 16 of the 16 x 16 block
+  for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 2; ++b)
+      for (int v = 0; v < 4; ++v) {
+        const int i = i0 + wi + a * 16 + (lane >> 4) + 4 * v;
+        const int j = j0 + wj + b * 16 + (lane & 15);
+        if (i >= g.M || j >= g.N) continue;
+        if (g.ksplit > 1)
+          g.C[blockIdx.z * g.pstride + static_cast<int64_t>(i) * g.ldc + j] = acc[a][b][v];
+        else
+          gemm_store(g, i, j, acc[a][b][v]);
+      }
+}
+
+// Sum of the split-K slabs P [z][M][N] in slab order, then the epilogue into
+// g.C.
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs g, const double* P) {
+  const int64_t total = static_cast<int64_t>(g.M) * g.N;
+  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < total; e += static_cast<int64_t>(gridDim.x) * 256) {
+    double s = 0.0;
+    for (int z = 0; z < g.ksplit; ++z) s += P[z * total + e];
+    gemm_store(g, static_cast<int>(e / g.N), static_cast<int>(e % g.N), s);
+  }
+}
+
+// Partner of index k in step s of the round-robin (circle) ordering of n2
+// (even) indices: every pair meets once in n2 - 1 steps, each step's pairs are
+// disjoint.
+__device__ __forceinline__ void rr_pair(int n2, int s, int k, int& p, int& q) {
+  if (k == 0) {
+    p = n2 - 1;
+    q = s;
+  } else {
+    p = (s + k) % (n2 - 1);
+    q = (s - k + n2 - 1) % (n2 - 1);
+  }
+  if (p > q) {
+    const int t = p;
+    p = q;
+    q = t;
+  }
+}
+
+// Eigen-decomposition of a symmetric b x b matrix A (row-major, overwritten)
+// by the cyclic Jacobi method with the round-robin ordering: each step rotates
+// b/2 disjoint pairs at once (A <- J^T A J, the accumulated J in Et, one
+// eigenvector per row), until a sweep rotates nothing (|a_pq| <= 1e-15
+// sqrt(|a_pp a_qq|), or below 1e-17 of the largest starting diagonal entry)
+// or kEigMaxSweeps sweeps.  Eigenvalues descending (index order on ties) to
+// lam; eigenvectors to the columns of E [b x b].  mode 1 (orthonormalisation):
+// column k of E is scaled by lambda_k^-1/2, or zeroed when lambda_k <= 1e-14
+// lambda_max.  One workgroup; the matrix lives in LDS when b <= kEigLdsMax.
+template <bool kLds>
+__global__ __launch_bounds__(kEigThreads) void jacobi_eig_kernel(double* A, double* Et, double* E, double* lam,
+                                                                  int b, int mode) {
+  extern __shared__ double eig_smem[];
+  __shared__ int pp[kMaxBlock / 2], pq[kMaxBlock / 2];
+  __shared__ double pc[kMaxBlock / 2], ps[kMaxBlock / 2];
+  __shared__ int rot;
+  __shared__ double floor_abs;
+  const int tid = threadIdx.x;
+  const int n2 = b + (b & 1), np = n2 / 2;
+  double* M = kLds ? eig_smem : A;
+  if (kLds)
+    for (int e = tid; e < b * b; e += kEigThreads) M[e] = A[e];
+  for (int e = tid; e < b * b; e += kEigThreads) Et[e] = (e / b == e % b) ? 1.0 : 0.0;
+  if (tid == 0) {
+    double mx = 0.0;
+    for (int i = 0; i < b; ++i) mx = fmax(mx, fabs(A[static_cast<int64_t>(i) * b + i]));
+    floor_abs = 1e-17 * mx;
+  }
+  __syncthreads();
+  for (int sweep = 0; sweep < kEigMaxSweeps; ++sweep) {
+    if (tid == 0) rot = 0;
+    __syncthreads();
+    for (int s = 0; s < n2 - 1; ++s) {
+      if (tid < np) {
+        int p, q;
+        rr_pair(n2, s, tid, p, q);
+        double c = 1.0, sn = 0.0;
+        bool act = false;
+        if (q < b) {
+          const double app = M[p * b + p], aqq = M[q * b + q], apq = M[p * b + q];
+          if (apq != 0.0 && fabs(apq) > 1e-15 * sqrt(fabs(app * aqq)) && fabs(apq) > floor_abs) {
+            const double zeta = (aqq - app) / (2.0 * apq);
+            const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+            c = 1.0 / sqrt(1.0 + t * t);
+            sn = c * t;
+            act = true;
+          }
+        }
+        pp[tid] = act ? p : -1;
+        pq[tid] = q;
+        pc[tid] = c;
+        ps[tid] = sn;
+        if (act) atomicAdd(&rot, 1);
+      }
+      __syncthreads();
+      // rows p, q of A and of Et
+      for (int e = tid; e < np * b; e += kEigThreads) {
+        const int k = e / b, j = e % b;
+        const int p = pp[k];
+        if (p < 0) continue;
+        const int q = pq[k];
+        const double c = pc[k], sn = ps[k];
+        const double rp = M[p * b + j], rq = M[q * b + j];
+        M[p * b + j] = c * rp - sn * rq;
+        M[q * b + j] = sn * rp + c * rq;
+        const double ep = Et[static_cast<int64_t>(p) * b + j], eq = Et[static_cast<int64_t>(q) * b + j];
+        Et[static_cast<int64_t>(p) * b + j] = c * ep - sn * eq;
+        Et[static_cast<int64_t>(q) * b + j] = sn * ep + c * eq;
+      }
+      __syncthreads();
+      // columns p, q of A
+      for (int e = tid; e < np * b; e += kEigThreads) {
+        const int k = e / b, i = e % b;
+        const int p = pp[k];
+        if (p < 0) continue;
+        const int q = pq[k];
+        const double c = pc[k], sn = ps[k];
+        const double cp = M[i * b + p], cq = M[i * b + q];
+        M[i * b + p] = c * cp - sn * cq;
+        M[i * b + q] = sn * cp + c * cq;
+      }
+      __syncthreads();
+    }
+    if (rot == 0) break;
+    __syncthreads();
+  }
+  // rank of each eigenvalue (descending, index order on ties), then the outputs
+  double lmax = 0.0;
+  for (int i = 0; i < b; ++i) lmax = fmax(lmax, M[i * b + i]);
+  for (int i = tid; i < b; i += kEigThreads) {
+    const double li = M[i * b + i];
+    int rank = 0;
+    for (int j = 0; j < b; ++j) {
+      const double lj = M[j * b + j];
+      rank += (lj > li || (lj == li && j < i)) ? 1 : 0;
+    }
+    lam[rank] = li;
+    double f = 1.0;
+    if (mode == 1) f = (li > 0.0 && li > kDropRel * lmax) ? 1.0 / sqrt(li) : 0.0;
+    for (int row = 0; row < b; ++row)
+      E[static_cast<int64_t>(row) * b + rank] = f * Et[static_cast<int64_t>(i) * b + row];
+  }
+}
+
+// Uniform values in [-1, 1) from the SplitMix64 generator (Steele, Lea and
+// Flood, 2014) at counter seed + idx: the subspace iteration's starting block.
+__global__ void rand_fill_kernel(double* Z, int64_t n, uint64_t seed) {
+  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n; i += static_cast<int64_t>(gridDim.x) * 256) {
+    uint64_t z = seed + static_cast<uint64_t>(i + 1) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    z ^= z >> 31;
+    Z[i] = static_cast<double>(z >> 11) * 0x1.0p-52 - 1.0;
+  }
+}
+
+// Fixed-order sum of v[0 .. n) over one workgroup of 256 threads (strided
+// partial sums, then a tree); every thread gets the result.
+__device__ double block_sum(double v, double* red) {
+  const int tid = threadIdx.x;
+  red[tid] = v;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (tid < w) red[tid] += red[tid + w];
+    __syncthreads();
+  }
+  const double s = red[0];
+  __syncthreads();
+  return s;
+}
+
+// One workgroup per singular pair k: sigma_k = sqrt(max(lambda_k, 0)); the
+// left vector (column k of U) signed so that its entry of largest magnitude is
+// positive (first index on a tie), the right vector = Vraw[:, k] / sigma_k
+// (zero if sigma_k == 0) with the same sign; U' = U sqrt(sigma), V' = V
+// sqrt(sigma), fp64 to Ul, Vl and fp32 to the caller's arrays.
+__global__ __launch_bounds__(256) void sign_scale_kernel(const double* U, const double* Vraw, const double* lam, int m,
+                                                         int n, int r, double* Ul, double* Vl, float* Uo, float* Vo,
+                                                         float* sig) {
+  __shared__ double bv[256];
+  __shared__ int bi[256];
+  const int k = blockIdx.x, tid = threadIdx.x;
+  double best = -1.0;
+  int besti = 0;
+  for (int i = tid; i < m; i += 256) {
+    const double v = fabs(U[static_cast<int64_t>(i) * r + k]);
+    if (v > best) {
+      best = v;
+      besti = i;
+    }
+  }
+  bv[tid] = best;
+  bi[tid] = besti;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (tid < w) {
+      const double o = bv[tid + w];
+      const int oi = bi[tid + w];
+      if (o > bv[tid] || (o == bv[tid] && oi < bi[tid])) {
+        bv[tid] = o;
+        bi[tid] = oi;
+      }
+    }
+    __syncthreads();
+  }
+  const double s = sqrt(fmax(lam[k], 0.0));
+  const double f = U[static_cast<int64_t>(bi[0]) * r + k] < 0.0 ? -1.0 : 1.0;
+  const double rs = sqrt(s);
+  if (tid == 0 && sig) sig[k] = static_cast<float>(s);
+  for (int i = tid; i < m; i += 256) {
+    const int64_t e = static_cast<int64_t>(i) * r + k;
+    const double v = f * U[e] * rs;
+    Ul[e] = v;
+    Uo[e] = static_cast<float>(v);
+  }
+  for (int j = tid; j < n; j += 256) {
+    const int64_t e = static_cast<int64_t>(j) * r + k;
+    const double v = s > 0.0 ? f * (Vraw[e] / s) * rs : 0.0;
+    Vl[e] = v;
+    Vo[e] = static_cast<float>(v);
+  }
+}
+
+// Rank-1 factors of a nonnegative M [d x r] from the top eigenpair (lambda_1,
+// e_1) of M^T M and u = M e_1: sigma_1 = sqrt(lambda_1), left factor
+// f u / sqrt(sigma_1), right factor f sqrt(sigma_1) e_1, f = +-1 so that the
+// left factor sums to >= 0 (zero factors when lambda_1 <= 0).  One workgroup.
+__global__ __launch_bounds__(256) void rank1_finish_kernel(const double* u, const double* lam, const double* E, int d,
+                                                           int r, double* left, float* left_o, double* right) {
+  __shared__ double red[256];
+  const int tid = threadIdx.x;
+  double part = 0.0;
+  for (int i = tid; i < d; i += 256) part += u[i];
+  const double sum = block_sum(part, red);
+  const double f = sum >= 0.0 ? 1.0 : -1.0;
+  const double l1 = lam[0];
+  const double q = l1 > 0.0 ? sqrt(sqrt(l1)) : 0.0;
+  for (int i = tid; i < d; i += 256) {
+    const double v = q > 0.0 ? f * u[i] / q : 0.0;
+    left[i] = v;
+    left_o[i] = static_cast<float>(v);
+  }
+  for (int k = tid; k < r; k += 256) right[k] = f * q * E[static_cast<int64_t>(k) * r];
+}
+
+// l = l_u (.) l_v; the operands of the effective weight, Us[i][k] =
+// sign(U'[i][k]) l[k] and Vs[j][k] = sign(V'[j][k]) (sign: -1 iff < 0).
+__global__ void latent_and_signs_kernel(const double* lu, const double* lv, const double* Ul, const double* Vl, int m,
+                                        int n, int r, double* l, float* l_o, double* Us, double* Vs) {
+  const int64_t nu = static_cast<int64_t>(m) * r, nv = static_cast<int64_t>(n) * r;
+  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < nu + nv + r; e += static_cast<int64_t>(gridDim.x) * 256) {
+    if (e < nu) {
+      const int k = static_cast<int>(e % r);
+      Us[e] = (Ul[e] < 0.0 ? -1.0 : 1.0) * (lu[k] * lv[k]);
+    } else if (e < nu + nv) {
+      const int64_t f = e - nu;
+      Vs[f] = Vl[f] < 0.0 ? -1.0 : 1.0;
+    } else {
+      const int k = static_cast<int>(e - nu - nv);
+      l[k] = lu[k] * lv[k];
+      l_o[k] = static_cast<float>(l[k]);
+    }
+  }
+}
+
+__global__ void f64_to_f32_kernel(const double* s, float* d, int64_t n) {
+  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < n; i += static_cast<int64_t>(gridDim.x) * 256)
+    d[i] = static_cast<float>(s[i]);
+}
+
+int grid_for(int64_t n) { return static_cast<int>(std::min<int64_t>(4096, std::max<int64_t>(1, (n + 255) / 256))); }
+
+size_t a256(size_t b) { return (b + 255) / 256 * 256; }
+
+struct SvidLayout {
+  int m, n, r, b;
+  size_t wres, y, q, z, z2, part, gram, e, et, lam, ud, vd, ul, vl, us, vs, u, h, g, lu, lv, l, total;
+  size_t part_elems;
+};
+
+SvidLayout svid_layout(int m, int n, int r, int over) {
+  SvidLayout L{};
+  L.m = m;
+  L.n = n;
+  L.r = r;
+  L.b = std::min<int64_t>(static_cast<int64_t>(r) + over, std::min(m, n));
+  const size_t b = L.b, mx = std::max(m, n);
+  L.part_elems = std::max<size_t>(64 * b * b, 8 * mx * b);
+  size_t off = 0;
+  auto take = [&](size_t elems) {
+    const size_t o = off;
+    off += a256(elems * sizeof(double));
+    return o;
+  };
+  L.wres = take(static_cast<size_t>(m) * n);
+  L.y = take(static_cast<size_t>(m) * b);
+  L.q = take(static_cast<size_t>(m) * b);
+  L.z = take(static_cast<size_t>(n) * b);
+  L.z2 = take(static_cast<size_t>(n) * b);
+  L.part = take(L.part_elems);
+  L.gram = take(b * b);
+  L.e = take(b * b);
+  L.et = take(b * b);
+  L.lam = take(b);
+  L.ud = take(static_cast<size_t>(m) * r);
+  L.vd = take(static_cast<size_t>(n) * r);
+  L.ul = take(static_cast<size_t>(m) * r);
+  L.vl = take(static_cast<size_t>(n) * r);
+  L.us = take(static_cast<size_t>(m) * r);
+  L.vs = take(static_cast<size_t>(n) * r);
+  L.u = take(mx);
+  L.h = take(m);
+  L.g = take(n);
+  L.lu = take(r);
+  L.lv = take(r);
+  L.l = take(r);
+  L.total = off;
+  return L;
+}
+
+struct Svid {
+  const SvidLayout& L;
+  char* ws;
+  hipStream_t st;
+  double* at(size_t off) const { return reinterpret_cast<double*>(ws + off); }
+
+  // C [M x N] = op(A) [M x K] * B [K x N]; K split so that the launch has
+  // about 512 workgroups, when the partial slabs fit and each split keeps at
+  // least 256 of K.
+  hipError_t gemm(GemmArgs g) const {
+    if (g.M <= 0 || g.N <= 0) return hipSuccess;
+    const int tiles = ((g.M + kGT - 1) / kGT) * ((g.N + kGT - 1) / kGT);
+    const size_t slab = static_cast<size_t>(g.M) * g.N;
+    int split = std::max(1, 512 / tiles);
+    split = std::min(split, std::max(1, g.K / 256));
+    split = static_cast<int>(std::min<size_t>(split, std::max<size_t>(1, L.part_elems / slab)));
+    const int kchunk = std::max(kGK, ((g.K + split - 1) / split + kGK - 1) / kGK * kGK);
+    split = std::max(1, (g.K + kchunk - 1) / kchunk);
+    g.kchunk = kchunk;
+    g.ksplit = split;
+    GemmArgs run = g;
+    if (split > 1) {
+      run.C = at(L.part);
+      run.ldc = g.N;
+      run.pstride = static_cast<int64_t>(slab);
+    }
+    const dim3 grid((g.M + kGT - 1) / kGT, (g.N + kGT - 1) / kGT, split);
+    const bool ak = g.sak == 1, bj = g.sbj == 1;
+    if (ak && bj)
+      hipLaunchKernelGGL((gemm64_kernel<true, true>), grid, dim3(256), 0, st, run);
+    else if (ak)
+      hipLaunchKernelGGL((gemm64_kernel<true, false>), grid, dim3(256), 0, st, run);
+    else if (bj)
+      hipLaunchKernelGGL((gemm64_kernel<false, true>), grid, dim3(256), 0, st, run);
+    else
+      hipLaunchKernelGGL((gemm64_kernel<false, false>), grid, dim3(256), 0, st, run);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || split == 1) return e;
+    hipLaunchKernelGGL(gemm_reduce_kernel, dim3(grid_for(static_cast<int64_t>(slab))), dim3(256), 0, st, g,
+                       static_cast<const double*>(at(L.part)));
+    return hipGetLastError();
+  }
+
+  hipError_t eig(double* A, double* E, double* lam, int b, int mode) const {
+    if (b <= kEigLdsMax) {
+      const int smem = static_cast<int>(sizeof(double) * b * b);
+      if (smem > 65536) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&jacobi_eig_kernel<true>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return e;
+      }
+      hipLaunchKernelGGL((jacobi_eig_kernel<true>), dim3(1), dim3(kEigThreads), sizeof(double) * b * b, st, A,
+                         at(L.et), E, lam, b, mode);
+    } else {
+      hipLaunchKernelGGL((jacobi_eig_kernel<false>), dim3(1), dim3(kEigThreads), 0, st, A, at(L.et), E, lam, b,
+                         mode);
+    }
+    return hipGetLastError();
+  }
+
+  // C = op(A) * B with A, B given by element strides (see GemmArgs)
+  hipError_t mm(const void* A, int adt, int64_t sai, int64_t sak, bool aabs, const void* B, int bdt, int64_t sbk,
+                int64_t sbj, bool babs, double* C, int64_t ldc, int M, int N, int K) const {
+    GemmArgs g{};
+    g.A = A;
+    g.a_dt = adt;
+    g.a_abs = aabs;
+    g.sai = sai;
+    g.sak = sak;
+    g.B = B;
+    g.b_dt = bdt;
+    g.b_abs = babs;
+    g.sbk = sbk;
+    g.sbj = sbj;
+    g.C = C;
+    g.ldc = ldc;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.epi = kEpiStore;
+    return gemm(g);
+  }
+
+  // Y [rows x b] -> an orthonormal basis of its range in Qo [rows x b]:
+  // G = Y^T Y, G = E diag(lambda) E^T, Qo = Y E diag(lambda)^-1/2 (dropped
+  // directions give zero columns)
+  hipError_t orth(const double* Y, double* Qo, int rows) const {
+    const int b = L.b;
+    hipError_t e;
+    if ((e = mm(Y, kDtF64, 1, b, false, Y, kDtF64, b, 1, false, at(L.gram), b, b, b, rows)) != hipSuccess) return e;
+    if ((e = eig(at(L.gram), at(L.e), at(L.lam), b, 1)) != hipSuccess) return e;
+    return mm(Y, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, Qo, b, rows, b, b);
+  }
+
+  // Rank-1 factors of |F| for F [d x r] (fp64): left to left/left_o, right to right
+  hipError_t rank1(const double* F, int d, double* left, float* left_o, double* right) const {
+    const int r = L.r;
+    hipError_t e;
+    if ((e = mm(F, kDtF64, 1, r, true, F, kDtF64, r, 1, true, at(L.gram), r, r, r, d)) != hipSuccess) return e;
+    if ((e = eig(at(L.gram), at(L.e), at(L.lam), r, 0)) != hipSuccess) return e;
+    // u = |F| e_1 (the first column of E)
+    if ((e = mm(F, kDtF64, r, 1, true, at(L.e), kDtF64, r, 1, false, at(L.u), 1, d, 1, r)) != hipSuccess) return e;
+    hipLaunchKernelGGL(rank1_finish_kernel, dim3(1), dim3(256), 0, st, static_cast<const double*>(at(L.u)),
+                       static_cast<const double*>(at(L.lam)), static_cast<const double*>(at(L.e)), d, r, left, left_o,
+                       right);
+    return hipGetLastError();
+  }
+
+  // One path from W (dtype wdt, [m x n] row-major) into the caller's outputs.
+  hipError_t path(const void* W, int wdt, const lb_svid_out& o, int iters, uint64_t seed) const {
+    const int m = L.m, n = L.n, r = L.r, b = L.b;
+    double *Y = at(L.y), *Q = at(L.q), *Z = at(L.z), *Z2 = at(L.z2);
+    hipError_t e;
+    hipLaunchKernelGGL(rand_fill_kernel, dim3(grid_for(static_cast<int64_t>(n) * b)), dim3(256), 0, st, Z,
+                       static_cast<int64_t>(n) * b, seed);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // Y = W Z, Q = orth(Y)
+    if ((e = mm(W, wdt, n, 1, false, Z, kDtF64, b, 1, false, Y, b, m, b, n)) != hipSuccess) return e;
+    if ((e = orth(Y, Q, m)) != hipSuccess) return e;
+    for (int it = 0; it < iters; ++it) {
+      // Z = orth(W^T Q), Q = orth(W Z)
+      if ((e = mm(W, wdt, 1, n, false, Q, kDtF64, b, 1, false, Z2, b, n, b, m)) != hipSuccess) return e;
+      if ((e = orth(Z2, Z, n)) != hipSuccess) return e;
+      if ((e = mm(W, wdt, n, 1, false, Z, kDtF64, b, 1, false, Y, b, m, b, n)) != hipSuccess) return e;
+      if ((e = orth(Y, Q, m)) != hipSuccess) return e;
+    }
+    // Rayleigh-Ritz: Z = W^T Q, Z^T Z = E diag(lambda) E^T, U = Q E_r, V = Z E_r / sigma
+    if ((e = mm(W, wdt, 1, n, false, Q, kDtF64, b, 1, false, Z, b, n, b, m)) != hipSuccess) return e;
+    if ((e = mm(Z, kDtF64, 1, b, false, Z, kDtF64, b, 1, false, at(L.gram), b, b, b, n)) != hipSuccess) return e;
+    if ((e = eig(at(L.gram), at(L.e), at(L.lam), b, 0)) != hipSuccess) return e;
+    if ((e = mm(Q, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, at(L.ud), r, m, r, b)) != hipSuccess) return e;
+    if ((e = mm(Z, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, at(L.vd), r, n, r, b)) != hipSuccess) return e;
+    hipLaunchKernelGGL(sign_scale_kernel, dim3(r), dim3(256), 0, st, static_cast<const double*>(at(L.ud)),
+                       static_cast<const double*>(at(L.vd)), static_cast<const double*>(at(L.lam)), m, n, r,
+                       at(L.ul), at(L.vl), o.U_latent, o.V_latent, o.sigma);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = rank1(at(L.ul), m, at(L.h), o.h, at(L.lu))) != hipSuccess) return e;
+    if ((e = rank1(at(L.vl), n, at(L.g), o.g, at(L.lv))) != hipSuccess) return e;
+    const int64_t nl = static_cast<int64_t>(m + n) * r + r;
+    hipLaunchKernelGGL(latent_and_signs_kernel, dim3(grid_for(nl)), dim3(256), 0, st,
+                       static_cast<const double*>(at(L.lu)), static_cast<const double*>(at(L.lv)),
+                       static_cast<const double*>(at(L.ul)), static_cast<const double*>(at(L.vl)), m, n, r, at(L.l),
+                       o.l, at(L.us), at(L.vs));
+    return hipGetLastError();
+  }
+
+  // W_res = W - diag(h) sign(U') diag(l) sign(V')^T diag(g) of the path just run
+  hipError_t residual(const void* W, int wdt) const {
+    const int m = L.m, n = L.n, r = L.r;
+    GemmArgs g{};
+    g.A = at(L.us);
+    g.a_dt = kDtF64;
+    g.sai = r;
+    g.sak = 1;
+    g.B = at(L.vs);
+    g.b_dt = kDtF64;
+    g.sbk = 1;
+    g.sbj = r;
+    g.C = at(L.wres);
+    g.ldc = n;
+    g.M = m;
+    g.N = n;
+    g.K = r;
+    g.epi = kEpiResid;
+    g.W = W;
+    g.w_dt = wdt;
+    g.ldw = n;
+    g.h = at(L.h);
+    g.g = at(L.g);
+    return gemm(g);
+  }
+};
+
+}  // namespace
+
+bool svid_supports(int64_t d_out, int64_t d_in, int64_t r, int64_t over) {
+  if (d_out <= 0 || d_in <= 0 || r <= 0 || over < 0) return false;
+  if (r > std::min(d_out, d_in)) return false;
+  return std::min<int64_t>(r + over, std::min(d_out, d_in)) <= kMaxBlock;
+}
+
+size_t svid_workspace_bytes(int d_out, int d_in, int r, int over) {
+  return svid_layout(d_out, d_in, r, over).total;
+}
+
+hipError_t launch_dual_svid(const void* W, int wdt, int d_out, int d_in, int r, int over, int iters, uint64_t seed,
+                            const lb_svid_out* out, float* W_res, void* ws, hipStream_t stream) {
+  const SvidLayout L = svid_layout(d_out, d_in, r, over);
+  const Svid S{L, static_cast<char*>(ws), stream};
+  hipError_t e;
+  if ((e = S.path(W, wdt, out[0], iters, seed)) != hipSuccess) return e;
+  if ((e = S.residual(W, wdt)) != hipSuccess) return e;
+  if (W_res) {
+    const int64_t nw = static_cast<int64_t>(d_out) * d_in;
+    hipLaunchKernelGGL(f64_to_f32_kernel, dim3(grid_for(nw)), dim3(256), 0, stream,
+                       static_cast<const double*>(S.at(L.wres)), W_res, nw);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return S.path(S.at(L.wres), kDtF64, out[1], iters, seed + 0x632BE59BD9B4E019ull);
+}
+
+}  // namespace lb

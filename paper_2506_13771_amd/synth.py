@@ -115,6 +115,21 @@ def make_linear(d_in: int, d_out: int, r: int, T: int, act_dtype: str = BF16, sc
                         V_words=V_w if direct_words else None)
 
 
+_T_W = 6
+
+
+def dense_weight(d_out: int, d_in: int, k: int, noise: float, cfg: int, linear: int = 0) -> np.ndarray:
+    """A dense weight for the Dual-SVID conversion, fp32 [d_out, d_in]: a rank-k part whose column
+    scales fall linearly from 3 to 1 (A [d_out, k], B [d_in, k] standard normal, A diag(s) B^T /
+    sqrt(k)) plus i.i.d. N(0, noise^2) entries -- a decaying spectrum above a noise floor, as in the
+    pretrained weights the conversion is applied to."""
+    rs = rng(cfg, linear, _T_W)
+    A = rs.standard_normal((d_out, k)) * np.linspace(3.0, 1.0, k) if k > 0 else np.zeros((d_out, 0))
+    B = rs.standard_normal((d_in, k))
+    W = A @ B.T / np.sqrt(max(k, 1)) + noise * rs.standard_normal((d_out, d_in))
+    return W.astype(np.float32)
+
+
 # ----------------------------------------------------------------------------
 # The benchmark configurations (shapes of Llama-2 7B / 13B / 70B linears).
 # ----------------------------------------------------------------------------

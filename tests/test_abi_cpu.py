@@ -170,6 +170,46 @@ def test_noalloc_validation_errors(lib):
     assert na(d_out=0) == lb.LB_OK
 
 
+def test_dual_svid_workspace_and_validation(lib):
+    ws = lb.lb_dual_svid_workspace_bytes
+    # the residual weight (8 d_out d_in bytes) dominates at layer sizes
+    assert ws(4096, 4096, 80, 40) >= 8 * 4096 * 4096
+    assert ws(4096, 4096, 80, 40) < 8 * 4096 * 4096 + (64 << 20)
+    assert ws(64, 32, 8, 4) > 0 and ws(64, 32, 32, 0) > 0
+    for bad in ((0, 32, 8, 4), (64, 0, 8, 4), (64, 32, 0, 4), (64, 32, 33, 0), (64, 32, 8, -1),
+                (4096, 4096, 1000, 100), (1 << 20, 1 << 12, 8, 0)):
+        assert ws(*bad) == 0, bad
+    out = (lb.lb_svid_out * 2)()
+    for p in range(2):
+        out[p] = lb.lb_svid_out(FAKE, FAKE, FAKE, FAKE, FAKE, 0)
+
+    def call(W=FAKE, dt=lb.LB_F32, d_out=64, d_in=32, r=8, over=4, iters=5, o=out, wres=0, w=FAKE,
+             wb=1 << 30):
+        return lib.lb_dual_svid(W, dt, d_out, d_in, r, over, iters, 0, o, wres, w, wb, None)
+
+    assert call(dt=9) == lb.LB_ERR_DTYPE
+    assert call(r=0) == lb.LB_ERR_SHAPE
+    assert call(r=33) == lb.LB_ERR_SHAPE
+    assert call(over=-1) == lb.LB_ERR_SHAPE
+    assert call(d_out=4096, d_in=4096, r=1000, over=100) == lb.LB_ERR_SHAPE
+    assert call(iters=-1) == lb.LB_ERR_ARG
+    assert call(iters=1001) == lb.LB_ERR_ARG
+    assert call(W=0) == lb.LB_ERR_NULL
+    assert call(o=None) == lb.LB_ERR_NULL
+    assert call(w=0) == lb.LB_ERR_NULL
+    bad = (lb.lb_svid_out * 2)()
+    bad[0] = lb.lb_svid_out(FAKE, FAKE, FAKE, FAKE, 0, 0)
+    bad[1] = out[1]
+    assert call(o=bad) == lb.LB_ERR_NULL
+    bad[0] = lb.lb_svid_out(FAKE, FAKE, FAKE + 2, FAKE, FAKE, 0)
+    assert call(o=bad) == lb.LB_ERR_ALIGN
+    assert call(W=FAKE + 2) == lb.LB_ERR_ALIGN
+    assert call(W=FAKE + 2, dt=lb.LB_BF16, wb=1024) == lb.LB_ERR_WORKSPACE  # 2-byte aligned is enough for bf16
+    assert call(wres=FAKE + 1) == lb.LB_ERR_ALIGN
+    assert call(w=FAKE + 64) == lb.LB_ERR_ALIGN
+    assert call(wb=1024) == lb.LB_ERR_WORKSPACE
+
+
 def test_pack_validation_errors(lib):
     assert lib.lb_pack_signs(FAKE, lb.LB_F32, 64, 16, 5, FAKE * 2, None, None) == lb.LB_ERR_ARG
     assert lib.lb_pack_signs(FAKE, 3, 64, 16, lb.LB_ROLE_U, FAKE * 2, None, None) == lb.LB_ERR_DTYPE
