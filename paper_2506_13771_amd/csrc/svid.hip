@@ -20,11 +20,13 @@
 // The contractions (W and W^T times a block, Gram matrices, basis changes, the
 // effective weight) run on the fp64 matrix cores; the small symmetric
 // eigenproblems (b x b and r x r) run as a parallel cyclic Jacobi method on one
-// workgroup.  Orthonormalisation is by the Gram matrix's eigenvectors
-// (Q = Y E diag(lambda)^-1/2, directions with lambda <= 1e-14 lambda_max
-// dropped), so a rank-deficient block needs no special case.  Sums are in a
-// fixed order (split-K partial sums added in slab order), so a call is
-// deterministic.
+// workgroup.  Inside the iteration a block is orthonormalised by Cholesky of
+// its Gram matrix (CholQR, pivots below 1e-13 of the largest dropped); the
+// final block by the Gram matrix's eigenvectors (Q = Y E diag(lambda)^-1/2,
+// directions with lambda <= 1e-14 lambda_max dropped), so that the
+// Rayleigh-Ritz basis is orthonormal to rounding and a rank-deficient block
+// needs no special case.  Sums are in a fixed order (split-K partial sums added
+// in slab order), so a call is deterministic.
 #include <algorithm>
 #include <cmath>
 
@@ -190,7 +192,7 @@ template <bool kLds>
 __global__ __launch_bounds__(kEigThreads) void jacobi_eig_kernel(double* A, double* Et, double* E, double* lam,
                                                                   int b, int mode) {
   extern __shared__ double eig_smem[];
-  __shared__ int pp[kMaxBlock / 2], pq[kMaxBlock / 2];
+  __shared__ int pp[kMaxBlock / 2], pq[kMaxBlock / 2], pa[kMaxBlock / 2];
   __shared__ double pc[kMaxBlock / 2], ps[kMaxBlock / 2];
   __shared__ int rot;
   __shared__ double floor_abs;
@@ -225,38 +227,41 @@ __global__ __launch_bounds__(kEigThreads) void jacobi_eig_kernel(double* A, doub
             act = true;
           }
         }
-        pp[tid] = act ? p : -1;
+        pp[tid] = p;
         pq[tid] = q;
+        pa[tid] = act ? 1 : 0;
         pc[tid] = c;
         ps[tid] = sn;
         if (act) atomicAdd(&rot, 1);
       }
       __syncthreads();
-      // rows p, q of A and of Et
+      // A <- J^T A J one 2 x 2 block (rows of pair kr, columns of pair kc) at a
+      // time: the blocks are disjoint, so one phase does the whole step; the
+      // rows of the inactive pairs' and the dummy index's blocks are identity.
+      for (int e = tid; e < np * np; e += kEigThreads) {
+        const int kr = e / np, kc = e - kr * np;
+        if (!pa[kr] && !pa[kc]) continue;
+        const int p = pp[kr], q = pq[kr], u = pp[kc], v = pq[kc];
+        const bool qv = q < b, vv = v < b;
+        const double cr = pc[kr], sr = ps[kr], cc = pc[kc], sc = ps[kc];
+        const double a00 = M[p * b + u], a01 = vv ? M[p * b + v] : 0.0;
+        const double a10 = qv ? M[q * b + u] : 0.0, a11 = (qv && vv) ? M[q * b + v] : 0.0;
+        const double b00 = cr * a00 - sr * a10, b01 = cr * a01 - sr * a11;
+        const double b10 = sr * a00 + cr * a10, b11 = sr * a01 + cr * a11;
+        M[p * b + u] = cc * b00 - sc * b01;
+        if (vv) M[p * b + v] = sc * b00 + cc * b01;
+        if (qv) M[q * b + u] = cc * b10 - sc * b11;
+        if (qv && vv) M[q * b + v] = sc * b10 + cc * b11;
+      }
+      // rows p, q of the accumulated rotations
       for (int e = tid; e < np * b; e += kEigThreads) {
-        const int k = e / b, j = e % b;
-        const int p = pp[k];
-        if (p < 0) continue;
-        const int q = pq[k];
+        const int k = e / b, j = e - k * b;
+        if (!pa[k]) continue;
+        const int p = pp[k], q = pq[k];
         const double c = pc[k], sn = ps[k];
-        const double rp = M[p * b + j], rq = M[q * b + j];
-        M[p * b + j] = c * rp - sn * rq;
-        M[q * b + j] = sn * rp + c * rq;
         const double ep = Et[static_cast<int64_t>(p) * b + j], eq = Et[static_cast<int64_t>(q) * b + j];
         Et[static_cast<int64_t>(p) * b + j] = c * ep - sn * eq;
         Et[static_cast<int64_t>(q) * b + j] = sn * ep + c * eq;
-      }
-      __syncthreads();
-      // columns p, q of A
-      for (int e = tid; e < np * b; e += kEigThreads) {
-        const int k = e / b, i = e % b;
-        const int p = pp[k];
-        if (p < 0) continue;
-        const int q = pq[k];
-        const double c = pc[k], sn = ps[k];
-        const double cp = M[i * b + p], cq = M[i * b + q];
-        M[i * b + p] = c * cp - sn * cq;
-        M[i * b + q] = sn * cp + c * cq;
       }
       __syncthreads();
     }
@@ -278,6 +283,61 @@ __global__ __launch_bounds__(kEigThreads) void jacobi_eig_kernel(double* A, doub
     if (mode == 1) f = (li > 0.0 && li > kDropRel * lmax) ? 1.0 / sqrt(li) : 0.0;
     for (int row = 0; row < b; ++row)
       E[static_cast<int64_t>(row) * b + rank] = f * Et[static_cast<int64_t>(i) * b + row];
+  }
+}
+
+// Orthonormalisation by Cholesky (CholQR): for the Gram matrix G = Y^T Y
+// [b x b], G = L L^T (lower, in place in G's lower triangle), then T = L^-T
+// (upper) into T, so that Q = Y T has orthonormal columns.  A pivot <= 1e-13
+// of the largest diagonal entry is dropped (that column of L and of L^-1 is
+// zero), so a rank-deficient block gives zero columns instead of a breakdown.
+// X [b x b] is scratch for L^-1, computed by right-looking forward
+// substitution.  One workgroup; G lives in LDS when b <= kEigLdsMax.
+template <bool kLds>
+__global__ __launch_bounds__(kEigThreads) void chol_orth_kernel(double* G, double* X, double* T, int b) {
+  extern __shared__ double chol_smem[];
+  __shared__ double invs[kMaxBlock];
+  __shared__ double thr;
+  const int tid = threadIdx.x;
+  double* L = kLds ? chol_smem : G;
+  if (kLds)
+    for (int e = tid; e < b * b; e += kEigThreads) L[e] = G[e];
+  for (int e = tid; e < b * b; e += kEigThreads) X[e] = (e / b == e % b) ? 1.0 : 0.0;
+  if (tid == 0) {
+    double mx = 0.0;
+    for (int i = 0; i < b; ++i) mx = fmax(mx, G[static_cast<int64_t>(i) * b + i]);
+    thr = 1e-13 * mx;
+  }
+  __syncthreads();
+  for (int k = 0; k < b; ++k) {
+    const double d = L[k * b + k];
+    const double inv = d > thr ? 1.0 / sqrt(d) : 0.0;
+    if (tid == 0) invs[k] = inv;
+    for (int i = k + 1 + tid; i < b; i += kEigThreads) L[i * b + k] *= inv;
+    __syncthreads();
+    const int w = b - k - 1;
+    for (int e = tid; e < w * w; e += kEigThreads) {
+      const int i = k + 1 + e / w, j = k + 1 + e % w;
+      if (j <= i) L[i * b + j] -= L[i * b + k] * L[j * b + k];
+    }
+    __syncthreads();
+  }
+  // X = L^-1: row k = (row k of the updated right-hand side) / L_kk, then the
+  // rows below subtract L_ik times it (only columns c <= k are nonzero)
+  for (int k = 0; k < b; ++k) {
+    const double inv = invs[k];
+    for (int c = tid; c <= k; c += kEigThreads) X[static_cast<int64_t>(k) * b + c] *= inv;
+    __syncthreads();
+    const int w = b - k - 1;
+    for (int e = tid; e < w * (k + 1); e += kEigThreads) {
+      const int i = k + 1 + e / (k + 1), c = e % (k + 1);
+      X[static_cast<int64_t>(i) * b + c] -= L[i * b + k] * X[static_cast<int64_t>(k) * b + c];
+    }
+    __syncthreads();
+  }
+  for (int e = tid; e < b * b; e += kEigThreads) {
+    const int j = e / b, k = e % b;
+    T[e] = X[static_cast<int64_t>(k) * b + j];
   }
 }
 
@@ -540,6 +600,31 @@ struct Svid {
     return gemm(g);
   }
 
+  // Y [rows x b] -> a basis of its range in Qo [rows x b] by CholQR: G =
+  // Y^T Y = L L^T, Qo = Y L^-T (dropped pivots give zero columns); the
+  // columns are orthonormal up to about cond(Y)^2 times the rounding unit,
+  // which is all the iteration needs
+  hipError_t orth_chol(const double* Y, double* Qo, int rows) const {
+    const int b = L.b;
+    hipError_t e;
+    if ((e = mm(Y, kDtF64, 1, b, false, Y, kDtF64, b, 1, false, at(L.gram), b, b, b, rows)) != hipSuccess) return e;
+    if (b <= kEigLdsMax) {
+      const int smem = static_cast<int>(sizeof(double) * b * b);
+      if (smem > 65536) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&chol_orth_kernel<true>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return e;
+      }
+      hipLaunchKernelGGL((chol_orth_kernel<true>), dim3(1), dim3(kEigThreads), smem, st, at(L.gram), at(L.et),
+                         at(L.e), b);
+    } else {
+      hipLaunchKernelGGL((chol_orth_kernel<false>), dim3(1), dim3(kEigThreads), 0, st, at(L.gram), at(L.et),
+                         at(L.e), b);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return mm(Y, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, Qo, b, rows, b, b);
+  }
+
   // Y [rows x b] -> an orthonormal basis of its range in Qo [rows x b]:
   // G = Y^T Y, G = E diag(lambda) E^T, Qo = Y E diag(lambda)^-1/2 (dropped
   // directions give zero columns)
@@ -573,16 +658,16 @@ struct Svid {
     hipLaunchKernelGGL(rand_fill_kernel, dim3(grid_for(static_cast<int64_t>(n) * b)), dim3(256), 0, st, Z,
                        static_cast<int64_t>(n) * b, seed);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // Y = W Z, Q = orth(Y)
+    // Y = W Z; per round Q = orth(Y), Z = orth(W^T Q), Y = W Z (CholQR); then
+    // Q = an orthonormal basis of Y's range by eigenvectors
     if ((e = mm(W, wdt, n, 1, false, Z, kDtF64, b, 1, false, Y, b, m, b, n)) != hipSuccess) return e;
-    if ((e = orth(Y, Q, m)) != hipSuccess) return e;
     for (int it = 0; it < iters; ++it) {
-      // Z = orth(W^T Q), Q = orth(W Z)
+      if ((e = orth_chol(Y, Q, m)) != hipSuccess) return e;
       if ((e = mm(W, wdt, 1, n, false, Q, kDtF64, b, 1, false, Z2, b, n, b, m)) != hipSuccess) return e;
-      if ((e = orth(Z2, Z, n)) != hipSuccess) return e;
+      if ((e = orth_chol(Z2, Z, n)) != hipSuccess) return e;
       if ((e = mm(W, wdt, n, 1, false, Z, kDtF64, b, 1, false, Y, b, m, b, n)) != hipSuccess) return e;
-      if ((e = orth(Y, Q, m)) != hipSuccess) return e;
     }
+    if ((e = orth(Y, Q, m)) != hipSuccess) return e;
     // Rayleigh-Ritz: Z = W^T Q, Z^T Z = E diag(lambda) E^T, U = Q E_r, V = Z E_r / sigma
     if ((e = mm(W, wdt, 1, n, false, Q, kDtF64, b, 1, false, Z, b, n, b, m)) != hipSuccess) return e;
     if ((e = mm(Z, kDtF64, 1, b, false, Z, kDtF64, b, 1, false, at(L.gram), b, b, b, n)) != hipSuccess) return e;
