@@ -674,8 +674,9 @@ class StreamListCall:
 
 def list_timing(res, T, steps, warmup):
     """ms per list call over every linear of `res` at T tokens, graph-replayed, with the derived
-    rates: the streaming list forward (lb_list_forward) where the list is in its scope (T <= 2),
-    else lb_linear_forward_many; for T <= 2 lb_linear_forward_many is timed beside it."""
+    rates: the streaming list forward (lb_list_forward: look-up-table kernels for T <= 2,
+    matrix-core kernels up to 64 tokens) where the list is in its scope, else
+    lb_linear_forward_many; at T = 1 lb_linear_forward_many is timed beside it."""
     import torch
     import paper_2506_13771_amd as lb
     n = len(res.items)
@@ -684,10 +685,11 @@ def list_timing(res, T, steps, warmup):
     if lb.lb_list_workspace_bytes(descs, n) > 0:
         call = StreamListCall(descs, n)
         api = "lb_list_forward"
-        many = ListCall(descs, n)
-        ms_many, _ = time_calls([many], steps, warmup, use_graph=True, per_graph=1)
-        extra["ms_per_call_forward_many"] = ms_many
-        del many
+        if T == 1:
+            many = ListCall(descs, n)
+            ms_many, _ = time_calls([many], steps, warmup, use_graph=True, per_graph=1)
+            extra["ms_per_call_forward_many"] = ms_many
+            del many
     else:
         call = ListCall(descs, n)
         api = "lb_linear_forward_many"
@@ -710,8 +712,8 @@ RANKS_7B = {0.1: {4096: 80, 11008: 128}, 0.55: {4096: 544, 11008: 800}}
 def run_sweep70b(ts, steps, warmup):
     """The Llama2-70B-shaped decode sweep: 80 layers x 7 linears at 0.1 BPW resident in HBM
     (about 0.81 GB of packed signs and scales, more than three times the Infinity Cache, so
-    every call streams its weights from HBM), all 560 linears in one lb_linear_forward_many
-    call, T tokens per linear."""
+    every call streams its weights from HBM), all 560 linears in one list call, T tokens per
+    linear."""
     import torch
     from paper_2506_13771_amd import synth
     t0 = time.perf_counter()
@@ -720,7 +722,8 @@ def run_sweep70b(ts, steps, warmup):
     res = ResidentLinears(shapes, max(ts), cfg=4, direct_words=True)
     setup_s = time.perf_counter() - t0
     out = {"workload": "Llama2-70B shapes, 80 layers x (q,k,v,o,gate,up,down) at 0.1 BPW, bf16 x, fp16 scales, "
-                       "one list call per sweep (lb_list_forward for T <= 2, else lb_linear_forward_many)",
+                       "one lb_list_forward call per sweep (look-up-table kernels for T <= 2, matrix-core "
+                       "kernels for larger T)",
            "linears": len(shapes), "weights_bytes": res.bytes_and_flops(1)[1], "setup_s": setup_s, "per_T": []}
     for T in ts:
         rec = list_timing(res, T, steps, warmup)
@@ -738,8 +741,9 @@ def run_block7b(ts, steps, warmup, bpw=0.1):
     from paper_2506_13771_amd import synth
     shapes = [(name, d_in, d_out, RANKS_7B[bpw][max(d_in, d_out)]) for (name, d_in, d_out) in synth.LLAMA2_7B]
     res = ResidentLinears(shapes, max(ts), cfg=2, direct_words=False)
-    out = {"workload": f"Llama2-7B block, 7 linears at {bpw} BPW, bf16 x, fp16 scales, one list call "
-                       "(lb_list_forward for T <= 2, else lb_linear_forward_many; weights warm in the caches)",
+    out = {"workload": f"Llama2-7B block, 7 linears at {bpw} BPW, bf16 x, fp16 scales, one lb_list_forward "
+                       "call (look-up-table kernels for T <= 2, matrix-core kernels for larger T; weights warm in "
+                       "the caches)",
            "bpw": bpw, "per_T": []}
     for T in ts:
         rec = list_timing(res, T, max(steps, 50), max(warmup, 10))

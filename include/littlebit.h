@@ -254,19 +254,27 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
    Decoding Throughput"), e.g. all linears of all layers of a model for a
    batch of independent inputs, or the q/k/v or gate/up projections of one
    layer.  Each linear is computed as lb_linear_forward computes it
-   (Proposition 1, Eq. proposition1, both paths, Eq. final_weight_approx_res)
-   and the result is bit-identical to lb_linear_forward_kernel(...,
-   LB_KERNEL_DECODE) for that linear; the whole list takes three launches
-   (latent partial sums of every linear, their sums times l, every output),
-   with no workgroup waiting for another.
+   (Proposition 1, Eq. proposition1, both paths, Eq. final_weight_approx_res);
+   the whole list takes three kinds of launch (latent partial sums of every
+   linear, their sums times l, every output), with no workgroup waiting for
+   another.
+     - Lists whose linears all have 1 <= T <= 2 tokens run on the look-up-
+       table kernels: each result is bit-identical to
+       lb_linear_forward_kernel(..., LB_KERNEL_DECODE) for that linear.
+     - Lists with a linear of 3 <= T <= 64 tokens run on the matrix-core
+       kernels (every linear of the list): g and x enter as exact bf16 terms,
+       products are exact and sums fp32, w enters stage 2 as 2 bf16 terms
+       (3 for fp32 activations); results meet the tolerance of
+       lb_linear_forward, and repeated calls give the same bits.
 
-   Scope: every linear with work has 1 <= T <= 2 tokens, r <= 1024, a d_in
-   whose runs fit the look-up-table kernel (d_in <= 32768 at r <= 1024 is
-   always accepted), and the list shares one activation and one scale dtype
-   (LB_ERR_SHAPE / LB_ERR_DTYPE otherwise); linears with T == 0 or d_out == 0
-   are skipped, those with d_in == 0 or r == 0 get y = 0.  n <= 65535.  No y
-   may overlap another linear's x or y (LB_ERR_ARG); other checks as for
-   lb_linear_forward.
+   Scope: every linear with work has r <= 1024 and the list shares one
+   activation and one scale dtype; for the look-up-table kernels a d_in whose
+   runs fit them (d_in <= 32768 at r <= 1024 is always accepted); for the
+   matrix-core kernels T <= 64, d_in a multiple of 4 and x, g_0, g_1 aligned
+   to four elements (LB_ERR_SHAPE / LB_ERR_DTYPE otherwise); linears with
+   T == 0 or d_out == 0 are skipped, those with d_in == 0 or r == 0 get
+   y = 0.  n <= 65535.  No y may overlap another linear's x or y (LB_ERR_ARG);
+   other checks as for lb_linear_forward.
 
    The list's descriptors live in the workspace (the "plan"):
    lb_list_workspace_bytes: host, pure; bytes of a workspace for this list

@@ -17,10 +17,13 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblittlebit.so")
 SOURCES = ["api.cpp", "pack.hip", "decode.hip", "decode_mma.hip", "prefill.hip", "latent_small.hip", "backward.hip",
-           "dense_ref.hip", "stream.hip", "svid.hip"]
+           "dense_ref.hip", "stream.hip", "stream_mma.hip", "svid.hip"]
 # the look-up-table kernels of decode.hip and stream.hip give bit-identical
 # results only if neither contracts a multiply and an add into one fma
-EXTRA_FLAGS = {"decode.hip": ["-ffp-contract=off"], "stream.hip": ["-ffp-contract=off"]}
+# the matrix-core list kernels keep their accumulators in ordinary VGPRs (in
+# AGPRs the compiler moves them back and forth on every iteration)
+EXTRA_FLAGS = {"decode.hip": ["-ffp-contract=off"], "stream.hip": ["-ffp-contract=off"],
+               "stream_mma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 ARCH = os.environ.get("LB_OFFLOAD_ARCH", "gfx950")
 
 

@@ -553,6 +553,7 @@ lb_status list_check(const lb_linear_desc* descs, int64_t n, std::vector<lb::For
     }
     args.push_back(a);
   }
+  if (!lb::stream_list_supports(args.data(), static_cast<int>(n))) return LB_ERR_SHAPE;
   if (!list_outputs_disjoint(descs, n)) return LB_ERR_ARG;
   return LB_OK;
 }

@@ -220,9 +220,16 @@ size_t from_latent_workspace_bytes(int T, int r);
 hipError_t launch_latent(const ForwardArgs& a, int lat_dt, hipStream_t stream);
 hipError_t launch_from_latent(const ForwardArgs& a, const void* lat, int lat_dt, hipStream_t stream);
 hipError_t launch_dense_ref(const ForwardArgs& a, float* W, hipStream_t stream);
-// Streaming list of decode-sized linears (stream.hip): three launches for the
-// whole list, the plan (descriptors and work maps) in the workspace.
+// Streaming list forward (stream.hip, stream_mma.hip): three kinds of launch
+// for the whole list, the plan (descriptors and work maps) in the workspace.
+// Lists whose linears have at most 2 tokens use the look-up-table kernels,
+// other lists (up to 64 tokens) the matrix-core kernels.
 bool stream_supports(const ForwardArgs& a);
+bool stream_list_supports(const ForwardArgs* a, int n);
+bool stream_mma_supports(const ForwardArgs& a);
+size_t stream_mma_workspace_bytes(const ForwardArgs* a, int n);
+hipError_t stream_mma_init(const ForwardArgs* a, int n, uint64_t fingerprint, void* ws, hipStream_t stream);
+hipError_t stream_mma_forward(const ForwardArgs* a, int n, uint64_t fingerprint, void* ws, hipStream_t stream);
 size_t stream_workspace_bytes(const ForwardArgs* a, int n);
 hipError_t stream_init(const ForwardArgs* a, int n, uint64_t fingerprint, void* ws, hipStream_t stream);
 hipError_t stream_forward(const ForwardArgs* a, int n, uint64_t fingerprint, void* ws, hipStream_t stream);

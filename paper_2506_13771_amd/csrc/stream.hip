@@ -34,11 +34,20 @@
 #include <vector>
 
 #include "lut_common.h"
+#include "stream_plan.h"
 
 namespace lb {
 
 namespace {
 
+using splan::align256;
+using splan::has_work;
+using splan::kHdrCounts;
+using splan::kHdrFp;
+using splan::kHdrN;
+using splan::packed_bytes64;
+using splan::plan_ok;
+using splan::StreamLinear;
 using lut::build_table;
 using lut::kBlk;
 using lut::kChunk;
@@ -51,35 +60,6 @@ constexpr int kRpl = 2;                   // stage-2 output rows per lane
 constexpr int kRowsS2 = kRpl * kThreads;  // stage-2 output rows per workgroup
 constexpr int kMaxTokens = 2;
 constexpr int kMaxRank = 1024;
-
-struct alignas(16) StreamLinear {
-  const void* x;
-  void* y;
-  const void* U[2];
-  const void* V[2];
-  const void* h[2];
-  const void* g[2];
-  const void* l[2];
-  float* part;  // [2][T][s1d][r] partial sums l (.) z of each run
-  float* wlat;  // [2][T][r]      w = l (.) z
-  int T, d_in, d_out, r;
-  int s1d, bpr;
-  uint32_t x_bytes, g_bytes, h_bytes, l_bytes, v_bytes, u_bytes;
-};
-
-// plan header: the control block's words (error word at kCtrlError), the
-// fingerprint at words 4-5, the list length and the three work counts
-constexpr int kHdrFp = 4;
-constexpr int kHdrN = 6;
-constexpr int kHdrCounts = 7;
-
-__device__ __forceinline__ bool plan_ok(const uint32_t* hdr, uint64_t fp) {
-  const uint64_t have = (static_cast<uint64_t>(hdr[kHdrFp + 1]) << 32) | hdr[kHdrFp];
-  if (have == fp) return true;
-  if (threadIdx.x == 0) __hip_atomic_fetch_or(const_cast<uint32_t*>(hdr) + kCtrlError, 2u, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT);
-  return false;
-}
 
 // ---------------------------------------------------------------------------
 // LDS addressing for the look-ups: a table set of one block is 512 bytes (8
@@ -415,15 +395,6 @@ __global__ void __launch_bounds__(kThreads) stream_s2_kernel(const uint32_t* __r
 // ---------------------------------------------------------------------------
 // host side: plan layout, work counts and launches
 // ---------------------------------------------------------------------------
-size_t align256(size_t b) { return (b + 255) / 256 * 256; }
-
-int64_t packed_bytes64(int64_t n_out, int64_t n_red) {
-  const int64_t w = n_red & 31;
-  return 4 * (n_red >> 5) * n_out + (w == 0 ? 0 : (w <= 16 ? 2 : 4)) * n_out;
-}
-
-bool has_work(const ForwardArgs& a) { return a.T > 0 && a.d_in > 0 && a.d_out > 0 && a.r > 0; }
-
 // the S1 class of run c of a linear (see launch_s1)
 int s1_class(const ForwardArgs& a, const DecodeGeom& g, int c) {
   const int nbt = nblocks32(a.d_in), nbv = a.d_in >> 5, tailv = a.d_in & 31;
@@ -561,7 +532,9 @@ void launch_act(const void* ws, const PlanLayout& P, int sc_dt, uint64_t fp, hip
 
 }  // namespace
 
-bool stream_supports(const ForwardArgs& a) {
+namespace {
+
+bool lut_supports(const ForwardArgs& a) {
   if (!has_work(a)) return true;
   if (a.T > kMaxTokens || a.r > kMaxRank || !decode_supports(a.T, a.d_in, a.d_out, a.r)) return false;
   if (a.d_out > 65535 * kRowsS2 || 2 * a.T * a.r > 65535 * kThreads) return false;
@@ -569,9 +542,30 @@ bool stream_supports(const ForwardArgs& a) {
   return g.bpr <= kMaxRunBlocks && g.s1d <= 255;
 }
 
-size_t stream_workspace_bytes(const ForwardArgs* a, int n) { return plan_layout(a, n).bytes; }
+// a list with a linear of more than kMaxTokens tokens runs on the matrix cores
+bool list_mma(const ForwardArgs* a, int n) {
+  for (int i = 0; i < n; ++i)
+    if (has_work(a[i]) && a[i].T > kMaxTokens) return true;
+  return false;
+}
+
+}  // namespace
+
+bool stream_supports(const ForwardArgs& a) { return lut_supports(a) || stream_mma_supports(a); }
+
+bool stream_list_supports(const ForwardArgs* a, int n) {
+  const bool mma = list_mma(a, n);
+  for (int i = 0; i < n; ++i)
+    if (!(mma ? stream_mma_supports(a[i]) : lut_supports(a[i]))) return false;
+  return true;
+}
+
+size_t stream_workspace_bytes(const ForwardArgs* a, int n) {
+  return list_mma(a, n) ? stream_mma_workspace_bytes(a, n) : plan_layout(a, n).bytes;
+}
 
 hipError_t stream_init(const ForwardArgs* a, int n, uint64_t fp, void* ws, hipStream_t stream) {
+  if (list_mma(a, n)) return stream_mma_init(a, n, fp, ws, stream);
   const PlanLayout P = plan_layout(a, n);
   std::vector<char> host(P.data_off, 0);
   uint32_t* hdr = reinterpret_cast<uint32_t*>(host.data());
@@ -632,6 +626,7 @@ hipError_t stream_init(const ForwardArgs* a, int n, uint64_t fp, void* ws, hipSt
 }
 
 hipError_t stream_forward(const ForwardArgs* a, int n, uint64_t fp, void* ws, hipStream_t stream) {
+  if (list_mma(a, n)) return stream_mma_forward(a, n, fp, ws, stream);
   const PlanLayout P = plan_layout(a, n);
   if (P.n1 == 0) return hipSuccess;
   int act = -1, sc = -1;

@@ -478,10 +478,19 @@ def test_list_validation(lib):
     arr = _list_descs(3)
     need = lib.lb_list_workspace_bytes(arr, 3)
     assert need > 0
-    # out of scope: three tokens, a rank above 1024, mixed dtypes
-    assert lib.lb_list_workspace_bytes(_list_descs(2, T=3), 2) == 0
+    # lists with more than two tokens run on the matrix cores (up to 64 tokens, d_in a multiple of 4)
+    assert lib.lb_list_workspace_bytes(_list_descs(2, T=3), 2) > 0
+    assert lib.lb_list_workspace_bytes(_list_descs(2, T=64, ystep=1 << 16), 2) > 0
+    mix = _list_descs(2)
+    mix[1].T = 8
+    assert lib.lb_list_workspace_bytes(mix, 2) > 0
+    # out of scope: 65 tokens, d_in not a multiple of 4 with more than two tokens, a rank above 1024,
+    # mixed dtypes
+    assert lib.lb_list_workspace_bytes(_list_descs(2, T=65), 2) == 0
+    assert lib.lb_list_workspace_bytes(_list_descs(2, T=8, d_in=30), 2) == 0
+    assert lib.lb_list_workspace_bytes(_list_descs(2, T=2, d_in=30), 2) > 0
     assert lib.lb_list_workspace_bytes(_list_descs(2, r=1040), 2) == 0
-    assert lib.lb_list_init(_list_descs(2, T=3), 2, FAKE, 1 << 30, None) == lb.LB_ERR_SHAPE
+    assert lib.lb_list_init(_list_descs(2, T=65), 2, FAKE, 1 << 30, None) == lb.LB_ERR_SHAPE
     mixed = _list_descs(2)
     mixed[1].act_dtype = lb.LB_F32
     assert lib.lb_list_init(mixed, 2, FAKE, 1 << 30, None) == lb.LB_ERR_DTYPE

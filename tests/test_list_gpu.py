@@ -1,10 +1,15 @@
-"""GPU parity of the streaming list forward (lb_list_init / lb_list_forward): every
-linear of a list must give bit for bit what the single-launch look-up-table decode
-kernel gives for it (lb_linear_forward_kernel(..., LB_KERNEL_DECODE)), and meet the
-oracle bar.  Lists mix ragged shapes (tails of d_in, r and d_out, ranks that are not
-a multiple of 64), one- and two-token linears, runs of one and of several 32-block
-chunks, empty linears; the plan check, graph replays and the Llama2-70B layer shapes
-are covered too."""
+"""GPU parity of the streaming list forward (lb_list_init / lb_list_forward).
+
+Lists of linears of at most two tokens run on the look-up-table kernels: every
+linear must give bit for bit what the single-launch look-up-table decode kernel
+gives for it (lb_linear_forward_kernel(..., LB_KERNEL_DECODE)) and meet the oracle
+bar.  Lists with a linear of more than two tokens run on the matrix-core kernels:
+every token of every linear meets the oracle bar of the forward (fp32: relative L2
+<= 1e-5; bf16 / f16: max relative error <= 1e-2 per token row), and repeated calls
+give the same bits.  Lists mix ragged shapes (tails of d_in, r and d_out, ranks that
+are not a multiple of 64 or 16, token counts that are not a multiple of 16), runs
+of one and of several blocks, empty linears; the plan check, graph replays and the
+Llama2-70B layer shapes are covered for both kinds."""
 import numpy as np
 import pytest
 
@@ -161,3 +166,77 @@ def test_list_graph_replays_match_eager():
         torch.cuda.synchronize()
         for i in range(len(lins)):
             assert _same_bits(ys[i], y_eager[i]), (rep, i)
+
+
+# ---------------------------------------------------------------------------
+# lists with linears of more than two tokens: the matrix-core kernels (every
+# linear of such a list, whatever its own token count); parity with the oracle
+# at the forward's bar, every token compared
+# ---------------------------------------------------------------------------
+RAGGED_MMA = [(3, 100, 77, 19), (8, 36, 200, 50), (16, 256, 130, 16), (17, 32, 64, 1), (64, 1000, 999, 96),
+              (33, 96, 4100, 48), (1, 4, 1, 1), (8, 4000, 300, 200), (5, 5000, 700, 80), (64, 2048, 640, 130),
+              (2, 700, 64, 64), (48, 6500, 2000, 288), (8, 3000, 1500, 176), (64, 4096, 4096, 1024)]
+
+
+@pytest.mark.parametrize("act,sc", [("bf16", "f16"), ("f32", "f32"), ("f16", "bf16"), ("bf16", "bf16")])
+def test_mma_list_ragged_matches_oracle(act, sc):
+    lins = _linears(RAGGED_MMA, cfg=44, act=act, sc=sc)
+    for j, (li, x, paths) in enumerate(lins):
+        rs = np.random.default_rng(100 + j)
+        for p in range(2):
+            li.h[p] = synth.quantize(rs.standard_normal(li.d_out), sc)
+            li.g[p] = synth.quantize(rs.standard_normal(li.d_in), sc)
+            li.l[p] = synth.quantize(rs.standard_normal(li.r), sc)
+            paths[p].h.copy_(U.raw_to_torch(li.h[p], sc))
+            paths[p].g.copy_(U.raw_to_torch(li.g[p], sc))
+            paths[p].l.copy_(U.raw_to_torch(li.l[p], sc))
+    L, ys = _run_list(lins)
+    for i, ((li, _, _), y) in enumerate(zip(lins, ys)):
+        _check(li, U.torch_to_raw(y, act), label=f"mma list {RAGGED_MMA[i]} {act}/{sc}")
+    assert lb.lb_workspace_status(L.workspace) == 0
+    # repeated forwards give the same bits (fixed summation order)
+    again = L.forward()
+    torch.cuda.synchronize()
+    assert all(_same_bits(a, b) for a, b in zip(again, ys))
+
+
+@pytest.mark.parametrize("T", [8, 64])
+def test_mma_list_llama2_70b_layer_shapes(T):
+    """One Llama2-70B layer at 0.1 bits per weight (q, k, v, o, gate, up, down), T tokens."""
+    ranks = {(8192, 8192): 176, (8192, 1024): 16, (8192, 28672): 288, (28672, 8192): 288}
+    specs = [(T, d_in, d_out, ranks[(d_in, d_out)]) for _, d_in, d_out in synth.LLAMA2_70B]
+    lins = _linears(specs, cfg=5, direct=True)
+    L, ys = _run_list(lins)
+    for i, ((li, _, _), y) in enumerate(zip(lins, ys)):
+        _check(li, U.torch_to_raw(y, "bf16"), label=f"70b mma list {specs[i]}")
+    assert lb.lb_workspace_status(L.workspace) == 0
+
+
+def test_mma_list_plan_mismatch_and_graph_replays():
+    specs = [(8, 2048, 1536, 64), (64, 1024, 4096, 80), (3, 512, 512, 32)]
+    lins = _linears(specs, cfg=45)
+    L, ys = _run_list(lins)
+    y_eager = [y.clone() for y in ys]
+    other = torch.full_like(ys[0], 3.0)
+    arr, _ = lb.make_descs([(x, paths, li.r, other if i == 0 else ys[i]) for i, (li, x, paths) in enumerate(lins)])
+    st = lb.load_library().lb_list_forward(arr, len(specs), L.workspace.data_ptr(), L.workspace.numel(),
+                                           torch.cuda.current_stream().cuda_stream)
+    assert st == lb.LB_OK
+    torch.cuda.synchronize()
+    assert torch.all(other == 3.0)
+    assert lb.lb_workspace_status(L.workspace) == 2
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        L.forward()
+    for rep in range(3):
+        for y in ys:
+            y.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i in range(len(lins)):
+            assert _same_bits(ys[i], y_eager[i]), (rep, i)
+        L.forward()
+        torch.cuda.synchronize()
+        for i in range(len(lins)):
+            assert _same_bits(ys[i], y_eager[i]), (rep, i)
+    assert lb.lb_workspace_status(L.workspace) == 0
