@@ -20,10 +20,11 @@ SOURCES = ["api.cpp", "pack.hip", "decode.hip", "decode_mma.hip", "prefill.hip",
            "dense_ref.hip", "stream.hip", "stream_mma.hip", "svid.hip"]
 # the look-up-table kernels of decode.hip and stream.hip give bit-identical
 # results only if neither contracts a multiply and an add into one fma
-# the matrix-core list kernels keep their accumulators in ordinary VGPRs (in
-# AGPRs the compiler moves them back and forth on every iteration)
+# the matrix-core kernels of these files keep their accumulators in ordinary
+# VGPRs (in AGPRs the compiler moves them back and forth on every iteration)
+_VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 EXTRA_FLAGS = {"decode.hip": ["-ffp-contract=off"], "stream.hip": ["-ffp-contract=off"],
-               "stream_mma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+               "stream_mma.hip": _VGPR_MFMA, "decode_mma.hip": _VGPR_MFMA, "backward.hip": _VGPR_MFMA}
 ARCH = os.environ.get("LB_OFFLOAD_ARCH", "gfx950")
 
 
