@@ -31,6 +31,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP64_TFLOPS = 78.6
 
 
 def log(*a):
@@ -401,6 +402,74 @@ def ingest_pmc(fetch_csv, write_csv, copy_mib, workload_key, commands):
     print(json.dumps(d[workload_key], indent=1))
 
 
+LIST_SOURCES = ["paper_2506_13771_amd/csrc/stream.hip", "paper_2506_13771_amd/csrc/stream_mma.hip",
+                "paper_2506_13771_amd/csrc/stream_plan.h", "paper_2506_13771_amd/csrc/lut_common.h",
+                "paper_2506_13771_amd/csrc/device_common.h", "paper_2506_13771_amd/csrc/lb_internal.h"]
+
+
+def sweep70b_alg_bytes(T):
+    """Algorithmic bytes of one 70B list sweep at T tokens (bf16 x, fp16 scales)."""
+    from paper_2506_13771_amd import synth
+    return sum(alg_bytes(T, d_in, d_out, RANKS_70B[(d_in, d_out)])[0] for _ in range(80)
+               for (_, d_in, d_out) in synth.LLAMA2_70B)
+
+
+def ingest_pmc_list(fetch_csv, write_csv, copy_mib, T, commands):
+    """HBM bytes of one lb_list_forward call of the 70B sweep at T tokens from two rocprofv3 --pmc
+    runs (FETCH_SIZE, then WRITE_SIZE) of `bench.py --sweep70b-tokens T --copy-probe MIB`: the list
+    kernels' counters summed per call (one stage-2 launch per call), scaled by the copy probe's
+    factor; beside the algorithmic bytes.  Writes profiles/traffic.json key list_llama2_70b_T<T>."""
+    n = float(int(copy_mib) << 20)
+    out = {"per_kernel": {}}
+    for name, path in (("fetch", fetch_csv), ("write", write_csv)):
+        counter = "FETCH_SIZE" if name == "fetch" else "WRITE_SIZE"
+        rows = _pmc_rows(path, counter)
+        lst = [(k, v) for k, v in rows if "stream_" in k or "sm_" in k]
+        calls = sum(1 for k, _ in lst if "stream_s2_kernel" in k or "sm_s2_kernel" in k)
+        cop = sorted((v for k, v in rows if "copyBuffer" in k), reverse=True)[:5]
+        if not lst or not calls or not cop:
+            raise SystemExit(f"{path}: no {counter} rows for the list kernels or the copy probe")
+        factor = n / (float(np.median(cop)) * 1024.0)
+        per_call = sum(v for _, v in lst) * 1024.0 * factor / calls
+        for k, v in lst:
+            short = k.replace("void lb::(anonymous namespace)::", "").replace("lb::(anonymous namespace)::", "")
+            short = short.split("(")[0]
+            d = out["per_kernel"].setdefault(short, {})
+            d[name + "_bytes_per_call"] = d.get(name + "_bytes_per_call", 0.0) + v * 1024.0 * factor / calls
+        out[name] = {"calls": calls, "factor": factor, "bytes_per_call": per_call}
+    alg = sweep70b_alg_bytes(T)
+    total = out["fetch"]["bytes_per_call"] + out["write"]["bytes_per_call"]
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    d = json.load(open(path)) if os.path.exists(path) else {}
+    d[f"list_llama2_70b_T{T}"] = {"bytes_per_call": total, "alg_bytes_per_call": alg, "ratio": total / alg,
+                                   "fetch": out["fetch"], "write": out["write"], "per_kernel": out["per_kernel"],
+                                   "sources": LIST_SOURCES, "source_digest": source_digest(LIST_SOURCES),
+                                   "commands": commands}
+    with open(path, "w") as fh:
+        json.dump(d, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(d[f"list_llama2_70b_T{T}"], indent=1))
+
+
+def summarize_pmc(paths, name_filter):
+    """Per-kernel means of every counter in rocprofv3 --pmc counter_collection.csv files (kernels
+    whose name contains name_filter), one line per kernel."""
+    import csv
+    import collections
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for path in paths:
+        with open(path, newline="") as fh:
+            for row in csv.DictReader(fh):
+                k = row.get("Kernel_Name", "")
+                if name_filter in k:
+                    vals[k][row["Counter_Name"]].append(float(row["Counter_Value"]))
+    for k, cs in sorted(vals.items()):
+        short = k.replace("void lb::(anonymous namespace)::", "").replace("lb::(anonymous namespace)::", "")
+        short = short.split("(")[0]
+        n = max(len(v) for v in cs.values())
+        print(f"{short} dispatches={n} " + " ".join(f"{c}={np.mean(v):.4g}" for c, v in sorted(cs.items())))
+
+
 def measured_traffic(workload_key):
     """HBM bytes per launch from committed rocprofv3 counter runs, or None if the kernel
     source changed since they were taken."""
@@ -485,7 +554,7 @@ def cpu_baseline(li, seconds):
 # ----------------------------------------------------------------------------
 # sweep of the other configurations (diagnostic lines written to a file)
 # ----------------------------------------------------------------------------
-def run_sweep(path, steps, warmup, only=("7b", "13b", "kv", "train", "70b")):
+def run_sweep(path, steps, warmup, only=("7b", "13b", "kv", "train", "70b", "svid")):
     import torch
     from paper_2506_13771_amd import synth
     out = open(path, "w")
@@ -561,6 +630,9 @@ def run_sweep(path, steps, warmup, only=("7b", "13b", "kv", "train", "70b")):
               "backward_tflops": fl / (ms_b * 1e-3) / 1e12,
               "backward_mfma_frac": fl / (ms_b * 1e-3) / 1e12 / PEAK_BF16_TFLOPS})
         del L, B
+    if "svid" in only:
+        for rec in run_svid(((4096, 4096), (11008, 4096), (4096, 11008)))["per_shape"]:
+            emit({"config": "llama2-7b-dual-svid", **rec})
     # 70B sweep: 80 layers x 7 linears resident, back-to-back on one stream
     ranks_70b = {(8192, 8192): 176, (8192, 1024): 16, (8192, 28672): 288, (28672, 8192): 288}
     for T in ((1, 8, 64) if "70b" in only else ()):
@@ -734,6 +806,51 @@ def run_sweep70b(ts, steps, warmup):
     return out
 
 
+def svid_gemm_flops(m, n, r, b, iters):
+    """Flops of the fp64 matrix-core products of one lb_dual_svid call (both paths): per path the
+    2 iters + 2 multiplications by W or W^T, the Gram matrices and basis changes of 2 iters + 1
+    orthonormalisations, the Rayleigh-Ritz products, the rank-1 Gram matrices; W_res once."""
+    mul = (2 * iters + 2) * 2.0 * m * n * b
+    orth = iters * (4.0 * m * b * b + 4.0 * n * b * b) + 4.0 * m * b * b
+    rr = 2.0 * n * b * b + 2.0 * m * b * r + 2.0 * n * b * r
+    rank1 = 2.0 * (m + n) * r * r + 2.0 * (m + n) * r
+    return 2 * (mul + orth + rr + rank1) + 2.0 * m * n * r
+
+
+def run_svid(shapes=((4096, 4096), ), reps=3):
+    """Dual-SVID conversion (lb_dual_svid) of dense Llama2-7B-shaped weights at 0.1 BPW: ms per
+    conversion (both paths, default block and rounds) and the rate of its fp64 matrix-core
+    products against the fp64 peak (78.6 TFLOP/s)."""
+    import torch
+    import paper_2506_13771_amd as lb
+    from paper_2506_13771_amd import synth
+    out = {"workload": "Dual-SVID of a dense weight (synthetic: rank-2r part with linearly falling scales plus "
+                       "N(0, 0.05^2) noise), both paths, default block and rounds", "per_shape": []}
+    for d_out, d_in in shapes:
+        r = lb.lb_rank_for_bpw(d_in, d_out, 0.1)
+        over, iters = lb.svid_defaults(r, d_out, d_in)
+        W = torch.from_numpy(synth.dense_weight(d_out, d_in, 2 * r, 0.05, cfg=73)).cuda()
+        ws = torch.empty(lb.lb_dual_svid_workspace_bytes(d_out, d_in, r, over), dtype=torch.uint8, device="cuda")
+        lb.lb_dual_svid(W, r, workspace=ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            lb.lb_dual_svid(W, r, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        b = min(r + over, d_out, d_in)
+        f = svid_gemm_flops(d_out, d_in, r, b, iters)
+        out["per_shape"].append({"d_out": d_out, "d_in": d_in, "r": r, "block": b, "iters": iters,
+                                 "ms_per_conversion": ms, "gemm_flops": f, "gemm_tflops": f / (ms * 1e-3) / 1e12,
+                                 "fp64_peak_frac": f / (ms * 1e-3) / 1e12 / PEAK_FP64_TFLOPS})
+        log(f"svid {d_out}x{d_in} r={r}: {ms:.1f} ms per conversion")
+        del W, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def run_block7b(ts, steps, warmup, bpw=0.1):
     """The 7 linears of one Llama2-7B block (q,k,v,o 4096x4096; gate, up 4096->11008; down
     11008->4096) in one lb_linear_forward_many call (weights warm: one block is about 2 MB)."""
@@ -783,10 +900,11 @@ def main():
     ap.add_argument("--no-sweep70b", action="store_true", help="skip the 70B 560-linear list sweep")
     ap.add_argument("--sweep70b-tokens", default="1,8,64", help="token counts of the 70B list sweep")
     ap.add_argument("--no-block7b", action="store_true", help="skip the 7B block list timing")
+    ap.add_argument("--no-svid", action="store_true", help="skip the Dual-SVID conversion timing")
     ap.add_argument("--sweep", default=None, help="write per-configuration JSON lines to this file")
-    ap.add_argument("--sweep-only", default="7b,13b,kv,train,70b",
+    ap.add_argument("--sweep-only", default="7b,13b,kv,train,70b,svid",
                     help="comma list of the sweep's parts to run (7b block, 13b prefill, 7b latent K/V cache, "
-                         "7b training-step backward, 70b decode sweep)")
+                         "7b training-step backward, 70b decode sweep, 7b Dual-SVID conversions)")
     ap.add_argument("--no-warm", action="store_true",
                     help="skip the warm-cache measurements (counter runs: every decode dispatch is then a "
                          "cold-rotation one)")
@@ -795,6 +913,11 @@ def main():
     ap.add_argument("--ingest-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"), default=None,
                     help="no GPU: turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
                          "WRITE_SIZE) of runs with --copy-probe into profiles/traffic.json")
+    ap.add_argument("--ingest-pmc-list", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "T"), default=None,
+                    help="no GPU: the same for the list kernels of a --sweep70b-tokens T run")
+    ap.add_argument("--summarize-pmc", nargs="+", metavar="CSV", default=None,
+                    help="no GPU: per-kernel means of the counters in rocprofv3 --pmc CSV files")
+    ap.add_argument("--pmc-kernel", default="", help="with --summarize-pmc: kernel name filter")
     ap.add_argument("--pmc-command", action="append", default=[],
                     help="with --ingest-pmc: the command lines that produced the files (recorded)")
     args = ap.parse_args()
@@ -802,6 +925,13 @@ def main():
     if args.ingest_pmc:
         ingest_pmc(args.ingest_pmc[0], args.ingest_pmc[1], args.copy_probe or 64,
                    "decode_q_proj_4096_r80_T1", args.pmc_command)
+        return
+    if args.ingest_pmc_list:
+        ingest_pmc_list(args.ingest_pmc_list[0], args.ingest_pmc_list[1], args.copy_probe or 64,
+                        int(args.ingest_pmc_list[2]), args.pmc_command)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc, args.pmc_kernel)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -881,6 +1011,8 @@ def main():
         rec["sweep70b"] = run_sweep70b(ts, args.steps, args.warmup)
     if not args.no_block7b:
         rec["block7b"] = run_block7b((1, 16, 64), args.steps, args.warmup)
+    if not args.no_svid:
+        rec["svid7b"] = run_svid()
     rec["paper_context"] = PAPER_CONTEXT
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(li, args.cpu_seconds)
