@@ -79,8 +79,8 @@ typedef enum lb_kernel {
                                  PREFILL otherwise (each where its size limits allow) */
   LB_KERNEL_DECODE = 1,       /* single launch, 4-bit look-up tables, fp32 sign-flip accumulation;
                                  T <= 4, r <= 1024 */
-  LB_KERNEL_PREFILL = 2,      /* three launches of matrix-core (MFMA) tiles (latent sums of exact
-                                 bf16 term products, latent scale and term split, outputs);
+  LB_KERNEL_PREFILL = 2,      /* three launches of matrix-core (MFMA) tiles with exact bf16 term
+                                 products (latent sums, latent scale and term split, outputs);
                                  any size within 32-bit buffer offsets */
   LB_KERNEL_DECODE_MFMA = 3   /* single launch, matrix-core contractions: stage 1 multiplies exact
                                  bf16 terms of x by the signs carried on exact bf16 terms of g,
@@ -174,12 +174,9 @@ int64_t lb_decode_max_tokens(void);
    BF16).  Accumulation is fp32.  The look-up-table decode kernel uses exact
    fp32 products; the matrix-core kernels multiply exact bf16 terms (the
    stored x and g cut into 1, 2 or 3 terms, the V sign carried on the g
-   terms), then the +-1 U signs times l (.) z: for fp32 outputs cut into three
-   bf16 terms (the full fp32 significand); for bf16/f16 outputs cut into two
-   terms (16 significant bits) by the single-launch matrix-core kernel and
-   rounded to one bf16 term by the prefill kernels (relative error at most
-   2^-9, the size of the output's own rounding).  If d_in == 0 or r == 0, y is
-   zero-filled.
+   terms; then the +-1 U signs times l (.) z cut into two bf16 terms, 16
+   significant bits, for bf16/f16 outputs, or three, the full fp32
+   significand, for fp32 outputs).  If d_in == 0 or r == 0, y is zero-filled.
    workspace: >= lb_forward_workspace_bytes(T, d_in, d_out, r) bytes. */
 lb_status lb_linear_forward(const void* x, lb_dtype act_dtype, int64_t T, int64_t d_in, int64_t d_out,
                             int64_t r, const lb_path* paths, lb_dtype scale_dtype, void* y,
@@ -266,9 +263,9 @@ lb_status lb_linear_forward_many(const lb_linear_desc* descs, int64_t n, void* w
        lb_linear_forward_kernel(..., LB_KERNEL_DECODE) for that linear.
      - Lists with a linear of 3 <= T <= 64 tokens run on the matrix-core
        kernels (every linear of the list): g and x enter as exact bf16 terms,
-       products are exact and sums fp32, w enters stage 2 rounded to bf16
-       (as 3 exact bf16 terms for fp32 activations); results meet the
-       tolerance of lb_linear_forward, and repeated calls give the same bits.
+       products are exact and sums fp32, w enters stage 2 as 2 bf16 terms
+       (3 for fp32 activations); results meet the tolerance of
+       lb_linear_forward, and repeated calls give the same bits.
 
    Scope: every linear with work has r <= 1024 and the list shares one
    activation and one scale dtype; for the look-up-table kernels a d_in whose
@@ -329,9 +326,8 @@ lb_status lb_linear_latent(const void* x, lb_dtype act_dtype, int64_t T, int64_t
    w [T x 2 x r] (latent_dtype) as lb_linear_latent writes it, y [T x d_out]
    in out_dtype (F32, F16 or BF16), rounded once from the fp32 sum of both
    paths.  Only U and h of the paths are read (V, g and l may be NULL).  One
-   pass cuts w into bf16 terms (one, rounded to nearest, for 16-bit outputs;
-   three for fp32 ones, as the prefill kernels do), then stage 2 of the
-   prefill kernels.  r == 0
+   pass cuts w into bf16 terms (two for 16-bit outputs, three for fp32 ones,
+   as lb_linear_forward does), then stage 2 of the prefill kernels.  r == 0
    zero-fills y.  y must not overlap w (LB_ERR_ARG).  workspace: 256-byte
    aligned, >= lb_from_latent_workspace_bytes(T, r) bytes (no zero-fill
    needed). */
@@ -378,7 +374,7 @@ size_t lb_backward_workspace_bytes(int64_t T, int64_t d_in, int64_t d_out, int64
    paths: V (packed with LB_ROLE_V, as for the forward), h, g and l are read;
    U may be NULL.  train[2]: the latent factors, their signs packed in the
    other orientation, and the gradient outputs.  The binary contractions run
-   on the prefill kernels (as in lb_linear_forward, fp32 accumulation); the
+   on the prefill kernels (exact bf16 term products, fp32 accumulation); the
    two contractions over tokens run on the matrix cores with exact bf16 terms
    (three for w and dz) and fp32 accumulation.  Any size may be 0 (the
    non-empty gradients are then zero).  dx must not overlap x or dy

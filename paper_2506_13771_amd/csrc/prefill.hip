@@ -7,13 +7,12 @@
 //   P1b: w_p[t][k] = l_p[k] z_p[t][k], cut into bf16 terms
 //   P2:  y[t][i]   = sum_p h_p[i] sum_k s(U_p)[i][k] w_p[t][k]    (M = outputs, N = tokens, K = r)
 //
-// Every product of P1 is exact: its A operand is the sign of V_p XORed into
+// Every product is exact: the A operand of P1 is the sign of V_p XORed into
 // the sign bits of exact bf16 terms of g_p (1 term for bf16, 2 for f16, 3 for
 // fp32 scales), its B operand the exact bf16 terms of x (1, 2 or 3 by the
-// activation dtype).  P2 multiplies exact +-1 signs by w cut into NW bf16
-// terms: for fp32 outputs 3 (all 24 significant bits); for bf16/f16 outputs 1,
-// w rounded to nearest bf16 (relative error at most 2^-9, the size of the
-// output's own rounding).  The matrix cores accumulate in fp32.
+// activation dtype); P2 multiplies exact +-1 signs by w cut into NW bf16 terms
+// (2 for bf16/f16 outputs: 16 significant bits; 3 for fp32 outputs: all 24).
+// The matrix cores accumulate in fp32.
 //
 // P1.  A workgroup of 8 waves owns 64 tokens, a range of d_in (split over
 // `ks` workgroups, about 256 in all) and a tile of latents.  Waves 0-1 take
@@ -465,7 +464,7 @@ __device__ __forceinline__ void store_wterm(const PrefillParams& P, const PairIt
 
 template <int ACT, int SC>
 __global__ void __launch_bounds__(kThreads) prefill_p1b(PrefillParams P) {
-  constexpr int NW = ACT == kDtF32 ? 3 : 1;
+  constexpr int NW = ACT == kDtF32 ? 3 : 2;
   PairItem it;
   if (!pair_item(P, it)) return;
   float w0[4], w1[4];
@@ -517,7 +516,7 @@ __global__ void __launch_bounds__(kThreads) prefill_sums2(PrefillParams Q0, Pref
 
 template <int ACT, int LD, int SC = -1>
 __global__ void __launch_bounds__(kThreads) prefill_latent_in(PrefillParams P) {
-  constexpr int NW = ACT == kDtF32 ? 3 : 1;
+  constexpr int NW = ACT == kDtF32 ? 3 : 2;
   PairItem it;
   if (!pair_item(P, it)) return;
   const int r = P.r;
@@ -591,7 +590,7 @@ __device__ __forceinline__ u32x4 sign_ones(uint32_t word, int gq, uint32_t M, ui
 // per unit through registers and y element by element
 template <int ACT, int SC, bool FAST>
 __global__ void __launch_bounds__(kThreads2, 1) prefill_p2(PrefillParams P) {
-  constexpr int NW = ACT == kDtF32 ? 3 : 1;
+  constexpr int NW = ACT == kDtF32 ? 3 : 2;
   constexpr int ES = SC == kDtF32 ? 4 : 2;
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -1023,7 +1022,7 @@ int p2_wdp(const PrefillGeom& g, bool fast) {
 void plan_lds(PrefillGeom& g, int act, int sc, bool vw, bool fast) {
   const int G = sc == kDtF32 ? 3 : (sc == kDtF16 ? 2 : 1);
   g.smem1 = p1_lds(g.kb_per, G, act, g.ms, vw);
-  const int nw = act == kDtF32 ? 3 : 1;
+  const int nw = act == kDtF32 ? 3 : 2;
   // U-word slots: 16-byte loads fill 4 blocks at a time, so each path's run
   // of slots is a multiple of 4 (FAST)
   const int nkb4 = fast ? (g.nkb + 3) / 4 * 4 : g.nkb;
@@ -1145,7 +1144,7 @@ PrefillParams prefill_params(const ForwardArgs& a, PrefillGeom& g) {
   P.g_bytes = static_cast<uint32_t>(a.d_in * es);
   P.h_bytes = static_cast<uint32_t>(a.d_out * es);
   P.l_bytes = static_cast<uint32_t>(a.r * es);
-  const int nw = a.act_dt == kDtF32 ? 3 : 1;
+  const int nw = a.act_dt == kDtF32 ? 3 : 2;
   P.wt_bytes = static_cast<uint32_t>(static_cast<int64_t>(2) * nw * g.nkb * a.T * 64);
   P.wd_off = static_cast<uint32_t>(p2_w_bytes(g.res ? 2 * g.nkb : g.kbc, nw));
   return P;

@@ -18,9 +18,8 @@
 //       once (one launch per token tile count).
 // Operands as in the single-launch matrix-core kernel: g and x are cut into
 // exact bf16 terms (1, 2 or 3 per value for bf16, f16, fp32), so every product
-// of stage 1 is exact and the sums are fp32; w enters stage 2 as 3 bf16 terms
-// for fp32 outputs (all 24 significant bits), else as one bf16 term rounded to
-// nearest (relative error at most 2^-9, the size of the output's rounding).
+// is exact and the sums are fp32; w is cut into 2 bf16 terms (3 for fp32
+// outputs), which carries 16 (24) significant bits into stage 2.
 //
 // Inputs of this path: x and g read as aligned groups of four (d_in a
 // multiple of 4, x and g aligned to four elements).
@@ -247,13 +246,13 @@ __global__ void __launch_bounds__(kThreads) sm_s1_kernel(const uint32_t* __restr
 
 // ---------------------------------------------------------------------------
 // R: w = l (.) z, the runs' partial sums in ascending run order, written as NW
-// bf16 terms (nw_of) straight into the matrix-core B fragments of stage 2: for path
+// bf16 terms straight into the matrix-core B fragments of stage 2: for path
 // p, token tile tt, 32-latent block kb and term a, one u32x4 per lane, lane
 // (n16, gq) register v holding the term of w at token 16 tt + n16 and latents
 // 32 kb + 4 gq + v (low half) and + 16 (high half); tokens past T and latents
 // past r are zero
 // ---------------------------------------------------------------------------
-__host__ __device__ constexpr int nw_of(int act) { return act == kDtF32 ? 3 : 1; }
+__host__ __device__ constexpr int nw_of(int act) { return act == kDtF32 ? 3 : 2; }
 
 __host__ __device__ inline size_t frag_bytes(int T, int r, int nw) {
   return static_cast<size_t>(2) * ((T + 15) / 16) * nblocks32(r) * nw * 1024;
