@@ -44,6 +44,9 @@ constexpr int kEigThreads = 1024;
 constexpr int kMaxBlock = 1024;     // largest eigenproblem: one workgroup, one pair per thread
 constexpr int kEigLdsMax = 128;     // b <= 128: the matrix stays in LDS during the sweeps
 constexpr int kEigMaxSweeps = 80;
+constexpr int kApplyCols = 8;       // rotation replay: columns of the accumulated rotations per workgroup
+constexpr int kApplyThreads = 256;
+constexpr int kRotBatch = 16;       // rotation replay: steps whose coefficients are staged in LDS at once
 constexpr double kDropRel = 1e-14;  // orthonormalisation: dropped Gram eigenvalues, relative to the largest
 
 __device__ __forceinline__ double load_op(const void* p, int64_t idx, int dt) {
@@ -165,12 +168,15 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs g, const doub
 // (even) indices: every pair meets once in n2 - 1 steps, each step's pairs are
 // disjoint.
 __device__ __forceinline__ void rr_pair(int n2, int s, int k, int& p, int& q) {
+  const int m = n2 - 1;  // 0 <= s < m, 0 <= k < n2 / 2: one subtraction reduces modulo m
   if (k == 0) {
-    p = n2 - 1;
+    p = m;
     q = s;
   } else {
-    p = (s + k) % (n2 - 1);
-    q = (s - k + n2 - 1) % (n2 - 1);
+    p = s + k;
+    if (p >= m) p -= m;
+    q = s - k + m;
+    if (q >= m) q -= m;
   }
   if (p > q) {
     const int t = p;
@@ -286,23 +292,199 @@ __global__ __launch_bounds__(kEigThreads) void jacobi_eig_kernel(double* A, doub
   }
 }
 
+// The same Jacobi iteration for b <= kEigLdsMax in two kernels, so that the
+// accumulated rotations never need global memory inside the iteration:
+// jacobi_log_kernel (one workgroup, the matrix in LDS) writes the eigenvalues
+// (unsorted) to lraw, the number of sweeps to nsw and every step's rotations
+// to rlog [sweep][step][pair] as (c, s) ((1, 0) for a pair not rotated);
+// rot_apply_kernel then replays them on column slabs of the accumulated
+// rotation matrix (its columns are independent under row rotations) and
+// writes the outputs of jacobi_eig_kernel.
+__global__ __launch_bounds__(kEigThreads) void jacobi_log_kernel(const double* A, double* lraw, int* nsw, double2* rlog,
+                                                                 int b) {
+  extern __shared__ double eig_smem[];
+  __shared__ int pp[kEigLdsMax / 2], pq[kEigLdsMax / 2], pa[kEigLdsMax / 2];
+  __shared__ double pc[kEigLdsMax / 2], ps[kEigLdsMax / 2];
+  __shared__ int rot;
+  __shared__ double floor_abs;
+  const int tid = threadIdx.x;
+  const int n2 = b + (b & 1), np = n2 / 2;
+  double* M = eig_smem;
+  for (int e = tid; e < b * b; e += kEigThreads) M[e] = A[e];
+  if (tid == 0) {
+    double mx = 0.0;
+    for (int i = 0; i < b; ++i) mx = fmax(mx, fabs(A[static_cast<int64_t>(i) * b + i]));
+    floor_abs = 1e-17 * mx;
+  }
+  __syncthreads();
+  int sweeps = kEigMaxSweeps;
+  for (int sweep = 0; sweep < kEigMaxSweeps; ++sweep) {
+    if (tid == 0) rot = 0;
+    __syncthreads();
+    for (int s = 0; s < n2 - 1; ++s) {
+      if (tid < np) {
+        int p, q;
+        rr_pair(n2, s, tid, p, q);
+        double c = 1.0, sn = 0.0;
+        bool act = false;
+        if (q < b) {
+          const double app = M[p * b + p], aqq = M[q * b + q], apq = M[p * b + q];
+          if (apq != 0.0 && fabs(apq) > 1e-15 * sqrt(fabs(app * aqq)) && fabs(apq) > floor_abs) {
+            const double zeta = (aqq - app) / (2.0 * apq);
+            const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+            c = 1.0 / sqrt(1.0 + t * t);
+            sn = c * t;
+            act = true;
+          }
+        }
+        pp[tid] = p;
+        pq[tid] = q;
+        pa[tid] = act ? 1 : 0;
+        pc[tid] = c;
+        ps[tid] = sn;
+        rlog[(static_cast<int64_t>(sweep) * (n2 - 1) + s) * np + tid] = make_double2(c, sn);
+        if (act) atomicAdd(&rot, 1);
+      }
+      __syncthreads();
+      // A <- J^T A J one 2 x 2 block at a time (rows of pair kr, columns of
+      // pair kc): thread t takes row pair t / 16 and column pairs t % 16 + 16 j
+      {
+        const int kr = tid >> 4;
+        if (kr < np) {
+          const int p = pp[kr], q = pq[kr];
+          const bool ar = pa[kr] != 0, qv = q < b;
+          const double cr = pc[kr], sr = ps[kr];
+          for (int kc = tid & 15; kc < np; kc += 16) {
+            if (!ar && !pa[kc]) continue;
+            const int u = pp[kc], v = pq[kc];
+            const bool vv = v < b;
+            const double cc = pc[kc], sc = ps[kc];
+            const double a00 = M[p * b + u], a01 = vv ? M[p * b + v] : 0.0;
+            const double a10 = qv ? M[q * b + u] : 0.0, a11 = (qv && vv) ? M[q * b + v] : 0.0;
+            const double b00 = cr * a00 - sr * a10, b01 = cr * a01 - sr * a11;
+            const double b10 = sr * a00 + cr * a10, b11 = sr * a01 + cr * a11;
+            const double d00 = cc * b00 - sc * b01, d01 = sc * b00 + cc * b01;
+            const double d10 = cc * b10 - sc * b11, d11 = sc * b10 + cc * b11;
+            M[p * b + u] = d00;
+            if (vv) M[p * b + v] = d01;
+            if (qv) M[q * b + u] = d10;
+            if (qv && vv) M[q * b + v] = d11;
+          }
+        }
+      }
+      __syncthreads();
+    }
+    if (rot == 0) {
+      sweeps = sweep;  // a sweep that rotated nothing need not be replayed
+      break;
+    }
+    __syncthreads();
+  }
+  for (int i = tid; i < b; i += kEigThreads) lraw[i] = M[i * b + i];
+  if (tid == 0) *nsw = sweeps;
+}
+
+// Replay of jacobi_log_kernel's rotations on columns [kApplyCols * blockIdx.x,
+// + kApplyCols) of the accumulated rotation matrix (identity at the start;
+// row i is eigenvector i), then the outputs: eigenvalues descending (index
+// order on ties) to lam, eigenvectors to the columns of E, scaled as in
+// jacobi_eig_kernel for mode 1.
+__global__ __launch_bounds__(kApplyThreads) void rot_apply_kernel(const double2* __restrict__ rlog,
+                                                                  const int* __restrict__ nsw,
+                                                                  const double* __restrict__ lraw, double* E,
+                                                                  double* lam, int b, int mode) {
+  extern __shared__ double ap_smem[];
+  constexpr int C = kApplyCols;
+  const int tid = threadIdx.x;
+  const int n2 = b + (b & 1), np = n2 / 2, nst = n2 - 1;
+  const int j0 = blockIdx.x * C;
+  double* Ec = ap_smem;                                             // [b][C]
+  double2* cs = reinterpret_cast<double2*>(ap_smem + b * C);        // [2][kRotBatch * np]
+  const int per = kRotBatch * np;
+  constexpr int kPer = (kRotBatch * (kEigLdsMax / 2) + kApplyThreads - 1) / kApplyThreads;
+  for (int e = tid; e < b * C; e += kApplyThreads) Ec[e] = (e / C == j0 + e % C) ? 1.0 : 0.0;
+  const int total = *nsw * nst;
+  const int nbatch = (total + kRotBatch - 1) / kRotBatch;
+  // coefficients of batch bb: rlog entries [bb * per, (bb + 1) * per) (steps past the log: identity)
+  auto fetch = [&](int bb, int e) {
+    const int64_t g = static_cast<int64_t>(bb) * per + e;
+    return bb * kRotBatch + e / np < total ? rlog[g] : make_double2(1.0, 0.0);
+  };
+  for (int e = tid; e < per; e += kApplyThreads) cs[e] = fetch(0, e);
+  __syncthreads();
+  for (int bb = 0; bb < nbatch; ++bb) {
+    double2 nxt[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + kApplyThreads * u;
+      nxt[u] = (e < per && bb + 1 < nbatch) ? fetch(bb + 1, e) : make_double2(1.0, 0.0);
+    }
+    const double2* cur = cs + (bb & 1) * per;
+    for (int st = 0; st < kRotBatch; ++st) {
+      const int gs = bb * kRotBatch + st;
+      if (gs >= total) break;
+      const int s = gs % nst;
+      for (int e = tid; e < np * C; e += kApplyThreads) {
+        const int k = e / C, jj = e - k * C;
+        int p, q;
+        rr_pair(n2, s, k, p, q);
+        if (q < b) {
+          const double2 r = cur[st * np + k];
+          const double ep = Ec[p * C + jj], eq = Ec[q * C + jj];
+          Ec[p * C + jj] = r.x * ep - r.y * eq;
+          Ec[q * C + jj] = r.y * ep + r.x * eq;
+        }
+      }
+      __syncthreads();
+    }
+    double2* other = cs + ((bb + 1) & 1) * per;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + kApplyThreads * u;
+      if (e < per) other[e] = nxt[u];
+    }
+    __syncthreads();
+  }
+  double lmax = 0.0;
+  for (int i = 0; i < b; ++i) lmax = fmax(lmax, lraw[i]);
+  for (int i = tid; i < b; i += kApplyThreads) {
+    const double li = lraw[i];
+    int rank = 0;
+    for (int j = 0; j < b; ++j) {
+      const double lj = lraw[j];
+      rank += (lj > li || (lj == li && j < i)) ? 1 : 0;
+    }
+    if (blockIdx.x == 0) lam[rank] = li;
+    double f = 1.0;
+    if (mode == 1) f = (li > 0.0 && li > kDropRel * lmax) ? 1.0 / sqrt(li) : 0.0;
+    for (int jj = 0; jj < C && j0 + jj < b; ++jj) E[static_cast<int64_t>(j0 + jj) * b + rank] = f * Ec[i * C + jj];
+  }
+}
+
 // Orthonormalisation by Cholesky (CholQR): for the Gram matrix G = Y^T Y
 // [b x b], G = L L^T (lower, in place in G's lower triangle), then T = L^-T
 // (upper) into T, so that Q = Y T has orthonormal columns.  A pivot <= 1e-13
 // of the largest diagonal entry is dropped (that column of L and of L^-1 is
 // zero), so a rank-deficient block gives zero columns instead of a breakdown.
-// X [b x b] is scratch for L^-1, computed by right-looking forward
-// substitution.  One workgroup; G lives in LDS when b <= kEigLdsMax.
+// X = L^-1 (lower triangular) is computed by right-looking forward
+// substitution; its diagonal is 1 / L_kk.  One workgroup.  When b <=
+// kEigLdsMax everything stays in LDS: L in the lower triangle of one b x b
+// array and the strict lower part of X, flipped, in its upper triangle
+// (X[i][c] at [b-1-i][b-1-c], c < i, so that a row of X is contiguous); column
+// k of L is copied to a vector while it is scaled.  Else G and the scratch X
+// [b x b] are used in global memory.
 template <bool kLds>
 __global__ __launch_bounds__(kEigThreads) void chol_orth_kernel(double* G, double* X, double* T, int b) {
   extern __shared__ double chol_smem[];
   __shared__ double invs[kMaxBlock];
+  __shared__ double colk[kMaxBlock];
   __shared__ double thr;
   const int tid = threadIdx.x;
   double* L = kLds ? chol_smem : G;
   if (kLds)
     for (int e = tid; e < b * b; e += kEigThreads) L[e] = G[e];
-  for (int e = tid; e < b * b; e += kEigThreads) X[e] = (e / b == e % b) ? 1.0 : 0.0;
+  else
+    for (int e = tid; e < b * b; e += kEigThreads) X[e] = (e / b == e % b) ? 1.0 : 0.0;
   if (tid == 0) {
     double mx = 0.0;
     for (int i = 0; i < b; ++i) mx = fmax(mx, G[static_cast<int64_t>(i) * b + i]);
@@ -313,31 +495,62 @@ __global__ __launch_bounds__(kEigThreads) void chol_orth_kernel(double* G, doubl
     const double d = L[k * b + k];
     const double inv = d > thr ? 1.0 / sqrt(d) : 0.0;
     if (tid == 0) invs[k] = inv;
-    for (int i = k + 1 + tid; i < b; i += kEigThreads) L[i * b + k] *= inv;
+    for (int i = k + 1 + tid; i < b; i += kEigThreads) {
+      const double v = L[i * b + k] * inv;
+      L[i * b + k] = v;
+      colk[i] = v;
+    }
     __syncthreads();
-    const int w = b - k - 1;
-    for (int e = tid; e < w * w; e += kEigThreads) {
-      const int i = k + 1 + e / w, j = k + 1 + e % w;
-      if (j <= i) L[i * b + j] -= L[i * b + k] * L[j * b + k];
+    // trailing update of the lower triangle: rows k + 1 + tid / 32 + 32 n,
+    // columns k + 1 + tid % 32 + 32 n' <= row
+    for (int i = k + 1 + (tid >> 5); i < b; i += kEigThreads / 32) {
+      const double lik = colk[i];
+      for (int j = k + 1 + (tid & 31); j <= i; j += 32) L[i * b + j] -= lik * colk[j];
     }
     __syncthreads();
   }
-  // X = L^-1: row k = (row k of the updated right-hand side) / L_kk, then the
-  // rows below subtract L_ik times it (only columns c <= k are nonzero)
-  for (int k = 0; k < b; ++k) {
-    const double inv = invs[k];
-    for (int c = tid; c <= k; c += kEigThreads) X[static_cast<int64_t>(k) * b + c] *= inv;
+  if constexpr (kLds) {
+    const int b1 = b - 1;
+    // X's strict lower part (in the upper triangle) starts at 0
+    for (int e = tid; e < b * b; e += kEigThreads)
+      if (e % b > e / b) L[e] = 0.0;
+    for (int i = tid; i < b; i += kEigThreads) colk[i] = 0.0;
     __syncthreads();
-    const int w = b - k - 1;
-    for (int e = tid; e < w * (k + 1); e += kEigThreads) {
-      const int i = k + 1 + e / (k + 1), c = e % (k + 1);
-      X[static_cast<int64_t>(i) * b + c] -= L[i * b + k] * X[static_cast<int64_t>(k) * b + c];
+    // row k of X: X[k][c] = invs[k] * (updated right-hand side), c <= k (the
+    // diagonal is invs[k] itself); the rows below subtract L_ik times it
+    for (int k = 0; k < b; ++k) {
+      const double inv = invs[k];
+      double* xk = L + (b1 - k) * b + b1;  // X[k][c] at xk[-c]
+      for (int c = tid; c < k; c += kEigThreads) xk[-c] *= inv;
+      for (int i = k + 1 + tid; i < b; i += kEigThreads) colk[i] = L[i * b + k];
+      __syncthreads();
+      for (int i = k + 1 + (tid >> 5); i < b; i += kEigThreads / 32) {
+        const double lik = colk[i];
+        double* xi = L + (b1 - i) * b + b1;
+        for (int c = tid & 31; c <= k; c += 32) xi[-c] -= lik * (c < k ? xk[-c] : inv);
+      }
+      __syncthreads();
     }
-    __syncthreads();
-  }
-  for (int e = tid; e < b * b; e += kEigThreads) {
-    const int j = e / b, k = e % b;
-    T[e] = X[static_cast<int64_t>(k) * b + j];
+    for (int e = tid; e < b * b; e += kEigThreads) {
+      const int j = e / b, k = e % b;  // T[j][k] = X[k][j]
+      T[e] = j < k ? L[(b1 - k) * b + (b1 - j)] : (j == k ? invs[k] : 0.0);
+    }
+  } else {
+    for (int k = 0; k < b; ++k) {
+      const double inv = invs[k];
+      for (int c = tid; c <= k; c += kEigThreads) X[static_cast<int64_t>(k) * b + c] *= inv;
+      __syncthreads();
+      const int w = b - k - 1;
+      for (int e = tid; e < w * (k + 1); e += kEigThreads) {
+        const int i = k + 1 + e / (k + 1), c = e % (k + 1);
+        X[static_cast<int64_t>(i) * b + c] -= L[i * b + k] * X[static_cast<int64_t>(k) * b + c];
+      }
+      __syncthreads();
+    }
+    for (int e = tid; e < b * b; e += kEigThreads) {
+      const int j = e / b, k = e % b;
+      T[e] = X[static_cast<int64_t>(k) * b + j];
+    }
   }
 }
 
@@ -473,7 +686,7 @@ size_t a256(size_t b) { return (b + 255) / 256 * 256; }
 
 struct SvidLayout {
   int m, n, r, b;
-  size_t wres, y, q, z, z2, part, gram, e, et, lam, ud, vd, ul, vl, us, vs, u, h, g, lu, lv, l, total;
+  size_t wres, y, q, z, z2, part, gram, e, et, lam, lraw, nsw, rlog, ud, vd, ul, vl, us, vs, u, h, g, lu, lv, l, total;
   size_t part_elems;
 };
 
@@ -501,6 +714,16 @@ SvidLayout svid_layout(int m, int n, int r, int over) {
   L.e = take(b * b);
   L.et = take(b * b);
   L.lam = take(b);
+  L.lraw = take(b);
+  L.nsw = take(1);
+  {
+    // rotation log of the largest eigenproblem solved in LDS (b or r)
+    size_t bl = 0;
+    if (b <= static_cast<size_t>(kEigLdsMax)) bl = b;
+    if (static_cast<size_t>(r) <= static_cast<size_t>(kEigLdsMax) && static_cast<size_t>(r) > bl) bl = r;
+    const size_t n2 = bl + (bl & 1);
+    L.rlog = take(bl > 0 ? 2 * static_cast<size_t>(kEigMaxSweeps) * (n2 - 1) * (n2 / 2) : 0);
+  }
   L.ud = take(static_cast<size_t>(m) * r);
   L.vd = take(static_cast<size_t>(n) * r);
   L.ul = take(static_cast<size_t>(m) * r);
@@ -564,12 +787,20 @@ struct Svid {
     if (b <= kEigLdsMax) {
       const int smem = static_cast<int>(sizeof(double) * b * b);
       if (smem > 65536) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&jacobi_eig_kernel<true>),
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&jacobi_log_kernel),
                                                  hipFuncAttributeMaxDynamicSharedMemorySize, smem);
         if (e != hipSuccess) return e;
       }
-      hipLaunchKernelGGL((jacobi_eig_kernel<true>), dim3(1), dim3(kEigThreads), sizeof(double) * b * b, st, A,
-                         at(L.et), E, lam, b, mode);
+      double2* rl = reinterpret_cast<double2*>(at(L.rlog));
+      int* ns = reinterpret_cast<int*>(at(L.nsw));
+      hipLaunchKernelGGL(jacobi_log_kernel, dim3(1), dim3(kEigThreads), smem, st, static_cast<const double*>(A),
+                         at(L.lraw), ns, rl, b);
+      if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+      const int np = (b + (b & 1)) / 2;
+      const size_t smem2 = sizeof(double) * b * kApplyCols + sizeof(double2) * 2 * kRotBatch * np;
+      hipLaunchKernelGGL(rot_apply_kernel, dim3((b + kApplyCols - 1) / kApplyCols), dim3(kApplyThreads), smem2, st,
+                         static_cast<const double2*>(rl), static_cast<const int*>(ns),
+                         static_cast<const double*>(at(L.lraw)), E, lam, b, mode);
     } else {
       hipLaunchKernelGGL((jacobi_eig_kernel<false>), dim3(1), dim3(kEigThreads), 0, st, A, at(L.et), E, lam, b,
                          mode);

@@ -172,9 +172,10 @@ def test_noalloc_validation_errors(lib):
 
 def test_dual_svid_workspace_and_validation(lib):
     ws = lb.lb_dual_svid_workspace_bytes
-    # the residual weight (8 d_out d_in bytes) dominates at layer sizes
+    # the residual weight (8 d_out d_in bytes) dominates at layer sizes; the rest are the blocks,
+    # the split-K slabs and the eigensolver's rotation log (9 MB for a block of 120)
     assert ws(4096, 4096, 80, 40) >= 8 * 4096 * 4096
-    assert ws(4096, 4096, 80, 40) < 8 * 4096 * 4096 + (64 << 20)
+    assert ws(4096, 4096, 80, 40) < 8 * 4096 * 4096 + (80 << 20)
     assert ws(64, 32, 8, 4) > 0 and ws(64, 32, 32, 0) > 0
     for bad in ((0, 32, 8, 4), (64, 0, 8, 4), (64, 32, 0, 4), (64, 32, 33, 0), (64, 32, 8, -1),
                 (4096, 4096, 1000, 100), (1 << 20, 1 << 12, 8, 0)):
