@@ -380,7 +380,7 @@ def ingest_pmc(fetch_csv, write_csv, copy_mib, workload_key, commands):
     for name, path in (("fetch", fetch_csv), ("write", write_csv)):
         counter = "FETCH_SIZE" if name == "fetch" else "WRITE_SIZE"
         rows = _pmc_rows(path, counter)
-        dec = [v for k, v in rows if "decode_kernel" in k or "decode_fused_kernel" in k]
+        dec = [v for k, v in rows if "decode_kernel" in k]
         # the probe's five copies are the five largest copy-kernel dispatches of the run
         cop = sorted((v for k, v in rows if "copyBuffer" in k), reverse=True)[:5]
         if not dec or not cop:
