@@ -71,6 +71,7 @@ constexpr int kKc = 16;                 // latent columns per stage-1 tile
 constexpr int kKQ = 4;                  // stage 2: lanes per output row
 constexpr int kRows2 = kThreads / kKQ;  // stage 2: output rows per workgroup
 constexpr int kGather = 8;              // stage 2: slots a thread gathers per round
+constexpr int kOwnRuns = 4;             // stage 2: runs up to which each table builder loads its own slots
 constexpr int kDirectMaxSlots = kThreads * kGather;  // stage 2 reads every partial up to this many
 constexpr size_t kLds2Max = 64 * 1024;  // stage-2 LDS budget per token chunk (bytes)
 
@@ -221,7 +222,7 @@ __device__ __forceinline__ float quad_sum(float v) {
 
 // RB blocks of kRows2 output rows per workgroup (list launches take several:
 // the gathered partials and their tables serve every block)
-template <int TM, int ACT, int SC, int WPL, int RB>
+template <int TM, int ACT, int SC, int WPL, int RB, bool OWN = false>
 __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
   const int tid = threadIdx.x;
   const int kq = tid & (kKQ - 1);
@@ -272,8 +273,80 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
   const int ngrp = 8 * nw;
   const int bpt = tid / ngrp, bgrp = tid - bpt * ngrp, bstep = kThreads / ngrp;
 
+  // few enough builders for one pass, few runs: every builder thread loads
+  // the slots of its own 4 latents itself (no LDS round trip or barrier
+  // between the gather and the tables; the sums are the same)
+  // (decided on the host: own_builders; OWN = false keeps this path out of the code)
+  const bool own = OWN && P.direct && nsrc <= kOwnRuns && 2 * tch * ngrp <= kThreads;
+
   for (int t0 = 0; t0 < T; t0 += tch) {
     const int tn = min(tch, T - t0);
+    if (own) {
+      const bool bld = bpt < 2 * tn;
+      const int pp = bpt >= tn ? 1 : 0;
+      const int tl = bpt - pp * tn;
+      const uint64_t* src = P.partial + (static_cast<int64_t>(pp * T + t0 + tl) * nsrc) * r;  // [run][k]
+      const bool wave_bld = __builtin_amdgcn_readfirstlane(bpt) < 2 * tn;  // lane 0 builds if any lane does
+      uint64_t sv[kOwnRuns][4];
+      if (wave_bld) {
+        // every load issued at once (a slot this thread does not need reads
+        // the first slot of the buffer and is replaced below)
+#pragma unroll
+        for (int c = 0; c < kOwnRuns; ++c)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const bool need = bld && c < nsrc && 4 * bgrp + j < r;
+            sv[c][j] = get_slot(need ? src + c * r + 4 * bgrp + j : P.partial);
+          }
+      }
+      if (t0 == 0) {
+        pin(epoch);
+        tag = epoch + 1u;
+        // count this workgroup as one that has read the epoch (the returned
+        // count is used at the end)
+        if (tid == 0) done_before = atomic_add_relaxed(P.ctr, 1u);
+      }
+      if (wave_bld) {
+        // a slot not needed counts as ready with value +0 (a sum that starts
+        // at +0 is unchanged by adding +0)
+        const uint64_t none = static_cast<uint64_t>(tag) << 32;
+#pragma unroll
+        for (int c = 0; c < kOwnRuns; ++c)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (!(bld && c < nsrc && 4 * bgrp + j < r)) sv[c][j] = none;
+        for (uint32_t it = 0;; ++it) {
+          bool ready = true;
+#pragma unroll
+          for (int c = 0; c < kOwnRuns; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) ready = ready && slot_ready(sv[c][j], tag);
+          if (ready) break;
+          if (it >= kSpinLimit) {
+            ok = false;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int c = 0; c < kOwnRuns; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              if (!slot_ready(sv[c][j], tag)) sv[c][j] = get_slot(src + c * r + 4 * bgrp + j);
+        }
+        if (bld) {
+          // l (.) z of the 4 latents: their partials in ascending run order (a
+          // slot a timed-out wait never saw carrying this call's tag is NaN)
+          float w4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int c = 0; c < kOwnRuns; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) w4[j] += slot_ready(sv[c][j], tag) ? slot_value(sv[c][j]) : __builtin_nanf("");
+          build_table(tb2 + ((pp * tch + tl) * nw + (bgrp >> 3)) * kBlk + 16 * (bgrp & 7), bgrp & 7, w4[0], w4[1],
+                      w4[2], w4[3]);
+        }
+      }
+      __syncthreads();
+    } else {
     // zero the padding of the gathered rows (latents r .. R4 - 1)
     if (R4 != r) {
       for (int e = tid; e < 2 * tch * nsrc * (R4 - r); e += kThreads) {
@@ -347,6 +420,7 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
                   w4[2], w4[3]);
     }
     __syncthreads();
+    }
     // contraction of row i with both paths; lane kq covers words kq, kq + 4, ...
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
@@ -397,14 +471,14 @@ __device__ void stage2(const DecodeParams& P, int q2, float* smem) {
   }
 }
 
-template <int TM, int ACT, int SC, bool VEC, int WPL>
+template <int TM, int ACT, int SC, bool VEC, int WPL, bool OWN>
 __global__ void __launch_bounds__(kThreads, 2) decode_kernel(DecodeParams P) {
   extern __shared__ __attribute__((aligned(16))) float smem[];
   const int wg = blockIdx.x;
   if (wg < P.n_s1)
     stage1<TM, ACT, SC, VEC>(P, wg, smem);
   else
-    stage2<TM, ACT, SC, WPL, 1>(P, wg - P.n_s1, smem);
+    stage2<TM, ACT, SC, WPL, 1, OWN>(P, wg - P.n_s1, smem);
 }
 
 // A list of independent linears in one launch: the stage-1 workgroups of
@@ -466,6 +540,13 @@ __global__ void __launch_bounds__(kThreads) decode_batch_s1_kernel(DecodeBatch B
   stage1<TM, ACT, SC, VEC>(P, wg - (i ? B.s1_end[i - 1] : 0), smem);
 }
 
+// whether stage 2 of a single call takes the path in which each table
+// builder loads its own slots (the condition stage2 checks again)
+inline bool own_builders(const DecodeParams& P) {
+  const int nsrc = P.direct ? P.s1d : 1;
+  return P.direct && nsrc <= kOwnRuns && 2 * P.tch * 8 * nblocks32(P.r) <= kThreads;
+}
+
 // one launch of the single-linear (DecodeParams) or list (DecodeBatch) kernel
 template <int TM, int ACT, int SC, bool VEC, int WPL, typename A>
 hipError_t launch_one(const A& args, dim3 grid, size_t smem, hipStream_t stream) {
@@ -475,14 +556,25 @@ hipError_t launch_one(const A& args, dim3 grid, size_t smem, hipStream_t stream)
   // same shape make no attribute call
   static std::atomic<size_t> limit{65536};
   if (smem > limit.load()) {
-    const void* fn = kOne ? reinterpret_cast<const void*>(&decode_kernel<TM, ACT, SC, VEC, WPL>)
-                          : reinterpret_cast<const void*>(&decode_batch_kernel<TM, ACT, SC, VEC, WPL>);
-    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
+    hipError_t e = hipSuccess;
+    if constexpr (kOne) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_kernel<TM, ACT, SC, VEC, WPL, false>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
+      if (e == hipSuccess)
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_kernel<TM, ACT, SC, VEC, WPL, true>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
+    } else {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&decode_batch_kernel<TM, ACT, SC, VEC, WPL>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
+    }
     if (e != hipSuccess) return e;
     limit.store(smem);
   }
   if constexpr (kOne) {
-    hipLaunchKernelGGL((decode_kernel<TM, ACT, SC, VEC, WPL>), grid, dim3(kThreads), smem, stream, args);
+    if (own_builders(args))
+      hipLaunchKernelGGL((decode_kernel<TM, ACT, SC, VEC, WPL, true>), grid, dim3(kThreads), smem, stream, args);
+    else
+      hipLaunchKernelGGL((decode_kernel<TM, ACT, SC, VEC, WPL, false>), grid, dim3(kThreads), smem, stream, args);
   } else {
     const int s1 = args.s1_end[args.n - 1];
     if (s1 <= kSplitMinS1) {

@@ -41,6 +41,7 @@ constexpr int kDtF64 = 100;  // operand code of the internal fp64 arrays
 constexpr int kGT = 64;      // GEMM output tile (rows and columns)
 constexpr int kGK = 16;      // GEMM K per LDS stage
 constexpr int kEigThreads = 1024;
+constexpr int kCholThreads = 1024;  // CholQR: one workgroup (fewer threads were slower at b = 120)
 constexpr int kMaxBlock = 1024;     // largest eigenproblem: one workgroup, one pair per thread
 constexpr int kEigLdsMax = 128;     // b <= 128: the matrix stays in LDS during the sweeps
 constexpr int kEigMaxSweeps = 80;
@@ -474,7 +475,7 @@ __global__ __launch_bounds__(kApplyThreads) void rot_apply_kernel(const double2*
 // k of L is copied to a vector while it is scaled.  Else G and the scratch X
 // [b x b] are used in global memory.
 template <bool kLds>
-__global__ __launch_bounds__(kEigThreads) void chol_orth_kernel(double* G, double* X, double* T, int b) {
+__global__ __launch_bounds__(kCholThreads) void chol_orth_kernel(double* G, double* X, double* T, int b) {
   extern __shared__ double chol_smem[];
   __shared__ double invs[kMaxBlock];
   __shared__ double colk[kMaxBlock];
@@ -482,9 +483,9 @@ __global__ __launch_bounds__(kEigThreads) void chol_orth_kernel(double* G, doubl
   const int tid = threadIdx.x;
   double* L = kLds ? chol_smem : G;
   if (kLds)
-    for (int e = tid; e < b * b; e += kEigThreads) L[e] = G[e];
+    for (int e = tid; e < b * b; e += kCholThreads) L[e] = G[e];
   else
-    for (int e = tid; e < b * b; e += kEigThreads) X[e] = (e / b == e % b) ? 1.0 : 0.0;
+    for (int e = tid; e < b * b; e += kCholThreads) X[e] = (e / b == e % b) ? 1.0 : 0.0;
   if (tid == 0) {
     double mx = 0.0;
     for (int i = 0; i < b; ++i) mx = fmax(mx, G[static_cast<int64_t>(i) * b + i]);
@@ -495,7 +496,7 @@ __global__ __launch_bounds__(kEigThreads) void chol_orth_kernel(double* G, doubl
     const double d = L[k * b + k];
     const double inv = d > thr ? 1.0 / sqrt(d) : 0.0;
     if (tid == 0) invs[k] = inv;
-    for (int i = k + 1 + tid; i < b; i += kEigThreads) {
+    for (int i = k + 1 + tid; i < b; i += kCholThreads) {
       const double v = L[i * b + k] * inv;
       L[i * b + k] = v;
       colk[i] = v;
@@ -503,7 +504,7 @@ __global__ __launch_bounds__(kEigThreads) void chol_orth_kernel(double* G, doubl
     __syncthreads();
     // trailing update of the lower triangle: rows k + 1 + tid / 32 + 32 n,
     // columns k + 1 + tid % 32 + 32 n' <= row
-    for (int i = k + 1 + (tid >> 5); i < b; i += kEigThreads / 32) {
+    for (int i = k + 1 + (tid >> 5); i < b; i += kCholThreads / 32) {
       const double lik = colk[i];
       for (int j = k + 1 + (tid & 31); j <= i; j += 32) L[i * b + j] -= lik * colk[j];
     }
@@ -512,42 +513,42 @@ __global__ __launch_bounds__(kEigThreads) void chol_orth_kernel(double* G, doubl
   if constexpr (kLds) {
     const int b1 = b - 1;
     // X's strict lower part (in the upper triangle) starts at 0
-    for (int e = tid; e < b * b; e += kEigThreads)
+    for (int e = tid; e < b * b; e += kCholThreads)
       if (e % b > e / b) L[e] = 0.0;
-    for (int i = tid; i < b; i += kEigThreads) colk[i] = 0.0;
+    for (int i = tid; i < b; i += kCholThreads) colk[i] = 0.0;
     __syncthreads();
     // row k of X: X[k][c] = invs[k] * (updated right-hand side), c <= k (the
     // diagonal is invs[k] itself); the rows below subtract L_ik times it
     for (int k = 0; k < b; ++k) {
       const double inv = invs[k];
       double* xk = L + (b1 - k) * b + b1;  // X[k][c] at xk[-c]
-      for (int c = tid; c < k; c += kEigThreads) xk[-c] *= inv;
-      for (int i = k + 1 + tid; i < b; i += kEigThreads) colk[i] = L[i * b + k];
+      for (int c = tid; c < k; c += kCholThreads) xk[-c] *= inv;
+      for (int i = k + 1 + tid; i < b; i += kCholThreads) colk[i] = L[i * b + k];
       __syncthreads();
-      for (int i = k + 1 + (tid >> 5); i < b; i += kEigThreads / 32) {
+      for (int i = k + 1 + (tid >> 5); i < b; i += kCholThreads / 32) {
         const double lik = colk[i];
         double* xi = L + (b1 - i) * b + b1;
         for (int c = tid & 31; c <= k; c += 32) xi[-c] -= lik * (c < k ? xk[-c] : inv);
       }
       __syncthreads();
     }
-    for (int e = tid; e < b * b; e += kEigThreads) {
+    for (int e = tid; e < b * b; e += kCholThreads) {
       const int j = e / b, k = e % b;  // T[j][k] = X[k][j]
       T[e] = j < k ? L[(b1 - k) * b + (b1 - j)] : (j == k ? invs[k] : 0.0);
     }
   } else {
     for (int k = 0; k < b; ++k) {
       const double inv = invs[k];
-      for (int c = tid; c <= k; c += kEigThreads) X[static_cast<int64_t>(k) * b + c] *= inv;
+      for (int c = tid; c <= k; c += kCholThreads) X[static_cast<int64_t>(k) * b + c] *= inv;
       __syncthreads();
       const int w = b - k - 1;
-      for (int e = tid; e < w * (k + 1); e += kEigThreads) {
+      for (int e = tid; e < w * (k + 1); e += kCholThreads) {
         const int i = k + 1 + e / (k + 1), c = e % (k + 1);
         X[static_cast<int64_t>(i) * b + c] -= L[i * b + k] * X[static_cast<int64_t>(k) * b + c];
       }
       __syncthreads();
     }
-    for (int e = tid; e < b * b; e += kEigThreads) {
+    for (int e = tid; e < b * b; e += kCholThreads) {
       const int j = e / b, k = e % b;
       T[e] = X[static_cast<int64_t>(k) * b + j];
     }
@@ -846,10 +847,10 @@ struct Svid {
                                 hipFuncAttributeMaxDynamicSharedMemorySize, smem);
         if (e != hipSuccess) return e;
       }
-      hipLaunchKernelGGL((chol_orth_kernel<true>), dim3(1), dim3(kEigThreads), smem, st, at(L.gram), at(L.et),
+      hipLaunchKernelGGL((chol_orth_kernel<true>), dim3(1), dim3(kCholThreads), smem, st, at(L.gram), at(L.et),
                          at(L.e), b);
     } else {
-      hipLaunchKernelGGL((chol_orth_kernel<false>), dim3(1), dim3(kEigThreads), 0, st, at(L.gram), at(L.et),
+      hipLaunchKernelGGL((chol_orth_kernel<false>), dim3(1), dim3(kCholThreads), 0, st, at(L.gram), at(L.et),
                          at(L.e), b);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
