@@ -44,6 +44,7 @@ constexpr int kEigThreads = 1024;
 constexpr int kCholThreads = 1024;  // CholQR: one workgroup (fewer threads were slower at b = 120)
 constexpr int kMaxBlock = 1024;     // largest eigenproblem: one workgroup, one pair per thread
 constexpr int kEigLdsMax = 128;     // b <= 128: the matrix stays in LDS during the sweeps
+constexpr int kPackMax = 192;       // b <= 192: one triangle of it stays in LDS (b (b + 1) / 2 doubles)
 constexpr int kEigMaxSweeps = 80;
 constexpr int kApplyCols = 8;       // rotation replay: columns of the accumulated rotations per workgroup
 constexpr int kApplyThreads = 256;
@@ -385,6 +386,110 @@ __global__ __launch_bounds__(kEigThreads) void jacobi_log_kernel(const double* A
   if (tid == 0) *nsw = sweeps;
 }
 
+// jacobi_log_kernel for kEigLdsMax < b <= kPackMax: the symmetric matrix as
+// its upper triangle in LDS (row i holds columns i .. b-1), each unordered
+// 2 x 2 block {pair kr, pair kc} updated once; the thread group g (16
+// threads) takes row pairs g and np - 1 - g, so every group has np + 1 blocks.
+__device__ __forceinline__ int tri_up(int i, int j, int b) { return i * b - ((i * (i - 1)) >> 1) + (j - i); }
+__device__ __forceinline__ int sym_at(int i, int j, int b) { return i <= j ? tri_up(i, j, b) : tri_up(j, i, b); }
+
+__global__ __launch_bounds__(kEigThreads) void jacobi_log_packed_kernel(const double* A, double* lraw, int* nsw,
+                                                                        double2* rlog, int b) {
+  extern __shared__ double eig_smem[];
+  __shared__ int pp[kPackMax / 2], pq[kPackMax / 2], pa[kPackMax / 2];
+  __shared__ double pc[kPackMax / 2], ps[kPackMax / 2];
+  __shared__ int rot;
+  __shared__ double floor_abs;
+  const int tid = threadIdx.x;
+  const int n2 = b + (b & 1), np = n2 / 2;
+  double* M = eig_smem;  // upper triangle, tri_up
+  for (int i = tid >> 5; i < b; i += kEigThreads / 32)
+    for (int j = i + (tid & 31); j < b; j += 32) M[tri_up(i, j, b)] = A[static_cast<int64_t>(i) * b + j];
+  if (tid == 0) {
+    double mx = 0.0;
+    for (int i = 0; i < b; ++i) mx = fmax(mx, fabs(A[static_cast<int64_t>(i) * b + i]));
+    floor_abs = 1e-17 * mx;
+  }
+  __syncthreads();
+  const int grp = tid >> 4, gl = tid & 15;
+  const int ngrp = (np + 1) / 2;
+  int sweeps = kEigMaxSweeps;
+  for (int sweep = 0; sweep < kEigMaxSweeps; ++sweep) {
+    if (tid == 0) rot = 0;
+    __syncthreads();
+    for (int s = 0; s < n2 - 1; ++s) {
+      if (tid < np) {
+        int p, q;
+        rr_pair(n2, s, tid, p, q);
+        double c = 1.0, sn = 0.0;
+        bool act = false;
+        if (q < b) {
+          const double app = M[tri_up(p, p, b)], aqq = M[tri_up(q, q, b)], apq = M[tri_up(p, q, b)];
+          if (apq != 0.0 && fabs(apq) > 1e-15 * sqrt(fabs(app * aqq)) && fabs(apq) > floor_abs) {
+            const double zeta = (aqq - app) / (2.0 * apq);
+            const double t = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+            c = 1.0 / sqrt(1.0 + t * t);
+            sn = c * t;
+            act = true;
+          }
+        }
+        pp[tid] = p;
+        pq[tid] = q;
+        pa[tid] = act ? 1 : 0;
+        pc[tid] = c;
+        ps[tid] = sn;
+        rlog[(static_cast<int64_t>(sweep) * (n2 - 1) + s) * np + tid] = make_double2(c, sn);
+        if (act) atomicAdd(&rot, 1);
+      }
+      __syncthreads();
+      if (grp < ngrp) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int kr = h == 0 ? grp : np - 1 - grp;
+          if (h == 1 && kr == grp) break;  // np odd: the middle row pair once
+          const int p = pp[kr], q = pq[kr];
+          const bool ar = pa[kr] != 0, qv = q < b;
+          const double cr = pc[kr], sr = ps[kr];
+          for (int kc = kr + gl; kc < np; kc += 16) {
+            if (!ar && !pa[kc]) continue;
+            const int u = pp[kc], v = pq[kc];
+            const bool vv = v < b;
+            const double cc = pc[kc], sc = ps[kc];
+            const int i00 = sym_at(p, u, b), i01 = vv ? sym_at(p, v, b) : 0;
+            const int i10 = qv ? sym_at(q, u, b) : 0, i11 = (qv && vv) ? sym_at(q, v, b) : 0;
+            const double a00 = M[i00], a01 = vv ? M[i01] : 0.0;
+            const double a10 = qv ? M[i10] : 0.0, a11 = (qv && vv) ? M[i11] : 0.0;
+            const double b00 = cr * a00 - sr * a10, b01 = cr * a01 - sr * a11;
+            const double b10 = sr * a00 + cr * a10, b11 = sr * a01 + cr * a11;
+            const double d00 = cc * b00 - sc * b01, d01 = sc * b00 + cc * b01;
+            const double d10 = cc * b10 - sc * b11, d11 = sc * b10 + cc * b11;
+            M[i00] = d00;
+            if (kc == kr) {
+              // the diagonal block: (p, q) once, from the upper element
+              if (qv) {
+                M[i01] = d01;
+                M[i11] = d11;
+              }
+            } else {
+              if (vv) M[i01] = d01;
+              if (qv) M[i10] = d10;
+              if (qv && vv) M[i11] = d11;
+            }
+          }
+        }
+      }
+      __syncthreads();
+    }
+    if (rot == 0) {
+      sweeps = sweep;
+      break;
+    }
+    __syncthreads();
+  }
+  for (int i = tid; i < b; i += kEigThreads) lraw[i] = M[tri_up(i, i, b)];
+  if (tid == 0) *nsw = sweeps;
+}
+
 // Replay of jacobi_log_kernel's rotations on columns [kApplyCols * blockIdx.x,
 // + kApplyCols) of the accumulated rotation matrix (identity at the start;
 // row i is eigenvector i), then the outputs: eigenvalues descending (index
@@ -402,7 +507,7 @@ __global__ __launch_bounds__(kApplyThreads) void rot_apply_kernel(const double2*
   double* Ec = ap_smem;                                             // [b][C]
   double2* cs = reinterpret_cast<double2*>(ap_smem + b * C);        // [2][kRotBatch * np]
   const int per = kRotBatch * np;
-  constexpr int kPer = (kRotBatch * (kEigLdsMax / 2) + kApplyThreads - 1) / kApplyThreads;
+  constexpr int kPer = (kRotBatch * (kPackMax / 2) + kApplyThreads - 1) / kApplyThreads;
   for (int e = tid; e < b * C; e += kApplyThreads) Ec[e] = (e / C == j0 + e % C) ? 1.0 : 0.0;
   const int total = *nsw * nst;
   const int nbatch = (total + kRotBatch - 1) / kRotBatch;
@@ -552,6 +657,68 @@ __global__ __launch_bounds__(kCholThreads) void chol_orth_kernel(double* G, doub
       const int j = e / b, k = e % b;
       T[e] = X[static_cast<int64_t>(k) * b + j];
     }
+  }
+}
+
+// CholQR for kEigLdsMax < b <= kPackMax: L as its lower triangle in LDS (row
+// i holds columns 0 .. i), factorised as in chol_orth_kernel; then L^-1 in
+// place, from the last column to the first: column j of L^-1 below the
+// diagonal is -(1 / L_jj) times the already inverted trailing block applied to
+// column j of L (each row's sum on 32 lanes); the diagonal is 1 / L_jj (0 for
+// a dropped pivot, whose row and column of L^-1 are then 0).  T = L^-T.
+__device__ __forceinline__ int tri_lo(int i, int j) { return ((i * (i + 1)) >> 1) + j; }
+
+__global__ __launch_bounds__(kCholThreads) void chol_orth_packed_kernel(const double* G, double* T, int b) {
+  extern __shared__ double chol_smem[];
+  __shared__ double invs[kPackMax];
+  __shared__ double colk[kPackMax];
+  __shared__ double thr;
+  const int tid = threadIdx.x;
+  const int lane32 = tid & 31;
+  double* L = chol_smem;  // tri_lo
+  for (int i = tid >> 5; i < b; i += kCholThreads / 32)
+    for (int j = lane32; j <= i; j += 32) L[tri_lo(i, j)] = G[static_cast<int64_t>(i) * b + j];
+  if (tid == 0) {
+    double mx = 0.0;
+    for (int i = 0; i < b; ++i) mx = fmax(mx, G[static_cast<int64_t>(i) * b + i]);
+    thr = 1e-13 * mx;
+  }
+  __syncthreads();
+  for (int k = 0; k < b; ++k) {
+    const double d = L[tri_lo(k, k)];
+    const double inv = d > thr ? 1.0 / sqrt(d) : 0.0;
+    if (tid == 0) invs[k] = inv;
+    for (int i = k + 1 + tid; i < b; i += kCholThreads) {
+      const double v = L[tri_lo(i, k)] * inv;
+      L[tri_lo(i, k)] = v;
+      colk[i] = v;
+    }
+    __syncthreads();
+    for (int i = k + 1 + (tid >> 5); i < b; i += kCholThreads / 32) {
+      const double lik = colk[i];
+      double* row = L + tri_lo(i, 0);
+      for (int j = k + 1 + lane32; j <= i; j += 32) row[j] -= lik * colk[j];
+    }
+    __syncthreads();
+  }
+  for (int i = tid; i < b; i += kCholThreads) L[tri_lo(i, i)] = invs[i];
+  __syncthreads();
+  for (int j = b - 1; j >= 0; --j) {
+    for (int i = j + 1 + tid; i < b; i += kCholThreads) colk[i] = L[tri_lo(i, j)];
+    __syncthreads();
+    for (int i = j + 1 + (tid >> 5); i < b; i += kCholThreads / 32) {
+      const double* row = L + tri_lo(i, 0);
+      double acc = 0.0;
+      for (int c = j + 1 + lane32; c <= i; c += 32) acc += row[c] * colk[c];
+#pragma unroll
+      for (int o = 16; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+      if (lane32 == 0) L[tri_lo(i, j)] = -invs[j] * acc;
+    }
+    __syncthreads();
+  }
+  for (int e = tid; e < b * b; e += kCholThreads) {
+    const int jj = e / b, k = e - jj * b;  // T[jj][k] = X[k][jj]
+    T[e] = jj <= k ? L[tri_lo(k, jj)] : 0.0;
   }
 }
 
@@ -720,8 +887,8 @@ SvidLayout svid_layout(int m, int n, int r, int over) {
   {
     // rotation log of the largest eigenproblem solved in LDS (b or r)
     size_t bl = 0;
-    if (b <= static_cast<size_t>(kEigLdsMax)) bl = b;
-    if (static_cast<size_t>(r) <= static_cast<size_t>(kEigLdsMax) && static_cast<size_t>(r) > bl) bl = r;
+    if (b <= static_cast<size_t>(kPackMax)) bl = b;
+    if (static_cast<size_t>(r) <= static_cast<size_t>(kPackMax) && static_cast<size_t>(r) > bl) bl = r;
     const size_t n2 = bl + (bl & 1);
     L.rlog = take(bl > 0 ? 2 * static_cast<size_t>(kEigMaxSweeps) * (n2 - 1) * (n2 / 2) : 0);
   }
@@ -785,17 +952,24 @@ struct Svid {
   }
 
   hipError_t eig(double* A, double* E, double* lam, int b, int mode) const {
-    if (b <= kEigLdsMax) {
-      const int smem = static_cast<int>(sizeof(double) * b * b);
+    if (b <= kPackMax) {
+      // full matrix in LDS up to kEigLdsMax, its upper triangle above
+      const bool full = b <= kEigLdsMax;
+      const int smem = static_cast<int>(sizeof(double) * (full ? b * b : b * (b + 1) / 2));
+      const void* fn = full ? reinterpret_cast<const void*>(&jacobi_log_kernel)
+                            : reinterpret_cast<const void*>(&jacobi_log_packed_kernel);
       if (smem > 65536) {
-        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&jacobi_log_kernel),
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
         if (e != hipSuccess) return e;
       }
       double2* rl = reinterpret_cast<double2*>(at(L.rlog));
       int* ns = reinterpret_cast<int*>(at(L.nsw));
-      hipLaunchKernelGGL(jacobi_log_kernel, dim3(1), dim3(kEigThreads), smem, st, static_cast<const double*>(A),
-                         at(L.lraw), ns, rl, b);
+      if (full)
+        hipLaunchKernelGGL(jacobi_log_kernel, dim3(1), dim3(kEigThreads), smem, st, static_cast<const double*>(A),
+                           at(L.lraw), ns, rl, b);
+      else
+        hipLaunchKernelGGL(jacobi_log_packed_kernel, dim3(1), dim3(kEigThreads), smem, st,
+                           static_cast<const double*>(A), at(L.lraw), ns, rl, b);
       if (const hipError_t e = hipGetLastError(); e != hipSuccess) return e;
       const int np = (b + (b & 1)) / 2;
       const size_t smem2 = sizeof(double) * b * kApplyCols + sizeof(double2) * 2 * kRotBatch * np;
@@ -849,6 +1023,15 @@ struct Svid {
       }
       hipLaunchKernelGGL((chol_orth_kernel<true>), dim3(1), dim3(kCholThreads), smem, st, at(L.gram), at(L.et),
                          at(L.e), b);
+    } else if (b <= kPackMax) {
+      const int smem = static_cast<int>(sizeof(double) * b * (b + 1) / 2);
+      if (smem > 65536) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&chol_orth_packed_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return e;
+      }
+      hipLaunchKernelGGL(chol_orth_packed_kernel, dim3(1), dim3(kCholThreads), smem, st,
+                         static_cast<const double*>(at(L.gram)), at(L.e), b);
     } else {
       hipLaunchKernelGGL((chol_orth_kernel<false>), dim3(1), dim3(kCholThreads), 0, st, at(L.gram), at(L.et),
                          at(L.e), b);

@@ -73,7 +73,8 @@ CASES = [
     (320, 256, 32, 48, 0.02),   # several 64-row tiles and split-K Gram sums
     (70, 50, 50, 40, 0.1),      # r = min(d_out, d_in): the block is the whole space
     (33, 65, 7, 5, 0.1),        # ragged tiles everywhere
-    (384, 320, 120, 124, 0.05),  # block b = 136 > 128: the eigen and Cholesky kernels in global memory
+    (384, 320, 120, 124, 0.05),  # block b = 136 > 128: one triangle of each small matrix in LDS
+    (290, 250, 113, 118, 0.05),  # odd block b = 129 (the round-robin ordering's dummy index)
 ]
 
 
