@@ -39,7 +39,7 @@ typedef double d4 __attribute__((ext_vector_type(4)));
 
 constexpr int kDtF64 = 100;  // operand code of the internal fp64 arrays
 constexpr int kGT = 64;      // GEMM output tile (rows and columns)
-constexpr int kGK = 16;      // GEMM K per LDS stage
+constexpr int kGK = 32;      // GEMM K per LDS stage
 constexpr int kEigThreads = 1024;
 constexpr int kCholThreads = 1024;  // CholQR: one workgroup (fewer threads were slower at b = 120)
 constexpr int kMaxBlock = 1024;     // largest eigenproblem: one workgroup, one pair per thread
@@ -54,6 +54,14 @@ constexpr double kDropRel = 1e-14;  // orthonormalisation: dropped Gram eigenval
 __device__ __forceinline__ double load_op(const void* p, int64_t idx, int dt) {
   if (dt == kDtF64) return static_cast<const double*>(p)[idx];
   return static_cast<double>(load_as_f32(p, idx, dt));
+}
+// the same with the dtype fixed at compile time
+template <int DT>
+__device__ __forceinline__ double load_t(const void* p, int64_t idx) {
+  if constexpr (DT == kDtF64)
+    return static_cast<const double*>(p)[idx];
+  else
+    return static_cast<double>(load_as_f32(p, idx, DT));
 }
 
 enum { kEpiStore = 0, kEpiResid = 1 };
@@ -91,10 +99,12 @@ __device__ __forceinline__ void gemm_store(const GemmArgs& g, int i, int j, doub
 // [z * kchunk, (z + 1) * kchunk) and, when ksplit > 1, writes its own slab.
 // AK: A's k stride is 1 (else its i stride is); BJ: B's j stride is 1 (else
 // its k stride is) -- the tile loads walk the contiguous index.
-template <bool AK, bool BJ>
+// (ADT: A's dtype; B is always fp64)
+template <bool AK, bool BJ, int ADT>
 __global__ __launch_bounds__(256) void gemm64_kernel(GemmArgs g) {
   __shared__ double As[kGK][kGT + 1];
   __shared__ double Bs[kGK][kGT + 1];
+  constexpr int kPer = kGT * kGK / 256;  // elements of each operand a thread stages
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int i0 = blockIdx.x * kGT, j0 = blockIdx.y * kGT;
   const int kz0 = blockIdx.z * g.kchunk;
@@ -103,30 +113,47 @@ __global__ __launch_bounds__(256) void gemm64_kernel(GemmArgs g) {
   d4 acc[2][2];
   for (int a = 0; a < 2; ++a)
     for (int b = 0; b < 2; ++b) acc[a][b] = d4{0.0, 0.0, 0.0, 0.0};
+  // the stage at k0 into registers: element e = tid + 256 u of each operand
+  // tile, the source's contiguous index walking fastest; with 256 threads,
+  // 64-wide tiles and 32-deep stages, element u of a thread sits at a fixed
+  // offset plus u times a uniform stride (rows 8 u or k 4 u further)
+  static_assert(kGT == 64 && kGK == 32, "the staging map assumes 64 x 32 tiles and 256 threads");
+  const int a_i = AK ? (tid >> 5) : (tid & 63), a_k = AK ? (tid & 31) : (tid >> 6);
+  const int a_di = AK ? 8 : 0, a_dk = AK ? 0 : 4;
+  const int b_j = BJ ? (tid & 63) : (tid >> 5), b_k = BJ ? (tid >> 6) : (tid & 31);
+  const int b_dj = BJ ? 0 : 8, b_dk = BJ ? 4 : 0;
+  const int64_t a_step = static_cast<int64_t>(a_di) * g.sai + static_cast<int64_t>(a_dk) * g.sak;
+  const int64_t b_step = static_cast<int64_t>(b_dk) * g.sbk + static_cast<int64_t>(b_dj) * g.sbj;
+  double ra[kPer], rb[kPer];
+  auto load_stage = [&](int k0) {
+    const int64_t a0 = static_cast<int64_t>(i0 + a_i) * g.sai + static_cast<int64_t>(k0 + a_k) * g.sak;
+    const int64_t b0 = static_cast<int64_t>(k0 + b_k) * g.sbk + static_cast<int64_t>(j0 + b_j) * g.sbj;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      // out-of-range elements read element 0 and are replaced by 0
+      const bool oka = i0 + a_i + a_di * u < g.M && k0 + a_k + a_dk * u < kz1;
+      double va = load_t<ADT>(g.A, oka ? a0 + u * a_step : 0);
+      if (g.a_abs) va = fabs(va);
+      ra[u] = oka ? va : 0.0;
+      const bool okb = j0 + b_j + b_dj * u < g.N && k0 + b_k + b_dk * u < kz1;
+      double vb = load_t<kDtF64>(g.B, okb ? b0 + u * b_step : 0);
+      if (g.b_abs) vb = fabs(vb);
+      rb[u] = okb ? vb : 0.0;
+    }
+  };
+  auto store_stage = [&]() {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      As[a_k + a_dk * u][a_i + a_di * u] = ra[u];
+      Bs[b_k + b_dk * u][b_j + b_dj * u] = rb[u];
+    }
+  };
+  load_stage(kz0);
   for (int k0 = kz0; k0 < kz1; k0 += kGK) {
-    for (int e = tid; e < kGT * kGK; e += 256) {
-      const int ii = AK ? e / kGK : e % kGT;
-      const int kk = AK ? e % kGK : e / kGT;
-      const int i = i0 + ii, k = k0 + kk;
-      double v = 0.0;
-      if (i < g.M && k < kz1) {
-        v = load_op(g.A, static_cast<int64_t>(i) * g.sai + static_cast<int64_t>(k) * g.sak, g.a_dt);
-        if (g.a_abs) v = fabs(v);
-      }
-      As[kk][ii] = v;
-    }
-    for (int e = tid; e < kGT * kGK; e += 256) {
-      const int jj = BJ ? e % kGT : e / kGK;
-      const int kk = BJ ? e / kGT : e % kGK;
-      const int j = j0 + jj, k = k0 + kk;
-      double v = 0.0;
-      if (j < g.N && k < kz1) {
-        v = load_op(g.B, static_cast<int64_t>(k) * g.sbk + static_cast<int64_t>(j) * g.sbj, g.b_dt);
-        if (g.b_abs) v = fabs(v);
-      }
-      Bs[kk][jj] = v;
-    }
+    store_stage();
     __syncthreads();
+    // the next stage's loads are in flight while this stage's products run
+    if (k0 + kGK < kz1) load_stage(k0 + kGK);
 #pragma unroll
     for (int kk = 0; kk < kGK; kk += 4) {
       double av[2], bv[2];
@@ -914,6 +941,19 @@ struct Svid {
   hipStream_t st;
   double* at(size_t off) const { return reinterpret_cast<double*>(ws + off); }
 
+  template <int ADT>
+  void launch_gemm(const GemmArgs& run, dim3 grid) const {
+    const bool ak = run.sak == 1, bj = run.sbj == 1;
+    if (ak && bj)
+      hipLaunchKernelGGL((gemm64_kernel<true, true, ADT>), grid, dim3(256), 0, st, run);
+    else if (ak)
+      hipLaunchKernelGGL((gemm64_kernel<true, false, ADT>), grid, dim3(256), 0, st, run);
+    else if (bj)
+      hipLaunchKernelGGL((gemm64_kernel<false, true, ADT>), grid, dim3(256), 0, st, run);
+    else
+      hipLaunchKernelGGL((gemm64_kernel<false, false, ADT>), grid, dim3(256), 0, st, run);
+  }
+
   // C [M x N] = op(A) [M x K] * B [K x N]; K split so that the launch has
   // about 512 workgroups, when the partial slabs fit and each split keeps at
   // least 256 of K.
@@ -935,15 +975,13 @@ struct Svid {
       run.pstride = static_cast<int64_t>(slab);
     }
     const dim3 grid((g.M + kGT - 1) / kGT, (g.N + kGT - 1) / kGT, split);
-    const bool ak = g.sak == 1, bj = g.sbj == 1;
-    if (ak && bj)
-      hipLaunchKernelGGL((gemm64_kernel<true, true>), grid, dim3(256), 0, st, run);
-    else if (ak)
-      hipLaunchKernelGGL((gemm64_kernel<true, false>), grid, dim3(256), 0, st, run);
-    else if (bj)
-      hipLaunchKernelGGL((gemm64_kernel<false, true>), grid, dim3(256), 0, st, run);
-    else
-      hipLaunchKernelGGL((gemm64_kernel<false, false>), grid, dim3(256), 0, st, run);
+    if (g.b_dt != kDtF64) return hipErrorInvalidValue;  // every B operand is an fp64 array of this file
+    switch (g.a_dt) {
+      case kDtF64: launch_gemm<kDtF64>(run, grid); break;
+      case kDtF32: launch_gemm<kDtF32>(run, grid); break;
+      case kDtF16: launch_gemm<kDtF16>(run, grid); break;
+      default: launch_gemm<kDtBF16>(run, grid); break;
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || split == 1) return e;
     hipLaunchKernelGGL(gemm_reduce_kernel, dim3(grid_for(static_cast<int64_t>(slab))), dim3(256), 0, st, g,
