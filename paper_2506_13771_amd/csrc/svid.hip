@@ -687,6 +687,97 @@ __global__ __launch_bounds__(kCholThreads) void chol_orth_kernel(double* G, doub
   }
 }
 
+// Top eigenpair of the r x r Gram matrix A = F^T F of a nonnegative F (the
+// rank-1 factors need nothing else) by power iteration from the all-ones
+// vector, whose projection on the (nonnegative) Perron vector is positive:
+// v <- A v / ||A v|| until ||A v - lambda v|| <= 1e-13 lambda (lambda = v^T A
+// v) or kPowMaxIter steps.  The vector to column 0 of E, lambda to lam[0]
+// (0 with v = e_1 for a zero matrix).  One workgroup; A in LDS when r <=
+// kEigLdsMax, else read from global memory.
+constexpr int kPowMaxIter = 20000;
+
+__global__ __launch_bounds__(kEigThreads) void top_eig_kernel(const double* A, double* E, double* lam, int r) {
+  extern __shared__ double pw_smem[];
+  __shared__ double v[kMaxBlock], w[kMaxBlock];
+  __shared__ double red[kEigThreads / 64][2];
+  __shared__ int done;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const bool in_lds = r <= kEigLdsMax;
+  const double* M = in_lds ? pw_smem : A;
+  if (in_lds)
+    for (int e = tid; e < r * r; e += kEigThreads) pw_smem[e] = A[e];
+  const double v0 = 1.0 / sqrt(static_cast<double>(r));
+  for (int i = tid; i < r; i += kEigThreads) v[i] = v0;
+  if (tid == 0) done = 0;
+  __syncthreads();
+  // two block sums (each wave's lanes by shuffles, then the waves in order)
+  auto sum2 = [&](double a, double b, double& sa, double& sb) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      a += __shfl_xor(a, o);
+      b += __shfl_xor(b, o);
+    }
+    if (lane == 0) {
+      red[wv][0] = a;
+      red[wv][1] = b;
+    }
+    __syncthreads();
+    sa = 0.0;
+    sb = 0.0;
+    for (int k = 0; k < kEigThreads / 64; ++k) {
+      sa += red[k][0];
+      sb += red[k][1];
+    }
+    __syncthreads();
+  };
+  double lambda = 0.0;
+  for (int it = 0; it < kPowMaxIter; ++it) {
+    // w = A v: 8 threads per row, rows tid / 8 + 128 n
+    for (int i0 = 0; i0 < r; i0 += kEigThreads / 8) {
+      const int i = i0 + (tid >> 3);
+      double s = 0.0;
+      if (i < r)
+        for (int j = tid & 7; j < r; j += 8) s += M[static_cast<int64_t>(i) * r + j] * v[j];
+      s += __shfl_xor(s, 4);
+      s += __shfl_xor(s, 2);
+      s += __shfl_xor(s, 1);
+      if (i < r && (tid & 7) == 0) w[i] = s;
+    }
+    __syncthreads();
+    double pa = 0.0, pb = 0.0;
+    for (int i = tid; i < r; i += kEigThreads) {
+      pa += v[i] * w[i];
+      pb += w[i] * w[i];
+    }
+    double vw, ww;
+    sum2(pa, pb, vw, ww);
+    lambda = vw;
+    // residual ||w - lambda v||^2 and the new v
+    double pr = 0.0;
+    for (int i = tid; i < r; i += kEigThreads) {
+      const double d = w[i] - lambda * v[i];
+      pr += d * d;
+    }
+    double rr, unused;
+    sum2(pr, 0.0, rr, unused);
+    if (ww <= 0.0) {
+      // a zero matrix: lambda 0, v = e_1
+      lambda = 0.0;
+      for (int i = tid; i < r; i += kEigThreads) v[i] = i == 0 ? 1.0 : 0.0;
+      __syncthreads();
+      break;
+    }
+    const bool conv = sqrt(rr) <= 1e-13 * fabs(lambda);
+    const double inv = 1.0 / sqrt(ww);
+    if (!conv)
+      for (int i = tid; i < r; i += kEigThreads) v[i] = w[i] * inv;
+    __syncthreads();
+    if (conv) break;
+  }
+  for (int i = tid; i < r; i += kEigThreads) E[static_cast<int64_t>(i) * r] = v[i];
+  if (tid == 0) lam[0] = lambda;
+}
+
 // CholQR for kEigLdsMax < b <= kPackMax: L as its lower triangle in LDS (row
 // i holds columns 0 .. i), factorised as in chol_orth_kernel; then L^-1 in
 // place, from the last column to the first: column j of L^-1 below the
@@ -1094,7 +1185,18 @@ struct Svid {
     const int r = L.r;
     hipError_t e;
     if ((e = mm(F, kDtF64, 1, r, true, F, kDtF64, r, 1, true, at(L.gram), r, r, r, d)) != hipSuccess) return e;
-    if ((e = eig(at(L.gram), at(L.e), at(L.lam), r, 0)) != hipSuccess) return e;
+    // the top eigenpair of |F|^T |F| (column 0 of E, lam[0])
+    {
+      const int smem = r <= kEigLdsMax ? static_cast<int>(sizeof(double) * r * r) : 0;
+      if (smem > 65536) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&top_eig_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return e;
+      }
+      hipLaunchKernelGGL(top_eig_kernel, dim3(1), dim3(kEigThreads), smem, st, static_cast<const double*>(at(L.gram)),
+                         at(L.e), at(L.lam), r);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
     // u = |F| e_1 (the first column of E)
     if ((e = mm(F, kDtF64, r, 1, true, at(L.e), kDtF64, r, 1, false, at(L.u), 1, d, 1, r)) != hipSuccess) return e;
     hipLaunchKernelGGL(rank1_finish_kernel, dim3(1), dim3(256), 0, st, static_cast<const double*>(at(L.u)),
