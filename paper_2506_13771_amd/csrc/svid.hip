@@ -700,7 +700,6 @@ __global__ __launch_bounds__(kEigThreads) void top_eig_kernel(const double* A, d
   extern __shared__ double pw_smem[];
   __shared__ double v[kMaxBlock], w[kMaxBlock];
   __shared__ double red[kEigThreads / 64][2];
-  __shared__ int done;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const bool in_lds = r <= kEigLdsMax;
   const double* M = in_lds ? pw_smem : A;
@@ -708,7 +707,6 @@ __global__ __launch_bounds__(kEigThreads) void top_eig_kernel(const double* A, d
     for (int e = tid; e < r * r; e += kEigThreads) pw_smem[e] = A[e];
   const double v0 = 1.0 / sqrt(static_cast<double>(r));
   for (int i = tid; i < r; i += kEigThreads) v[i] = v0;
-  if (tid == 0) done = 0;
   __syncthreads();
   // two block sums (each wave's lanes by shuffles, then the waves in order)
   auto sum2 = [&](double a, double b, double& sa, double& sb) {
