@@ -606,8 +606,11 @@ __global__ __launch_bounds__(kApplyThreads) void rot_apply_kernel(const double2*
 // (X[i][c] at [b-1-i][b-1-c], c < i, so that a row of X is contiguous); column
 // k of L is copied to a vector while it is scaled.  Else G and the scratch X
 // [b x b] are used in global memory.
+// factor_only (LDS variant): stop after the factorisation and write L to T
+// with 1 / L_kk on its diagonal (for chol_solve_kernel).
 template <bool kLds>
-__global__ __launch_bounds__(kCholThreads) void chol_orth_kernel(double* G, double* X, double* T, int b) {
+__global__ __launch_bounds__(kCholThreads) void chol_orth_kernel(double* G, double* X, double* T, int b,
+                                                                 int factor_only) {
   extern __shared__ double chol_smem[];
   __shared__ double invs[kMaxBlock];
   __shared__ double colk[kMaxBlock];
@@ -643,6 +646,13 @@ __global__ __launch_bounds__(kCholThreads) void chol_orth_kernel(double* G, doub
     __syncthreads();
   }
   if constexpr (kLds) {
+    if (factor_only) {
+      for (int e = tid; e < b * b; e += kCholThreads) {
+        const int i = e / b, j = e - i * b;
+        T[e] = j < i ? L[e] : (j == i ? invs[i] : 0.0);
+      }
+      return;
+    }
     const int b1 = b - 1;
     // X's strict lower part (in the upper triangle) starts at 0
     for (int e = tid; e < b * b; e += kCholThreads)
@@ -774,6 +784,76 @@ __global__ __launch_bounds__(kEigThreads) void top_eig_kernel(const double* A, d
   }
   for (int i = tid; i < r; i += kEigThreads) E[static_cast<int64_t>(i) * r] = v[i];
   if (tid == 0) lam[0] = lambda;
+}
+
+// Q = Y L^-T for CholQR with b <= kEigLdsMax, row by row: q L^T = y, so
+// q_k = (y_k - sum_{c<k} q_c L_kc) / L_kk.  64 rows per workgroup, 16 lanes
+// per row (one DPP row): lane t holds y_c and q_c for c = t + 16 j in
+// registers (the steps are unrolled, so the slot j is a constant), its part
+// of each sum is added over the row by DPP, and the lane that holds y_k
+// computes q_k; no LDS traffic or barrier per step.  L (lower, 1 / L_kk on
+// the diagonal, as chol_orth_kernel's factor_only output) as its packed lower
+// triangle in LDS.
+constexpr int kSolveRows = 64;
+constexpr int kSolveSlots = kEigLdsMax / 16;
+
+// a double moved across lanes by a DPP control (both 32-bit halves)
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t u = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(u & 0xffffffffu), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(u >> 32), CTRL, 0xF, 0xF, false);
+  return __longlong_as_double((static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo));
+}
+// the sum over the 16 lanes of a DPP row, in every lane (quad swaps, then the
+// half-row and row mirrors)
+__device__ __forceinline__ double row16_sum(double v) {
+  v += dpp_f64<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_f64<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_f64<0x141>(v);  // row_half_mirror
+  v += dpp_f64<0x140>(v);  // row_mirror
+  return v;
+}
+
+__global__ __launch_bounds__(kCholThreads) void chol_solve_kernel(const double* Y, const double* Lf, double* Q,
+                                                                  int rows, int b) {
+  extern __shared__ double sv_smem[];
+  double* Lp = sv_smem;  // tri_lo
+  const int tid = threadIdx.x;
+  for (int i = tid >> 5; i < b; i += kCholThreads / 32)
+    for (int j = tid & 31; j <= i; j += 32) Lp[((i * (i + 1)) >> 1) + j] = Lf[static_cast<int64_t>(i) * b + j];
+  const int t = tid & 15;
+  const int row = blockIdx.x * kSolveRows + (tid >> 4);
+  const bool ok = row < rows;
+  double q[kSolveSlots];
+#pragma unroll
+  for (int j = 0; j < kSolveSlots; ++j) {
+    const int c = t + 16 * j;
+    q[j] = ok && c < b ? Y[static_cast<int64_t>(row) * b + c] : 0.0;  // y, replaced by q step by step
+  }
+  __syncthreads();
+#pragma unroll
+  for (int kb = 0; kb < kSolveSlots; ++kb) {
+#pragma unroll
+    for (int t0 = 0; t0 < 16; ++t0) {
+      const int k = 16 * kb + t0;
+      if (k >= b) break;
+      const double* lk = Lp + ((k * (k + 1)) >> 1);
+      double s = 0.0;
+#pragma unroll
+      for (int j = 0; j <= kb; ++j) {
+        const int c = t + 16 * j;
+        if (c < k) s += q[j] * lk[c];
+      }
+      s = row16_sum(s);
+      if (t == t0) q[kb] = (q[kb] - s) * lk[k];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kSolveSlots; ++j) {
+    const int c = t + 16 * j;
+    if (ok && c < b) Q[static_cast<int64_t>(row) * b + c] = q[j];
+  }
 }
 
 // CholQR for kEigLdsMax < b <= kPackMax: L as its lower triangle in LDS (row
@@ -1149,7 +1229,17 @@ struct Svid {
         if (e != hipSuccess) return e;
       }
       hipLaunchKernelGGL((chol_orth_kernel<true>), dim3(1), dim3(kCholThreads), smem, st, at(L.gram), at(L.et),
-                         at(L.e), b);
+                         at(L.e), b, 1);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      const int smem2 = static_cast<int>(sizeof(double) * b * (b + 1) / 2);
+      if (smem2 > 65536) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&chol_solve_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, smem2);
+        if (e != hipSuccess) return e;
+      }
+      hipLaunchKernelGGL(chol_solve_kernel, dim3((rows + kSolveRows - 1) / kSolveRows), dim3(kCholThreads), smem2,
+                         st, Y, static_cast<const double*>(at(L.e)), Qo, rows, b);
+      return hipGetLastError();
     } else if (b <= kPackMax) {
       const int smem = static_cast<int>(sizeof(double) * b * (b + 1) / 2);
       if (smem > 65536) {
@@ -1161,7 +1251,7 @@ struct Svid {
                          static_cast<const double*>(at(L.gram)), at(L.e), b);
     } else {
       hipLaunchKernelGGL((chol_orth_kernel<false>), dim3(1), dim3(kCholThreads), 0, st, at(L.gram), at(L.et),
-                         at(L.e), b);
+                         at(L.e), b, 0);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return mm(Y, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, Qo, b, rows, b, b);
