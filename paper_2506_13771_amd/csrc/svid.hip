@@ -786,7 +786,7 @@ __global__ __launch_bounds__(kEigThreads) void top_eig_kernel(const double* A, d
   if (tid == 0) lam[0] = lambda;
 }
 
-// Q = Y L^-T for CholQR with b <= kEigLdsMax, row by row: q L^T = y, so
+// Q = Y L^-T for CholQR with b <= kPackMax, row by row: q L^T = y, so
 // q_k = (y_k - sum_{c<k} q_c L_kc) / L_kk.  64 rows per workgroup, 16 lanes
 // per row (one DPP row): lane t holds y_c and q_c for c = t + 16 j in
 // registers (the steps are unrolled, so the slot j is a constant), its part
@@ -795,7 +795,6 @@ __global__ __launch_bounds__(kEigThreads) void top_eig_kernel(const double* A, d
 // the diagonal, as chol_orth_kernel's factor_only output) as its packed lower
 // triangle in LDS.
 constexpr int kSolveRows = 64;
-constexpr int kSolveSlots = kEigLdsMax / 16;
 
 // a double moved across lanes by a DPP control (both 32-bit halves)
 template <int CTRL>
@@ -815,6 +814,7 @@ __device__ __forceinline__ double row16_sum(double v) {
   return v;
 }
 
+template <int kSolveSlots>  // b <= 16 kSolveSlots
 __global__ __launch_bounds__(kCholThreads) void chol_solve_kernel(const double* Y, const double* Lf, double* Q,
                                                                   int rows, int b) {
   extern __shared__ double sv_smem[];
@@ -856,7 +856,8 @@ __global__ __launch_bounds__(kCholThreads) void chol_solve_kernel(const double* 
   }
 }
 
-// CholQR for kEigLdsMax < b <= kPackMax: L as its lower triangle in LDS (row
+// CholQR for kEigLdsMax < b <= kPackMax (factor_only: stop after the
+// factorisation, as chol_orth_kernel): L as its lower triangle in LDS (row
 // i holds columns 0 .. i), factorised as in chol_orth_kernel; then L^-1 in
 // place, from the last column to the first: column j of L^-1 below the
 // diagonal is -(1 / L_jj) times the already inverted trailing block applied to
@@ -864,7 +865,8 @@ __global__ __launch_bounds__(kCholThreads) void chol_solve_kernel(const double* 
 // a dropped pivot, whose row and column of L^-1 are then 0).  T = L^-T.
 __device__ __forceinline__ int tri_lo(int i, int j) { return ((i * (i + 1)) >> 1) + j; }
 
-__global__ __launch_bounds__(kCholThreads) void chol_orth_packed_kernel(const double* G, double* T, int b) {
+__global__ __launch_bounds__(kCholThreads) void chol_orth_packed_kernel(const double* G, double* T, int b,
+                                                                        int factor_only) {
   extern __shared__ double chol_smem[];
   __shared__ double invs[kPackMax];
   __shared__ double colk[kPackMax];
@@ -899,6 +901,14 @@ __global__ __launch_bounds__(kCholThreads) void chol_orth_packed_kernel(const do
   }
   for (int i = tid; i < b; i += kCholThreads) L[tri_lo(i, i)] = invs[i];
   __syncthreads();
+  if (factor_only) {
+    // L with 1 / L_kk on its diagonal, for chol_solve_kernel
+    for (int e = tid; e < b * b; e += kCholThreads) {
+      const int i = e / b, j = e - i * b;
+      T[e] = j <= i ? L[tri_lo(i, j)] : 0.0;
+    }
+    return;
+  }
   for (int j = b - 1; j >= 0; --j) {
     for (int i = j + 1 + tid; i < b; i += kCholThreads) colk[i] = L[tri_lo(i, j)];
     __syncthreads();
@@ -1217,6 +1227,25 @@ struct Svid {
   // Y^T Y = L L^T, Qo = Y L^-T (dropped pivots give zero columns); the
   // columns are orthonormal up to about cond(Y)^2 times the rounding unit,
   // which is all the iteration needs
+  // Qo = Y L^-T from the factor chol_orth_*_kernel left in L.e (b <= kPackMax)
+  hipError_t solve(const double* Y, double* Qo, int rows, int b) const {
+    const int smem = static_cast<int>(sizeof(double) * b * (b + 1) / 2);
+    const void* fn = b <= 128 ? reinterpret_cast<const void*>(&chol_solve_kernel<8>)
+                              : reinterpret_cast<const void*>(&chol_solve_kernel<12>);
+    if (smem > 65536) {
+      const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+      if (e != hipSuccess) return e;
+    }
+    const dim3 grid((rows + kSolveRows - 1) / kSolveRows);
+    if (b <= 128)
+      hipLaunchKernelGGL(chol_solve_kernel<8>, grid, dim3(kCholThreads), smem, st, Y,
+                         static_cast<const double*>(at(L.e)), Qo, rows, b);
+    else
+      hipLaunchKernelGGL(chol_solve_kernel<12>, grid, dim3(kCholThreads), smem, st, Y,
+                         static_cast<const double*>(at(L.e)), Qo, rows, b);
+    return hipGetLastError();
+  }
+
   hipError_t orth_chol(const double* Y, double* Qo, int rows) const {
     const int b = L.b;
     hipError_t e;
@@ -1231,15 +1260,7 @@ struct Svid {
       hipLaunchKernelGGL((chol_orth_kernel<true>), dim3(1), dim3(kCholThreads), smem, st, at(L.gram), at(L.et),
                          at(L.e), b, 1);
       if ((e = hipGetLastError()) != hipSuccess) return e;
-      const int smem2 = static_cast<int>(sizeof(double) * b * (b + 1) / 2);
-      if (smem2 > 65536) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&chol_solve_kernel),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, smem2);
-        if (e != hipSuccess) return e;
-      }
-      hipLaunchKernelGGL(chol_solve_kernel, dim3((rows + kSolveRows - 1) / kSolveRows), dim3(kCholThreads), smem2,
-                         st, Y, static_cast<const double*>(at(L.e)), Qo, rows, b);
-      return hipGetLastError();
+      return solve(Y, Qo, rows, b);
     } else if (b <= kPackMax) {
       const int smem = static_cast<int>(sizeof(double) * b * (b + 1) / 2);
       if (smem > 65536) {
@@ -1248,7 +1269,9 @@ struct Svid {
         if (e != hipSuccess) return e;
       }
       hipLaunchKernelGGL(chol_orth_packed_kernel, dim3(1), dim3(kCholThreads), smem, st,
-                         static_cast<const double*>(at(L.gram)), at(L.e), b);
+                         static_cast<const double*>(at(L.gram)), at(L.e), b, 1);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      return solve(Y, Qo, rows, b);
     } else {
       hipLaunchKernelGGL((chol_orth_kernel<false>), dim3(1), dim3(kCholThreads), 0, st, at(L.gram), at(L.et),
                          at(L.e), b, 0);
