@@ -20,13 +20,11 @@
 // The contractions (W and W^T times a block, Gram matrices, basis changes, the
 // effective weight) run on the fp64 matrix cores; the small symmetric
 // eigenproblems (b x b and r x r) run as a parallel cyclic Jacobi method on one
-// workgroup.  Inside the iteration a block is orthonormalised by Cholesky of
-// its Gram matrix (CholQR, pivots below 1e-13 of the largest dropped); the
-// final block by the Gram matrix's eigenvectors (Q = Y E diag(lambda)^-1/2,
-// directions with lambda <= 1e-14 lambda_max dropped), so that the
-// Rayleigh-Ritz basis is orthonormal to rounding and a rank-deficient block
-// needs no special case.  Sums are in a fixed order (split-K partial sums added
-// in slab order), so a call is deterministic.
+// workgroup.  Every block, the final one included, is orthonormalised by
+// Cholesky of its Gram matrix (CholQR, pivots below 1e-13 of the largest
+// dropped), so a rank-deficient block gives zero columns, which the
+// Rayleigh-Ritz step carries as zero eigenvalues.  Sums are in a fixed order
+// (split-K partial sums added in slab order), so a call is deterministic.
 #include <algorithm>
 #include <cmath>
 
@@ -49,7 +47,6 @@ constexpr int kEigMaxSweeps = 80;
 constexpr int kApplyCols = 8;       // rotation replay: columns of the accumulated rotations per workgroup
 constexpr int kApplyThreads = 256;
 constexpr int kRotBatch = 16;       // rotation replay: steps whose coefficients are staged in LDS at once
-constexpr double kDropRel = 1e-14;  // orthonormalisation: dropped Gram eigenvalues, relative to the largest
 
 __device__ __forceinline__ double load_op(const void* p, int64_t idx, int dt) {
   if (dt == kDtF64) return static_cast<const double*>(p)[idx];
@@ -220,12 +217,11 @@ __device__ __forceinline__ void rr_pair(int n2, int s, int k, int& p, int& q) {
 // eigenvector per row), until a sweep rotates nothing (|a_pq| <= 1e-15
 // sqrt(|a_pp a_qq|), or below 1e-17 of the largest starting diagonal entry)
 // or kEigMaxSweeps sweeps.  Eigenvalues descending (index order on ties) to
-// lam; eigenvectors to the columns of E [b x b].  mode 1 (orthonormalisation):
-// column k of E is scaled by lambda_k^-1/2, or zeroed when lambda_k <= 1e-14
-// lambda_max.  One workgroup; the matrix lives in LDS when b <= kEigLdsMax.
+// lam; eigenvectors to the columns of E [b x b].  One workgroup; the matrix
+// lives in LDS when b <= kEigLdsMax.
 template <bool kLds>
 __global__ __launch_bounds__(kEigThreads) void jacobi_eig_kernel(double* A, double* Et, double* E, double* lam,
-                                                                  int b, int mode) {
+                                                                  int b) {
   extern __shared__ double eig_smem[];
   __shared__ int pp[kMaxBlock / 2], pq[kMaxBlock / 2], pa[kMaxBlock / 2];
   __shared__ double pc[kMaxBlock / 2], ps[kMaxBlock / 2];
@@ -304,8 +300,6 @@ __global__ __launch_bounds__(kEigThreads) void jacobi_eig_kernel(double* A, doub
     __syncthreads();
   }
   // rank of each eigenvalue (descending, index order on ties), then the outputs
-  double lmax = 0.0;
-  for (int i = 0; i < b; ++i) lmax = fmax(lmax, M[i * b + i]);
   for (int i = tid; i < b; i += kEigThreads) {
     const double li = M[i * b + i];
     int rank = 0;
@@ -314,10 +308,7 @@ __global__ __launch_bounds__(kEigThreads) void jacobi_eig_kernel(double* A, doub
       rank += (lj > li || (lj == li && j < i)) ? 1 : 0;
     }
     lam[rank] = li;
-    double f = 1.0;
-    if (mode == 1) f = (li > 0.0 && li > kDropRel * lmax) ? 1.0 / sqrt(li) : 0.0;
-    for (int row = 0; row < b; ++row)
-      E[static_cast<int64_t>(row) * b + rank] = f * Et[static_cast<int64_t>(i) * b + row];
+    for (int row = 0; row < b; ++row) E[static_cast<int64_t>(row) * b + rank] = Et[static_cast<int64_t>(i) * b + row];
   }
 }
 
@@ -520,12 +511,11 @@ __global__ __launch_bounds__(kEigThreads) void jacobi_log_packed_kernel(const do
 // Replay of jacobi_log_kernel's rotations on columns [kApplyCols * blockIdx.x,
 // + kApplyCols) of the accumulated rotation matrix (identity at the start;
 // row i is eigenvector i), then the outputs: eigenvalues descending (index
-// order on ties) to lam, eigenvectors to the columns of E, scaled as in
-// jacobi_eig_kernel for mode 1.
+// order on ties) to lam, eigenvectors to the columns of E.
 __global__ __launch_bounds__(kApplyThreads) void rot_apply_kernel(const double2* __restrict__ rlog,
                                                                   const int* __restrict__ nsw,
                                                                   const double* __restrict__ lraw, double* E,
-                                                                  double* lam, int b, int mode) {
+                                                                  double* lam, int b) {
   extern __shared__ double ap_smem[];
   constexpr int C = kApplyCols;
   const int tid = threadIdx.x;
@@ -578,8 +568,6 @@ __global__ __launch_bounds__(kApplyThreads) void rot_apply_kernel(const double2*
     }
     __syncthreads();
   }
-  double lmax = 0.0;
-  for (int i = 0; i < b; ++i) lmax = fmax(lmax, lraw[i]);
   for (int i = tid; i < b; i += kApplyThreads) {
     const double li = lraw[i];
     int rank = 0;
@@ -588,9 +576,7 @@ __global__ __launch_bounds__(kApplyThreads) void rot_apply_kernel(const double2*
       rank += (lj > li || (lj == li && j < i)) ? 1 : 0;
     }
     if (blockIdx.x == 0) lam[rank] = li;
-    double f = 1.0;
-    if (mode == 1) f = (li > 0.0 && li > kDropRel * lmax) ? 1.0 / sqrt(li) : 0.0;
-    for (int jj = 0; jj < C && j0 + jj < b; ++jj) E[static_cast<int64_t>(j0 + jj) * b + rank] = f * Ec[i * C + jj];
+    for (int jj = 0; jj < C && j0 + jj < b; ++jj) E[static_cast<int64_t>(j0 + jj) * b + rank] = Ec[i * C + jj];
   }
 }
 
@@ -1168,7 +1154,7 @@ struct Svid {
     return hipGetLastError();
   }
 
-  hipError_t eig(double* A, double* E, double* lam, int b, int mode) const {
+  hipError_t eig(double* A, double* E, double* lam, int b) const {
     if (b <= kPackMax) {
       // full matrix in LDS up to kEigLdsMax, its upper triangle above
       const bool full = b <= kEigLdsMax;
@@ -1192,10 +1178,9 @@ struct Svid {
       const size_t smem2 = sizeof(double) * b * kApplyCols + sizeof(double2) * 2 * kRotBatch * np;
       hipLaunchKernelGGL(rot_apply_kernel, dim3((b + kApplyCols - 1) / kApplyCols), dim3(kApplyThreads), smem2, st,
                          static_cast<const double2*>(rl), static_cast<const int*>(ns),
-                         static_cast<const double*>(at(L.lraw)), E, lam, b, mode);
+                         static_cast<const double*>(at(L.lraw)), E, lam, b);
     } else {
-      hipLaunchKernelGGL((jacobi_eig_kernel<false>), dim3(1), dim3(kEigThreads), 0, st, A, at(L.et), E, lam, b,
-                         mode);
+      hipLaunchKernelGGL((jacobi_eig_kernel<false>), dim3(1), dim3(kEigThreads), 0, st, A, at(L.et), E, lam, b);
     }
     return hipGetLastError();
   }
@@ -1280,17 +1265,6 @@ struct Svid {
     return mm(Y, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, Qo, b, rows, b, b);
   }
 
-  // Y [rows x b] -> an orthonormal basis of its range in Qo [rows x b]:
-  // G = Y^T Y, G = E diag(lambda) E^T, Qo = Y E diag(lambda)^-1/2 (dropped
-  // directions give zero columns)
-  hipError_t orth(const double* Y, double* Qo, int rows) const {
-    const int b = L.b;
-    hipError_t e;
-    if ((e = mm(Y, kDtF64, 1, b, false, Y, kDtF64, b, 1, false, at(L.gram), b, b, b, rows)) != hipSuccess) return e;
-    if ((e = eig(at(L.gram), at(L.e), at(L.lam), b, 1)) != hipSuccess) return e;
-    return mm(Y, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, Qo, b, rows, b, b);
-  }
-
   // Rank-1 factors of |F| for F [d x r] (fp64): left to left/left_o, right to right
   hipError_t rank1(const double* F, int d, double* left, float* left_o, double* right) const {
     const int r = L.r;
@@ -1324,8 +1298,8 @@ struct Svid {
     hipLaunchKernelGGL(rand_fill_kernel, dim3(grid_for(static_cast<int64_t>(n) * b)), dim3(256), 0, st, Z,
                        static_cast<int64_t>(n) * b, seed);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // Y = W Z; per round Q = orth(Y), Z = orth(W^T Q), Y = W Z (CholQR); then
-    // Q = an orthonormal basis of Y's range by eigenvectors
+    // Y = W Z; per round Q = orth(Y), Z = orth(W^T Q), Y = W Z; then Q =
+    // orth(Y) (every orth by CholQR)
     if ((e = mm(W, wdt, n, 1, false, Z, kDtF64, b, 1, false, Y, b, m, b, n)) != hipSuccess) return e;
     for (int it = 0; it < iters; ++it) {
       if ((e = orth_chol(Y, Q, m)) != hipSuccess) return e;
@@ -1333,11 +1307,11 @@ struct Svid {
       if ((e = orth_chol(Z2, Z, n)) != hipSuccess) return e;
       if ((e = mm(W, wdt, n, 1, false, Z, kDtF64, b, 1, false, Y, b, m, b, n)) != hipSuccess) return e;
     }
-    if ((e = orth(Y, Q, m)) != hipSuccess) return e;
+    if ((e = orth_chol(Y, Q, m)) != hipSuccess) return e;
     // Rayleigh-Ritz: Z = W^T Q, Z^T Z = E diag(lambda) E^T, U = Q E_r, V = Z E_r / sigma
     if ((e = mm(W, wdt, 1, n, false, Q, kDtF64, b, 1, false, Z, b, n, b, m)) != hipSuccess) return e;
     if ((e = mm(Z, kDtF64, 1, b, false, Z, kDtF64, b, 1, false, at(L.gram), b, b, b, n)) != hipSuccess) return e;
-    if ((e = eig(at(L.gram), at(L.e), at(L.lam), b, 0)) != hipSuccess) return e;
+    if ((e = eig(at(L.gram), at(L.e), at(L.lam), b)) != hipSuccess) return e;
     if ((e = mm(Q, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, at(L.ud), r, m, r, b)) != hipSuccess) return e;
     if ((e = mm(Z, kDtF64, b, 1, false, at(L.e), kDtF64, b, 1, false, at(L.vd), r, n, r, b)) != hipSuccess) return e;
     hipLaunchKernelGGL(sign_scale_kernel, dim3(r), dim3(256), 0, st, static_cast<const double*>(at(L.ud)),
