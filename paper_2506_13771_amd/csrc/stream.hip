@@ -169,6 +169,23 @@ __global__ void __launch_bounds__(kThreads) stream_s1_kernel(const uint32_t* __r
         wd[8 * ch + j] = v | (lo & 0xffffu);
       }
   };
+  // the g and x elements of the run's tables (and zero tables up to
+  // MAXBLK: thread e builds table e % 8 of block e / 8) are loaded first, so
+  // that the tables can be built while the words are still in flight
+  // (vector-memory loads complete in issue order)
+  static_assert((8 * MAXBLK) % kThreads == 0, "whole table items per thread");
+  constexpr int kItems = 8 * MAXBLK / kThreads;
+  uint32_t gb[kItems][4], xb[kItems][TM][4];
+#pragma unroll
+  for (int n = 0; n < kItems; ++n) {
+    const int e = tid + kThreads * n;
+    const int bi = e >> 3, q = e & 7;
+    const int jb = 32 * (b0 + bi) + 4 * q;
+    const bool in = bi < nblk;
+    bload4<SC, false>(gr, jb, in, gb[n]);
+#pragma unroll
+    for (int t = 0; t < TM; ++t) bload4<ACT, false>(xr, t * d_in + jb, in && t < T, xb[n][t]);
+  }
   // NTALL > 0 (every rank of the list <= 64 NTALL): every tile's words are
   // loaded at once, in flight while the tables are built; else two tiles'
   // words at a time
@@ -180,25 +197,19 @@ __global__ void __launch_bounds__(kThreads) stream_s1_kernel(const uint32_t* __r
   } else {
     load_tile(0, wbuf[0]);
   }
-
-  for (int k = tid; k < r; k += kThreads) lsh[k] = bits_to_f32<SC>(bload<SC>(lr, k));
-  // the tables of the run's blocks and zero tables up to MAXBLK: thread e
-  // builds table e % 8 of block e / 8
-  for (int e = tid; e < 8 * MAXBLK; e += kThreads) {
+#pragma unroll
+  for (int n = 0; n < kItems; ++n) {
+    const int e = tid + kThreads * n;
     const int bi = e >> 3, q = e & 7;
     const int jb = 32 * (b0 + bi) + 4 * q;
-    const bool in = bi < nblk;
-    uint32_t gb[4], xb[TM][4];
-    bload4<SC, false>(gr, jb, in, gb);
-#pragma unroll
-    for (int t = 0; t < TM; ++t) bload4<ACT, false>(xr, t * d_in + jb, in && t < T, xb[t]);
 #pragma unroll
     for (int t = 0; t < TM; ++t) {
       float a[4];
-      lut::table_inputs<ACT, SC, false>(xb[t], gb, jb, d_in, tailv, a);
+      lut::table_inputs<ACT, SC, false>(xb[n][t], gb[n], jb, d_in, tailv, a);
       lut::build_table_plain(tbl + (t * MAXBLK + bi) * kSet + 16 * q, a[0], a[1], a[2], a[3]);
     }
   }
+  for (int k = tid; k < r; k += kThreads) lsh[k] = bits_to_f32<SC>(bload<SC>(lr, k));
   __syncthreads();
 
   uint32_t sel[4];
