@@ -103,6 +103,24 @@ def test_dual_svid_exact_family(d_out, d_in, r):
     assert np.abs(got["W_res"]).max() <= 1e-5 * np.abs(W).max()
 
 
+def test_dual_svid_steep_spectrum():
+    # every block is orthonormalised through its Gram matrix, which squares its condition
+    # number: top-16 singular values falling geometrically from 1 to 1e-4, then 8 near 1e-8
+    # (a gap of 1e-4) and nothing else, so the 32-column block is rank-deficient and its
+    # kept part has a condition number near 1e4; the bars of the other cases still hold
+    d_out, d_in, r, k = 160, 128, 16, 24
+    rng = np.random.default_rng(7401)
+    Uo, _ = np.linalg.qr(rng.standard_normal((d_out, k)))
+    Vo, _ = np.linalg.qr(rng.standard_normal((d_in, k)))
+    s = np.concatenate([10.0 ** (-4.0 * np.arange(r) / (r - 1)), 1e-8 * 10.0 ** (-np.arange(k - r) / 8.0)])
+    W = ((Uo * s) @ Vo.T).astype(np.float32)
+    ref = O.dual_svid(W.astype(np.float64), r)
+    got = _run(W, r, oversample=16, iters=10)
+    _check_path(got, ref, 0, "steep spectrum path 0")
+    assert np.abs(got["W_res"] - ref["Wres"]).max() <= TOL * np.abs(W).max()
+    _check_path(got, ref, 1, "steep spectrum path 1")
+
+
 def test_dual_svid_bf16_weight_and_determinism():
     d_out, d_in, r = 128, 96, 12
     W = synth.dense_weight(d_out, d_in, 16, 0.05, cfg=71)
