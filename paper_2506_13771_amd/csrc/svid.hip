@@ -1298,8 +1298,8 @@ struct Svid {
     hipLaunchKernelGGL(rand_fill_kernel, dim3(grid_for(static_cast<int64_t>(n) * b)), dim3(256), 0, st, Z,
                        static_cast<int64_t>(n) * b, seed);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // Y = W Z; per round Q = orth(Y), Z = orth(W^T Q), Y = W Z; then Q =
-    // orth(Y) (every orth by CholQR)
+    // Y = W Z; per round Q = orth_chol(Y), Z = orth_chol(W^T Q), Y = W Z;
+    // then Q = orth_chol(Y)
     if ((e = mm(W, wdt, n, 1, false, Z, kDtF64, b, 1, false, Y, b, m, b, n)) != hipSuccess) return e;
     for (int it = 0; it < iters; ++it) {
       if ((e = orth_chol(Y, Q, m)) != hipSuccess) return e;
